@@ -1,0 +1,178 @@
+"""Oracle executors.
+
+``run_canonical`` is the plain definition of what the hot path computes:
+the operator graph evaluated in logical index space, each operator in
+float64 and its result rounded to the edge dtype (float32, or bfloat16 via
+float32), in row-major storage.  Layout and arena choices transform only the
+execution blueprint of a fixed graph, so the planned execution must reach
+this same result.
+
+``run_in_arena`` executes the same graph with every edge stored in its own
+layout inside one byte arena at its planned offset (views aliasing their
+root's bytes).  It uses the same operator functions, so for any valid layout
+assignment and any valid arena plan it must return bit-identical outputs;
+the arena is filled with NaN bytes first, so reading a byte before it is
+written, or a buffer overwritten while still live, shows up as a mismatch.
+
+Operator semantics follow ONNX, the paper's front-end format:
+  MatMul      numpy matmul (batch broadcast; weights are 2-D [K, N])
+  Add / Mul   elementwise with numpy broadcasting (bias [N])
+  Transpose   Y = X.transpose(perm);  Reshape: row-major reinterpretation
+  Softmax     over the last axis of scale*x; with causal, key k > query q is
+              excluded and its probability is exactly 0
+  LayerNorm   (x - mean) / sqrt(biased var + eps) * gamma + beta, last axis
+  RMSNorm     x / sqrt(mean(x^2) + eps) * gamma, last axis
+  GELU        0.5 x (1 + erf(x / sqrt 2));  SiLU: x / (1 + exp(-x))
+  RoPE        rotate-half on the last axis of [B, S, NH, D] with tables
+              cos/sin [S, D/2] indexed by the position (axis 1)
+"""
+from __future__ import annotations
+
+import numpy as np
+from scipy.special import erf
+
+from . import numerics
+from .layouts import node_is_view
+
+
+def op_matmul(a, b):
+    return np.matmul(a, b)
+
+
+def op_softmax(x, scale, causal):
+    z = np.float64(scale) * x
+    if causal:
+        q, k = x.shape[-2], x.shape[-1]
+        mask = np.arange(k)[None, :] > np.arange(q)[:, None]
+        z = np.where(mask, -np.inf, z)
+    m = z.max(axis=-1, keepdims=True)
+    e = np.exp(z - m)
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def op_layernorm(x, gamma, beta, eps):
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + np.float64(eps)) * gamma + beta
+
+
+def op_rmsnorm(x, gamma, eps):
+    ms = (x * x).mean(axis=-1, keepdims=True)
+    return x / np.sqrt(ms + np.float64(eps)) * gamma
+
+
+def op_gelu(x):
+    return 0.5 * x * (1.0 + erf(x / np.sqrt(2.0)))
+
+
+def op_silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+def op_rope(x, cos, sin):
+    h = x.shape[-1] // 2
+    c = cos[None, :, None, :]
+    s = sin[None, :, None, :]
+    x1, x2 = x[..., :h], x[..., h:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def eval_node(nd, args):
+    """float64 result of one operator on float64 arguments (not yet rounded)."""
+    op = nd.op
+    if op == "matmul":
+        return op_matmul(args[0], args[1])
+    if op == "add":
+        return args[0] + args[1]
+    if op == "mul":
+        return args[0] * args[1]
+    if op == "transpose":
+        return np.transpose(args[0], nd.perm)
+    if op == "reshape":
+        return args[0].reshape(nd.out_shape)
+    if op == "softmax":
+        return op_softmax(args[0], nd.fattr, nd.iattr)
+    if op == "layernorm":
+        return op_layernorm(args[0], args[1], args[2], nd.fattr)
+    if op == "rmsnorm":
+        return op_rmsnorm(args[0], args[1], nd.fattr)
+    if op == "gelu":
+        return op_gelu(args[0])
+    if op == "silu":
+        return op_silu(args[0])
+    if op == "rope":
+        return op_rope(args[0], args[1], args[2])
+    raise ValueError(op)
+
+
+def _const_values(g, consts):
+    out = []
+    for (role, shape, dt), a in zip(g.consts, consts):
+        a = np.asarray(a, dtype=np.float64).reshape(shape)
+        out.append(numerics.round_to(a, dt))
+    return out
+
+
+def run_canonical(g, inputs, consts, keep=False):
+    """Row-major reference execution.  Returns the graph outputs (float64
+    arrays of dtype-representable values); with ``keep`` also every edge."""
+    cv = _const_values(g, consts)
+    vals = {}
+    for e, a in enumerate(inputs):
+        vals[e] = numerics.round_to(np.asarray(a, np.float64).reshape(g.input_shapes[e]), g.dtype)
+    for n, nd in enumerate(g.nodes):
+        args = [vals[v] if v >= 0 else cv[~v] for v in nd.ins]
+        y = eval_node(nd, args)
+        assert tuple(y.shape) == tuple(nd.out_shape), (n, nd.op, y.shape, nd.out_shape)
+        vals[g.out_edge(n)] = numerics.round_to(y, g.dtype)
+    outs = [vals[e] for e in g.outputs]
+    return (outs, vals) if keep else outs
+
+
+def run_in_arena(g, layout_of_edge, root_of_edge, offset_of_root, peak,
+                 inputs, consts, poison=True):
+    """Execute with each edge stored permuted inside one uint8 arena.
+
+    ``layout_of_edge[e]`` is a permutation; ``root_of_edge[e]`` the buffer
+    edge e lives in; ``offset_of_root[r]`` the byte offset of arena buffer r.
+    Graph inputs and outputs live in separate caller buffers (row-major).
+    """
+    isz = numerics.itemsize(g.dtype)
+    arena = np.full(max(int(peak), 1), 0xFF if poison else 0, dtype=np.uint8)
+    ext = {}
+    for e, a in enumerate(inputs):
+        v = numerics.round_to(np.asarray(a, np.float64).reshape(g.input_shapes[e]), g.dtype)
+        ext[e] = numerics.to_bytes(v, g.dtype).copy()
+    for e in g.outputs:
+        ext[e] = np.full(int(np.prod(g.edge_shape(e))) * isz, 0xFF, np.uint8)
+
+    def buf(e):
+        r = root_of_edge[e]
+        if r in ext:
+            return ext[r], 0
+        return arena, int(offset_of_root[r])
+
+    def load(e):
+        shape = g.edge_shape(e)
+        perm = tuple(layout_of_edge[e])
+        cnt = int(np.prod(shape))
+        b, off = buf(e)
+        flat = numerics.from_bytes(b[off: off + cnt * isz], g.dtype, cnt)
+        phys = flat.reshape([shape[d] for d in perm])
+        return phys.transpose(np.argsort(perm))
+
+    def store(e, val):
+        perm = tuple(layout_of_edge[e])
+        phys = np.ascontiguousarray(val.transpose(perm))
+        raw = numerics.to_bytes(phys, g.dtype)
+        b, off = buf(e)
+        b[off: off + raw.size] = raw
+
+    cv = _const_values(g, consts)
+    for n, nd in enumerate(g.nodes):
+        if node_is_view(g, n, layout_of_edge):
+            continue
+        args = [load(v) if v >= 0 else cv[~v] for v in nd.ins]
+        y = numerics.round_to(eval_node(nd, args), g.dtype)
+        store(g.out_edge(n), y)
+    return [load(e) for e in g.outputs]

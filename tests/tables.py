@@ -1,0 +1,78 @@
+"""Synthetic cost tables for planner tests (test helper; uses the oracle).
+
+The tables are seeded inputs to both planners.  Candidate layout lists and
+the view predicate come from the oracle; costs are random integers, so the
+same file can be handed to the oracle planner and to the C++ planner.
+"""
+from __future__ import annotations
+
+import json
+
+import numpy as np
+
+from oracle import layouts
+
+
+def _sig_key(g, n):
+    nd = g.nodes[n]
+    ins = [tuple(g.edge_shape(e)) for e in g.act_inputs(n)]
+    cs = [tuple(g.consts[~v][1]) for v in nd.ins if v < 0]
+    return (nd.op, tuple(ins), tuple(cs), tuple(nd.out_shape), nd.perm,
+            nd.fattr, nd.iattr)
+
+
+def synthetic_table(g, seed, mode="random", n_variants=3, lo=1, hi=1000,
+                    drop_identity_node=None):
+    """Build a cost table dict.  Modes:
+      random    -- uniform integer costs in [lo, hi] per variant (some -1)
+      ties      -- every non-view cost equal (ties everywhere)
+      identity  -- identity combination cheapest for every node
+      distinct  -- all costs distinct (no ties anywhere in sums is likely)
+    """
+    rng = np.random.default_rng(seed)
+    L = layouts.edge_layouts(g)
+    sig_index, sigs, node_sig = {}, [], []
+    for n, nd in enumerate(g.nodes):
+        key = _sig_key(g, n)
+        if key in sig_index and n != drop_identity_node:
+            node_sig.append(sig_index[key])
+            continue
+        slot_shapes = [g.edge_shape(e) for e in g.act_inputs(n)]
+        lists = [layouts.layout_list(s) for s in slot_shapes]
+        out_list = layouts.layout_list(nd.out_shape)
+        entries = []
+        for combo in __import__("itertools").product(*lists, out_list):
+            ins, out = combo[:-1], combo[-1]
+            if nd.op in ("transpose", "reshape") and layouts.is_view(
+                    nd.op, nd.perm, slot_shapes[0], nd.out_shape, ins[0], out):
+                entries.append([[list(p) for p in ins], list(out), [0]])
+                continue
+            ident = all(p == tuple(range(len(p))) for p in combo)
+            if n == drop_identity_node and ident:
+                continue
+            if mode == "ties":
+                costs = [100] * n_variants
+            elif mode == "identity":
+                costs = [10 if ident else int(rng.integers(11, hi + 1))
+                         for _ in range(n_variants)]
+            elif mode == "distinct":
+                costs = [int(rng.integers(0, 1 << 40)) for _ in range(n_variants)]
+            else:
+                costs = [int(rng.integers(lo, hi + 1)) for _ in range(n_variants)]
+                for v in range(1, n_variants):
+                    if rng.random() < 0.2:
+                        costs[v] = -1
+            entries.append([[list(p) for p in ins], list(out), costs])
+        sig_index.setdefault(key, len(sigs))
+        node_sig.append(len(sigs))
+        sigs.append({"op": nd.op, "in_shapes": [list(s) for s in slot_shapes],
+                     "out_shape": list(nd.out_shape), "entries": entries})
+    return {"format": "fluid-cost-table/1",
+            "edges": [[list(p) for p in lst] for lst in L],
+            "sigs": sigs, "node_sig": node_sig}
+
+
+def write_table(obj, path):
+    with open(path, "w") as f:
+        json.dump(obj, f)
+    return str(path)

@@ -1,0 +1,201 @@
+"""Pins for the oracle layout planner (Alg. 1-3, Eq. 1, vote)."""
+import itertools
+
+import numpy as np
+import pytest
+
+import synth_inputs
+from oracle import brute, costtable, graph, plan_layout as PL
+from oracle.graph import Graph
+from tables import synthetic_table
+from tinygraphs import chain_graph, diamond_graph, t1_graph, t2_graph
+
+
+def _all_paths_len(g, S):
+    """Brute force: the largest node count of any producer->consumer path in S."""
+    Sset = set(S)
+    succ = {n: [] for n in S}
+    for n in S:
+        for e in g.act_inputs(n):
+            p = g.producer(e)
+            if p is not None and p in Sset:
+                succ[p].append(n)
+    best = 0
+
+    def dfs(n, k):
+        nonlocal best
+        best = max(best, k)
+        for m in succ[n]:
+            dfs(m, k + 1)
+    for n in S:
+        dfs(n, 1)
+    return best
+
+
+def _random_dag(rng, n):
+    g = Graph(dtype="f32")
+    g.add_input((2, 3))
+    for i in range(n):
+        k = int(rng.integers(1, 3))
+        ins = sorted({int(rng.integers(0, g.n_edges)) for _ in range(k)})
+        if len(ins) == 1:
+            g.add_node("gelu", ins, (2, 3))
+        else:
+            g.add_node("add", ins[:2], (2, 3))
+    g.outputs = [g.n_edges - 1]
+    return g
+
+
+def test_longest_path_is_longest_and_split_partitions():
+    rng = np.random.default_rng(0)
+    for _ in range(200):
+        g = _random_dag(rng, int(rng.integers(1, 12)))
+        S = list(range(len(g.nodes)))
+        p = PL.longest_path(g, S)
+        assert len(p) == _all_paths_len(g, S)
+        for a, b in zip(p, p[1:]):
+            assert a in [g.producer(e) for e in g.act_inputs(b)]
+        paths = PL.split(g)
+        flat = sorted(n for q in paths for n in q)
+        assert flat == S
+        for q in paths:
+            for a, b in zip(q, q[1:]):
+                assert a in [g.producer(e) for e in g.act_inputs(b)]
+
+
+def test_post_ln_layer_paths():
+    g = graph.build_transformer(synth_inputs.config(1))
+    paths = PL.split(g)
+    assert paths[0] == [0, 1, 2, 3, 12, 13, 14, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 26, 27]
+    assert paths[1:] == [[4, 5, 6, 7], [8, 9, 10, 11]]
+
+
+def _ct(g, **kw):
+    return costtable.load(synthetic_table(g, **kw), g)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_dp_on_pure_chain_equals_brute_force(seed):
+    g = chain_graph(4, (2, 3, 4))
+    mode = "distinct" if seed % 2 else "random"
+    ct = _ct(g, seed=seed, mode=mode, lo=1, hi=20)
+    plan = PL.plan_layouts(g, ct, PL.NO_GUARD)
+    opt_total, opt_lay = brute.best_layouts(g, ct)
+    assert plan.total == opt_total
+    if mode == "distinct":
+        assert plan.layout_idx == opt_lay
+    # the variant-0 column is an independent table for the same check
+    plan0 = PL.plan_layouts(g, ct, PL.NO_GUARD | PL.NO_VARIANTS)
+    assert plan0.total == brute.best_layouts(g, ct, use_v0=True)[0]
+
+
+@pytest.mark.parametrize("builder", [diamond_graph, t1_graph, t2_graph])
+@pytest.mark.parametrize("seed", range(4))
+def test_branched_plan_between_optimum_and_identity(builder, seed):
+    g = builder()
+    ct = _ct(g, seed=seed, mode="random", lo=1, hi=50)
+    plan = PL.plan_layouts(g, ct)
+    ident = PL.plan_cost(g, ct, False, [0] * g.n_edges)
+    opt, _ = brute.best_layouts(g, ct)
+    assert opt <= plan.total <= ident
+    assert plan.total == PL.plan_cost(g, ct, False, plan.layout_idx)
+
+
+def _rank2_table(g, costs):
+    """costs[n] : dict {(slot layout idx..., out idx): cost}; layouts of a
+    [2,3] tensor are (0,1) row-major = 0 and (1,0) = 1."""
+    P = [[0, 1], [1, 0]]
+    L = []
+    for e in range(g.n_edges):
+        pinned = e < g.n_inputs or e in g.outputs
+        L.append([P[0]] if pinned else P)
+    sigs = []
+    for n in range(len(g.nodes)):
+        ents = [[[P[i] for i in key[:-1]], P[key[-1]], [c]] for key, c in costs[n].items()]
+        sigs.append({"op": g.nodes[n].op, "in_shapes": [], "out_shape": [2, 3], "entries": ents})
+    return {"format": "fluid-cost-table/1", "edges": L, "sigs": sigs,
+            "node_sig": list(range(len(g.nodes)))}
+
+
+def _hand_diamond():
+    """x -> a=gelu(x) -> {b=silu(a), c=gelu(a)}; b2=silu(b); d=add(b2,c);
+    y=gelu(d).  Paths: [a b b2 d y] and [c]; shared edges a and c."""
+    g = Graph(dtype="f32")
+    x = g.add_input((2, 3))
+    a = g.add_node("gelu", [x], (2, 3))
+    b = g.add_node("silu", [a], (2, 3))
+    c = g.add_node("gelu", [a], (2, 3))
+    b2 = g.add_node("silu", [b], (2, 3))
+    d = g.add_node("add", [b2, c], (2, 3))
+    y = g.add_node("gelu", [d], (2, 3))
+    g.outputs = [y]
+    same = {(0, 0): 10, (1, 1): 10, (0, 1): 50, (1, 0): 50}
+    costs = [
+        {(0, 0): 10, (0, 1): 10},                           # a
+        dict(same),                                         # b
+        {(0, 0): 25, (1, 1): 1, (0, 1): 50, (1, 0): 50},    # c
+        dict(same),                                         # b2
+        {k: (10 if k[0] == k[1] == k[2] else 100)
+         for k in itertools.product((0, 1), repeat=3)},     # d
+        {(0, 0): 10, (1, 0): 30},                           # y (output pinned)
+    ]
+    return g, costs
+
+
+def test_hand_worked_vote_with_cost_tie_breaks():
+    """Worked by hand.  Alone, path [a b b2 d y] is cheapest all row-major
+    (50) and path [c] prefers a, c column-major (cost 1), so edges a and c
+    each get one ballot per layout.  Tie on a: fixing a row-major costs
+    50 + 25 = 75 over the two paths, column-major 70 + 1 = 71 -> column.
+    Tie on c (a fixed column): row 90 + 50 = 140, column 70 + 1 = 71 -> column.
+    Re-optimised plan: a b c b2 d all column-major, total 71 < row-major 75."""
+    g, costs = _hand_diamond()
+    ct = costtable.load(_rank2_table(g, costs), g)
+    paths = PL.split(g)
+    assert paths == [[0, 1, 3, 4, 5], [2]]
+    infos = [PL.PathInfo(g, p) for p in paths]
+    t0, s0, b0 = PL.dp_path(g, ct, False, infos[0], {})
+    t1, s1, b1 = PL.dp_path(g, ct, False, infos[1], {})
+    assert (t0, s0) == (50, [0, 0, 0, 0, 0]) and b0[3] == {3: 0}
+    assert (t1, s1) == (1, [1]) and b1[0] == {1: 1}
+    plan = PL.plan_layouts(g, ct)
+    assert plan.layout_idx == [0, 1, 1, 1, 1, 1, 0]
+    assert plan.total == 71 and plan.guard_used == 0
+    assert PL.plan_cost(g, ct, False, [0] * 7) == 75
+
+
+def test_guard_returns_identity_when_vote_hurts():
+    g, costs = _hand_diamond()
+    costs[2] = {(0, 0): 11, (1, 1): 1, (0, 1): 50, (1, 0): 50}   # row-major c cheaper now
+    costs[5] = {(0, 0): 10, (1, 0): 200}
+    ct = costtable.load(_rank2_table(g, costs), g)
+    plan = PL.plan_layouts(g, ct)
+    ident = PL.plan_cost(g, ct, False, [0] * 7)
+    assert plan.total <= ident
+
+
+def test_missing_identity_entry_is_infeasible():
+    g = chain_graph(3, (2, 3, 4))
+    obj = synthetic_table(g, seed=0, drop_identity_node=1)
+    ct = costtable.load(obj, g)
+    with pytest.raises(PL.Infeasible):
+        PL.plan_layouts(g, ct)
+
+
+def test_no_dp_returns_identity_and_ties_prefer_identity():
+    g = graph.build_transformer(synth_inputs.config(1))
+    ct = _ct(g, seed=3)
+    p = PL.plan_layouts(g, ct, PL.NO_DP)
+    assert p.layout_idx == [0] * g.n_edges and p.guard_used == 0
+    pt = PL.plan_layouts(g, _ct(g, seed=3, mode="ties"))
+    # with every copy costing the same, the plan removes transposes (views
+    # cost 0) and never costs more than row-major
+    ident = PL.plan_cost(g, _ct(g, seed=3, mode="ties"), False, [0] * g.n_edges)
+    assert pt.total <= ident
+
+
+def test_identity_favouring_table_gives_identity_plan():
+    g = graph.build_transformer(synth_inputs.config(1))
+    ct = _ct(g, seed=4, mode="identity")
+    p = PL.plan_layouts(g, ct)
+    assert p.total <= PL.plan_cost(g, ct, False, [0] * g.n_edges)
