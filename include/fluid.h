@@ -1,0 +1,262 @@
+/*
+ * fluid.h -- C ABI of the layout-planned transformer hot path for MI355X.
+ *
+ * Method: FluidML (arXiv 2411.09242), Section 3.  A frozen operator graph
+ * with known shapes gets (1) a memory layout -- a dimension permutation --
+ * for every intermediate tensor, chosen by longest-path decomposition
+ * (Alg. 1-2) and a dynamic program over measured kernel times (Eq. 1,
+ * Alg. 3) with majority-vote conflict resolution; (2) a static placement of
+ * every tensor inside one pre-allocated buffer by Greedy-by-Size over tensor
+ * lifetimes (Alg. 4); then (3) the operators run as GPU kernels whose loads
+ * and stores follow each tensor's layout, inside that single buffer.
+ *
+ * Conventions for every entry point:
+ *  - Every call returns a fluid_status; nothing throws across the ABI.  On
+ *    failure fluid_last_error() describes the cause (thread-local string,
+ *    valid until the next fluid_* call on the same thread).
+ *  - Handles (graph, cost table, plans) are created and owned by the
+ *    library, immutable after creation, and released with their *_free
+ *    function (NULL is accepted).  Out-pointers are written only on success.
+ *  - All device memory (arena, constants, graph inputs and outputs, scratch)
+ *    is owned by the caller; the library never allocates or frees device
+ *    memory.  Arguments are validated before any HIP call.
+ *  - Tensor shapes are int64 element counts, at most FLUID_MAX_RANK dims.
+ *    Constants, graph inputs and graph outputs are always dense row-major.
+ *  - The host-only build of this library (no GPU code) exports the same
+ *    symbols; there fluid_run and fluid_measure_costs return
+ *    FLUID_E_UNSUPPORTED.
+ */
+#ifndef FLUID_H
+#define FLUID_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FLUID_MAX_RANK 6
+#define FLUID_MAX_IN 4
+
+typedef enum {
+  FLUID_OK = 0,
+  FLUID_E_INVALID = -1,         /* malformed argument, graph or file          */
+  FLUID_E_UNSUPPORTED = -2,     /* valid but not implemented (or host build)  */
+  FLUID_E_INFEASIBLE = -3,      /* no finite-cost layout plan exists          */
+  FLUID_E_ARENA_TOO_SMALL = -4, /* arena_bytes below the plan's peak          */
+  FLUID_E_HIP = -5,             /* a HIP runtime call failed                  */
+  FLUID_E_NOMEM = -6            /* host allocation failed                     */
+} fluid_status;
+
+const char* fluid_last_error(void);
+
+typedef enum { FLUID_F32 = 0, FLUID_BF16 = 1 } fluid_dtype;
+
+/* Operators of the transformer chain.  Semantics (ONNX, the paper's front-end
+ * format; Section 4):
+ *  MATMUL    in[0] A [..., M, K] activation; in[1] B either a 2-D constant or
+ *            activation [K, N], or an activation [..., K, N] with the same
+ *            leading dims as A.  out [..., M, N].  fp32 accumulation.
+ *  ADD, MUL  in[0] activation; in[1] activation of the same shape, or (ADD
+ *            only) a constant [N] broadcast over the last dim.
+ *  TRANSPOSE out dim i = in dim perm[i].
+ *  RESHAPE   row-major reinterpretation; only "split one dim into two
+ *            adjacent dims" and "merge two adjacent dims" are accepted.
+ *  SOFTMAX   over the last dim of f_attr[0] * x; i_attr[0] = 1 masks key
+ *            k > query q (second-to-last dim) and writes exact zeros there.
+ *  LAYERNORM in[1] gamma [H], in[2] beta [H] constants; eps = f_attr[0];
+ *            biased variance over the last dim.
+ *  RMSNORM   in[1] gamma [H]; x / sqrt(mean(x^2) + eps) * gamma.
+ *  GELU      0.5 x (1 + erf(x / sqrt 2));  SILU  x / (1 + exp(-x)).
+ *  ROPE      in[0] [B, S, NH, D] (D even); in[1] cos, in[2] sin: fp32
+ *            constants [S, D/2]; rotate-half: for i < D/2,
+ *            y_i = x_i c - x_{i+D/2} s,  y_{i+D/2} = x_{i+D/2} c + x_i s.   */
+typedef enum {
+  FLUID_OP_MATMUL = 0, FLUID_OP_ADD = 1, FLUID_OP_MUL = 2,
+  FLUID_OP_TRANSPOSE = 3, FLUID_OP_RESHAPE = 4, FLUID_OP_SOFTMAX = 5,
+  FLUID_OP_LAYERNORM = 6, FLUID_OP_RMSNORM = 7, FLUID_OP_GELU = 8,
+  FLUID_OP_SILU = 9, FLUID_OP_ROPE = 10
+} fluid_op;
+
+/* Informational tag of a constant (how the synthetic workloads fill it). */
+typedef enum {
+  FLUID_ROLE_OTHER = 0, FLUID_ROLE_WEIGHT = 1, FLUID_ROLE_BIAS = 2,
+  FLUID_ROLE_GAMMA = 3, FLUID_ROLE_BETA = 4, FLUID_ROLE_ROPE_COS = 5,
+  FLUID_ROLE_ROPE_SIN = 6
+} fluid_const_role;
+
+/* One node.  Node id = index in the node array, which must be topological.
+ * Edges: graph inputs are edges 0..n_inputs-1; the output of node n is edge
+ * n_inputs + n.  in[i] >= 0 names an edge; in[i] < 0 names constant ~in[i]. */
+typedef struct {
+  int32_t op;                          /* fluid_op                              */
+  int32_t n_in;
+  int32_t in[FLUID_MAX_IN];
+  int32_t out_rank;
+  int64_t out_shape[FLUID_MAX_RANK];
+  int32_t perm[FLUID_MAX_RANK];        /* TRANSPOSE only                        */
+  float f_attr[2];                     /* SOFTMAX scale; LAYERNORM/RMSNORM eps  */
+  int32_t i_attr[2];                   /* SOFTMAX causal flag                   */
+} fluid_node_desc;
+
+/* Shapes of inputs / constants: arrays of n * FLUID_MAX_RANK int64, row i
+ * holding the dims of item i (entries past its rank are ignored). */
+typedef struct {
+  int32_t dtype;                       /* fluid_dtype of activations/weights   */
+  int32_t n_inputs;
+  const int32_t* input_rank;
+  const int64_t* input_shapes;
+  int32_t n_consts;
+  const int32_t* const_rank;
+  const int64_t* const_shapes;
+  const int32_t* const_dtype;          /* fluid_dtype per constant             */
+  const int32_t* const_role;           /* fluid_const_role per constant (NULL ok) */
+  int32_t n_nodes;
+  const fluid_node_desc* nodes;
+  int32_t n_outputs;
+  const int32_t* output_edges;         /* must be node outputs                 */
+} fluid_graph_desc;
+
+typedef struct fluid_graph fluid_graph;
+typedef struct fluid_cost_table fluid_cost_table;
+typedef struct fluid_layout_plan fluid_layout_plan;
+typedef struct fluid_arena_plan fluid_arena_plan;
+
+/* Builds and validates a graph (Section 4 "Compiler": the model as a graph
+ * linearised into one operator sequence).  Checks arity, constant and edge
+ * references, topological order and every output shape; errors:
+ * FLUID_E_INVALID, FLUID_E_UNSUPPORTED (e.g. a general reshape). */
+fluid_status fluid_build_graph(const fluid_graph_desc* desc, fluid_graph** out);
+
+/* Transformer stacks used by the synthetic workloads.  arch 0: post-LN
+ * encoder layer (BERT); 1: pre-LN decoder layer with causal attention and a
+ * final LayerNorm (GPT-2); 2: Llama-style decoder (RMSNorm, RoPE, causal,
+ * SwiGLU FFN, final RMSNorm, no biases).  Node order per layer: q, k, v
+ * projections (MatMul [+ bias Add], Reshape to heads, [RoPE], Transpose to
+ * [B,NH,S,D], keys to [B,NH,D,S]), scores MatMul, Softmax(1/sqrt(D)),
+ * context MatMul, Transpose + Reshape back, output projection, residual,
+ * norm, FFN, residual[, norm]. */
+typedef struct {
+  int32_t arch;
+  int32_t layers, batch, seq, hidden, heads, ffn;
+  int32_t dtype;                       /* fluid_dtype                           */
+  float eps;                           /* norm epsilon (1e-5)                   */
+  float rope_base;                     /* 10000                                 */
+} fluid_model_cfg;
+fluid_status fluid_build_transformer(const fluid_model_cfg* cfg, fluid_graph** out);
+
+/* Counts of a graph (any pointer may be NULL). */
+fluid_status fluid_graph_info(const fluid_graph* g, int32_t* n_inputs, int32_t* n_consts,
+                              int32_t* n_nodes, int32_t* n_edges, int32_t* dtype);
+
+/* Canonical JSON description: dtype, inputs, consts (role, shape, dtype),
+ * nodes (op, ins, out_shape, perm, fattr, iattr), outputs, and the candidate
+ * layout list L(e) of every edge.  Writes at most cap bytes (NUL-terminated
+ * when it fits) and the full length to *len; call with cap = 0 to size. */
+fluid_status fluid_graph_export_json(const fluid_graph* g, char* buf, uint64_t cap, uint64_t* len);
+
+/* Cost table: the measured time of every node for every combination of
+ * input and output layouts (the eval() of Alg. 3), the minimum over kernel
+ * variants kept with its variant id (the GPU form of Section 3 "Loop
+ * Reordering").  JSON file format "fluid-cost-table/1": "edges" (L(e) per
+ * edge, identity first), "sigs" (op, in_shapes, out_shape, entries
+ * [[slot perms], out perm, [ns per variant, -1 = unavailable]]), "node_sig".
+ * Load validates the file against the graph (FLUID_E_INVALID on mismatch,
+ * a missing identity layout, or a nonzero cost on a view combination). */
+fluid_status fluid_cost_table_load(const char* json_path, const fluid_graph* g, fluid_cost_table** out);
+fluid_status fluid_cost_table_save(const fluid_cost_table* t, const char* json_path);
+
+/* Device scratch needed by fluid_measure_costs for this graph (bytes). */
+fluid_status fluid_measure_scratch_bytes(const fluid_graph* g, uint64_t* bytes);
+
+/* Measures the cost table on the GPU (Alg. 3's eval: real kernel time).
+ * For every operator signature, every candidate layout combination and
+ * every kernel variant: warm-up launches, then `reps` launches timed with
+ * HIP events; the median is rounded to integer nanoseconds.  View
+ * combinations of Transpose/Reshape cost 0.  Candidate lists: all
+ * dimension permutations (deduplicated), trimmed for tensors with more than
+ * six candidates to those whose innermost dim is one of the last two
+ * logical dims.  scratch: caller device memory of at least
+ * fluid_measure_scratch_bytes, 256-B aligned; its contents are overwritten.
+ * Synchronises hip_stream.  GPU build only. */
+fluid_status fluid_measure_costs(const fluid_graph* g, uint32_t reps, void* scratch,
+                                 uint64_t scratch_bytes, void* hip_stream, fluid_cost_table** out);
+
+#define FLUID_NO_DP 1u        /* return the all-row-major plan                */
+#define FLUID_NO_VARIANTS 2u  /* plan on the variant-0 column only (ablation) */
+#define FLUID_NO_GUARD 4u     /* keep the voted plan even if it costs more    */
+
+/* Layout plan (Section 3, Alg. 1-3, Eq. 1 and the vote): longest-path
+ * decomposition; per-path dynamic program over output layouts; majority vote
+ * on edges shared between paths (ties: lowest re-optimised cost of the
+ * touching paths, then lowest index); one re-optimisation with shared edges
+ * fixed; then, unless FLUID_NO_GUARD, the all-row-major plan if it is
+ * cheaper.  Errors: FLUID_E_INFEASIBLE (no identity entry, or no finite
+ * plan), FLUID_E_INVALID. */
+fluid_status fluid_plan_layouts(const fluid_graph* g, const fluid_cost_table* t, uint32_t flags,
+                                fluid_layout_plan** out);
+
+/* Plan contents: layout index into L(e) per edge (n_edges), kernel variant per
+ * node (n_nodes; -1 = view, no kernel), summed table cost, guard flag. */
+fluid_status fluid_layout_plan_get(const fluid_layout_plan* lp, int32_t* layout_idx_per_edge,
+                                   int32_t* variant_per_node, int64_t* total_ns, int32_t* guard_used);
+/* The permutation chosen for one edge (rank entries written to perm_out). */
+fluid_status fluid_edge_layout(const fluid_graph* g, const fluid_layout_plan* lp, int32_t edge,
+                               int32_t* perm_out);
+
+#define FLUID_ARENA_NO_REUSE 1u  /* naive plan: every buffer its own slice     */
+
+/* Arena plan (Alg. 4, Greedy-by-Size): a Transpose/Reshape that the layouts
+ * make a view owns no bytes; every other non-output node result is a buffer
+ * of size rounded up to `align` (a power of two >= 16; 256 recommended)
+ * with lifetime [producer, last reader]; buffers by size descending take
+ * the smallest fitting gap among lifetime-overlapping buffers, else the end.
+ * FLUID_ARENA_NO_REUSE places them at prefix sums in edge order instead. */
+fluid_status fluid_plan_arena(const fluid_graph* g, const fluid_layout_plan* lp, uint64_t align,
+                              uint32_t flags, fluid_arena_plan** out);
+
+/* Arena contents: peak bytes; the no-reuse total of the row-major plan; the
+ * max-live lower bound of this plan's buffers; per edge the byte offset of
+ * the edge's bytes (-1 if not in the arena: graph inputs/outputs) and its
+ * root edge (the buffer it aliases).  Any pointer may be NULL. */
+fluid_status fluid_arena_plan_get(const fluid_arena_plan* ap, uint64_t* peak_bytes, uint64_t* naive_bytes,
+                                  uint64_t* lower_bound_bytes, int64_t* offset_per_edge,
+                                  int32_t* root_per_edge);
+
+/* Executes the graph (Section 4 "Virtual Machine": the invoke interface):
+ * enqueues one kernel per non-view node, in node order, on hip_stream; the
+ * caller synchronises.  arena: device memory of at least the plan's peak,
+ * 256-B aligned; consts[i], inputs[i], outputs[i]: device pointers to dense
+ * row-major tensors of the graph's dtype (RoPE tables fp32).  No device
+ * allocation.  Errors before any launch: FLUID_E_INVALID (NULL pointer,
+ * misaligned arena, plans of another graph), FLUID_E_ARENA_TOO_SMALL;
+ * FLUID_E_HIP if a launch fails.  Concurrent calls on different streams
+ * with different arenas are safe; calls sharing an arena race. */
+fluid_status fluid_run(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
+                       void* arena, uint64_t arena_bytes, const void* const* consts,
+                       const void* const* inputs, void* const* outputs, void* hip_stream);
+
+/* Per-node timing of later fluid_run calls (profiling aid).  While enabled,
+ * fluid_run records a HIP event pair around every launch of a node whose
+ * node_mask entry is nonzero (NULL mask = all nodes), for at most
+ * max_records launches in total.  After the caller has synchronised,
+ * fluid_trace_collect adds the elapsed milliseconds and launch counts per
+ * node into its arrays (n_nodes each) and disables tracing.  Global state:
+ * not for concurrent use.  GPU build only. */
+fluid_status fluid_trace_enable(const fluid_graph* g, const uint8_t* node_mask, int32_t max_records);
+fluid_status fluid_trace_collect(const fluid_graph* g, double* ms_per_node, int32_t* launches_per_node);
+
+/* Name of the kernel a node runs under a plan ("view" for views), e.g.
+ * "gemm_f32_m128n128_ak_bn_cn". */
+fluid_status fluid_node_kernel(const fluid_graph* g, const fluid_layout_plan* lp, int32_t node,
+                               char* buf, uint64_t cap);
+
+void fluid_graph_free(fluid_graph* g);
+void fluid_cost_table_free(fluid_cost_table* t);
+void fluid_layout_plan_free(fluid_layout_plan* lp);
+void fluid_arena_plan_free(fluid_arena_plan* ap);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FLUID_H */

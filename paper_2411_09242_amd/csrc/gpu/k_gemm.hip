@@ -1,0 +1,548 @@
+// Permuted-stride batched GEMM on MFMA (gfx950).
+//
+//   C[g, m, n] = sum_k A[g, m, k] * B[g, k, n]
+//
+// Every operand is addressed through its own strides, so any layout the
+// planner picks for A, B or C runs without a relayout copy.  A block of 256
+// threads (4 wavefronts, 2 x 2) computes a BM x BN tile; operand tiles are
+// staged through LDS, where they are stored in the orientation the MFMA
+// fragments read, whichever dim is unit-stride in HBM:
+//   A: K-contiguous ("k") or M-contiguous ("mn") 16-byte loads, else scalar
+//   B: N-contiguous ("mn") or K-contiguous ("k") 16-byte loads, else scalar
+//   C: N-contiguous stores, M-contiguous 4-row stores, else scalar.
+// fp32 uses v_mfma_f32_32x32x2_f32 (lane l: A[l%32][l/32], B[l/32][l%32]);
+// bf16 uses v_mfma_f32_32x32x16_bf16 (lane l: 8 consecutive k of row l%32,
+// k-group l/32) with fp32 accumulation.  Accumulator v of lane l holds
+// C[8(v/4) + 4(l/32) + v%4][l%32].  The next K-tile is loaded into
+// registers while the current one is multiplied.
+#include "dev.h"
+#include "launch.h"
+
+namespace fluid {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+struct TileCoord {
+  uint32_t m0, n0;
+  int32_t a_base, b_base, c_base;
+};
+
+__device__ __forceinline__ TileCoord tile_coord(const GemmParams& p, uint32_t BM, uint32_t BN) {
+  const uint32_t per_g = p.tiles_m * p.tiles_n;
+  const uint32_t bid = blockIdx.x;
+  const uint32_t g = bid / per_g;
+  const uint32_t r = bid - g * per_g;
+  const uint32_t tm = r / p.tiles_n;
+  const uint32_t tn = r - tm * p.tiles_n;
+  const uint32_t g1 = fdiv(g, p.g2div);
+  const uint32_t g2 = g - g1 * p.G2;
+  TileCoord t;
+  t.m0 = tm * BM;
+  t.n0 = tn * BN;
+  t.a_base = (int32_t)g1 * p.a_g1 + (int32_t)g2 * p.a_g2;
+  t.b_base = (int32_t)g1 * p.b_g1 + (int32_t)g2 * p.b_g2;
+  t.c_base = (int32_t)g1 * p.c_g1 + (int32_t)g2 * p.c_g2;
+  return t;
+}
+
+// Offset of row m of A (or C) given the two-level row decomposition.
+__device__ __forceinline__ int32_t row_off(const GemmParams& p, uint32_t m, int32_t s1, int32_t s2) {
+  const uint32_t m1 = fdiv(m, p.m2div);
+  return (int32_t)m1 * s1 + (int32_t)(m - m1 * p.M2) * s2;
+}
+
+// ============================================================== fp32
+template <int BM, int BN, int AM, int BMD>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
+  constexpr int BK = 16;
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int AP = BM + 4, BP = BN + 4;
+  __shared__ float As[BK * AP];
+  __shared__ float Bs[BK * BP];
+  const TileCoord tc = tile_coord(p, BM, BN);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // ---- per-thread load plan (rows are fixed across K-tiles)
+  constexpr int A_ELEMS = BM * BK / 256;  // 8 or 4
+  constexpr int A_VECS = A_ELEMS / 4;
+  constexpr int B_ELEMS = BN * BK / 256;
+  constexpr int B_VECS = B_ELEMS / 4;
+  int32_t a_off[A_ELEMS];
+  bool a_ok[A_ELEMS];
+  int a_m[A_ELEMS], a_k[A_ELEMS];
+  if constexpr (AM == GM_K) {
+#pragma unroll
+    for (int r = 0; r < A_VECS; ++r) {
+      const int idx = tid + 256 * r;
+      a_m[r] = idx / (BK / 4);
+      a_k[r] = (idx % (BK / 4)) * 4;
+      const uint32_t m = tc.m0 + a_m[r];
+      a_ok[r] = m < p.M;
+      a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+    }
+  } else if constexpr (AM == GM_MN) {
+#pragma unroll
+    for (int r = 0; r < A_VECS; ++r) {
+      const int idx = tid + 256 * r;
+      a_k[r] = idx / (BM / 4);
+      a_m[r] = (idx % (BM / 4)) * 4;
+      const uint32_t m = tc.m0 + a_m[r];
+      a_ok[r] = m < p.M;
+      a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < A_ELEMS; ++r) {
+      const int idx = tid + 256 * r;
+      a_m[r] = idx % BM;
+      a_k[r] = idx / BM;
+      const uint32_t m = tc.m0 + a_m[r];
+      a_ok[r] = m < p.M;
+      a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+    }
+  }
+  int b_k[B_ELEMS], b_n[B_ELEMS];
+  bool b_ok[B_ELEMS];
+  if constexpr (BMD == GM_MN) {
+#pragma unroll
+    for (int r = 0; r < B_VECS; ++r) {
+      const int idx = tid + 256 * r;
+      b_k[r] = idx / (BN / 4);
+      b_n[r] = (idx % (BN / 4)) * 4;
+      b_ok[r] = tc.n0 + b_n[r] < p.N;
+    }
+  } else if constexpr (BMD == GM_K) {
+#pragma unroll
+    for (int r = 0; r < B_VECS; ++r) {
+      const int idx = tid + 256 * r;
+      b_n[r] = idx / (BK / 4);
+      b_k[r] = (idx % (BK / 4)) * 4;
+      b_ok[r] = tc.n0 + b_n[r] < p.N;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < B_ELEMS; ++r) {
+      const int idx = tid + 256 * r;
+      b_n[r] = idx % BN;
+      b_k[r] = idx / BN;
+      b_ok[r] = tc.n0 + b_n[r] < p.N;
+    }
+  }
+
+  float ra[A_ELEMS], rb[B_ELEMS];
+  const float* A = (const float*)p.A;
+  const float* B = (const float*)p.B;
+  auto gload = [&](uint32_t k0) {
+    if constexpr (AM == GM_K) {
+#pragma unroll
+      for (int r = 0; r < A_VECS; ++r) {
+        const uint32_t k = k0 + a_k[r];
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (a_ok[r] && k < p.K) v = *(const float4*)(A + a_off[r] + (int32_t)k);
+        ra[4 * r] = v.x; ra[4 * r + 1] = v.y; ra[4 * r + 2] = v.z; ra[4 * r + 3] = v.w;
+      }
+    } else if constexpr (AM == GM_MN) {
+#pragma unroll
+      for (int r = 0; r < A_VECS; ++r) {
+        const uint32_t k = k0 + a_k[r];
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (a_ok[r] && k < p.K) v = *(const float4*)(A + a_off[r] + (int32_t)k * p.a_k);
+        ra[4 * r] = v.x; ra[4 * r + 1] = v.y; ra[4 * r + 2] = v.z; ra[4 * r + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < A_ELEMS; ++r) {
+        const uint32_t k = k0 + a_k[r];
+        ra[r] = (a_ok[r] && k < p.K) ? A[a_off[r] + (int32_t)k * p.a_k] : 0.f;
+      }
+    }
+    if constexpr (BMD == GM_MN) {
+#pragma unroll
+      for (int r = 0; r < B_VECS; ++r) {
+        const uint32_t k = k0 + b_k[r];
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (b_ok[r] && k < p.K) v = *(const float4*)(B + tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]));
+        rb[4 * r] = v.x; rb[4 * r + 1] = v.y; rb[4 * r + 2] = v.z; rb[4 * r + 3] = v.w;
+      }
+    } else if constexpr (BMD == GM_K) {
+#pragma unroll
+      for (int r = 0; r < B_VECS; ++r) {
+        const uint32_t k = k0 + b_k[r];
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (b_ok[r] && k < p.K) v = *(const float4*)(B + tc.b_base + (int32_t)k + (int32_t)(tc.n0 + b_n[r]) * p.b_n);
+        rb[4 * r] = v.x; rb[4 * r + 1] = v.y; rb[4 * r + 2] = v.z; rb[4 * r + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < B_ELEMS; ++r) {
+        const uint32_t k = k0 + b_k[r];
+        rb[r] = (b_ok[r] && k < p.K) ? B[tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]) * p.b_n] : 0.f;
+      }
+    }
+  };
+  auto lstore = [&]() {
+    if constexpr (AM == GM_K) {
+#pragma unroll
+      for (int r = 0; r < A_VECS; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) As[(a_k[r] + j) * AP + a_m[r]] = ra[4 * r + j];
+    } else if constexpr (AM == GM_MN) {
+#pragma unroll
+      for (int r = 0; r < A_VECS; ++r)
+        *(float4*)&As[a_k[r] * AP + a_m[r]] = make_float4(ra[4 * r], ra[4 * r + 1], ra[4 * r + 2], ra[4 * r + 3]);
+    } else {
+#pragma unroll
+      for (int r = 0; r < A_ELEMS; ++r) As[a_k[r] * AP + a_m[r]] = ra[r];
+    }
+    if constexpr (BMD == GM_MN) {
+#pragma unroll
+      for (int r = 0; r < B_VECS; ++r)
+        *(float4*)&Bs[b_k[r] * BP + b_n[r]] = make_float4(rb[4 * r], rb[4 * r + 1], rb[4 * r + 2], rb[4 * r + 3]);
+    } else if constexpr (BMD == GM_K) {
+#pragma unroll
+      for (int r = 0; r < B_VECS; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) Bs[(b_k[r] + j) * BP + b_n[r]] = rb[4 * r + j];
+    } else {
+#pragma unroll
+      for (int r = 0; r < B_ELEMS; ++r) Bs[b_k[r] * BP + b_n[r]] = rb[r];
+    }
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int lr = lane & 31, lk = lane >> 5;
+  gload(0);
+  for (uint32_t k0 = 0; k0 < p.K; k0 += BK) {
+    __syncthreads();
+    lstore();
+    __syncthreads();
+    if (k0 + BK < p.K) gload(k0 + BK);
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 2) {
+      float a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) a[i] = As[(kk + lk) * AP + wm * WM + i * 32 + lr];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) b[j] = Bs[(kk + lk) * BP + wn * WN + j * 32 + lr];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  // ---- epilogue
+  float* C = (float*)p.C;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const uint32_t n = tc.n0 + wn * WN + j * 32 + lr;
+#pragma unroll
+      for (int vg = 0; vg < 4; ++vg) {
+        const uint32_t mb = tc.m0 + wm * WM + i * 32 + 8 * vg + 4 * lk;
+        if (n >= p.N || mb >= p.M) continue;
+        if (p.cmode == 2) {
+          const int32_t o = tc.c_base + row_off(p, mb, p.c_m1, p.c_m2) + (int32_t)n * p.c_n;
+          *(float4*)(C + o) = make_float4(acc[i][j][4 * vg], acc[i][j][4 * vg + 1], acc[i][j][4 * vg + 2], acc[i][j][4 * vg + 3]);
+        } else {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const uint32_t m = mb + t;
+            if (m < p.M) C[tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n * p.c_n] = acc[i][j][4 * vg + t];
+          }
+        }
+      }
+    }
+}
+
+// ============================================================== bf16
+// LDS holds both operands K-contiguous ([row][k], k fastest) so that each
+// lane fetches its 8 bf16 MFMA inputs with one 16-byte LDS read.  An
+// M-/N-contiguous HBM operand is transposed on the way in: each thread loads
+// a 4(k) x 4(m|n) block with four 8-byte loads and writes four 8-byte rows.
+template <int BM, int BN, int AM, int BMD>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
+  constexpr int BK = 32;
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int KP = BK + 8;  // padded row pitch (elements)
+  __shared__ uint16_t As[BM * KP];
+  __shared__ uint16_t Bs[BN * KP];
+  const TileCoord tc = tile_coord(p, BM, BN);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const uint16_t* A = (const uint16_t*)p.A;
+  const uint16_t* B = (const uint16_t*)p.B;
+
+  // A plan
+  constexpr int A_ELEMS = BM * BK / 256;  // 16 or 8
+  constexpr int A_CH = A_ELEMS / 8;       // 16-byte chunks (K mode)
+  constexpr int A_BL = A_ELEMS / 16;      // 4x4 blocks (MN mode), may be 0
+  int a_m[A_ELEMS], a_k[A_ELEMS];
+  int32_t a_off[A_ELEMS];
+  bool a_ok[A_ELEMS];
+  if constexpr (AM == GM_K) {
+#pragma unroll
+    for (int r = 0; r < A_CH; ++r) {
+      const int idx = tid + 256 * r;
+      a_m[r] = idx / (BK / 8);
+      a_k[r] = (idx % (BK / 8)) * 8;
+      const uint32_t m = tc.m0 + a_m[r];
+      a_ok[r] = m < p.M;
+      a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+    }
+  } else if constexpr (AM == GM_MN && A_BL > 0) {
+#pragma unroll
+    for (int r = 0; r < A_BL; ++r) {
+      const int idx = tid + 256 * r;
+      a_m[r] = (idx % (BM / 4)) * 4;
+      a_k[r] = (idx / (BM / 4)) * 4;
+      const uint32_t m = tc.m0 + a_m[r];
+      a_ok[r] = m < p.M;
+      a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < A_ELEMS; ++r) {
+      const int idx = tid + 256 * r;
+      a_k[r] = idx % BK;
+      a_m[r] = idx / BK;
+      const uint32_t m = tc.m0 + a_m[r];
+      a_ok[r] = m < p.M;
+      a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+    }
+  }
+  constexpr int B_ELEMS = BN * BK / 256;
+  constexpr int B_CH = B_ELEMS / 8;
+  constexpr int B_BL = B_ELEMS / 16;
+  int b_n[B_ELEMS], b_k[B_ELEMS];
+  bool b_ok[B_ELEMS];
+  if constexpr (BMD == GM_K) {
+#pragma unroll
+    for (int r = 0; r < B_CH; ++r) {
+      const int idx = tid + 256 * r;
+      b_n[r] = idx / (BK / 8);
+      b_k[r] = (idx % (BK / 8)) * 8;
+      b_ok[r] = tc.n0 + b_n[r] < p.N;
+    }
+  } else if constexpr (BMD == GM_MN && B_BL > 0) {
+#pragma unroll
+    for (int r = 0; r < B_BL; ++r) {
+      const int idx = tid + 256 * r;
+      b_n[r] = (idx % (BN / 4)) * 4;
+      b_k[r] = (idx / (BN / 4)) * 4;
+      b_ok[r] = tc.n0 + b_n[r] < p.N;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < B_ELEMS; ++r) {
+      const int idx = tid + 256 * r;
+      b_k[r] = idx % BK;
+      b_n[r] = idx / BK;
+      b_ok[r] = tc.n0 + b_n[r] < p.N;
+    }
+  }
+  constexpr bool A_VEC_K = AM == GM_K;
+  constexpr bool A_VEC_MN = AM == GM_MN && A_BL > 0;
+  constexpr bool B_VEC_K = BMD == GM_K;
+  constexpr bool B_VEC_MN = BMD == GM_MN && B_BL > 0;
+
+  uint4 ca[A_CH > 0 ? A_CH : 1];
+  uint2 ba[A_BL > 0 ? A_BL * 4 : 1];
+  uint16_t sa[A_ELEMS];
+  uint4 cb[B_CH > 0 ? B_CH : 1];
+  uint2 bb[B_BL > 0 ? B_BL * 4 : 1];
+  uint16_t sb[B_ELEMS];
+
+  auto gload = [&](uint32_t k0) {
+    if constexpr (A_VEC_K) {
+#pragma unroll
+      for (int r = 0; r < A_CH; ++r) {
+        const uint32_t k = k0 + a_k[r];
+        ca[r] = (a_ok[r] && k < p.K) ? *(const uint4*)(A + a_off[r] + (int32_t)k) : make_uint4(0, 0, 0, 0);
+      }
+    } else if constexpr (A_VEC_MN) {
+#pragma unroll
+      for (int r = 0; r < A_BL; ++r)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const uint32_t k = k0 + a_k[r] + t;
+          ba[4 * r + t] = (a_ok[r] && k < p.K) ? *(const uint2*)(A + a_off[r] + (int32_t)k * p.a_k) : make_uint2(0, 0);
+        }
+    } else {
+#pragma unroll
+      for (int r = 0; r < A_ELEMS; ++r) {
+        const uint32_t k = k0 + a_k[r];
+        sa[r] = (a_ok[r] && k < p.K) ? A[a_off[r] + (int32_t)k * p.a_k] : (uint16_t)0;
+      }
+    }
+    if constexpr (B_VEC_K) {
+#pragma unroll
+      for (int r = 0; r < B_CH; ++r) {
+        const uint32_t k = k0 + b_k[r];
+        cb[r] = (b_ok[r] && k < p.K) ? *(const uint4*)(B + tc.b_base + (int32_t)k + (int32_t)(tc.n0 + b_n[r]) * p.b_n)
+                                     : make_uint4(0, 0, 0, 0);
+      }
+    } else if constexpr (B_VEC_MN) {
+#pragma unroll
+      for (int r = 0; r < B_BL; ++r)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const uint32_t k = k0 + b_k[r] + t;
+          bb[4 * r + t] = (b_ok[r] && k < p.K)
+                              ? *(const uint2*)(B + tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]))
+                              : make_uint2(0, 0);
+        }
+    } else {
+#pragma unroll
+      for (int r = 0; r < B_ELEMS; ++r) {
+        const uint32_t k = k0 + b_k[r];
+        sb[r] = (b_ok[r] && k < p.K) ? B[tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]) * p.b_n] : (uint16_t)0;
+      }
+    }
+  };
+  // rows[t] holds 4 elements (one per m|n) at k + t; emit 4 rows of 4 k
+  auto transpose4 = [](const uint2* rows, uint2* out) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t e[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const uint32_t w = (j < 2) ? rows[t].x : rows[t].y;
+        e[t] = (j & 1) ? (w >> 16) : (w & 0xffffu);
+      }
+      out[j] = make_uint2(e[0] | (e[1] << 16), e[2] | (e[3] << 16));
+    }
+  };
+  auto lstore = [&]() {
+    if constexpr (A_VEC_K) {
+#pragma unroll
+      for (int r = 0; r < A_CH; ++r) *(uint4*)&As[a_m[r] * KP + a_k[r]] = ca[r];
+    } else if constexpr (A_VEC_MN) {
+#pragma unroll
+      for (int r = 0; r < A_BL; ++r) {
+        uint2 o[4];
+        transpose4(&ba[4 * r], o);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *(uint2*)&As[(a_m[r] + j) * KP + a_k[r]] = o[j];
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < A_ELEMS; ++r) As[a_m[r] * KP + a_k[r]] = sa[r];
+    }
+    if constexpr (B_VEC_K) {
+#pragma unroll
+      for (int r = 0; r < B_CH; ++r) *(uint4*)&Bs[b_n[r] * KP + b_k[r]] = cb[r];
+    } else if constexpr (B_VEC_MN) {
+#pragma unroll
+      for (int r = 0; r < B_BL; ++r) {
+        uint2 o[4];
+        transpose4(&bb[4 * r], o);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *(uint2*)&Bs[(b_n[r] + j) * KP + b_k[r]] = o[j];
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < B_ELEMS; ++r) Bs[b_n[r] * KP + b_k[r]] = sb[r];
+    }
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int lr = lane & 31, lk = (lane >> 5) * 8;
+  gload(0);
+  for (uint32_t k0 = 0; k0 < p.K; k0 += BK) {
+    __syncthreads();
+    lstore();
+    __syncthreads();
+    if (k0 + BK < p.K) gload(k0 + BK);
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      bf16x8 a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        uint4 q = *(const uint4*)&As[(wm * WM + i * 32 + lr) * KP + kk + lk];
+        a[i] = __builtin_bit_cast(bf16x8, q);
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        uint4 q = *(const uint4*)&Bs[(wn * WN + j * 32 + lr) * KP + kk + lk];
+        b[j] = __builtin_bit_cast(bf16x8, q);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  uint16_t* C = (uint16_t*)p.C;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const uint32_t n = tc.n0 + wn * WN + j * 32 + lr;
+      if (n >= p.N) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const uint32_t m = tc.m0 + wm * WM + i * 32 + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
+        if (m < p.M) C[tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n * p.c_n] = f32_to_bf16(acc[i][j][v]);
+      }
+    }
+}
+
+namespace {
+
+template <int T, int AM, int BMD>
+hipError_t gemm_go(const NodeKernel& k, hipStream_t s) {
+  const GemmParams& p = k.gemm;
+  const dim3 grid(p.tiles_m * p.tiles_n * p.G);
+  if (k.dtype == DT_BF16) hipLaunchKernelGGL((gemm_bf16_kernel<T, T, AM, BMD>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((gemm_f32_kernel<T, T, AM, BMD>), grid, dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+template <int T, int AM>
+hipError_t gemm_b(const NodeKernel& k, hipStream_t s) {
+  switch (k.bmode) {
+    case GM_K: return gemm_go<T, AM, GM_K>(k, s);
+    case GM_MN: return gemm_go<T, AM, GM_MN>(k, s);
+    default: return gemm_go<T, AM, GM_GENERIC>(k, s);
+  }
+}
+
+template <int T>
+hipError_t gemm_a(const NodeKernel& k, hipStream_t s) {
+  switch (k.amode) {
+    case GM_K: return gemm_b<T, GM_K>(k, s);
+    case GM_MN: return gemm_b<T, GM_MN>(k, s);
+    default: return gemm_b<T, GM_GENERIC>(k, s);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const NodeKernel& k, hipStream_t s) {
+  const GemmParams& p = k.gemm;
+  if ((uint64_t)p.tiles_m * p.tiles_n * p.G >= (1ull << 31)) return hipErrorInvalidValue;
+  return k.gemm_tile == 0 ? gemm_a<128>(k, s) : gemm_a<64>(k, s);
+}
+
+}  // namespace fluid

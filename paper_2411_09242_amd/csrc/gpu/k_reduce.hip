@@ -1,0 +1,200 @@
+// Row reductions over the last logical dim: Softmax (with fused scale and
+// causal mask), LayerNorm and RMSNorm, in two families.
+//  * row (variant 0): one 64-lane wavefront per row; the row is held in
+//    registers (up to 4096 values), reduced with cross-lane butterflies, and
+//    written once -- one HBM read and one write per element.  Coalesced when
+//    the reduced dim is unit-stride.
+//  * column (variant 1): one lane per row, consecutive lanes on consecutive
+//    rows, so a layout whose unit-stride dim is a row dim still reads and
+//    writes coalesced; the row is streamed twice (three times for
+//    LayerNorm's exact two-pass variance).
+// Causal softmax: keys k > q (q = index along the second-to-last logical
+// dim) get probability exactly 0.  All arithmetic is fp32.
+#include <math.h>
+
+#include "dev.h"
+#include "launch.h"
+
+namespace fluid {
+
+__device__ __forceinline__ void row_offsets(const RedParams& p, uint32_t row, int32_t& io, int32_t& oo, uint32_t& qi) {
+  io = 0; oo = 0; qi = 0;
+  uint32_t rest = row;
+#pragma unroll
+  for (int d = kMaxDims - 1; d >= 0; --d) {
+    if (d < p.nrd) {
+      const uint32_t q = fdiv(rest, p.rdiv[d]);
+      const uint32_t i = rest - q * p.rext[d];
+      rest = q;
+      io += (int32_t)i * p.ris[d];
+      oo += (int32_t)i * p.ros[d];
+      if (d == p.qdim) qi = i;
+    }
+  }
+}
+
+template <typename T, int NPL, int OP>
+__global__ __launch_bounds__(256) void red_row_kernel(RedParams p) {
+  const uint32_t row = blockIdx.x * 4u + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= p.nrows) return;  // uniform per wavefront
+  int32_t io, oo;
+  uint32_t qi;
+  row_offsets(p, row, io, oo, qi);
+  const uint32_t R = p.R;
+  const uint32_t valid = (OP == RED_SOFTMAX && p.causal) ? min(R, qi + 1u) : R;
+  float v[NPL];
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const uint32_t k = (uint32_t)lane + 64u * j;
+    v[j] = k < valid ? Elem<T>::load(p.x, io + (int32_t)k * p.irs) : 0.f;
+  }
+  if constexpr (OP == RED_SOFTMAX) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const uint32_t k = (uint32_t)lane + 64u * j;
+      v[j] *= p.attr;
+      if (k < valid) m = fmaxf(m, v[j]);
+    }
+    m = wave_max(m);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const uint32_t k = (uint32_t)lane + 64u * j;
+      v[j] = k < valid ? expf(v[j] - m) : 0.f;
+      s += v[j];
+    }
+    s = wave_sum(s);
+    const float inv = 1.0f / s;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const uint32_t k = (uint32_t)lane + 64u * j;
+      if (k < R) Elem<T>::store(p.y, oo + (int32_t)k * p.ors, v[j] * inv);
+    }
+  } else {
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) s += (OP == RED_LAYERNORM) ? v[j] : v[j] * v[j];
+    s = wave_sum(s);
+    const float invR = 1.0f / (float)R;
+    float mean = 0.f, rstd;
+    if constexpr (OP == RED_LAYERNORM) {
+      mean = s * invR;
+      float q = 0.f;
+#pragma unroll
+      for (int j = 0; j < NPL; ++j) {
+        const uint32_t k = (uint32_t)lane + 64u * j;
+        const float d = v[j] - mean;
+        q += k < R ? d * d : 0.f;
+      }
+      q = wave_sum(q);
+      rstd = 1.0f / sqrtf(q * invR + p.attr);
+    } else {
+      rstd = 1.0f / sqrtf(s * invR + p.attr);
+    }
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const uint32_t k = (uint32_t)lane + 64u * j;
+      if (k < R) {
+        float y = (v[j] - mean) * rstd * Elem<T>::load(p.gamma, k);
+        if constexpr (OP == RED_LAYERNORM) y += Elem<T>::load(p.beta, k);
+        Elem<T>::store(p.y, oo + (int32_t)k * p.ors, y);
+      }
+    }
+  }
+}
+
+template <typename T, int OP>
+__global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
+  const uint32_t row = blockIdx.x * 256u + threadIdx.x;
+  if (row >= p.nrows) return;
+  int32_t io, oo;
+  uint32_t qi;
+  row_offsets(p, row, io, oo, qi);
+  const uint32_t R = p.R;
+  if constexpr (OP == RED_SOFTMAX) {
+    const uint32_t valid = p.causal ? min(R, qi + 1u) : R;
+    float m = -INFINITY, s = 0.f;
+    for (uint32_t k = 0; k < valid; ++k) {
+      const float z = p.attr * Elem<T>::load(p.x, io + (int32_t)k * p.irs);
+      if (z > m) {
+        s = s * expf(m - z) + 1.f;
+        m = z;
+      } else {
+        s += expf(z - m);
+      }
+    }
+    const float inv = 1.0f / s;
+    for (uint32_t k = 0; k < R; ++k) {
+      float y = 0.f;
+      if (k < valid) y = expf(p.attr * Elem<T>::load(p.x, io + (int32_t)k * p.irs) - m) * inv;
+      Elem<T>::store(p.y, oo + (int32_t)k * p.ors, y);
+    }
+  } else {
+    const float invR = 1.0f / (float)R;
+    float mean = 0.f, rstd;
+    if constexpr (OP == RED_LAYERNORM) {
+      float s = 0.f;
+      for (uint32_t k = 0; k < R; ++k) s += Elem<T>::load(p.x, io + (int32_t)k * p.irs);
+      mean = s * invR;
+      float q = 0.f;
+      for (uint32_t k = 0; k < R; ++k) {
+        const float d = Elem<T>::load(p.x, io + (int32_t)k * p.irs) - mean;
+        q += d * d;
+      }
+      rstd = 1.0f / sqrtf(q * invR + p.attr);
+    } else {
+      float q = 0.f;
+      for (uint32_t k = 0; k < R; ++k) {
+        const float x = Elem<T>::load(p.x, io + (int32_t)k * p.irs);
+        q += x * x;
+      }
+      rstd = 1.0f / sqrtf(q * invR + p.attr);
+    }
+    for (uint32_t k = 0; k < R; ++k) {
+      float y = (Elem<T>::load(p.x, io + (int32_t)k * p.irs) - mean) * rstd * Elem<T>::load(p.gamma, k);
+      if constexpr (OP == RED_LAYERNORM) y += Elem<T>::load(p.beta, k);
+      Elem<T>::store(p.y, oo + (int32_t)k * p.ors, y);
+    }
+  }
+}
+
+namespace {
+
+template <typename T, int OP>
+hipError_t red_dispatch_op(const NodeKernel& k, hipStream_t s) {
+  const RedParams& p = k.red;
+  if (k.family == KF_RED_COL) {
+    hipLaunchKernelGGL((red_col_kernel<T, OP>), dim3((p.nrows + 255u) / 256u), dim3(256), 0, s, p);
+    return hipGetLastError();
+  }
+  const dim3 grid((p.nrows + 3u) / 4u);
+  const uint32_t npl = (p.R + 63u) / 64u;
+  if (npl <= 1) hipLaunchKernelGGL((red_row_kernel<T, 1, OP>), grid, dim3(256), 0, s, p);
+  else if (npl <= 2) hipLaunchKernelGGL((red_row_kernel<T, 2, OP>), grid, dim3(256), 0, s, p);
+  else if (npl <= 4) hipLaunchKernelGGL((red_row_kernel<T, 4, OP>), grid, dim3(256), 0, s, p);
+  else if (npl <= 8) hipLaunchKernelGGL((red_row_kernel<T, 8, OP>), grid, dim3(256), 0, s, p);
+  else if (npl <= 16) hipLaunchKernelGGL((red_row_kernel<T, 16, OP>), grid, dim3(256), 0, s, p);
+  else if (npl <= 32) hipLaunchKernelGGL((red_row_kernel<T, 32, OP>), grid, dim3(256), 0, s, p);
+  else if (npl <= 64) hipLaunchKernelGGL((red_row_kernel<T, 64, OP>), grid, dim3(256), 0, s, p);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t red_dispatch(const NodeKernel& k, hipStream_t s) {
+  switch (k.red.op) {
+    case RED_SOFTMAX: return red_dispatch_op<T, RED_SOFTMAX>(k, s);
+    case RED_LAYERNORM: return red_dispatch_op<T, RED_LAYERNORM>(k, s);
+    default: return red_dispatch_op<T, RED_RMSNORM>(k, s);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_reduce(const NodeKernel& k, hipStream_t s) {
+  return k.dtype == DT_BF16 ? red_dispatch<uint16_t>(k, s) : red_dispatch<float>(k, s);
+}
+
+}  // namespace fluid

@@ -1,0 +1,28 @@
+// Kernel launchers (one per kernel family); each returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "../host/dispatch.h"
+
+namespace fluid {
+
+hipError_t launch_elementwise(const NodeKernel& k, hipStream_t s);
+hipError_t launch_rope(const NodeKernel& k, hipStream_t s);
+hipError_t launch_reduce(const NodeKernel& k, hipStream_t s);
+hipError_t launch_gemm(const NodeKernel& k, hipStream_t s);
+hipError_t launch_fill(void* p, uint64_t bytes, uint32_t seed, hipStream_t s);
+
+inline hipError_t launch_node_kernel(const NodeKernel& k, hipStream_t s) {
+  switch (k.family) {
+    case KF_EW:
+    case KF_EW_TILED: return launch_elementwise(k, s);
+    case KF_ROPE: return launch_rope(k, s);
+    case KF_RED_ROW:
+    case KF_RED_COL: return launch_reduce(k, s);
+    case KF_GEMM: return launch_gemm(k, s);
+    default: return hipSuccess;
+  }
+}
+
+}  // namespace fluid

@@ -1,0 +1,465 @@
+// GPU entry points of the C ABI: the executor (fluid_run), the cost-table
+// measurement (fluid_measure_costs) and per-node tracing.
+//
+// fluid_run is the paper's VM invoke path (Section 4): every non-view node
+// becomes one kernel launch, in node order, on the caller's stream, with
+// all activations inside the caller's single arena at their planned
+// offsets.  The per-node launch parameters depend only on the graph and the
+// two plans, so they are prepared once per (layout plan, arena plan) pair
+// and cached; each call only patches the five base addresses.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <tuple>
+#include <vector>
+
+#include "../host/handles.h"
+#include "../host/layouts.h"
+#include "launch.h"
+
+namespace fluid {
+
+namespace {
+
+enum BindKind : int { BK_ARENA = 0, BK_INPUT = 1, BK_OUTPUT = 2, BK_CONST = 3 };
+
+struct Bind {
+  int kind = BK_ARENA;
+  int index = 0;
+  int64_t off = 0;  // bytes from the base
+};
+
+struct PreparedNode {
+  int node = 0;
+  NodeKernel k;
+  std::vector<Bind> in;  // one per node input (activations and constants)
+  Bind out;
+};
+
+struct Prepared {
+  std::vector<PreparedNode> nodes;
+};
+
+std::mutex g_cache_mu;
+
+// Bases are validated to be 256-byte (arena) or 16-byte (caller tensors)
+// aligned, so preparing with base address 0 keeps every alignment decision
+// valid for the real addresses.
+const void* fake_ptr(const Bind& b) { return (const void*)(uintptr_t)b.off; }
+
+Bind bind_edge(const Graph& g, const ArenaPlan& ap, int e) {
+  Bind b;
+  const int r = ap.root[e];
+  if (r < g.n_inputs()) {
+    b.kind = BK_INPUT;
+    b.index = r;
+  } else if (g.is_output[r]) {
+    b.kind = BK_OUTPUT;
+    b.index = (int)(std::find(g.outputs.begin(), g.outputs.end(), r) - g.outputs.begin());
+  } else {
+    b.kind = BK_ARENA;
+    b.off = ap.offset[e];
+  }
+  return b;
+}
+
+std::shared_ptr<Prepared> prepare(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah) {
+  const Graph& g = gh->g;
+  const LayoutPlan& lp = lh->p;
+  const ArenaPlan& ap = ah->a;
+  auto P = std::make_shared<Prepared>();
+  for (int n = 0; n < g.n_nodes(); ++n) {
+    if (lp.variant[n] < 0) continue;  // view: no kernel
+    const Node& nd = g.nodes[n];
+    PreparedNode pn;
+    pn.node = n;
+    std::vector<Operand> ins;
+    for (int v : nd.ins) {
+      Operand o;
+      Bind b;
+      if (v >= 0) {
+        b = bind_edge(g, ap, v);
+        o.shape = g.edge_shape(v);
+        o.stride = dense_strides(o.shape, lp.perm[v]);
+        o.dtype = g.dtype;
+      } else {
+        b.kind = BK_CONST;
+        b.index = ~v;
+        o.shape = g.consts[~v].shape;
+        o.stride = row_major_strides(o.shape);
+        o.dtype = g.consts[~v].dtype;
+      }
+      o.ptr = fake_ptr(b);
+      ins.push_back(o);
+      pn.in.push_back(b);
+    }
+    const int eo = g.out_edge(n);
+    pn.out = bind_edge(g, ap, eo);
+    Operand out;
+    out.shape = nd.out_shape;
+    out.stride = dense_strides(out.shape, lp.perm[eo]);
+    out.dtype = g.dtype;
+    out.ptr = fake_ptr(pn.out);
+    pn.k = prepare_node(nd, lp.variant[n], g.dtype, ins, out);
+    if (!pn.k.available)
+      fail(FLUID_E_INVALID, "node " + std::to_string(n) + ": variant " + std::to_string(lp.variant[n]) +
+                                " cannot run with these layouts (" + pn.k.why + ")");
+    P->nodes.push_back(std::move(pn));
+  }
+  return P;
+}
+
+struct Bases {
+  char* arena;
+  const void* const* inputs;
+  void* const* outputs;
+  const void* const* consts;
+};
+
+inline void* resolve(const Bind& b, const Bases& B) {
+  switch (b.kind) {
+    case BK_ARENA: return B.arena + b.off;
+    case BK_INPUT: return const_cast<void*>(B.inputs[b.index]);
+    case BK_OUTPUT: return B.outputs[b.index];
+    default: return const_cast<void*>(B.consts[b.index]);
+  }
+}
+
+void patch(NodeKernel& k, const PreparedNode& pn, const Bases& B) {
+  void* out = resolve(pn.out, B);
+  void* in0 = resolve(pn.in[0], B);
+  void* in1 = pn.in.size() > 1 ? resolve(pn.in[1], B) : nullptr;
+  void* in2 = pn.in.size() > 2 ? resolve(pn.in[2], B) : nullptr;
+  switch (k.family) {
+    case KF_EW:
+    case KF_EW_TILED:
+      k.ew.x0 = in0; k.ew.x1 = in1; k.ew.y = out;
+      break;
+    case KF_ROPE:
+      k.rope.x = in0; k.rope.cos_t = (const float*)in1; k.rope.sin_t = (const float*)in2; k.rope.y = out;
+      break;
+    case KF_RED_ROW:
+    case KF_RED_COL:
+      k.red.x = in0; k.red.gamma = in1; k.red.beta = in2; k.red.y = out;
+      break;
+    case KF_GEMM:
+      k.gemm.A = in0; k.gemm.B = in1; k.gemm.C = out;
+      break;
+    default:
+      break;
+  }
+}
+
+// ------------------------------------------------------------ tracing
+struct Trace {
+  bool on = false;
+  std::vector<uint8_t> mask;
+  std::vector<hipEvent_t> ev;  // 2 per record
+  std::vector<int> node_of;    // per used record
+  int max_records = 0;
+  uint64_t graph_serial = 0;
+};
+std::mutex g_trace_mu;
+Trace g_trace;
+
+void hip_check(hipError_t e, const char* what) {
+  if (e != hipSuccess) fail(FLUID_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+}  // namespace
+
+// ------------------------------------------------------------ measurement
+namespace {
+
+struct SigKey {
+  int op;
+  float f;
+  int i;
+  Perm perm;
+  std::vector<Shape> in_shapes;   // activation slots
+  std::vector<Shape> const_shapes;
+  std::vector<int> const_dtypes;
+  std::vector<int> slot_is_const; // per input position
+  Shape out;
+  bool operator<(const SigKey& o) const {
+    return std::tie(op, f, i, perm, in_shapes, const_shapes, const_dtypes, slot_is_const, out) <
+           std::tie(o.op, o.f, o.i, o.perm, o.in_shapes, o.const_shapes, o.const_dtypes, o.slot_is_const, o.out);
+  }
+};
+
+SigKey sig_key(const Graph& g, int n) {
+  const Node& nd = g.nodes[n];
+  SigKey k;
+  k.op = nd.op;
+  k.f = nd.fattr;
+  k.i = nd.iattr;
+  k.perm = nd.perm;
+  for (int v : nd.ins) {
+    k.slot_is_const.push_back(v < 0);
+    if (v >= 0) {
+      k.in_shapes.push_back(g.edge_shape(v));
+    } else {
+      k.const_shapes.push_back(g.consts[~v].shape);
+      k.const_dtypes.push_back(g.consts[~v].dtype);
+    }
+  }
+  k.out = nd.out_shape;
+  return k;
+}
+
+uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+
+}  // namespace
+
+}  // namespace fluid
+
+using namespace fluid;
+
+extern "C" {
+
+fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah, void* arena,
+                       uint64_t arena_bytes, const void* const* consts, const void* const* inputs,
+                       void* const* outputs, void* hip_stream) {
+  return call_guarded([&] {
+    require(gh && lh && ah, "fluid_run: NULL graph or plan");
+    const Graph& g = gh->g;
+    require(lh->p.graph_serial == gh->serial && ah->a.graph_serial == gh->serial, "fluid_run: plans belong to another graph");
+    require(ah->a.root.size() == (size_t)g.n_edges(), "fluid_run: arena plan size mismatch");
+    if (ah->a.peak > 0) {
+      require(arena != nullptr, "fluid_run: NULL arena");
+      require(aligned(arena, 256), "fluid_run: arena must be 256-byte aligned");
+    }
+    if (arena_bytes < ah->a.peak)
+      fail(FLUID_E_ARENA_TOO_SMALL, "fluid_run: arena has " + std::to_string(arena_bytes) + " bytes, plan needs " +
+                                        std::to_string(ah->a.peak));
+    require(inputs && outputs, "fluid_run: NULL inputs/outputs array");
+    require(consts || g.consts.empty(), "fluid_run: NULL consts array");
+    for (int i = 0; i < g.n_inputs(); ++i)
+      require(inputs[i] && aligned(inputs[i], 16), "fluid_run: input " + std::to_string(i) + " is NULL or not 16-byte aligned");
+    for (size_t i = 0; i < g.outputs.size(); ++i)
+      require(outputs[i] && aligned(outputs[i], 16), "fluid_run: output " + std::to_string(i) + " is NULL or not 16-byte aligned");
+    for (size_t i = 0; i < g.consts.size(); ++i)
+      require(consts[i] && aligned(consts[i], 16), "fluid_run: const " + std::to_string(i) + " is NULL or not 16-byte aligned");
+    std::shared_ptr<Prepared> prep = nullptr;
+    {
+      std::lock_guard<std::mutex> lk(g_cache_mu);
+      // plan serials are never reused, so a stale entry can never match
+      static std::map<std::pair<uint64_t, uint64_t>, std::shared_ptr<Prepared>> cache;
+      auto key = std::make_pair(lh->serial, ah->serial);
+      auto it = cache.find(key);
+      if (it != cache.end()) {
+        prep = it->second;
+      } else {
+        prep = prepare(gh, lh, ah);
+        if (cache.size() > 256) cache.clear();
+        cache[key] = prep;
+      }
+    }
+    Bases B{(char*)arena, inputs, outputs, consts};
+    hipStream_t s = (hipStream_t)hip_stream;
+    std::unique_lock<std::mutex> tl(g_trace_mu);
+    const bool tracing = g_trace.on && g_trace.graph_serial == gh->serial;
+    if (!tracing) tl.unlock();
+    for (const PreparedNode& pn : prep->nodes) {
+      NodeKernel k = pn.k;
+      patch(k, pn, B);
+      int rec = -1;
+      if (tracing && g_trace.mask[pn.node] && (int)g_trace.node_of.size() < g_trace.max_records) {
+        rec = (int)g_trace.node_of.size();
+        g_trace.node_of.push_back(pn.node);
+        hip_check(hipEventRecord(g_trace.ev[2 * rec], s), "hipEventRecord");
+      }
+      hipError_t e = launch_node_kernel(k, s);
+      if (e != hipSuccess)
+        fail(FLUID_E_HIP, "node " + std::to_string(pn.node) + " (" + k.name() + "): " + hipGetErrorString(e));
+      if (rec >= 0) hip_check(hipEventRecord(g_trace.ev[2 * rec + 1], s), "hipEventRecord");
+    }
+  });
+}
+
+fluid_status fluid_trace_enable(const fluid_graph* gh, const uint8_t* mask, int32_t max_records) {
+  return call_guarded([&] {
+    require(gh && max_records > 0, "fluid_trace_enable: bad argument");
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    for (hipEvent_t e : g_trace.ev) (void)hipEventDestroy(e);
+    g_trace = Trace();
+    g_trace.mask.assign(gh->g.n_nodes(), 1);
+    if (mask)
+      for (int n = 0; n < gh->g.n_nodes(); ++n) g_trace.mask[n] = mask[n] ? 1 : 0;
+    g_trace.ev.resize(2 * (size_t)max_records);
+    for (auto& e : g_trace.ev) hip_check(hipEventCreate(&e), "hipEventCreate");
+    g_trace.max_records = max_records;
+    g_trace.graph_serial = gh->serial;
+    g_trace.on = true;
+  });
+}
+
+fluid_status fluid_trace_collect(const fluid_graph* gh, double* ms, int32_t* launches) {
+  return call_guarded([&] {
+    require(gh && ms && launches, "fluid_trace_collect: NULL argument");
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    require(g_trace.graph_serial == gh->serial, "fluid_trace_collect: tracing was enabled for another graph");
+    for (size_t r = 0; r < g_trace.node_of.size(); ++r) {
+      hip_check(hipEventSynchronize(g_trace.ev[2 * r + 1]), "hipEventSynchronize");
+      float t = 0.f;
+      hip_check(hipEventElapsedTime(&t, g_trace.ev[2 * r], g_trace.ev[2 * r + 1]), "hipEventElapsedTime");
+      ms[g_trace.node_of[r]] += t;
+      launches[g_trace.node_of[r]] += 1;
+    }
+    for (hipEvent_t e : g_trace.ev) (void)hipEventDestroy(e);
+    g_trace = Trace();
+  });
+}
+
+fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scratch, uint64_t scratch_bytes,
+                                 void* hip_stream, fluid_cost_table** out) {
+  return call_guarded([&] {
+    require(gh && out, "fluid_measure_costs: NULL argument");
+    const Graph& g = gh->g;
+    require(reps >= 1 && reps <= 1000, "fluid_measure_costs: reps must be 1..1000");
+    const uint64_t need = measure_scratch_bytes(g);
+    require(scratch && aligned(scratch, 256), "fluid_measure_costs: scratch must be non-NULL and 256-byte aligned");
+    require(scratch_bytes >= need, "fluid_measure_costs: scratch needs " + std::to_string(need) + " bytes");
+    hipStream_t s = (hipStream_t)hip_stream;
+    hip_check(launch_fill(scratch, scratch_bytes, 12345u, s), "fill");
+
+    CostTable t;
+    for (int e = 0; e < g.n_edges(); ++e)
+      t.L.push_back(g.pinned(e) ? std::vector<Perm>{identity_perm((int)g.edge_shape(e).size())}
+                                : measured_layout_list(g.edge_shape(e)));
+    std::map<SigKey, int> sig_of;
+    std::vector<int> rep_node;
+    for (int n = 0; n < g.n_nodes(); ++n) {
+      SigKey k = sig_key(g, n);
+      auto it = sig_of.find(k);
+      if (it == sig_of.end()) {
+        it = sig_of.emplace(k, (int)rep_node.size()).first;
+        rep_node.push_back(n);
+      }
+      t.node_sig.push_back(it->second);
+    }
+    // candidate list per slot / output of each signature: the union over
+    // its nodes (identity only if every node has that edge pinned)
+    std::vector<std::vector<std::vector<Perm>>> slot_lists(rep_node.size());
+    std::vector<std::vector<Perm>> out_lists(rep_node.size());
+    for (int n = 0; n < g.n_nodes(); ++n) {
+      const int si = t.node_sig[n];
+      const auto& slots = g.act_in[n];
+      auto& sl = slot_lists[si];
+      if (sl.empty()) sl.resize(slots.size());
+      for (size_t s2 = 0; s2 < slots.size(); ++s2)
+        if (t.L[slots[s2]].size() > sl[s2].size()) sl[s2] = t.L[slots[s2]];
+      const int eo = g.out_edge(n);
+      if (t.L[eo].size() > out_lists[si].size()) out_lists[si] = t.L[eo];
+    }
+    hipEvent_t ev[2 * 64];
+    const uint32_t R = std::min<uint32_t>(reps, 64);
+    for (auto& e : ev) hip_check(hipEventCreate(&e), "hipEventCreate");
+    struct EvGuard {
+      hipEvent_t* ev;
+      ~EvGuard() { for (int i = 0; i < 128; ++i) (void)hipEventDestroy(ev[i]); }
+    } evg{ev};
+    char* base = (char*)scratch;
+    for (size_t si = 0; si < rep_node.size(); ++si) {
+      const int n = rep_node[si];
+      const Node& nd = g.nodes[n];
+      Sig sig;
+      sig.op = nd.op;
+      for (int e : g.act_in[n]) sig.in_shapes.push_back(g.edge_shape(e));
+      sig.out_shape = nd.out_shape;
+      const auto& lists = slot_lists[si];
+      const auto& olist = out_lists[si];
+      const int ns = (int)lists.size();
+      std::vector<size_t> idx(ns + 1, 0);
+      int64_t best_so_far = -1;
+      for (;;) {
+        SigEntry en;
+        for (int i = 0; i < ns; ++i) en.in.push_back(lists[i][idx[i]]);
+        en.out = olist[idx[ns]];
+        const bool view = (nd.op == FLUID_OP_TRANSPOSE || nd.op == FLUID_OP_RESHAPE) &&
+                          is_view(nd.op, nd.perm, g.edge_shape(g.act_in[n][0]), nd.out_shape, en.in[0], en.out);
+        if (view) {
+          en.costs = {0};
+        } else {
+          // operands laid out one after another in the scratch buffer
+          std::vector<Operand> ins;
+          uint64_t off = 0;
+          int slot = 0;
+          for (int v : nd.ins) {
+            Operand o;
+            if (v >= 0) {
+              o.shape = g.edge_shape(v);
+              o.stride = dense_strides(o.shape, en.in[slot++]);
+              o.dtype = g.dtype;
+            } else {
+              o.shape = g.consts[~v].shape;
+              o.stride = row_major_strides(o.shape);
+              o.dtype = g.consts[~v].dtype;
+            }
+            o.ptr = base + off;
+            off = align256(off + (uint64_t)numel(o.shape) * dtype_bytes(o.dtype));
+            ins.push_back(o);
+          }
+          Operand ou;
+          ou.shape = nd.out_shape;
+          ou.stride = dense_strides(ou.shape, en.out);
+          ou.dtype = g.dtype;
+          ou.ptr = base + off;
+          for (int v = 0; v < num_variants(nd.op); ++v) {
+            NodeKernel k = prepare_node(nd, v, g.dtype, ins, ou);
+            if (!k.available) { en.costs.push_back(-1); continue; }
+            hip_check(launch_node_kernel(k, s), "warm-up launch");
+            hip_check(hipEventRecord(ev[0], s), "hipEventRecord");
+            hip_check(launch_node_kernel(k, s), "timed launch");
+            hip_check(hipEventRecord(ev[1], s), "hipEventRecord");
+            hip_check(hipEventSynchronize(ev[1]), "hipEventSynchronize");
+            float first = 0.f;
+            hip_check(hipEventElapsedTime(&first, ev[0], ev[1]), "hipEventElapsedTime");
+            std::vector<float> times = {first};
+            const int64_t first_ns = (int64_t)std::llround((double)first * 1e6);
+            // clearly losing combinations are not worth more launches
+            if (!(best_so_far >= 0 && first_ns > 8 * best_so_far) && R > 1) {
+              for (uint32_t r = 1; r < R; ++r) {
+                hip_check(hipEventRecord(ev[2 * r], s), "hipEventRecord");
+                hip_check(launch_node_kernel(k, s), "timed launch");
+                hip_check(hipEventRecord(ev[2 * r + 1], s), "hipEventRecord");
+              }
+              hip_check(hipEventSynchronize(ev[2 * R - 1]), "hipEventSynchronize");
+              for (uint32_t r = 1; r < R; ++r) {
+                float ms = 0.f;
+                hip_check(hipEventElapsedTime(&ms, ev[2 * r], ev[2 * r + 1]), "hipEventElapsedTime");
+                times.push_back(ms);
+              }
+            }
+            std::sort(times.begin(), times.end());
+            const int64_t ns_ = std::max<int64_t>(1, (int64_t)std::llround((double)times[times.size() / 2] * 1e6));
+            en.costs.push_back(ns_);
+            if (best_so_far < 0 || ns_ < best_so_far) best_so_far = ns_;
+          }
+        }
+        sig.entries.push_back(std::move(en));
+        int i = ns;
+        for (; i >= 0; --i) {
+          const size_t lim = i == ns ? olist.size() : lists[i].size();
+          if (++idx[i] < lim) break;
+          idx[i] = 0;
+        }
+        if (i < 0) break;
+      }
+      t.sigs.push_back(std::move(sig));
+    }
+    hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
+    t.bind(g);
+    auto h = std::make_unique<fluid_cost_table>();
+    h->t = std::move(t);
+    h->serial = gh->serial;
+    *out = h.release();
+  });
+}
+
+}  // extern "C"

@@ -1,0 +1,393 @@
+#include "dispatch.h"
+
+#include <algorithm>
+
+namespace fluid {
+
+FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  f.d = d ? d : 1;
+  uint32_t s = 0;
+  while ((uint64_t(1) << s) < f.d) ++s;
+  f.s = s;
+  f.m = (uint32_t)(((uint64_t(1) << 32) * ((uint64_t(1) << s) - f.d)) / f.d + 1);
+  return f;
+}
+
+std::vector<int64_t> row_major_strides(const Shape& s) {
+  std::vector<int64_t> st(s.size(), 1);
+  for (int i = (int)s.size() - 2; i >= 0; --i) st[i] = st[i + 1] * s[i + 1];
+  return st;
+}
+
+int num_variants(int op) {
+  switch (op) {
+    case FLUID_OP_MATMUL: return 2;
+    case FLUID_OP_GELU:
+    case FLUID_OP_SILU:
+    case FLUID_OP_TRANSPOSE:
+    case FLUID_OP_RESHAPE: return 2;
+    case FLUID_OP_SOFTMAX:
+    case FLUID_OP_LAYERNORM:
+    case FLUID_OP_RMSNORM: return 2;
+    default: return 1;
+  }
+}
+
+namespace {
+
+struct IterDim {
+  int64_t ext, os, s0, s1;
+};
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+std::vector<IterDim> canonicalize(std::vector<IterDim> d) {
+  std::vector<IterDim> k;
+  for (auto& x : d)
+    if (x.ext != 1) k.push_back(x);
+  std::stable_sort(k.begin(), k.end(), [](const IterDim& a, const IterDim& b) { return a.os > b.os; });
+  std::vector<IterDim> m;
+  for (int i = (int)k.size() - 1; i >= 0; --i) {
+    const IterDim& o = k[i];
+    if (!m.empty()) {
+      IterDim& in = m.back();
+      if (o.os == in.os * in.ext && o.s0 == in.s0 * in.ext && o.s1 == in.s1 * in.ext) {
+        in.ext *= o.ext;
+        continue;
+      }
+    }
+    m.push_back(o);
+  }
+  std::reverse(m.begin(), m.end());
+  if (m.empty()) m.push_back({1, 1, 0, 0});
+  return m;
+}
+
+void check_small(const Operand& o, const char* what) {
+  if (numel(o.shape) >= (int64_t(1) << 31))
+    fail(FLUID_E_UNSUPPORTED, std::string(what) + ": tensors of 2^31 or more elements are not supported");
+}
+
+int ew_op_of(int op) {
+  switch (op) {
+    case FLUID_OP_ADD: return EW_ADD;
+    case FLUID_OP_MUL: return EW_MUL;
+    case FLUID_OP_GELU: return EW_GELU;
+    case FLUID_OP_SILU: return EW_SILU;
+    default: return EW_COPY;
+  }
+}
+
+NodeKernel prepare_ew(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+  NodeKernel k;
+  k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
+  const Operand& x = ins[0];
+  const bool binary = nd.op == FLUID_OP_ADD || nd.op == FLUID_OP_MUL;
+  std::vector<IterDim> dims;
+  if (nd.op == FLUID_OP_TRANSPOSE) {
+    for (size_t i = 0; i < out.shape.size(); ++i)
+      dims.push_back({out.shape[i], out.stride[i], x.stride[nd.perm[i]], 0});
+  } else if (nd.op == FLUID_OP_RESHAPE) {
+    int a;
+    ReshapeKind rk = reshape_kind(x.shape, out.shape, &a);
+    if (rk == ReshapeKind::Same) {
+      for (size_t i = 0; i < out.shape.size(); ++i) dims.push_back({out.shape[i], out.stride[i], x.stride[i], 0});
+    } else if (rk == ReshapeKind::Split) {  // iterate the output's (finer) dims
+      for (int i = 0; i < (int)out.shape.size(); ++i) {
+        int64_t s0;
+        if (i < a) s0 = x.stride[i];
+        else if (i == a) s0 = x.stride[a] * out.shape[a + 1];
+        else if (i == a + 1) s0 = x.stride[a];
+        else s0 = x.stride[i - 1];
+        dims.push_back({out.shape[i], out.stride[i], s0, 0});
+      }
+    } else if (rk == ReshapeKind::Merge) {  // iterate the input's (finer) dims
+      for (int i = 0; i < (int)x.shape.size(); ++i) {
+        int64_t os;
+        if (i < a) os = out.stride[i];
+        else if (i == a) os = out.stride[a] * x.shape[a + 1];
+        else if (i == a + 1) os = out.stride[a];
+        else os = out.stride[i - 1];
+        dims.push_back({x.shape[i], os, x.stride[i], 0});
+      }
+    } else {
+      fail(FLUID_E_UNSUPPORTED, "reshape kind");
+    }
+  } else {
+    const size_t r = out.shape.size();
+    for (size_t i = 0; i < r; ++i) {
+      int64_t s1 = 0;
+      if (binary) {
+        const Operand& y = ins[1];
+        if (y.shape.size() == r) s1 = y.stride[i];
+        else s1 = (i == r - 1) ? y.stride[0] : 0;  // bias [N] broadcast
+      }
+      dims.push_back({out.shape[i], out.stride[i], x.stride[i], s1});
+    }
+  }
+  check_small(out, "elementwise");
+  std::vector<IterDim> c = canonicalize(dims);
+  const int R = (int)c.size();
+  if (R > kMaxDims) fail(FLUID_E_UNSUPPORTED, "elementwise rank");
+  EwParams& p = k.ew;
+  p.rank = R;
+  for (int d = 0; d < R; ++d) {
+    p.ext[d] = (uint32_t)c[d].ext;
+    p.os[d] = (int32_t)c[d].os;
+    p.is0[d] = (int32_t)c[d].s0;
+    p.is1[d] = (int32_t)c[d].s1;
+  }
+  p.x0 = x.ptr;
+  p.x1 = binary ? ins[1].ptr : nullptr;
+  p.y = const_cast<void*>(out.ptr);
+  p.op = ew_op_of(nd.op);
+  p.in1_dtype = binary ? (ins[1].dtype == FLUID_BF16 ? DT_BF16 : DT_F32) : k.dtype;
+  const uint32_t total = (uint32_t)numel(out.shape);
+  if (variant == 0) {
+    k.family = KF_EW;
+    const int VEC = k.dtype == DT_F32 ? 4 : 8;
+    const uint32_t inner = p.ext[R - 1];
+    int vec = (inner % VEC == 0 && aligned16(out.ptr)) ? VEC : 1;
+    auto vec_ok = [&](const int32_t* s, const void* ptr) {
+      if (vec == 1 || s[R - 1] != 1 || !aligned16(ptr)) return false;
+      for (int d = 0; d < R - 1; ++d)
+        if (s[d] % vec != 0) return false;
+      return true;
+    };
+    k.vec = vec;
+    k.vin0 = vec_ok(p.is0, p.x0);
+    k.vin1 = binary && p.in1_dtype == k.dtype && vec_ok(p.is1, p.x1);
+    for (int d = 0; d < R - 1; ++d) p.div[d] = make_fastdiv(p.ext[d]);
+    p.div[R - 1] = make_fastdiv(inner / vec);
+    p.total = total / vec;
+    k.available = true;
+    return k;
+  }
+  // variant 1: LDS-tiled relayout for unary ops whose input is contiguous
+  // along a dim other than the output's innermost one
+  k.family = KF_EW_TILED;
+  if (binary) { k.why = "tiled variant is unary only"; return k; }
+  int t = -1;
+  for (int d = 0; d < R - 1; ++d)
+    if (p.is0[d] == 1) t = d;
+  if (t < 0) { k.why = "input and output share the unit-stride dim"; return k; }
+  p.tdim = t;
+  p.tiles_inner = (p.ext[R - 1] + 63) / 64;
+  p.tiles_t = (p.ext[t] + 63) / 64;
+  p.div_ti = make_fastdiv(p.tiles_inner);
+  p.div_tt = make_fastdiv(p.tiles_t);
+  uint32_t other = 1;
+  for (int d = 0; d < R - 1; ++d)
+    if (d != t) { p.div[d] = make_fastdiv(p.ext[d]); other *= p.ext[d]; }
+  p.total = p.tiles_inner * p.tiles_t * other;  // blocks
+  k.available = true;
+  return k;
+}
+
+NodeKernel prepare_rope(const Node&, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+  NodeKernel k;
+  k.family = KF_ROPE;
+  k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
+  const Operand& x = ins[0];
+  check_small(out, "rope");
+  const int64_t half = x.shape[3] / 2;
+  struct D { int64_t ext, xs, ys; int logical; };
+  std::vector<D> d = {{x.shape[0], x.stride[0], out.stride[0], 0},
+                      {x.shape[1], x.stride[1], out.stride[1], 1},
+                      {x.shape[2], x.stride[2], out.stride[2], 2},
+                      {half, x.stride[3], out.stride[3], 3}};
+  std::stable_sort(d.begin(), d.end(), [](const D& a, const D& b) { return a.ys > b.ys; });
+  RopeParams& p = k.rope;
+  p.rank = 4;
+  for (int i = 0; i < 4; ++i) {
+    p.ext[i] = (uint32_t)d[i].ext;
+    p.div[i] = make_fastdiv(p.ext[i]);
+    p.xs[i] = (int32_t)d[i].xs;
+    p.ys[i] = (int32_t)d[i].ys;
+    if (d[i].logical == 1) p.pos_dim = i;
+    if (d[i].logical == 3) p.half_dim = i;
+  }
+  p.x_half = (int32_t)(x.stride[3] * half);
+  p.y_half = (int32_t)(out.stride[3] * half);
+  p.half = (uint32_t)half;
+  p.total = (uint32_t)(numel(out.shape) / 2);
+  p.x = x.ptr;
+  p.y = const_cast<void*>(out.ptr);
+  p.cos_t = (const float*)ins[1].ptr;
+  p.sin_t = (const float*)ins[2].ptr;
+  k.available = true;
+  return k;
+}
+
+NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+  NodeKernel k;
+  k.family = variant == 0 ? KF_RED_ROW : KF_RED_COL;
+  k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
+  const Operand& x = ins[0];
+  check_small(out, "reduction");
+  const int r = (int)x.shape.size();
+  RedParams& p = k.red;
+  p.op = nd.op == FLUID_OP_SOFTMAX ? RED_SOFTMAX : nd.op == FLUID_OP_LAYERNORM ? RED_LAYERNORM : RED_RMSNORM;
+  p.causal = nd.op == FLUID_OP_SOFTMAX ? nd.iattr : 0;
+  p.attr = nd.fattr;
+  p.R = (uint32_t)x.shape[r - 1];
+  p.irs = (int32_t)x.stride[r - 1];
+  p.ors = (int32_t)out.stride[r - 1];
+  struct D { int64_t ext, is, os; bool q; };
+  std::vector<D> rows;
+  for (int i = 0; i < r - 1; ++i) {
+    bool q = p.causal && i == r - 2;
+    if (x.shape[i] != 1 || q) rows.push_back({x.shape[i], x.stride[i], out.stride[i], q});
+  }
+  std::stable_sort(rows.begin(), rows.end(), [](const D& a, const D& b) { return a.is > b.is; });
+  if (rows.size() > (size_t)kMaxDims) fail(FLUID_E_UNSUPPORTED, "reduction rank");
+  p.nrd = (int)rows.size();
+  p.qdim = -1;
+  uint32_t nrows = 1;
+  for (int i = 0; i < p.nrd; ++i) {
+    p.rext[i] = (uint32_t)rows[i].ext;
+    p.rdiv[i] = make_fastdiv(p.rext[i]);
+    p.ris[i] = (int32_t)rows[i].is;
+    p.ros[i] = (int32_t)rows[i].os;
+    if (rows[i].q) p.qdim = i;
+    nrows *= p.rext[i];
+  }
+  p.nrows = nrows;
+  p.x = x.ptr;
+  p.y = const_cast<void*>(out.ptr);
+  p.gamma = ins.size() > 1 ? ins[1].ptr : nullptr;
+  p.beta = ins.size() > 2 ? ins[2].ptr : nullptr;
+  if (variant == 0 && p.R > 4096) { k.why = "row variant holds at most 4096 values per row"; return k; }
+  k.available = true;
+  return k;
+}
+
+NodeKernel prepare_gemm(const Node&, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+  NodeKernel k;
+  k.family = KF_GEMM;
+  k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
+  const Operand& A = ins[0];
+  const Operand& B = ins[1];
+  const Operand& C = out;
+  check_small(A, "matmul");
+  check_small(B, "matmul");
+  check_small(C, "matmul");
+  const int rA = (int)A.shape.size(), rB = (int)B.shape.size();
+  GemmParams& p = k.gemm;
+  p.A = A.ptr;
+  p.B = B.ptr;
+  p.C = const_cast<void*>(C.ptr);
+  p.K = (uint32_t)A.shape[rA - 1];
+  p.N = (uint32_t)B.shape[rB - 1];
+  p.a_k = (int32_t)A.stride[rA - 1];
+  p.b_k = (int32_t)B.stride[rB - 2];
+  p.b_n = (int32_t)B.stride[rB - 1];
+  p.c_n = (int32_t)C.stride[rA - 1];
+  uint32_t G1 = 1, G2 = 1, M1 = 1, M2 = 1;
+  p.a_g1 = p.a_g2 = p.a_m1 = p.b_g1 = p.b_g2 = p.c_g1 = p.c_g2 = p.c_m1 = 0;
+  if (rB == 2) {
+    if (rA == 2) {
+      M2 = (uint32_t)A.shape[0];
+      p.a_m2 = (int32_t)A.stride[0]; p.c_m2 = (int32_t)C.stride[0];
+    } else if (rA == 3) {
+      M1 = (uint32_t)A.shape[0]; M2 = (uint32_t)A.shape[1];
+      p.a_m1 = (int32_t)A.stride[0]; p.a_m2 = (int32_t)A.stride[1];
+      p.c_m1 = (int32_t)C.stride[0]; p.c_m2 = (int32_t)C.stride[1];
+    } else if (rA == 4) {
+      G1 = (uint32_t)A.shape[0]; G2 = (uint32_t)A.shape[1]; M2 = (uint32_t)A.shape[2];
+      p.a_g1 = (int32_t)A.stride[0]; p.a_g2 = (int32_t)A.stride[1]; p.a_m2 = (int32_t)A.stride[2];
+      p.c_g1 = (int32_t)C.stride[0]; p.c_g2 = (int32_t)C.stride[1]; p.c_m2 = (int32_t)C.stride[2];
+    } else {
+      fail(FLUID_E_UNSUPPORTED, "matmul rank");
+    }
+  } else {
+    M2 = (uint32_t)A.shape[rA - 2];
+    p.a_m2 = (int32_t)A.stride[rA - 2];
+    p.c_m2 = (int32_t)C.stride[rA - 2];
+    if (rA == 3) {
+      G2 = (uint32_t)A.shape[0];
+      p.a_g2 = (int32_t)A.stride[0]; p.b_g2 = (int32_t)B.stride[0]; p.c_g2 = (int32_t)C.stride[0];
+    } else if (rA == 4) {
+      G1 = (uint32_t)A.shape[0]; G2 = (uint32_t)A.shape[1];
+      p.a_g1 = (int32_t)A.stride[0]; p.a_g2 = (int32_t)A.stride[1];
+      p.b_g1 = (int32_t)B.stride[0]; p.b_g2 = (int32_t)B.stride[1];
+      p.c_g1 = (int32_t)C.stride[0]; p.c_g2 = (int32_t)C.stride[1];
+    } else if (rA != 2) {
+      fail(FLUID_E_UNSUPPORTED, "matmul rank");
+    }
+  }
+  p.G = G1 * G2;
+  p.G2 = G2;
+  p.M2 = M2;
+  p.M = M1 * M2;
+  p.g2div = make_fastdiv(G2);
+  p.m2div = make_fastdiv(M2);
+  const int VEC = k.dtype == DT_F32 ? 4 : 8;
+  auto mult = [&](std::initializer_list<int32_t> s) {
+    for (int32_t v : s)
+      if (v % VEC != 0) return false;
+    return true;
+  };
+  k.amode = GM_GENERIC;
+  if (aligned16(p.A)) {
+    if (p.a_k == 1 && p.K % VEC == 0 && mult({p.a_g1, p.a_g2, p.a_m1, p.a_m2})) k.amode = GM_K;
+    else if (p.a_m2 == 1 && p.M2 % VEC == 0 && mult({p.a_g1, p.a_g2, p.a_m1, p.a_k})) k.amode = GM_MN;
+  }
+  k.bmode = GM_GENERIC;
+  if (aligned16(p.B)) {
+    if (p.b_n == 1 && p.N % VEC == 0 && mult({p.b_g1, p.b_g2, p.b_k})) k.bmode = GM_MN;
+    else if (p.b_k == 1 && p.K % VEC == 0 && mult({p.b_g1, p.b_g2, p.b_n})) k.bmode = GM_K;
+  }
+  k.cmode = 0;
+  if (p.c_n == 1) k.cmode = 1;
+  else if (p.c_m2 == 1 && p.M2 % 4 == 0 && aligned16(p.C) && (p.c_m1 % 4 == 0) && (p.c_g1 % 4 == 0) &&
+           (p.c_g2 % 4 == 0) && (p.c_n % 4 == 0))
+    k.cmode = 2;
+  p.cmode = k.cmode;
+  k.gemm_tile = variant;
+  const uint32_t T = variant == 0 ? 128 : 64;
+  p.tiles_m = (p.M + T - 1) / T;
+  p.tiles_n = (p.N + T - 1) / T;
+  k.available = true;
+  return k;
+}
+
+}  // namespace
+
+NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+  if (variant < 0 || variant >= num_variants(nd.op)) {
+    NodeKernel k;
+    k.why = "no such variant";
+    return k;
+  }
+  switch (nd.op) {
+    case FLUID_OP_MATMUL: return prepare_gemm(nd, variant, dtype, ins, out);
+    case FLUID_OP_SOFTMAX:
+    case FLUID_OP_LAYERNORM:
+    case FLUID_OP_RMSNORM: return prepare_red(nd, variant, dtype, ins, out);
+    case FLUID_OP_ROPE: return prepare_rope(nd, dtype, ins, out);
+    default: return prepare_ew(nd, variant, dtype, ins, out);
+  }
+}
+
+std::string NodeKernel::name() const {
+  static const char* ew_names[] = {"copy", "add", "mul", "gelu", "silu"};
+  static const char* red_names[] = {"softmax", "layernorm", "rmsnorm"};
+  static const char* gm[] = {"g", "k", "mn"};
+  const std::string dt = dtype == DT_BF16 ? "bf16" : "f32";
+  switch (family) {
+    case KF_VIEW: return "view";
+    case KF_EW: return "ew_" + std::string(ew_names[ew.op]) + "_" + dt + "_v" + std::to_string(vec);
+    case KF_EW_TILED: return "ew_tiled_" + std::string(ew_names[ew.op]) + "_" + dt;
+    case KF_ROPE: return "rope_" + dt;
+    case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt;
+    case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
+    case KF_GEMM:
+      return "gemm_" + dt + "_t" + std::to_string(gemm_tile == 0 ? 128 : 64) + "_a" + gm[amode] +
+             "_b" + gm[bmode] + "_c" + (cmode == 1 ? "n" : cmode == 2 ? "m" : "g");
+  }
+  return "?";
+}
+
+}  // namespace fluid

@@ -1,0 +1,55 @@
+// Node -> kernel translation: given the layouts of a node's operands, pick
+// the kernel family for a variant id and fill its parameter block.  Shared by
+// the executor, the cost measurement and fluid_node_kernel; HIP-free.
+//
+// Variant ids per operator:
+//   MATMUL                      0: 128x128 tile, 1: 64x64 tile (MFMA)
+//   ADD MUL                     0: streaming elementwise in output order
+//   GELU SILU TRANSPOSE RESHAPE 0: streaming; 1: LDS-tiled (input and output
+//                               unit-stride dims differ)
+//   SOFTMAX LAYERNORM RMSNORM   0: one wavefront per row; 1: one lane per row
+//   ROPE                        0: streaming
+#pragma once
+
+#include <string>
+#include <vector>
+
+#include "graph.h"
+#include "kparams.h"
+
+namespace fluid {
+
+struct Operand {
+  const void* ptr = nullptr;
+  Shape shape;
+  std::vector<int64_t> stride;  // elements, per logical dim
+  int dtype = FLUID_F32;
+};
+
+enum KernelFamily : int { KF_VIEW, KF_EW, KF_EW_TILED, KF_ROPE, KF_RED_ROW, KF_RED_COL, KF_GEMM };
+
+enum GemmMode : int { GM_GENERIC = 0, GM_K = 1, GM_MN = 2 };  // A: K-/M-contig; B: K-/N-contig
+
+struct NodeKernel {
+  int family = KF_VIEW;
+  bool available = false;
+  std::string why;              // reason when not available
+  int dtype = DT_F32;
+  int vec = 1;                  // EW vector width (1, 4 or 8)
+  bool vin0 = false, vin1 = false;
+  EwParams ew{};
+  RopeParams rope{};
+  RedParams red{};
+  GemmParams gemm{};
+  int gemm_tile = 0, amode = 0, bmode = 0, cmode = 0;  // cmode 0 generic, 1 N-contig, 2 M-contig
+  std::string name() const;
+};
+
+int num_variants(int op);
+NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins,
+                        const Operand& out);
+
+// Row-major strides of a shape.
+std::vector<int64_t> row_major_strides(const Shape& s);
+
+}  // namespace fluid

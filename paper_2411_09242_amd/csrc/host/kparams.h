@@ -1,0 +1,99 @@
+// Kernel parameter blocks, filled on the host and passed by value to the
+// HIP kernels.  Plain C++ (no HIP types) so host code and tests can build
+// them without a GPU toolchain.  All offsets are in elements; every tensor
+// handed to a kernel has fewer than 2^31 elements.
+#pragma once
+
+#include <cstdint>
+
+namespace fluid {
+
+// Exact unsigned division by a runtime constant (Granlund-Montgomery):
+// q = (umulhi(n, m) + n) >> s for every n < 2^32.
+struct FastDiv {
+  uint32_t d = 1, m = 1, s = 0;
+};
+FastDiv make_fastdiv(uint32_t d);
+
+constexpr int kMaxDims = 6;
+
+enum EwOp : int { EW_COPY = 0, EW_ADD = 1, EW_MUL = 2, EW_GELU = 3, EW_SILU = 4 };
+enum DType : int { DT_F32 = 0, DT_BF16 = 1 };
+
+// Elementwise / relayout over a canonical iteration space: dims ordered
+// outer -> inner with the output's unit-stride dim last.
+struct EwParams {
+  int rank;
+  uint32_t ext[kMaxDims];
+  FastDiv div[kMaxDims];      // div[d] divides by ext[d] (div[rank-1] by ext/VEC)
+  int32_t os[kMaxDims];       // output strides
+  int32_t is0[kMaxDims];      // input 0 strides
+  int32_t is1[kMaxDims];      // input 1 strides (0 = broadcast)
+  uint32_t total;             // elements (or vectors) to produce
+  const void* x0;
+  const void* x1;
+  void* y;
+  int op;
+  int in1_dtype;              // dtype of input 1 (a bias constant may differ)
+  // tiled variant: the input's unit-stride dim and the grid decomposition
+  int tdim;                   // index of the input-contiguous dim (!= rank-1)
+  uint32_t tiles_inner, tiles_t;
+  FastDiv div_ti, div_tt;     // over tiles of dim rank-1 and of dim tdim
+};
+
+// RoPE over the iteration space [B, S, NH, D/2] (dims reordered by output
+// stride); pos_dim / half_dim give where S and D/2 landed.
+struct RopeParams {
+  int rank;
+  uint32_t ext[4];
+  FastDiv div[4];
+  int32_t xs[4], ys[4];       // strides of x and y for the 4 iteration dims
+  int32_t x_half, y_half;     // stride of D in x / y, times D/2
+  int pos_dim, half_dim;
+  uint32_t half;              // D/2 (row length of the tables)
+  uint32_t total;
+  const void* x;
+  void* y;
+  const float* cos_t;
+  const float* sin_t;
+};
+
+enum RedOp : int { RED_SOFTMAX = 0, RED_LAYERNORM = 1, RED_RMSNORM = 2 };
+
+// Row reductions over the last logical dim (length R).  Row dims are
+// ordered by input stride, outer -> inner.
+struct RedParams {
+  int nrd;
+  uint32_t rext[kMaxDims];
+  FastDiv rdiv[kMaxDims];
+  int32_t ris[kMaxDims], ros[kMaxDims];
+  int qdim;                   // row-dim index of the query dim (causal), -1 otherwise
+  uint32_t nrows;
+  uint32_t R;
+  int32_t irs, ors;           // input / output stride of the reduced dim
+  const void* x;
+  void* y;
+  const void* gamma;
+  const void* beta;
+  float attr;                 // softmax scale or norm eps
+  int causal;
+  int op;
+};
+
+// C[g, m, n] = sum_k A[g, m, k] * B[g, k, n]; g = g1 * G2 + g2 and
+// m = m1 * M2 + m2 (two-level decomposition of batch and row indices).
+struct GemmParams {
+  const void* A;
+  const void* B;
+  void* C;
+  uint32_t M, N, K, G;
+  uint32_t G2, M2;
+  FastDiv g2div, m2div;
+  int32_t a_g1, a_g2, a_m1, a_m2, a_k;
+  int32_t b_g1, b_g2, b_k, b_n;
+  int32_t c_g1, c_g2, c_m1, c_m2, c_n;
+  int32_t cmode;              // 0 scalar stores, 1 N-contiguous, 2 M-contiguous (4 rows)
+  uint32_t tiles_m, tiles_n;
+};
+
+}  // namespace fluid

@@ -1,0 +1,40 @@
+// Layout planner (Section 3: Alg. 1-3, Eq. 1, majority vote) and arena
+// planner (Alg. 4, Greedy-by-Size).
+#pragma once
+
+#include <vector>
+
+#include "costtable.h"
+#include "graph.h"
+
+namespace fluid {
+
+struct LayoutPlan {
+  std::vector<int> layout_idx;     // per edge, index into the table's L(e)
+  std::vector<Perm> perm;          // per edge, the chosen permutation
+  std::vector<int> variant;        // per node, -1 = view
+  int64_t total = 0;
+  int guard_used = 0;
+  std::vector<std::vector<int>> paths;
+  uint64_t graph_serial = 0;
+};
+
+std::vector<int> longest_path(const Graph& g, const std::vector<int>& S);
+std::vector<std::vector<int>> split_paths(const Graph& g);
+LayoutPlan plan_layouts(const Graph& g, const CostTable& t, uint32_t flags);
+LayoutPlan identity_plan(const Graph& g);  // row-major everywhere, variant 0
+
+struct ArenaPlan {
+  std::vector<int> root;            // per edge
+  std::vector<int64_t> offset;      // per edge (-1 = not in the arena)
+  std::vector<int> buffers;         // arena buffer edge ids
+  std::vector<uint64_t> size;       // per edge (0 if not a buffer)
+  std::vector<int> def, last;       // per edge (buffers only)
+  uint64_t peak = 0, naive = 0, lower_bound = 0;
+  uint64_t graph_serial = 0;
+};
+
+bool node_is_view(const Graph& g, int n, const std::vector<Perm>& perm_of_edge);
+ArenaPlan plan_arena(const Graph& g, const std::vector<Perm>& perm_of_edge, uint64_t align, bool no_reuse);
+
+}  // namespace fluid

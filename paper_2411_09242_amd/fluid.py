@@ -1,0 +1,394 @@
+"""ctypes binding of include/fluid.h (argument marshalling only).
+
+Every function named ``fluid_*`` here calls the C entry point of the same
+name; all computation happens in the native library.  ``load()`` picks the
+GPU library (lib/libfluid.so) or, with ``host_only=True``, the planner-only
+library (lib/libfluid_host.so).  A missing library raises immediately: there
+is no fallback implementation.
+
+The small classes at the end (Graph, CostTable, LayoutPlan, ArenaPlan,
+Executor) own handles and, for the executor, the torch device tensors that
+hold constants, inputs, outputs and the arena.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import json
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIBDIR = os.path.join(_PKG, "lib")
+
+MAX_RANK = 6
+MAX_IN = 4
+
+F32, BF16 = 0, 1
+OPS = {"matmul": 0, "add": 1, "mul": 2, "transpose": 3, "reshape": 4, "softmax": 5,
+       "layernorm": 6, "rmsnorm": 7, "gelu": 8, "silu": 9, "rope": 10}
+ROLES = {"other": 0, "weight": 1, "bias": 2, "gamma": 3, "beta": 4, "rope_cos": 5, "rope_sin": 6}
+ARCH = {"post_ln": 0, "pre_ln": 1, "llama": 2}
+NO_DP, NO_VARIANTS, NO_GUARD = 1, 2, 4
+ARENA_NO_REUSE = 1
+STATUS = {0: "OK", -1: "INVALID", -2: "UNSUPPORTED", -3: "INFEASIBLE", -4: "ARENA_TOO_SMALL",
+          -5: "HIP", -6: "NOMEM"}
+
+
+class FluidError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class NodeDesc(C.Structure):
+    _fields_ = [("op", C.c_int32), ("n_in", C.c_int32), ("in_", C.c_int32 * MAX_IN),
+                ("out_rank", C.c_int32), ("out_shape", C.c_int64 * MAX_RANK),
+                ("perm", C.c_int32 * MAX_RANK), ("f_attr", C.c_float * 2), ("i_attr", C.c_int32 * 2)]
+
+
+class GraphDesc(C.Structure):
+    _fields_ = [("dtype", C.c_int32),
+                ("n_inputs", C.c_int32), ("input_rank", C.POINTER(C.c_int32)),
+                ("input_shapes", C.POINTER(C.c_int64)),
+                ("n_consts", C.c_int32), ("const_rank", C.POINTER(C.c_int32)),
+                ("const_shapes", C.POINTER(C.c_int64)), ("const_dtype", C.POINTER(C.c_int32)),
+                ("const_role", C.POINTER(C.c_int32)),
+                ("n_nodes", C.c_int32), ("nodes", C.POINTER(NodeDesc)),
+                ("n_outputs", C.c_int32), ("output_edges", C.POINTER(C.c_int32))]
+
+
+class ModelCfg(C.Structure):
+    _fields_ = [("arch", C.c_int32), ("layers", C.c_int32), ("batch", C.c_int32), ("seq", C.c_int32),
+                ("hidden", C.c_int32), ("heads", C.c_int32), ("ffn", C.c_int32), ("dtype", C.c_int32),
+                ("eps", C.c_float), ("rope_base", C.c_float)]
+
+
+_VP = C.c_void_p
+_PROTOS = {
+    "fluid_last_error": (C.c_char_p, []),
+    "fluid_build_graph": (C.c_int, [C.POINTER(GraphDesc), C.POINTER(_VP)]),
+    "fluid_build_transformer": (C.c_int, [C.POINTER(ModelCfg), C.POINTER(_VP)]),
+    "fluid_graph_info": (C.c_int, [_VP] + [C.POINTER(C.c_int32)] * 5),
+    "fluid_graph_export_json": (C.c_int, [_VP, C.c_char_p, C.c_uint64, C.POINTER(C.c_uint64)]),
+    "fluid_cost_table_load": (C.c_int, [C.c_char_p, _VP, C.POINTER(_VP)]),
+    "fluid_cost_table_save": (C.c_int, [_VP, C.c_char_p]),
+    "fluid_measure_scratch_bytes": (C.c_int, [_VP, C.POINTER(C.c_uint64)]),
+    "fluid_measure_costs": (C.c_int, [_VP, C.c_uint32, _VP, C.c_uint64, _VP, C.POINTER(_VP)]),
+    "fluid_plan_layouts": (C.c_int, [_VP, _VP, C.c_uint32, C.POINTER(_VP)]),
+    "fluid_layout_plan_get": (C.c_int, [_VP, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                        C.POINTER(C.c_int64), C.POINTER(C.c_int32)]),
+    "fluid_edge_layout": (C.c_int, [_VP, _VP, C.c_int32, C.POINTER(C.c_int32)]),
+    "fluid_plan_arena": (C.c_int, [_VP, _VP, C.c_uint64, C.c_uint32, C.POINTER(_VP)]),
+    "fluid_arena_plan_get": (C.c_int, [_VP, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
+                                       C.POINTER(C.c_uint64), C.POINTER(C.c_int64), C.POINTER(C.c_int32)]),
+    "fluid_run": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
+                            C.POINTER(_VP), _VP]),
+    "fluid_trace_enable": (C.c_int, [_VP, C.POINTER(C.c_uint8), C.c_int32]),
+    "fluid_trace_collect": (C.c_int, [_VP, C.POINTER(C.c_double), C.POINTER(C.c_int32)]),
+    "fluid_node_kernel": (C.c_int, [_VP, _VP, C.c_int32, C.c_char_p, C.c_uint64]),
+    "fluid_graph_free": (None, [_VP]),
+    "fluid_cost_table_free": (None, [_VP]),
+    "fluid_layout_plan_free": (None, [_VP]),
+    "fluid_arena_plan_free": (None, [_VP]),
+}
+SYMBOLS = tuple(_PROTOS)
+
+_libs = {}
+_lib = None
+
+
+def load(host_only=False):
+    """Load (once) and return the native library; raises if it is not built."""
+    global _lib
+    name = "libfluid_host.so" if host_only else "libfluid.so"
+    if name in _libs:
+        _lib = _libs[name]
+        return _lib
+    path = os.path.join(LIBDIR, name)
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} is not built; run `python -m paper_2411_09242_amd.build`")
+    lib = C.CDLL(path)
+    for sym, (res, args) in _PROTOS.items():
+        f = getattr(lib, sym)
+        f.restype = res
+        f.argtypes = args
+    _libs[name] = lib
+    _lib = lib
+    return lib
+
+
+def _L():
+    if _lib is None:
+        load()
+    return _lib
+
+
+def _check(st):
+    if st != 0:
+        raise FluidError(st, _L().fluid_last_error().decode())
+
+
+# ----------------------------------------------------------------- raw calls
+def fluid_build_transformer(cfg: dict):
+    c = ModelCfg(ARCH[cfg["arch"]], cfg["layers"], cfg["batch"], cfg["seq"], cfg["hidden"],
+                 cfg["heads"], cfg["ffn"], BF16 if cfg["dtype"] == "bf16" else F32,
+                 cfg.get("eps", 1e-5), cfg.get("rope_base", 10000.0))
+    h = _VP()
+    _check(_L().fluid_build_transformer(C.byref(c), C.byref(h)))
+    return h
+
+
+def fluid_build_graph(desc: dict):
+    """desc: the canonical dict form (dtype, inputs, consts, nodes, outputs)."""
+    ni, nc, nn = len(desc["inputs"]), len(desc["consts"]), len(desc["nodes"])
+    irank = (C.c_int32 * max(ni, 1))(*[len(s) for s in desc["inputs"]])
+    ishape = (C.c_int64 * (max(ni, 1) * MAX_RANK))()
+    for i, s in enumerate(desc["inputs"]):
+        for j, d in enumerate(s):
+            ishape[i * MAX_RANK + j] = d
+    crank = (C.c_int32 * max(nc, 1))(*[len(c["shape"]) for c in desc["consts"]])
+    cshape = (C.c_int64 * (max(nc, 1) * MAX_RANK))()
+    cdt = (C.c_int32 * max(nc, 1))(*[BF16 if c["dtype"] == "bf16" else F32 for c in desc["consts"]])
+    crole = (C.c_int32 * max(nc, 1))(*[ROLES.get(c.get("role", "other"), 0) for c in desc["consts"]])
+    for i, c in enumerate(desc["consts"]):
+        for j, d in enumerate(c["shape"]):
+            cshape[i * MAX_RANK + j] = d
+    nodes = (NodeDesc * max(nn, 1))()
+    for i, nd in enumerate(desc["nodes"]):
+        x = nodes[i]
+        x.op = OPS[nd["op"]]
+        x.n_in = len(nd["ins"])
+        for j, v in enumerate(nd["ins"]):
+            x.in_[j] = v
+        x.out_rank = len(nd["out_shape"])
+        for j, d in enumerate(nd["out_shape"]):
+            x.out_shape[j] = d
+        for j, p in enumerate(nd.get("perm", [])):
+            x.perm[j] = p
+        x.f_attr[0] = nd.get("fattr", 0.0)
+        x.i_attr[0] = nd.get("iattr", 0)
+    outs = (C.c_int32 * max(len(desc["outputs"]), 1))(*desc["outputs"])
+    gd = GraphDesc(BF16 if desc["dtype"] == "bf16" else F32, ni, irank, ishape, nc, crank, cshape,
+                   cdt, crole, nn, nodes, len(desc["outputs"]), outs)
+    h = _VP()
+    _check(_L().fluid_build_graph(C.byref(gd), C.byref(h)))
+    return h
+
+
+def fluid_graph_info(g):
+    v = [C.c_int32() for _ in range(5)]
+    _check(_L().fluid_graph_info(g, *[C.byref(x) for x in v]))
+    return tuple(x.value for x in v)
+
+
+def fluid_graph_export_json(g):
+    n = C.c_uint64()
+    _check(_L().fluid_graph_export_json(g, None, 0, C.byref(n)))
+    buf = C.create_string_buffer(n.value + 1)
+    _check(_L().fluid_graph_export_json(g, buf, n.value + 1, C.byref(n)))
+    return buf.value.decode()
+
+
+def fluid_cost_table_load(path, g):
+    h = _VP()
+    _check(_L().fluid_cost_table_load(str(path).encode(), g, C.byref(h)))
+    return h
+
+
+def fluid_cost_table_save(t, path):
+    _check(_L().fluid_cost_table_save(t, str(path).encode()))
+
+
+def fluid_measure_scratch_bytes(g):
+    n = C.c_uint64()
+    _check(_L().fluid_measure_scratch_bytes(g, C.byref(n)))
+    return n.value
+
+
+def fluid_measure_costs(g, reps, scratch_ptr, scratch_bytes, stream):
+    h = _VP()
+    _check(_L().fluid_measure_costs(g, reps, scratch_ptr, scratch_bytes, stream, C.byref(h)))
+    return h
+
+
+def fluid_plan_layouts(g, t, flags=0):
+    h = _VP()
+    _check(_L().fluid_plan_layouts(g, t, flags, C.byref(h)))
+    return h
+
+
+def fluid_layout_plan_get(lp, n_edges, n_nodes):
+    lay = (C.c_int32 * n_edges)()
+    var = (C.c_int32 * n_nodes)()
+    tot = C.c_int64()
+    gu = C.c_int32()
+    _check(_L().fluid_layout_plan_get(lp, lay, var, C.byref(tot), C.byref(gu)))
+    return list(lay), list(var), tot.value, gu.value
+
+
+def fluid_edge_layout(g, lp, edge, rank):
+    p = (C.c_int32 * MAX_RANK)()
+    _check(_L().fluid_edge_layout(g, lp, edge, p))
+    return tuple(p[:rank])
+
+
+def fluid_plan_arena(g, lp, align=256, flags=0):
+    h = _VP()
+    _check(_L().fluid_plan_arena(g, lp, align, flags, C.byref(h)))
+    return h
+
+
+def fluid_arena_plan_get(ap, n_edges):
+    peak, naive, lb = C.c_uint64(), C.c_uint64(), C.c_uint64()
+    off = (C.c_int64 * n_edges)()
+    root = (C.c_int32 * n_edges)()
+    _check(_L().fluid_arena_plan_get(ap, C.byref(peak), C.byref(naive), C.byref(lb), off, root))
+    return peak.value, naive.value, lb.value, list(off), list(root)
+
+
+def _ptr_array(ptrs):
+    arr = (_VP * max(len(ptrs), 1))()
+    for i, p in enumerate(ptrs):
+        arr[i] = p
+    return arr
+
+
+def fluid_run(g, lp, ap, arena_ptr, arena_bytes, const_ptrs, input_ptrs, output_ptrs, stream):
+    _check(_L().fluid_run(g, lp, ap, arena_ptr, arena_bytes, _ptr_array(const_ptrs),
+                          _ptr_array(input_ptrs), _ptr_array(output_ptrs), stream))
+
+
+def fluid_trace_enable(g, mask, max_records):
+    m = None
+    if mask is not None:
+        m = (C.c_uint8 * len(mask))(*[1 if x else 0 for x in mask])
+    _check(_L().fluid_trace_enable(g, m, max_records))
+
+
+def fluid_trace_collect(g, n_nodes):
+    ms = (C.c_double * n_nodes)()
+    cnt = (C.c_int32 * n_nodes)()
+    _check(_L().fluid_trace_collect(g, ms, cnt))
+    return list(ms), list(cnt)
+
+
+def fluid_node_kernel(g, lp, node):
+    buf = C.create_string_buffer(128)
+    _check(_L().fluid_node_kernel(g, lp, node, buf, 128))
+    return buf.value.decode()
+
+
+# ----------------------------------------------------------------- handles
+class Graph:
+    def __init__(self, handle):
+        self.h = handle
+        self.n_inputs, self.n_consts, self.n_nodes, self.n_edges, dt = fluid_graph_info(handle)
+        self.dtype = "bf16" if dt == BF16 else "f32"
+        self.desc = json.loads(fluid_graph_export_json(handle))
+
+    @classmethod
+    def transformer(cls, cfg):
+        return cls(fluid_build_transformer(cfg))
+
+    @classmethod
+    def from_desc(cls, desc):
+        return cls(fluid_build_graph(desc))
+
+    def edge_shape(self, e):
+        if e < self.n_inputs:
+            return tuple(self.desc["inputs"][e])
+        return tuple(self.desc["nodes"][e - self.n_inputs]["out_shape"])
+
+    def const_specs(self):
+        return [(c["role"], tuple(c["shape"])) for c in self.desc["consts"]]
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.fluid_graph_free(self.h)
+            self.h = None
+
+
+class CostTable:
+    def __init__(self, handle, graph):
+        self.h, self.graph = handle, graph
+
+    @classmethod
+    def load(cls, path, graph):
+        return cls(fluid_cost_table_load(path, graph.h), graph)
+
+    @classmethod
+    def measure(cls, graph, reps=7, device="cuda"):
+        import torch
+        nbytes = fluid_measure_scratch_bytes(graph.h)
+        scratch = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        ptr = (scratch.data_ptr() + 255) // 256 * 256
+        h = fluid_measure_costs(graph.h, reps, ptr, nbytes, torch.cuda.current_stream().cuda_stream)
+        del scratch
+        return cls(h, graph)
+
+    def save(self, path):
+        fluid_cost_table_save(self.h, path)
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.fluid_cost_table_free(self.h)
+            self.h = None
+
+
+class LayoutPlan:
+    def __init__(self, graph, table, flags=0):
+        self.graph = graph
+        self.h = fluid_plan_layouts(graph.h, table.h, flags)
+        self.layout_idx, self.variant, self.total_ns, self.guard_used = fluid_layout_plan_get(
+            self.h, graph.n_edges, graph.n_nodes)
+
+    def perm(self, e):
+        return fluid_edge_layout(self.graph.h, self.h, e, len(self.graph.edge_shape(e)))
+
+    def kernel(self, n):
+        return fluid_node_kernel(self.graph.h, self.h, n)
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.fluid_layout_plan_free(self.h)
+            self.h = None
+
+
+class ArenaPlan:
+    def __init__(self, graph, lplan, align=256, no_reuse=False):
+        self.graph = graph
+        self.h = fluid_plan_arena(graph.h, lplan.h, align, ARENA_NO_REUSE if no_reuse else 0)
+        self.peak, self.naive, self.lower_bound, self.offset, self.root = fluid_arena_plan_get(
+            self.h, graph.n_edges)
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.fluid_arena_plan_free(self.h)
+            self.h = None
+
+
+class Executor:
+    """Device buffers (torch) for one graph + plans, and the fluid_run call."""
+
+    def __init__(self, graph, lplan, aplan, consts, inputs, device="cuda"):
+        import torch
+        self.torch = torch
+        self.graph, self.lplan, self.aplan = graph, lplan, aplan
+        dt = torch.bfloat16 if graph.dtype == "bf16" else torch.float32
+        self.consts = []
+        for c, a in zip(graph.desc["consts"], consts):
+            cdt = torch.bfloat16 if c["dtype"] == "bf16" else torch.float32
+            self.consts.append(torch.as_tensor(a).to(device=device, dtype=cdt).contiguous())
+        self.inputs = [torch.as_tensor(a).to(device=device, dtype=dt).contiguous() for a in inputs]
+        self.outputs = [torch.empty(graph.edge_shape(e), dtype=dt, device=device)
+                        for e in graph.desc["outputs"]]
+        self.arena = torch.empty(max(aplan.peak, 1) + 256, dtype=torch.uint8, device=device)
+        self.arena_ptr = (self.arena.data_ptr() + 255) // 256 * 256
+        self._cp = [t.data_ptr() for t in self.consts]
+        self._ip = [t.data_ptr() for t in self.inputs]
+        self._op = [t.data_ptr() for t in self.outputs]
+
+    def run(self, stream=None):
+        s = stream if stream is not None else self.torch.cuda.current_stream().cuda_stream
+        fluid_run(self.graph.h, self.lplan.h, self.aplan.h, self.arena_ptr, self.aplan.peak,
+                  self._cp, self._ip, self._op, s)
+        return self.outputs

@@ -1,0 +1,218 @@
+"""C-ABI library on the CPU: exported symbols, graph builder, and bit-exact
+parity of the C++ layout and arena planners with the oracle planners on the
+same (synthetic, seeded) cost tables."""
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth_inputs
+from oracle import costtable, graph as OG, layouts, plan_arena as PA, plan_layout as PL
+from paper_2411_09242_amd import fluid as F
+from tables import synthetic_table, write_table
+from tinygraphs import chain_graph, diamond_graph, ffn_block, mlp_graph, t1_graph, t2_graph
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def host_lib():
+    return F.load(host_only=True)
+
+
+def _header_symbols():
+    src = open(os.path.join(ROOT, "include", "fluid.h")).read()
+    return sorted(set(re.findall(r"\b(fluid_[a-z_]+)\s*\(", src)))
+
+
+@pytest.mark.parametrize("name", ["libfluid_host.so", "libfluid.so"])
+def test_library_exports_every_declared_symbol(name):
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(F.LIBDIR, name))
+    syms = _header_symbols()
+    assert len(syms) == 22
+    for s in syms:
+        assert hasattr(lib, s), s
+    assert set(syms) == set(F.SYMBOLS)
+
+
+def _parse(s):
+    return json.loads(s)
+
+
+CFGS = [synth_inputs.config(i) for i in range(1, 6)] + [
+    synth_inputs.config(1, arch="pre_ln", layers=2, seq=19, hidden=36, heads=3, ffn=52),
+    synth_inputs.config(1, arch="llama", layers=2, seq=21, hidden=48, heads=4, ffn=40, dtype="bf16"),
+    synth_inputs.config(1, arch="post_ln", layers=2, batch=3, seq=17, hidden=40, heads=5, ffn=72),
+]
+
+
+@pytest.mark.parametrize("cfg", CFGS, ids=lambda c: f"{c['arch']}-{c['layers']}-{c['seq']}-{c['hidden']}")
+def test_cpp_builder_matches_oracle_builder(cfg):
+    og = OG.build_transformer(cfg)
+    g = F.Graph.transformer(cfg)
+    cpp = g.desc
+    ref = og.export()
+    for k in ("dtype", "inputs", "consts", "outputs"):
+        assert cpp[k] == ref[k], k
+    assert len(cpp["nodes"]) == len(ref["nodes"])
+    for a, b in zip(cpp["nodes"], ref["nodes"]):
+        assert a == b
+    L = layouts.edge_layouts(og)
+    assert [[tuple(p) for p in lst] for lst in cpp["layouts"]] == L
+
+
+def _cpp_graph_from_oracle(og):
+    return F.Graph.from_desc(og.export())
+
+
+def _compare_plans(og, obj, tmp_path, flags=0):
+    path = write_table(obj, tmp_path / "t.json")
+    ct = costtable.load(obj, og)
+    try:
+        ref = PL.plan_layouts(og, ct, flags)
+        ref_err = None
+    except PL.Infeasible as e:
+        ref, ref_err = None, e
+    g = _cpp_graph_from_oracle(og)
+    t = F.CostTable.load(path, g)
+    if ref_err is not None:
+        with pytest.raises(F.FluidError) as ei:
+            F.LayoutPlan(g, t, flags)
+        assert ei.value.status == -3
+        return None
+    lp = F.LayoutPlan(g, t, flags)
+    assert lp.layout_idx == ref.layout_idx
+    assert lp.variant == ref.variant
+    assert lp.total_ns == ref.total
+    assert lp.guard_used == ref.guard_used
+    # arena on the chosen layouts
+    lay = {e: ct.L[e][ref.layout_idx[e]] for e in range(og.n_edges)}
+    for e in range(og.n_edges):
+        assert lp.perm(e) == lay[e]
+    oap = PA.plan_arena(og, lay)
+    ap = F.ArenaPlan(g, lp)
+    assert ap.peak == oap.peak
+    for e in range(og.n_edges):
+        assert ap.root[e] == oap.root[e]
+        r = oap.root[e]
+        assert ap.offset[e] == (oap.offset[r] if r in oap.offset else -1)
+    assert ap.lower_bound == PA.lower_bound(oap.buffers, oap.size, oap.defn, oap.last, len(og.nodes))
+    assert ap.naive == PA.naive_plan(og).peak
+    nv = F.ArenaPlan(g, lp, no_reuse=True)
+    off = 0
+    for b in sorted(oap.buffers):
+        assert nv.offset[b] == off
+        off += oap.size[b]
+    assert nv.peak == off
+    return lp
+
+
+TINY = [t1_graph, t2_graph, diamond_graph, chain_graph, ffn_block, mlp_graph]
+
+
+@pytest.mark.parametrize("builder", TINY, ids=lambda b: b.__name__)
+@pytest.mark.parametrize("mode", ["random", "ties", "identity", "distinct"])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_planner_parity_tiny(builder, mode, seed, tmp_path):
+    og = builder()
+    _compare_plans(og, synthetic_table(og, seed=seed, mode=mode, lo=1, hi=30), tmp_path)
+
+
+@pytest.mark.parametrize("flags", [PL.NO_DP, PL.NO_VARIANTS, PL.NO_GUARD, PL.NO_VARIANTS | PL.NO_GUARD])
+def test_planner_parity_flags(flags, tmp_path):
+    og = t1_graph()
+    _compare_plans(og, synthetic_table(og, seed=5, mode="random", lo=1, hi=30), tmp_path, flags)
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("mode", ["random", "ties"])
+def test_planner_parity_config_graphs(idx, mode, tmp_path):
+    og = OG.build_transformer(synth_inputs.config(idx))
+    _compare_plans(og, synthetic_table(og, seed=idx, mode=mode), tmp_path)
+
+
+def test_ragged_config_parity(tmp_path):
+    cfg = synth_inputs.config(1, arch="llama", layers=2, seq=21, hidden=48, heads=4, ffn=40, dtype="bf16")
+    og = OG.build_transformer(cfg)
+    _compare_plans(og, synthetic_table(og, seed=9, mode="random"), tmp_path)
+
+
+def test_infeasible_table_is_reported(tmp_path):
+    og = chain_graph(3, (2, 3, 4))
+    _compare_plans(og, synthetic_table(og, seed=0, drop_identity_node=1), tmp_path)
+
+
+def test_loader_rejects_bad_tables(tmp_path):
+    og = t1_graph()
+    g = _cpp_graph_from_oracle(og)
+    obj = synthetic_table(og, seed=1)
+    # a view combination with a nonzero cost
+    bad = json.loads(json.dumps(obj))
+    tnode = next(n for n, nd in enumerate(og.nodes) if nd.op == "transpose")
+    sig = bad["sigs"][bad["node_sig"][tnode]]
+    for ent in sig["entries"]:
+        if ent[2] == [0]:
+            ent[2] = [5]
+            break
+    with pytest.raises(F.FluidError) as ei:
+        F.CostTable.load(write_table(bad, tmp_path / "b1.json"), g)
+    assert ei.value.status == -1 and "view" in str(ei.value)
+    # wrong edge count / non-identity first / unknown format
+    for mut in (lambda o: o["edges"].pop(),
+                lambda o: o["edges"][1].reverse(),
+                lambda o: o.__setitem__("format", "x")):
+        bad = json.loads(json.dumps(obj))
+        mut(bad)
+        with pytest.raises(F.FluidError):
+            F.CostTable.load(write_table(bad, tmp_path / "b2.json"), g)
+    # truncated file
+    p = tmp_path / "b3.json"
+    p.write_text(json.dumps(obj)[:100])
+    with pytest.raises(F.FluidError):
+        F.CostTable.load(str(p), g)
+
+
+def test_table_save_load_roundtrip(tmp_path):
+    og = t2_graph()
+    g = _cpp_graph_from_oracle(og)
+    obj = synthetic_table(og, seed=4)
+    t = F.CostTable.load(write_table(obj, tmp_path / "a.json"), g)
+    t.save(str(tmp_path / "b.json"))
+    again = json.load(open(tmp_path / "b.json"))
+    assert again["edges"] == obj["edges"]
+    assert again["node_sig"] == obj["node_sig"]
+    assert [s["entries"] for s in again["sigs"]] == [s["entries"] for s in obj["sigs"]]
+
+
+def test_graph_validation_errors():
+    good = t1_graph().export()
+
+    def build(mut):
+        d = json.loads(json.dumps(good))
+        mut(d)
+        return F.fluid_build_graph(d)
+
+    with pytest.raises(F.FluidError) as e:     # input from a later node
+        build(lambda d: d["nodes"][0]["ins"].__setitem__(0, 5))
+    assert e.value.status == -1
+    with pytest.raises(F.FluidError):          # wrong output shape
+        build(lambda d: d["nodes"][0]["out_shape"].__setitem__(2, 7))
+    with pytest.raises(F.FluidError) as e:     # general reshape
+        build(lambda d: d["nodes"][1].__setitem__("out_shape", [1, 2, 12]))
+    assert e.value.status == -2
+    with pytest.raises(F.FluidError):          # bad constant id
+        build(lambda d: d["nodes"][0]["ins"].__setitem__(1, -99))
+    with pytest.raises(F.FluidError):          # not a permutation
+        build(lambda d: d["nodes"][2].__setitem__("perm", [0, 1, 1, 3]))
+
+
+def test_host_library_gpu_entry_points_are_unsupported():
+    import ctypes as C
+    lib = F.load(host_only=True)
+    st = lib.fluid_run(None, None, None, None, 0, None, None, None, None)
+    assert st == -2
+    st = lib.fluid_measure_costs(None, 1, None, 0, None, None)
+    assert st == -2
