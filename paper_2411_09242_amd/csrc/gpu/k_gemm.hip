@@ -508,7 +508,197 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
     }
 }
 
+// ============================================================== split-K
+// For GEMMs with few output tiles (a 128-token batch gives 24 tiles of
+// 64x64 for a 768-wide projection): W wavefronts of one workgroup share one
+// (32 FM) x (32 FN) output tile and each takes a contiguous 1/W of the K
+// range; partial tiles are summed through LDS at the end (no workspace, no
+// atomics).  Operands go straight from global memory into MFMA registers:
+// within a 16-wide K step, lane group h = lane / 32 owns k0 + 8h .. k0 + 8h + 7
+// (any pairing of k between A and B is valid as long as both use it), so a
+// K-contiguous operand is two 16-byte loads (fp32) or one (bf16) per lane,
+// and an M- or N-contiguous operand is a coalesced 32-lane row access.
+template <typename T, int FM, int FN, int W, bool AVK, bool BVK>
+__global__ __launch_bounds__(64 * W) void gemm_sk_kernel(GemmParams p) {
+  constexpr int TM = 32 * FM, TN = 32 * FN, RP = TN + 1;
+  constexpr bool BF = sizeof(T) == 2;
+  __shared__ float red[W * TM * RP];
+  const TileCoord tc = tile_coord(p, TM, TN);
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int h = lane >> 5, r = lane & 31;
+  const T* A = (const T*)p.A;
+  const T* B = (const T*)p.B;
+  // K slice of this wavefront (multiple of 16 wide)
+  const uint32_t kc = ((p.K + W - 1) / W + 15u) & ~15u;
+  const uint32_t kb = (uint32_t)w * kc;
+  const uint32_t ke = min(p.K, kb + kc);
+  int32_t arow[FM];
+  bool aok[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const uint32_t m = tc.m0 + 32 * i + r;
+    aok[i] = m < p.M;
+    arow[i] = tc.a_base + (aok[i] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+  }
+  int32_t bcol[FN];
+  bool bok[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const uint32_t n = tc.n0 + 32 * j + r;
+    bok[j] = n < p.N;
+    bcol[j] = tc.b_base + (bok[j] ? (int32_t)n * p.b_n : 0);
+  }
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  float fa[2][FM][8], fb[2][FN][8];
+  auto load = [&](int buf, uint32_t k0) {
+    const uint32_t kg = k0 + 8u * h;  // first k of this lane group
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      if constexpr (AVK && !BF) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (aok[i] && kg + 4u * q < ke) v = *(const float4*)((const float*)A + arow[i] + (int32_t)(kg + 4u * q));
+          fa[buf][i][4 * q] = v.x; fa[buf][i][4 * q + 1] = v.y; fa[buf][i][4 * q + 2] = v.z; fa[buf][i][4 * q + 3] = v.w;
+        }
+      } else if constexpr (AVK && BF) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (aok[i] && kg < ke) v = *(const uint4*)((const uint16_t*)A + arow[i] + (int32_t)kg);
+        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          fa[buf][i][2 * q] = __uint_as_float(wv[q] << 16);
+          fa[buf][i][2 * q + 1] = __uint_as_float(wv[q] & 0xffff0000u);
+        }
+      } else {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const uint32_t k = kg + s;
+          fa[buf][i][s] = (aok[i] && k < ke) ? Elem<T>::load(A, arow[i] + (int32_t)k * p.a_k) : 0.f;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      if constexpr (BVK && !BF) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (bok[j] && kg + 4u * q < ke) v = *(const float4*)((const float*)B + bcol[j] + (int32_t)(kg + 4u * q));
+          fb[buf][j][4 * q] = v.x; fb[buf][j][4 * q + 1] = v.y; fb[buf][j][4 * q + 2] = v.z; fb[buf][j][4 * q + 3] = v.w;
+        }
+      } else if constexpr (BVK && BF) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (bok[j] && kg < ke) v = *(const uint4*)((const uint16_t*)B + bcol[j] + (int32_t)kg);
+        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          fb[buf][j][2 * q] = __uint_as_float(wv[q] << 16);
+          fb[buf][j][2 * q + 1] = __uint_as_float(wv[q] & 0xffff0000u);
+        }
+      } else {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const uint32_t k = kg + s;
+          fb[buf][j][s] = (bok[j] && k < ke) ? Elem<T>::load(B, bcol[j] + (int32_t)k * p.b_k) : 0.f;
+        }
+      }
+    }
+  };
+  auto compute = [&](int buf) {
+    if constexpr (BF) {
+      bf16x8 av[FM], bv[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int s = 0; s < 8; ++s) av[i][s] = (__bf16)fa[buf][i][s];
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int s = 0; s < 8; ++s) bv[j][s] = (__bf16)fb[buf][j][s];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[buf][i][s], fb[buf][j][s], acc[i][j], 0, 0, 0);
+    }
+  };
+  // ping-pong with compile-time buffer indices, so that the loads of the
+  // next step stay in flight while the current step's MFMAs run
+  if (kb < ke) {
+    load(0, kb);
+    for (uint32_t k0 = kb;;) {
+      if (k0 + 16u < ke) load(1, k0 + 16u);
+      compute(0);
+      k0 += 16u;
+      if (k0 >= ke) break;
+      if (k0 + 16u < ke) load(0, k0 + 16u);
+      compute(1);
+      k0 += 16u;
+      if (k0 >= ke) break;
+    }
+  }
+  // partial tiles -> LDS, then each thread sums W partials for its outputs
+  float* mine = red + w * TM * RP;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = 32 * i + 8 * (v / 4) + 4 * h + (v % 4);
+        mine[m * RP + 32 * j + r] = acc[i][j][v];
+      }
+  __syncthreads();
+  const bool ncontig = p.c_n == 1;
+  for (int e = tid; e < TM * TN; e += 64 * W) {
+    const int ml = ncontig ? e / TN : e % TM;
+    const int nl = ncontig ? e % TN : e / TM;
+    const uint32_t m = tc.m0 + ml, n = tc.n0 + nl;
+    if (m >= p.M || n >= p.N) continue;
+    float sum = 0.f;
+#pragma unroll
+    for (int q = 0; q < W; ++q) sum += red[q * TM * RP + ml * RP + nl];
+    Elem<T>::store(p.C, tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n * p.c_n, sum);
+  }
+}
+
 namespace {
+
+template <typename T, int FM, int FN, int W>
+hipError_t gemm_sk_go(const NodeKernel& k, hipStream_t s) {
+  const GemmParams& p = k.gemm;
+  const dim3 grid(p.tiles_m * p.tiles_n * p.G);
+  const bool avk = k.amode == GM_K, bvk = k.bmode == GM_K;
+  if (avk && bvk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, true, true>), grid, dim3(64 * W), 0, s, p);
+  else if (avk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, true, false>), grid, dim3(64 * W), 0, s, p);
+  else if (bvk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, false, true>), grid, dim3(64 * W), 0, s, p);
+  else hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, false, false>), grid, dim3(64 * W), 0, s, p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t gemm_sk_dispatch(const NodeKernel& k, hipStream_t s) {
+  switch (k.gemm_tile) {
+    case 2: return gemm_sk_go<T, 1, 1, 4>(k, s);
+    case 3: return gemm_sk_go<T, 1, 1, 8>(k, s);
+    default: return gemm_sk_go<T, 2, 1, 4>(k, s);
+  }
+}
 
 template <int T, int AM, int BMD>
 hipError_t gemm_go(const NodeKernel& k, hipStream_t s) {
@@ -542,6 +732,7 @@ hipError_t gemm_a(const NodeKernel& k, hipStream_t s) {
 hipError_t launch_gemm(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   if ((uint64_t)p.tiles_m * p.tiles_n * p.G >= (1ull << 31)) return hipErrorInvalidValue;
+  if (k.gemm_tile >= 2) return k.dtype == DT_BF16 ? gemm_sk_dispatch<uint16_t>(k, s) : gemm_sk_dispatch<float>(k, s);
   return k.gemm_tile == 0 ? gemm_a<128>(k, s) : gemm_a<64>(k, s);
 }
 

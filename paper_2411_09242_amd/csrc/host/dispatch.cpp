@@ -22,7 +22,7 @@ std::vector<int64_t> row_major_strides(const Shape& s) {
 
 int num_variants(int op) {
   switch (op) {
-    case FLUID_OP_MATMUL: return 2;
+    case FLUID_OP_MATMUL: return 5;
     case FLUID_OP_GELU:
     case FLUID_OP_SILU:
     case FLUID_OP_TRANSPOSE:
@@ -346,9 +346,12 @@ NodeKernel prepare_gemm(const Node&, int variant, int dtype, const std::vector<O
     k.cmode = 2;
   p.cmode = k.cmode;
   k.gemm_tile = variant;
-  const uint32_t T = variant == 0 ? 128 : 64;
-  p.tiles_m = (p.M + T - 1) / T;
-  p.tiles_n = (p.N + T - 1) / T;
+  // tile sizes: 0: 128x128, 1: 64x64 (LDS-staged); 2, 3: 32x32 and 4: 64x32
+  // with the K range split over the workgroup's wavefronts
+  static const uint32_t TM[] = {128, 64, 32, 32, 64};
+  static const uint32_t TN[] = {128, 64, 32, 32, 32};
+  p.tiles_m = (p.M + TM[variant] - 1) / TM[variant];
+  p.tiles_n = (p.N + TN[variant] - 1) / TN[variant];
   k.available = true;
   return k;
 }
@@ -383,9 +386,11 @@ std::string NodeKernel::name() const {
     case KF_ROPE: return "rope_" + dt;
     case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt;
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
-    case KF_GEMM:
-      return "gemm_" + dt + "_t" + std::to_string(gemm_tile == 0 ? 128 : 64) + "_a" + gm[amode] +
-             "_b" + gm[bmode] + "_c" + (cmode == 1 ? "n" : cmode == 2 ? "m" : "g");
+    case KF_GEMM: {
+      static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4"};
+      return "gemm_" + dt + "_" + tiles[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
+             (cmode == 1 ? "n" : cmode == 2 ? "m" : "g");
+    }
   }
   return "?";
 }

@@ -392,3 +392,18 @@ class Executor:
         fluid_run(self.graph.h, self.lplan.h, self.aplan.h, self.arena_ptr, self.aplan.peak,
                   self._cp, self._ip, self._op, s)
         return self.outputs
+
+    def capture(self, steps=1):
+        """Record ``steps`` consecutive fluid_run calls into one HIP graph
+        (torch.cuda.CUDAGraph); replaying it re-issues the same launches
+        with one submission.  fluid_run only launches kernels, so the graph
+        holds kernel nodes (plus event nodes while tracing)."""
+        torch = self.torch
+        graph = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.graph(graph, stream=s):
+            for _ in range(steps):
+                self.run(s.cuda_stream)
+        torch.cuda.current_stream().wait_stream(s)
+        return graph

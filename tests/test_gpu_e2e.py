@@ -1,0 +1,105 @@
+"""End-to-end parity on the GPU: whole transformer graphs, layout plan from a
+cost table measured on the GPU, Greedy-by-Size arena, run through fluid_run,
+compared with the oracle's row-major execution of the same seeded inputs."""
+import numpy as np
+import pytest
+
+import synth_inputs
+from gpu_util import assert_close, forced_table, say
+from oracle import execute, graph as OG, layouts
+
+pytestmark = pytest.mark.gpu
+
+
+def _device_run(cfg, x, consts, table=None, flags=0, no_reuse=False, graph=None):
+    import torch
+    from paper_2411_09242_amd import fluid as F
+    g = graph if graph is not None else F.Graph.transformer(cfg)
+    t = table(g) if callable(table) else (table or F.CostTable.measure(g, reps=3))
+    lp = F.LayoutPlan(g, t, flags)
+    ap = F.ArenaPlan(g, lp, no_reuse=no_reuse)
+    assert ap.lower_bound <= ap.peak <= (ap.naive if not no_reuse else ap.peak)
+    ex = F.Executor(g, lp, ap, consts, [x])
+    ex.arena.fill_(0xFF)
+    ex.outputs[0].fill_(float("nan"))
+    out = ex.run()[0]
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy().astype(np.float64), g, lp, ap, t
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3])
+def test_config_planned_and_naive_match_oracle(idx):
+    cfg = synth_inputs.config(idx)
+    og = OG.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), idx)
+    say(f"cfg{idx}: oracle")
+    (ref,) = execute.run_canonical(og, [x], consts)
+    say(f"cfg{idx}: measure + plan + run")
+    out, g, lp, ap, t = _device_run(cfg, x, consts)
+    say(f"cfg{idx}: planned total {lp.total_ns} ns guard {lp.guard_used} peak {ap.peak} naive {ap.naive}")
+    err = assert_close(out, ref, cfg["dtype"], f"cfg{idx} planned")
+    say(f"cfg{idx}: planned max abs err {err:.3g}")
+    from paper_2411_09242_amd import fluid as F
+    out2, *_ = _device_run(cfg, x, consts, table=t, graph=g, flags=F.NO_DP, no_reuse=True)
+    assert_close(out2, ref, cfg["dtype"], f"cfg{idx} naive")
+
+
+@pytest.mark.parametrize("arch,dtype", [("post_ln", "f32"), ("pre_ln", "f32"), ("llama", "f32"), ("llama", "bf16")])
+def test_ragged_small_stacks(arch, dtype):
+    cfg = synth_inputs.config(1, arch=arch, dtype=dtype, layers=2, batch=2, seq=37, hidden=72, heads=3, ffn=100)
+    og = OG.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), 11)
+    (ref,) = execute.run_canonical(og, [x], consts)
+    out, *_ = _device_run(cfg, x, consts)
+    assert_close(out, ref, dtype, f"{arch} {dtype}")
+
+
+@pytest.mark.parametrize("idx", [1, 2])
+def test_hip_graph_replay_matches_eager(idx):
+    """fluid_run captured into a HIP graph: every replay, with eager work and
+    synchronisation between replays (arena re-poisoned each time), gives the
+    eager result bit for bit."""
+    import torch
+    from paper_2411_09242_amd import fluid as F
+    cfg = synth_inputs.config(idx)
+    g = F.Graph.transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, g.const_specs(), idx)
+    t = F.CostTable.measure(g, reps=2)
+    lp = F.LayoutPlan(g, t)
+    ap = F.ArenaPlan(g, lp)
+    ex = F.Executor(g, lp, ap, consts, [x])
+    ref = ex.run()[0].clone()
+    torch.cuda.synchronize()
+    graph = ex.capture(steps=2)
+    for rep in range(4):
+        ex.arena.fill_(0xFF)
+        ex.outputs[0].fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(ex.outputs[0], ref), f"replay {rep}"
+        # eager run in between
+        ex.run()
+        torch.cuda.synchronize()
+        assert torch.equal(ex.outputs[0], ref)
+
+
+def test_random_forced_layouts_on_one_layer(tmp_path):
+    """Many random layout assignments of the one-layer encoder: every kernel
+    family meets many stride patterns inside the real graph."""
+    import json
+    from paper_2411_09242_amd import fluid as F
+    cfg = synth_inputs.config(1)
+    og = OG.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), 1)
+    (ref,) = execute.run_canonical(og, [x], consts)
+    L = layouts.edge_layouts(og)
+    rng = np.random.default_rng(3)
+    for trial in range(40):
+        want = {e: L[e][int(rng.integers(0, len(L[e])))] for e in range(og.n_edges) if len(L[e]) > 1}
+        obj = forced_table(og, want)
+        path = tmp_path / f"t{trial}.json"
+        path.write_text(json.dumps(obj))
+        say(f"forced trial {trial}")
+        out, *_ = _device_run(cfg, x, consts, table=lambda gg: F.CostTable.load(str(path), gg))
+        assert_close(out, ref, "f32", f"trial {trial}")

@@ -1,0 +1,56 @@
+"""Parity at the two largest workload sizes, in the benchmark's launch
+configuration (GPU-measured cost table, planned layouts, Greedy-by-Size
+arena, fluid_run): the 24-layer BERT-large-shaped encoder (batch 8, seq 512,
+fp32) and the 8-layer Llama-style decoder (seq 2048, hidden 4096, bf16).
+
+The oracle needs minutes on the host for these, so its output is stored as
+a sample of whole output rows plus whole-output statistics
+(tests/golden/oracle_rows_cfg{4,5}.npz, written by tests/golden/make_golden.py
+from the oracle alone).  Sampled rows are compared element by element; the
+statistics check every element at once."""
+import os
+
+import numpy as np
+import pytest
+
+import synth_inputs
+from gpu_util import assert_close, say
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.mark.parametrize("idx", [4, 5])
+def test_large_config_matches_oracle_samples(idx):
+    import torch
+    from paper_2411_09242_amd import fluid as F
+    gold = np.load(os.path.join(HERE, "golden", f"oracle_rows_cfg{idx}.npz"), allow_pickle=False)
+    cfg = synth_inputs.config(idx)
+    say(f"cfg{idx}: inputs")
+    g = F.Graph.transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, g.const_specs(), idx)
+    say(f"cfg{idx}: measuring the cost table")
+    t = F.CostTable.measure(g, reps=2)
+    lp = F.LayoutPlan(g, t)
+    ap = F.ArenaPlan(g, lp)
+    say(f"cfg{idx}: plan {lp.total_ns} ns (guard {lp.guard_used}); arena {ap.peak / 2**20:.1f} MiB "
+        f"(naive {ap.naive / 2**20:.1f}, lower bound {ap.lower_bound / 2**20:.1f})")
+    assert ap.lower_bound <= ap.peak < ap.naive
+    ex = F.Executor(g, lp, ap, consts, [x])
+    del consts
+    ex.arena.fill_(0xFF)
+    ex.outputs[0].fill_(float("nan"))
+    y = ex.run()[0]
+    torch.cuda.synchronize()
+    y = y.float().cpu().numpy().astype(np.float64)
+    assert tuple(y.shape) == tuple(gold["shape"])
+    assert np.isfinite(y).all()
+    rows = gold["rows"]
+    got = y[rows[:, 0], rows[:, 1], :]
+    err = assert_close(got, gold["values"].astype(np.float64), cfg["dtype"], f"cfg{idx} sampled rows")
+    say(f"cfg{idx}: {len(rows)} sampled rows within tolerance, max abs err {err:.3g}")
+    # whole-output statistics (every element enters these sums)
+    rtol = 1e-5 if cfg["dtype"] == "f32" else 2e-3
+    assert abs(np.abs(y).mean() - float(gold["mean_abs"])) <= rtol * float(gold["mean_abs"])
+    assert abs((y * y).sum() - float(gold["sumsq"])) <= rtol * float(gold["sumsq"])
+    assert abs(y.mean() - float(gold["mean"])) <= 1e-3
