@@ -90,49 +90,28 @@ def cpu_baseline(cfg, budget_s=20.0):
             "sample": f"whole {cfg['layers']}-layer graph, {len(times)} run(s), median; float64 NumPy"}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2)
-    ap.add_argument("--reps", type=int, default=7, help="timed launches per cost-table entry")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--save-table", default=None)
-    a = ap.parse_args()
-    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(see DESIGN.md for how the graph would shard).", file=sys.stderr)
-        sys.exit(2)
-
-    import torch
-    import synth_inputs
-    from paper_2411_09242_amd import fluid as F
-
-    F.load()
-    cfg = synth_inputs.config(a.config)
+def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=None):
+    """Cost table (untimed), plans, then the two timed regions; returns a dict."""
     g = F.Graph.transformer(cfg)
-    log(f"workload {cfg['name']}: {g.n_nodes} nodes, {g.n_edges} edges")
-    x, consts = synth_inputs.make_inputs(cfg, g.const_specs(), a.config)
-    torch.cuda.init()
     stream = torch.cuda.current_stream().cuda_stream
-
     t = time.time()
-    table = F.CostTable.measure(g, reps=a.reps)
-    log(f"cost table measured in {time.time() - t:.1f} s")
-    if a.save_table:
-        table.save(a.save_table)
+    table = F.CostTable.measure(g, reps=reps)
+    t_measure = time.time() - t
+    log(f"{cfg['name']}: cost table measured in {t_measure:.1f} s")
+    if save_table:
+        table.save(save_table)
     lp = F.LayoutPlan(g, table)
     apl = F.ArenaPlan(g, lp)
     lp_naive = F.LayoutPlan(g, table, F.NO_DP)
     ap_naive = F.ArenaPlan(g, lp_naive, no_reuse=True)
     ex = F.Executor(g, lp, apl, consts, [x])
     ex_naive = F.Executor(g, lp_naive, ap_naive, consts, [x])
+    del consts
     n_launch = sum(1 for v in lp.variant if v >= 0)
     n_launch_naive = sum(1 for v in lp_naive.variant if v >= 0)
 
     # warm-up, then find the dominant kernel (largest summed time) untimed
-    for _ in range(a.warmup):
+    for _ in range(warmup):
         ex.run(stream)
         ex_naive.run(stream)
     torch.cuda.synchronize()
@@ -158,12 +137,12 @@ def main():
 
     # timed region 1: K eager steps, HIP events around every launch of the
     # dominant kernel (on the stream it is launched on) -> its duration
-    F.fluid_trace_enable(g.h, mask, len(dom_nodes) * a.steps + 8)
-    ms_eager = time_steps(ex, a.steps, stream, torch)
+    F.fluid_trace_enable(g.h, mask, len(dom_nodes) * steps + 8)
+    ms_eager = time_steps(ex, steps, stream, torch)
     tms, tcnt = F.fluid_trace_collect(g.h, g.n_nodes)
     # timed region 2 (the reported latency): the same K steps captured into
     # one HIP graph; one warm-up replay, then one timed replay
-    hg = ex.capture(steps=a.steps)
+    hg = ex.capture(steps=steps)
     hg.replay()
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -171,17 +150,18 @@ def main():
     hg.replay()
     ev1.record()
     torch.cuda.synchronize()
-    ms_step = ev0.elapsed_time(ev1) / a.steps
-    hg_naive = ex_naive.capture(steps=a.steps)
+    ms_step = ev0.elapsed_time(ev1) / steps
+    del hg
+    hg_naive = ex_naive.capture(steps=steps)
     hg_naive.replay()
     torch.cuda.synchronize()
     ev0.record()
     hg_naive.replay()
     ev1.record()
     torch.cuda.synchronize()
-    ms_naive = ev0.elapsed_time(ev1) / a.steps
-    ms_naive_eager = time_steps(ex_naive, a.steps, stream, torch)
-    del hg, hg_naive
+    ms_naive = ev0.elapsed_time(ev1) / steps
+    del hg_naive
+    ms_naive_eager = time_steps(ex_naive, steps, stream, torch)
 
     kind, work = node_work(g, dom_nodes[0])
     launches = sum(tcnt[n] for n in dom_nodes)
@@ -199,31 +179,108 @@ def main():
                  "avg_launch_us": round(avg_ms * 1e3, 3), "launches": launches,
                  "work_per_launch": work, "work_unit": "flop" if kind == "flop" else "byte"})
 
-    # parity spot check of this run against the naive plan (same kernels library)
+    # planned vs naive outputs (same inputs, different layouts and kernels)
     out = ex.run(stream)[0].float()
     out_n = ex_naive.run(stream)[0].float()
     torch.cuda.synchronize()
     agree = float((out - out_n).abs().max().item())
+    res = {
+        "ms_per_step": round(ms_step, 4), "eager_ms": round(ms_eager, 4),
+        "naive_ms": round(ms_naive, 4), "naive_eager_ms": round(ms_naive_eager, 4),
+        "speedup_vs_naive": round(ms_naive / ms_step, 3),
+        "peak_arena_mb": round(apl.peak / 2**20, 3), "naive_arena_mb": round(ap_naive.peak / 2**20, 3),
+        "max_live_lower_bound_mb": round(apl.lower_bound / 2**20, 3),
+        "launches_per_step": n_launch, "naive_launches_per_step": n_launch_naive,
+        "plan_table_ns": lp.total_ns, "naive_table_ns": lp_naive.total_ns, "guard_used": lp.guard_used,
+        "planned_vs_naive_max_abs_diff": agree, "cost_table_s": round(t_measure, 1),
+        "roofline": roof,
+    }
+    del ex, ex_naive
+    torch.cuda.empty_cache()
+    return res
 
+
+def device_inputs(torch, F, cfg, seed):
+    """Synthetic inputs drawn on the GPU (same distributions as the seeded
+    host recipe: x ~ N(0,1), weights 0.02 N(0,1), biases/beta 0, gamma 1,
+    RoPE tables from positions); used for the extra workloads to keep the
+    benchmark short.  Timing does not depend on the values."""
+    import synth_inputs
+    g = F.Graph.transformer(cfg)
+    dt = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    x = torch.randn((cfg["batch"], cfg["seq"], cfg["hidden"]), generator=gen, device="cuda").to(dt)
+    consts = []
+    for c in g.desc["consts"]:
+        shape, role = tuple(c["shape"]), c["role"]
+        cdt = torch.bfloat16 if c["dtype"] == "bf16" else torch.float32
+        if role == "weight":
+            a = (0.02 * torch.randn(shape, generator=gen, device="cuda")).to(cdt)
+        elif role == "gamma":
+            a = torch.ones(shape, device="cuda", dtype=cdt)
+        elif role in ("rope_cos", "rope_sin"):
+            c_, s_ = synth_inputs.rope_tables(shape[0], 2 * shape[1], cfg.get("rope_base", 10000.0))
+            a = torch.from_numpy(c_ if role == "rope_cos" else s_).cuda()
+        else:
+            a = torch.zeros(shape, device="cuda", dtype=cdt)
+        consts.append(a)
+    return x, consts
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--extra", default="3,4,5", help="extra workloads to report ('' for none)")
+    ap.add_argument("--reps", type=int, default=7, help="timed launches per cost-table entry")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--save-table", default=None)
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(see DESIGN.md for how the graph would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth_inputs
+    from paper_2411_09242_amd import fluid as F
+
+    F.load()
+    torch.cuda.init()
+    cfg = synth_inputs.config(a.config)
+    log(f"workload {cfg['name']}")
+    x, consts = synth_inputs.make_inputs(cfg, F.Graph.transformer(cfg).const_specs(), a.config)
+    r = measure_workload(F, torch, cfg, x, consts, a.steps, a.warmup, a.reps, a.save_table)
     res = {
         "metric": "graph latency (ms) + peak arena MB vs naive plan; kernel % of roofline",
-        "value": round(ms_step, 4), "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
-        "ms_per_step": round(ms_step, 4), "higher_is_better": False, "scaling": "weak",
-        "vs_baseline": None, "dtype": g.dtype, "data": "synthetic",
+        "value": r["ms_per_step"], "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": r["ms_per_step"], "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg["dtype"], "data": "synthetic",
         "config": {"workload": cfg["name"], "arch": cfg["arch"], "layers": cfg["layers"],
                    "batch": cfg["batch"], "seq": cfg["seq"], "hidden": cfg["hidden"],
                    "heads": cfg["heads"], "ffn": cfg["ffn"], "parallelism": "none (1 GPU)"},
         "timing": "value: K steps captured in one HIP graph, one timed replay; roofline kernel "
                   "durations: HIP events around each dominant-kernel launch in a K-step eager region",
-        "eager_ms": round(ms_eager, 4), "naive_eager_ms": round(ms_naive_eager, 4),
-        "naive_ms": round(ms_naive, 4), "speedup_vs_naive": round(ms_naive / ms_step, 3),
-        "peak_arena_mb": round(apl.peak / 2**20, 3), "naive_arena_mb": round(ap_naive.peak / 2**20, 3),
-        "max_live_lower_bound_mb": round(apl.lower_bound / 2**20, 3),
-        "launches_per_step": n_launch, "naive_launches_per_step": n_launch_naive,
-        "plan_table_ns": lp.total_ns, "naive_table_ns": lp_naive.total_ns, "guard_used": lp.guard_used,
-        "planned_vs_naive_max_abs_diff": agree,
-        "roofline": roof,
     }
+    res.update({k: v for k, v in r.items() if k != "ms_per_step"})
+    extras = {}
+    for idx in [int(s) for s in a.extra.split(",") if s.strip()]:
+        if idx == a.config:
+            continue
+        c = synth_inputs.config(idx)
+        log(f"extra workload {c['name']}")
+        xe, ce = device_inputs(torch, F, c, idx)
+        st = max(5, a.steps // 5) if idx in (4, 5) else a.steps
+        e = measure_workload(F, torch, c, xe, ce, st, max(2, a.warmup // 5), max(2, a.reps // 2))
+        e.update({"workload": c["name"], "dtype": c["dtype"], "steps": st,
+                  "data": "synthetic, drawn on the GPU"})
+        extras[f"cfg{idx}"] = e
+        del xe, ce
+        torch.cuda.empty_cache()
+    if extras:
+        res["extra_workloads"] = extras
     if not a.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         res["cpu_baseline"] = cpu_baseline(cfg)

@@ -1,0 +1,84 @@
+// Helpers shared by the GEMM kernels: tile coordinates, two-level row
+// offsets, MFMA vector types.
+#pragma once
+
+#include "dev.h"
+
+namespace fluid {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+struct TileCoord {
+  uint32_t m0, n0;
+  int32_t a_base, b_base, c_base;
+};
+
+// Workgroup -> (batch, tile row, tile column), row-major over tiles.
+__device__ __forceinline__ TileCoord tile_coord(const GemmParams& p, uint32_t BM, uint32_t BN) {
+  const uint32_t per_g = p.tiles_m * p.tiles_n;
+  const uint32_t bid = blockIdx.x;
+  const uint32_t g = bid / per_g;
+  const uint32_t r = bid - g * per_g;
+  const uint32_t tm = r / p.tiles_n;
+  const uint32_t tn = r - tm * p.tiles_n;
+  const uint32_t g1 = fdiv(g, p.g2div);
+  const uint32_t g2 = g - g1 * p.G2;
+  TileCoord t;
+  t.m0 = tm * BM;
+  t.n0 = tn * BN;
+  t.a_base = (int32_t)g1 * p.a_g1 + (int32_t)g2 * p.a_g2;
+  t.b_base = (int32_t)g1 * p.b_g1 + (int32_t)g2 * p.b_g2;
+  t.c_base = (int32_t)g1 * p.c_g1 + (int32_t)g2 * p.c_g2;
+  return t;
+}
+
+// Offset of row m of A (or C) given the two-level row decomposition.
+__device__ __forceinline__ int32_t row_off(const GemmParams& p, uint32_t m, int32_t s1, int32_t s2) {
+  const uint32_t m1 = fdiv(m, p.m2div);
+  return (int32_t)m1 * s1 + (int32_t)(m - m1 * p.M2) * s2;
+}
+
+// Four rows of four bf16 (rows[t] = elements 0..3 at k + t) -> four rows of
+// four k (out[j] = k .. k+3 of element j).
+__device__ __forceinline__ void transpose4x4_b16(const uint2* rows, uint2* out) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t e[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const uint32_t w = (j < 2) ? rows[t].x : rows[t].y;
+      e[t] = (j & 1) ? (w >> 16) : (w & 0xffffu);
+    }
+    out[j] = make_uint2(e[0] | (e[1] << 16), e[2] | (e[3] << 16));
+  }
+}
+
+// Writes the four transposed rows out[0..3] to LDS rows row0 .. row0+3
+// (pitch kp elements) at column kcol.
+__device__ __forceinline__ void store_rows4(uint16_t* lds, int row0, int kp, int kcol, const uint2* out) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) *(uint2*)&lds[(row0 + j) * kp + kcol] = out[j];
+}
+
+// Staging a 32-deep K-tile through LDS rows of pitch 40 elements (80 bytes).
+// Thread index -> (row, k) of the piece a thread carries:
+//  * K-contiguous operand, 16-byte pieces of 8 k: sixteen consecutive
+//    threads take sixteen consecutive rows at one k, so the 16-byte LDS
+//    writes of a wavefront hit every bank once (rows 80 bytes apart cover
+//    all bank groups); a row's four pieces still come from one 64-byte span
+//    of HBM within the same wavefront.
+//  * M-/N-contiguous operand, 4 x 4 blocks: eight consecutive threads take
+//    the eight k-groups of one 4-row block, so the 8-byte row writes after
+//    the in-register transpose spread over all banks instead of landing
+//    rows 4 x 80 bytes apart on the same few banks.
+__device__ __forceinline__ void kpiece_coord(int idx, int& row, int& k) {
+  row = (idx & 15) + 16 * (idx >> 6);
+  k = ((idx >> 4) & 3) * 8;
+}
+__device__ __forceinline__ void mnblock_coord(int idx, int& row, int& k) {
+  row = (idx >> 3) * 4;
+  k = (idx & 7) * 4;
+}
+
+}  // namespace fluid

@@ -15,42 +15,10 @@
 // k-group l/32) with fp32 accumulation.  Accumulator v of lane l holds
 // C[8(v/4) + 4(l/32) + v%4][l%32].  The next K-tile is loaded into
 // registers while the current one is multiplied.
-#include "dev.h"
+#include "gemm_common.h"
 #include "launch.h"
 
 namespace fluid {
-
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
-struct TileCoord {
-  uint32_t m0, n0;
-  int32_t a_base, b_base, c_base;
-};
-
-__device__ __forceinline__ TileCoord tile_coord(const GemmParams& p, uint32_t BM, uint32_t BN) {
-  const uint32_t per_g = p.tiles_m * p.tiles_n;
-  const uint32_t bid = blockIdx.x;
-  const uint32_t g = bid / per_g;
-  const uint32_t r = bid - g * per_g;
-  const uint32_t tm = r / p.tiles_n;
-  const uint32_t tn = r - tm * p.tiles_n;
-  const uint32_t g1 = fdiv(g, p.g2div);
-  const uint32_t g2 = g - g1 * p.G2;
-  TileCoord t;
-  t.m0 = tm * BM;
-  t.n0 = tn * BN;
-  t.a_base = (int32_t)g1 * p.a_g1 + (int32_t)g2 * p.a_g2;
-  t.b_base = (int32_t)g1 * p.b_g1 + (int32_t)g2 * p.b_g2;
-  t.c_base = (int32_t)g1 * p.c_g1 + (int32_t)g2 * p.c_g2;
-  return t;
-}
-
-// Offset of row m of A (or C) given the two-level row decomposition.
-__device__ __forceinline__ int32_t row_off(const GemmParams& p, uint32_t m, int32_t s1, int32_t s2) {
-  const uint32_t m1 = fdiv(m, p.m2div);
-  return (int32_t)m1 * s1 + (int32_t)(m - m1 * p.M2) * s2;
-}
 
 // ============================================================== fp32
 template <int BM, int BN, int AM, int BMD>
@@ -296,8 +264,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
     for (int r = 0; r < A_CH; ++r) {
       const int idx = tid + 256 * r;
-      a_m[r] = idx / (BK / 8);
-      a_k[r] = (idx % (BK / 8)) * 8;
+      kpiece_coord(idx, a_m[r], a_k[r]);
       const uint32_t m = tc.m0 + a_m[r];
       a_ok[r] = m < p.M;
       a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
@@ -306,8 +273,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
     for (int r = 0; r < A_BL; ++r) {
       const int idx = tid + 256 * r;
-      a_m[r] = (idx % (BM / 4)) * 4;
-      a_k[r] = (idx / (BM / 4)) * 4;
+      mnblock_coord(idx, a_m[r], a_k[r]);
       const uint32_t m = tc.m0 + a_m[r];
       a_ok[r] = m < p.M;
       a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
@@ -332,16 +298,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
     for (int r = 0; r < B_CH; ++r) {
       const int idx = tid + 256 * r;
-      b_n[r] = idx / (BK / 8);
-      b_k[r] = (idx % (BK / 8)) * 8;
+      kpiece_coord(idx, b_n[r], b_k[r]);
       b_ok[r] = tc.n0 + b_n[r] < p.N;
     }
   } else if constexpr (BMD == GM_MN && B_BL > 0) {
 #pragma unroll
     for (int r = 0; r < B_BL; ++r) {
       const int idx = tid + 256 * r;
-      b_n[r] = (idx % (BN / 4)) * 4;
-      b_k[r] = (idx / (BN / 4)) * 4;
+      mnblock_coord(idx, b_n[r], b_k[r]);
       b_ok[r] = tc.n0 + b_n[r] < p.N;
     }
   } else {
@@ -412,19 +376,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
       }
     }
   };
-  // rows[t] holds 4 elements (one per m|n) at k + t; emit 4 rows of 4 k
-  auto transpose4 = [](const uint2* rows, uint2* out) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      uint32_t e[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const uint32_t w = (j < 2) ? rows[t].x : rows[t].y;
-        e[t] = (j & 1) ? (w >> 16) : (w & 0xffffu);
-      }
-      out[j] = make_uint2(e[0] | (e[1] << 16), e[2] | (e[3] << 16));
-    }
-  };
   auto lstore = [&]() {
     if constexpr (A_VEC_K) {
 #pragma unroll
@@ -433,9 +384,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < A_BL; ++r) {
         uint2 o[4];
-        transpose4(&ba[4 * r], o);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) *(uint2*)&As[(a_m[r] + j) * KP + a_k[r]] = o[j];
+        transpose4x4_b16(&ba[4 * r], o);
+        store_rows4(As, a_m[r], KP, a_k[r], o);
       }
     } else {
 #pragma unroll
@@ -448,9 +398,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < B_BL; ++r) {
         uint2 o[4];
-        transpose4(&bb[4 * r], o);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) *(uint2*)&Bs[(b_n[r] + j) * KP + b_k[r]] = o[j];
+        transpose4x4_b16(&bb[4 * r], o);
+        store_rows4(Bs, b_n[r], KP, b_k[r], o);
       }
     } else {
 #pragma unroll
@@ -508,19 +457,25 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
     }
 }
 
+// (the large-tile, deeply pipelined bf16 kernel lives in k_gemm_bf16.hip)
+
 // ============================================================== split-K
 // For GEMMs with few output tiles (a 128-token batch gives 24 tiles of
 // 64x64 for a 768-wide projection): W wavefronts of one workgroup share one
 // (32 FM) x (32 FN) output tile and each takes a contiguous 1/W of the K
 // range; partial tiles are summed through LDS at the end (no workspace, no
 // atomics).  Operands go straight from global memory into MFMA registers:
-// within a 16-wide K step, lane group h = lane / 32 owns k0 + 8h .. k0 + 8h + 7
-// (any pairing of k between A and B is valid as long as both use it), so a
-// K-contiguous operand is two 16-byte loads (fp32) or one (bf16) per lane,
-// and an M- or N-contiguous operand is a coalesced 32-lane row access.
-template <typename T, int FM, int FN, int W, bool AVK, bool BVK>
+// within each 16-wide K step, lane group h = lane / 32 owns k0 + 8h .. k0 +
+// 8h + 7 (any pairing of k between A and B is valid as long as both use it),
+// so a K-contiguous operand is two 16-byte loads (fp32) or one (bf16) per
+// lane, and an M- or N-contiguous operand is a coalesced 32-lane row access.
+// Each iteration covers U such steps and the next iteration's loads are
+// issued before the current MFMAs (ping-pong registers with compile-time
+// indices), so 2 x 16U K-values per wavefront are in flight.
+template <typename T, int FM, int FN, int W, int U, bool AVK, bool BVK>
 __global__ __launch_bounds__(64 * W) void gemm_sk_kernel(GemmParams p) {
   constexpr int TM = 32 * FM, TN = 32 * FN, RP = TN + 1;
+  constexpr int KI = 16 * U;  // K values per iteration
   constexpr bool BF = sizeof(T) == 2;
   __shared__ float red[W * TM * RP];
   const TileCoord tc = tile_coord(p, TM, TN);
@@ -556,99 +511,103 @@ __global__ __launch_bounds__(64 * W) void gemm_sk_kernel(GemmParams p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  float fa[2][FM][8], fb[2][FN][8];
-  auto load = [&](int buf, uint32_t k0) {
-    const uint32_t kg = k0 + 8u * h;  // first k of this lane group
+  float fa0[FM][U][8], fb0[FN][U][8], fa1[FM][U][8], fb1[FN][U][8];
+  auto load = [&](float (&fa)[FM][U][8], float (&fb)[FN][U][8], uint32_t k0) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      if constexpr (AVK && !BF) {
+    for (int u = 0; u < U; ++u) {
+      const uint32_t kg = k0 + 16u * u + 8u * h;  // first k of this lane group
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (aok[i] && kg + 4u * q < ke) v = *(const float4*)((const float*)A + arow[i] + (int32_t)(kg + 4u * q));
-          fa[buf][i][4 * q] = v.x; fa[buf][i][4 * q + 1] = v.y; fa[buf][i][4 * q + 2] = v.z; fa[buf][i][4 * q + 3] = v.w;
-        }
-      } else if constexpr (AVK && BF) {
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (aok[i] && kg < ke) v = *(const uint4*)((const uint16_t*)A + arow[i] + (int32_t)kg);
-        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+      for (int i = 0; i < FM; ++i) {
+        if constexpr (AVK && !BF) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          fa[buf][i][2 * q] = __uint_as_float(wv[q] << 16);
-          fa[buf][i][2 * q + 1] = __uint_as_float(wv[q] & 0xffff0000u);
-        }
-      } else {
+          for (int q = 0; q < 2; ++q) {
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (aok[i] && kg + 4u * q < ke) v = *(const float4*)((const float*)A + arow[i] + (int32_t)(kg + 4u * q));
+            fa[i][u][4 * q] = v.x; fa[i][u][4 * q + 1] = v.y; fa[i][u][4 * q + 2] = v.z; fa[i][u][4 * q + 3] = v.w;
+          }
+        } else if constexpr (AVK && BF) {
+          uint4 v = make_uint4(0, 0, 0, 0);
+          if (aok[i] && kg < ke) v = *(const uint4*)((const uint16_t*)A + arow[i] + (int32_t)kg);
+          const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const uint32_t k = kg + s;
-          fa[buf][i][s] = (aok[i] && k < ke) ? Elem<T>::load(A, arow[i] + (int32_t)k * p.a_k) : 0.f;
+          for (int q = 0; q < 4; ++q) {
+            fa[i][u][2 * q] = __uint_as_float(wv[q] << 16);
+            fa[i][u][2 * q + 1] = __uint_as_float(wv[q] & 0xffff0000u);
+          }
+        } else {
+#pragma unroll
+          for (int s = 0; s < 8; ++s) {
+            const uint32_t k = kg + s;
+            fa[i][u][s] = (aok[i] && k < ke) ? Elem<T>::load(A, arow[i] + (int32_t)k * p.a_k) : 0.f;
+          }
         }
       }
-    }
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      if constexpr (BVK && !BF) {
+      for (int j = 0; j < FN; ++j) {
+        if constexpr (BVK && !BF) {
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (bok[j] && kg + 4u * q < ke) v = *(const float4*)((const float*)B + bcol[j] + (int32_t)(kg + 4u * q));
-          fb[buf][j][4 * q] = v.x; fb[buf][j][4 * q + 1] = v.y; fb[buf][j][4 * q + 2] = v.z; fb[buf][j][4 * q + 3] = v.w;
-        }
-      } else if constexpr (BVK && BF) {
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (bok[j] && kg < ke) v = *(const uint4*)((const uint16_t*)B + bcol[j] + (int32_t)kg);
-        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+          for (int q = 0; q < 2; ++q) {
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (bok[j] && kg + 4u * q < ke) v = *(const float4*)((const float*)B + bcol[j] + (int32_t)(kg + 4u * q));
+            fb[j][u][4 * q] = v.x; fb[j][u][4 * q + 1] = v.y; fb[j][u][4 * q + 2] = v.z; fb[j][u][4 * q + 3] = v.w;
+          }
+        } else if constexpr (BVK && BF) {
+          uint4 v = make_uint4(0, 0, 0, 0);
+          if (bok[j] && kg < ke) v = *(const uint4*)((const uint16_t*)B + bcol[j] + (int32_t)kg);
+          const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          fb[buf][j][2 * q] = __uint_as_float(wv[q] << 16);
-          fb[buf][j][2 * q + 1] = __uint_as_float(wv[q] & 0xffff0000u);
-        }
-      } else {
+          for (int q = 0; q < 4; ++q) {
+            fb[j][u][2 * q] = __uint_as_float(wv[q] << 16);
+            fb[j][u][2 * q + 1] = __uint_as_float(wv[q] & 0xffff0000u);
+          }
+        } else {
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const uint32_t k = kg + s;
-          fb[buf][j][s] = (bok[j] && k < ke) ? Elem<T>::load(B, bcol[j] + (int32_t)k * p.b_k) : 0.f;
+          for (int s = 0; s < 8; ++s) {
+            const uint32_t k = kg + s;
+            fb[j][u][s] = (bok[j] && k < ke) ? Elem<T>::load(B, bcol[j] + (int32_t)k * p.b_k) : 0.f;
+          }
         }
       }
     }
   };
-  auto compute = [&](int buf) {
-    if constexpr (BF) {
-      bf16x8 av[FM], bv[FN];
+  auto compute = [&](const float (&fa)[FM][U][8], const float (&fb)[FN][U][8]) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int s = 0; s < 8; ++s) av[i][s] = (__bf16)fa[buf][i][s];
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int s = 0; s < 8; ++s) bv[j][s] = (__bf16)fb[buf][j][s];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
-    } else {
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
+    for (int u = 0; u < U; ++u) {
+      if constexpr (BF) {
+        bf16x8 av[FM], bv[FN];
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
-          for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[buf][i][s], fb[buf][j][s], acc[i][j], 0, 0, 0);
+          for (int s = 0; s < 8; ++s) av[i][s] = (__bf16)fa[i][u][s];
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int s = 0; s < 8; ++s) bv[j][s] = (__bf16)fb[j][u][s];
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][u][s], fb[j][u][s], acc[i][j], 0, 0, 0);
+      }
     }
   };
-  // ping-pong with compile-time buffer indices, so that the loads of the
-  // next step stay in flight while the current step's MFMAs run
   if (kb < ke) {
-    load(0, kb);
+    load(fa0, fb0, kb);
     for (uint32_t k0 = kb;;) {
-      if (k0 + 16u < ke) load(1, k0 + 16u);
-      compute(0);
-      k0 += 16u;
+      if (k0 + KI < ke) load(fa1, fb1, k0 + KI);
+      compute(fa0, fb0);
+      k0 += KI;
       if (k0 >= ke) break;
-      if (k0 + 16u < ke) load(0, k0 + 16u);
-      compute(1);
-      k0 += 16u;
+      if (k0 + KI < ke) load(fa0, fb0, k0 + KI);
+      compute(fa1, fb1);
+      k0 += KI;
       if (k0 >= ke) break;
     }
   }
@@ -679,24 +638,25 @@ __global__ __launch_bounds__(64 * W) void gemm_sk_kernel(GemmParams p) {
 
 namespace {
 
-template <typename T, int FM, int FN, int W>
+template <typename T, int FM, int FN, int W, int U>
 hipError_t gemm_sk_go(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
   const bool avk = k.amode == GM_K, bvk = k.bmode == GM_K;
-  if (avk && bvk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, true, true>), grid, dim3(64 * W), 0, s, p);
-  else if (avk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, true, false>), grid, dim3(64 * W), 0, s, p);
-  else if (bvk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, false, true>), grid, dim3(64 * W), 0, s, p);
-  else hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, false, false>), grid, dim3(64 * W), 0, s, p);
+  if (avk && bvk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, true, true>), grid, dim3(64 * W), 0, s, p);
+  else if (avk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, true, false>), grid, dim3(64 * W), 0, s, p);
+  else if (bvk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, false, true>), grid, dim3(64 * W), 0, s, p);
+  else hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, false, false>), grid, dim3(64 * W), 0, s, p);
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t gemm_sk_dispatch(const NodeKernel& k, hipStream_t s) {
   switch (k.gemm_tile) {
-    case 2: return gemm_sk_go<T, 1, 1, 4>(k, s);
-    case 3: return gemm_sk_go<T, 1, 1, 8>(k, s);
-    default: return gemm_sk_go<T, 2, 1, 4>(k, s);
+    case 2: return gemm_sk_go<T, 1, 1, 4, 4>(k, s);
+    case 3: return gemm_sk_go<T, 1, 1, 8, 4>(k, s);
+    case 4: return gemm_sk_go<T, 2, 1, 4, 2>(k, s);
+    default: return gemm_sk_go<T, 1, 1, 16, 2>(k, s);
   }
 }
 
@@ -732,6 +692,7 @@ hipError_t gemm_a(const NodeKernel& k, hipStream_t s) {
 hipError_t launch_gemm(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   if ((uint64_t)p.tiles_m * p.tiles_n * p.G >= (1ull << 31)) return hipErrorInvalidValue;
+  if (k.gemm_tile >= 6) return launch_gemm_bf16_pipe(k, s);
   if (k.gemm_tile >= 2) return k.dtype == DT_BF16 ? gemm_sk_dispatch<uint16_t>(k, s) : gemm_sk_dispatch<float>(k, s);
   return k.gemm_tile == 0 ? gemm_a<128>(k, s) : gemm_a<64>(k, s);
 }

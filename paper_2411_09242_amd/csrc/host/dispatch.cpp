@@ -22,7 +22,7 @@ std::vector<int64_t> row_major_strides(const Shape& s) {
 
 int num_variants(int op) {
   switch (op) {
-    case FLUID_OP_MATMUL: return 5;
+    case FLUID_OP_MATMUL: return 8;
     case FLUID_OP_GELU:
     case FLUID_OP_SILU:
     case FLUID_OP_TRANSPOSE:
@@ -348,8 +348,14 @@ NodeKernel prepare_gemm(const Node&, int variant, int dtype, const std::vector<O
   k.gemm_tile = variant;
   // tile sizes: 0: 128x128, 1: 64x64 (LDS-staged); 2, 3: 32x32 and 4: 64x32
   // with the K range split over the workgroup's wavefronts
-  static const uint32_t TM[] = {128, 64, 32, 32, 64};
-  static const uint32_t TN[] = {128, 64, 32, 32, 32};
+  // 6: 256x128 and 7: 128x128, loads two K-tiles ahead (bf16 only)
+  static const uint32_t TM[] = {128, 64, 32, 32, 64, 32, 256, 128};
+  static const uint32_t TN[] = {128, 64, 32, 32, 32, 32, 128, 128};
+  if (variant >= 6 && k.dtype != DT_BF16) {
+    k.available = false;
+    k.why = "the deep-pipeline tiles are bf16 only";
+    return k;
+  }
   p.tiles_m = (p.M + TM[variant] - 1) / TM[variant];
   p.tiles_n = (p.N + TN[variant] - 1) / TN[variant];
   k.available = true;
@@ -387,7 +393,7 @@ std::string NodeKernel::name() const {
     case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt;
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
     case KF_GEMM: {
-      static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4"};
+      static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "p256x128", "p128"};
       return "gemm_" + dt + "_" + tiles[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
              (cmode == 1 ? "n" : cmode == 2 ? "m" : "g");
     }

@@ -3,7 +3,11 @@
 // the executor, the cost measurement and fluid_node_kernel; HIP-free.
 //
 // Variant ids per operator:
-//   MATMUL                      0: 128x128 tile, 1: 64x64 tile (MFMA)
+//   MATMUL                      0: 128x128 tile, 1: 64x64 tile (LDS-staged);
+//                               2, 3, 5: 32x32 tile with K split over 4, 8,
+//                               16 wavefronts; 4: 64x32 tile, K over 4;
+//                               6: 256x128, 7: 128x128 tile, loads two
+//                               K-tiles ahead, LDS double-buffered (bf16)
 //   ADD MUL                     0: streaming elementwise in output order
 //   GELU SILU TRANSPOSE RESHAPE 0: streaming; 1: LDS-tiled (input and output
 //                               unit-stride dims differ)
