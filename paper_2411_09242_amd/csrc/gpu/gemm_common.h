@@ -7,12 +7,32 @@
 namespace fluid {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 struct TileCoord {
   uint32_t m0, n0;
   int32_t a_base, b_base, c_base;
 };
+
+// Buffer resource over [base, base + bytes).  A buffer load at a byte offset
+// at or beyond `bytes` returns zeros without touching memory, so tile edges
+// are padded by pointing the load at kOOB instead of branching around it
+// (data format word as for every gfx9 target).
+constexpr uint32_t kOOB = 0x80000000u;
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ uint2 bload8(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+__device__ __forceinline__ uint16_t bload2(Rsrc r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
 
 // Workgroup -> (batch, tile row, tile column), row-major over tiles.
 __device__ __forceinline__ TileCoord tile_coord(const GemmParams& p, uint32_t BM, uint32_t BN) {

@@ -24,8 +24,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
   const TileCoord tc = tile_coord(p, BM, BN);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const uint16_t* A = (const uint16_t*)p.A;
-  const uint16_t* B = (const uint16_t*)p.B;
+  const Rsrc ra = make_rsrc(p.A, p.a_bytes);
+  const Rsrc rb = make_rsrc(p.B, p.b_bytes);
 
   // per-thread share of one K-tile: BM*32/256 elements of A, 16 of B
   constexpr int AE = BM * BK / 256;
@@ -45,6 +45,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
     a_off[r] = tc.a_base + (a_ok[r] ? row_off(p, m, p.a_m1, p.a_m2) : 0);
   }
   int b_n[BNN], b_k[BNN];
+  int32_t b_off[BNN];
   bool b_ok[BNN];
 #pragma unroll
   for (int r = 0; r < BNN; ++r) {
@@ -53,6 +54,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
     else if constexpr (BMD == GM_MN) mnblock_coord(idx, b_n[r], b_k[r]);
     else { b_k[r] = idx % BK; b_n[r] = idx / BK; }
     b_ok[r] = tc.n0 + b_n[r] < p.N;
+    b_off[r] = tc.b_base + (int32_t)(tc.n0 + b_n[r]) * p.b_n;
   }
 
   // One register set holds one K-tile's share, whatever the load mode.
@@ -66,41 +68,39 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
   };
   Regs R0, R1;
 
+  // Loads never branch: a piece outside the matrix (row past M or N, k past
+  // K) is read from kOOB and arrives as zeros.
   auto gload = [&](Regs& R, uint32_t k0) {
 #pragma unroll
     for (int r = 0; r < AN; ++r) {
       if constexpr (AM == GM_K) {
         const uint32_t k = k0 + a_k[r];
-        R.ca[r] = (a_ok[r] && k < p.K) ? *(const uint4*)(A + a_off[r] + (int32_t)k) : make_uint4(0, 0, 0, 0);
+        R.ca[r] = bload16(ra, (a_ok[r] && k < p.K) ? 2u * (uint32_t)(a_off[r] + (int32_t)k) : kOOB);
       } else if constexpr (AM == GM_MN) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const uint32_t k = k0 + a_k[r] + t;
-          R.ba[4 * r + t] = (a_ok[r] && k < p.K) ? *(const uint2*)(A + a_off[r] + (int32_t)k * p.a_k) : make_uint2(0, 0);
+          R.ba[4 * r + t] = bload8(ra, (a_ok[r] && k < p.K) ? 2u * (uint32_t)(a_off[r] + (int32_t)k * p.a_k) : kOOB);
         }
       } else {
         const uint32_t k = k0 + a_k[r];
-        R.sa[r] = (a_ok[r] && k < p.K) ? A[a_off[r] + (int32_t)k * p.a_k] : (uint16_t)0;
+        R.sa[r] = bload2(ra, (a_ok[r] && k < p.K) ? 2u * (uint32_t)(a_off[r] + (int32_t)k * p.a_k) : kOOB);
       }
     }
 #pragma unroll
     for (int r = 0; r < BNN; ++r) {
       if constexpr (BMD == GM_K) {
         const uint32_t k = k0 + b_k[r];
-        R.cb[r] = (b_ok[r] && k < p.K) ? *(const uint4*)(B + tc.b_base + (int32_t)k + (int32_t)(tc.n0 + b_n[r]) * p.b_n)
-                                       : make_uint4(0, 0, 0, 0);
+        R.cb[r] = bload16(rb, (b_ok[r] && k < p.K) ? 2u * (uint32_t)(b_off[r] + (int32_t)k) : kOOB);
       } else if constexpr (BMD == GM_MN) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const uint32_t k = k0 + b_k[r] + t;
-          R.bb[4 * r + t] = (b_ok[r] && k < p.K)
-                                ? *(const uint2*)(B + tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]))
-                                : make_uint2(0, 0);
+          R.bb[4 * r + t] = bload8(rb, (b_ok[r] && k < p.K) ? 2u * (uint32_t)(b_off[r] + (int32_t)k * p.b_k) : kOOB);
         }
       } else {
         const uint32_t k = k0 + b_k[r];
-        R.sb[r] = (b_ok[r] && k < p.K) ? B[tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]) * p.b_n]
-                                       : (uint16_t)0;
+        R.sb[r] = bload2(rb, (b_ok[r] && k < p.K) ? 2u * (uint32_t)(b_off[r] + (int32_t)k * p.b_k) : kOOB);
       }
     }
   };
@@ -161,25 +161,28 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
     }
   };
 
-  // K-tile t lives in LDS stage t % 2; register set (t % 2) carries tile t
-  // from global memory, issued two iterations before it is stored.
+  // K-tile t lives in LDS stage t % 2; register set t % 2 carries it from
+  // global memory, issued two tiles before it is stored.  Loads past the
+  // last tile read zeros (k >= K) and are never stored, so the loop body
+  // has no data-dependent branches and the memory counters stay exact.
   const uint32_t nt = (p.K + BK - 1) / BK;
   gload(R0, 0);
-  if (nt > 1) gload(R1, BK);
+  gload(R1, BK);
   lstore(R0, 0);
   __syncthreads();
-  if (nt > 2) gload(R0, 2 * BK);
-  for (uint32_t t = 0; t < nt; t += 2) {
-    compute(0);                                   // tile t
-    if (t + 1 < nt) lstore(R1, 1);                // tile t+1
+  gload(R0, 2 * BK);
+  uint32_t t = 0;
+  for (; t + 2 <= nt; t += 2) {
+    compute(0);            // tile t
+    lstore(R1, 1);         // tile t+1
     __syncthreads();
-    if (t + 3 < nt) gload(R1, (t + 3) * BK);
-    if (t + 1 >= nt) break;
-    compute(1);                                   // tile t+1
-    if (t + 2 < nt) lstore(R0, 0);                // tile t+2
+    gload(R1, (t + 3) * BK);
+    compute(1);            // tile t+1
+    lstore(R0, 0);         // tile t+2 (zeros past the end, never read)
     __syncthreads();
-    if (t + 4 < nt) gload(R0, (t + 4) * BK);
+    gload(R0, (t + 4) * BK);
   }
+  if (t < nt) compute(0);  // odd tile count: the last tile sits in stage 0
 
   uint16_t* C = (uint16_t*)p.C;
 #pragma unroll
@@ -220,6 +223,7 @@ hipError_t pipe_go(const NodeKernel& k, hipStream_t s) {
 
 hipError_t launch_gemm_bf16_pipe(const NodeKernel& k, hipStream_t s) {
   if (k.dtype != DT_BF16) return hipErrorInvalidValue;
+  if (k.gemm_tile == 6 && k.amode == GM_K && k.bmode == GM_MN) return launch_gemm_bf16_dl(k, s);
   return k.gemm_tile == 6 ? pipe_go<256>(k, s) : pipe_go<128>(k, s);
 }
 

@@ -345,6 +345,18 @@ NodeKernel prepare_gemm(const Node&, int variant, int dtype, const std::vector<O
            (p.c_g2 % 4 == 0) && (p.c_n % 4 == 0))
     k.cmode = 2;
   p.cmode = k.cmode;
+  const int64_t esz = k.dtype == DT_F32 ? 4 : 2;
+  auto span_bytes = [&](const Operand& o) {
+    int64_t s = 1;
+    for (size_t d = 0; d < o.shape.size(); ++d) {
+      if (o.shape[d] == 0) return int64_t(0);
+      s += (o.shape[d] - 1) * o.stride[d];
+    }
+    return s * esz;
+  };
+  const int64_t sa = span_bytes(A), sb = span_bytes(B);
+  p.a_bytes = (uint32_t)std::min<int64_t>(sa, 0x7fffffff);
+  p.b_bytes = (uint32_t)std::min<int64_t>(sb, 0x7fffffff);
   k.gemm_tile = variant;
   // tile sizes: 0: 128x128, 1: 64x64 (LDS-staged); 2, 3: 32x32 and 4: 64x32
   // with the K range split over the workgroup's wavefronts
@@ -354,6 +366,11 @@ NodeKernel prepare_gemm(const Node&, int variant, int dtype, const std::vector<O
   if (variant >= 6 && k.dtype != DT_BF16) {
     k.available = false;
     k.why = "the deep-pipeline tiles are bf16 only";
+    return k;
+  }
+  if (variant >= 6 && (sa >= 0x7fffffff || sb >= 0x7fffffff)) {
+    k.available = false;
+    k.why = "buffer-load tiles address at most 2 GiB per operand";
     return k;
   }
   p.tiles_m = (p.M + TM[variant] - 1) / TM[variant];

@@ -94,6 +94,7 @@ struct GemmParams {
   int32_t c_g1, c_g2, c_m1, c_m2, c_n;
   int32_t cmode;              // 0 scalar stores, 1 N-contiguous, 2 M-contiguous (4 rows)
   uint32_t tiles_m, tiles_n;
+  uint32_t a_bytes, b_bytes;  // byte span of A and B from their base pointers
 };
 
 }  // namespace fluid

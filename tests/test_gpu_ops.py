@@ -40,7 +40,8 @@ def proj_graph(B, S, K, N, dtype):
     return g, a, c
 
 
-PROJ_SHAPES = [(1, 37, 29, 53), (1, 130, 64, 70), (2, 65, 96, 40), (1, 256, 128, 256), (3, 8, 16, 200)]
+PROJ_SHAPES = [(1, 37, 29, 53), (1, 130, 64, 70), (2, 65, 96, 40), (1, 256, 128, 256), (3, 8, 16, 200),
+               (1, 300, 200, 264)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
