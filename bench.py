@@ -35,6 +35,35 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+class Markers:
+    """ROCTx ranges around the timed regions, so that a kernel trace taken
+    with rocprofv3 --marker-trace can be cut to exactly those dispatches.
+    No-ops when the ROCTx library is not present."""
+
+    def __init__(self):
+        import ctypes
+        self.lib = None
+        for name in ("librocprofiler-sdk-roctx.so.1", "librocprofiler-sdk-roctx.so", "libroctx64.so"):
+            try:
+                self.lib = ctypes.CDLL(name)
+                break
+            except OSError:
+                continue
+        if self.lib is not None:
+            self.lib.roctxRangePushA.argtypes = [ctypes.c_char_p]
+
+    def push(self, name):
+        if self.lib is not None:
+            self.lib.roctxRangePushA(name.encode())
+
+    def pop(self):
+        if self.lib is not None:
+            self.lib.roctxRangePop()
+
+
+MARK = Markers()
+
+
 def node_work(g, n):
     """Algorithmic work of one launch of node n: ('flop', 2MNK) for a MatMul,
     else ('bytes', inputs read once + output written once)."""
@@ -55,15 +84,31 @@ def node_work(g, n):
 
 
 def time_steps(ex, steps, stream, torch):
+    """K eager steps, an event after each: (mean ms, [per-step ms])."""
     torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record()
-    for _ in range(steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
         ex.run(stream)
-    t1.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    return t0.elapsed_time(t1) / steps
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return ev[0].elapsed_time(ev[-1]) / steps, per
+
+
+def calibration_copy(torch, mib=256):
+    """A plain device-to-device copy of known size, inside its own marker
+    range: HBM counters of the kernels are scaled by what the same counters
+    read for this copy."""
+    src = torch.empty(mib << 18, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    MARK.push(f"calibration_copy_{mib}MiB")
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    MARK.pop()
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 def cpu_baseline(cfg, budget_s=20.0):
@@ -93,9 +138,12 @@ def cpu_baseline(cfg, budget_s=20.0):
 def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=None):
     """Cost table (untimed), plans, then the two timed regions; returns a dict."""
     g = F.Graph.transformer(cfg)
+    wl = cfg["name"]
     stream = torch.cuda.current_stream().cuda_stream
     t = time.time()
+    MARK.push(f"{wl}/cost_table")
     table = F.CostTable.measure(g, reps=reps)
+    MARK.pop()
     t_measure = time.time() - t
     log(f"{cfg['name']}: cost table measured in {t_measure:.1f} s")
     if save_table:
@@ -130,6 +178,27 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
                      for v in nd["ins"]))
         by_sig.setdefault(key, []).append(n)
     dom_key = max(by_sig, key=lambda k: sum(ms[n] for n in by_sig[k]))
+    # per operator class: time per step and achieved rate against its bound
+    classes = {}
+    for n in range(g.n_nodes):
+        if cnt[n] == 0:
+            continue
+        op = g.desc["nodes"][n]["op"]
+        kind, work = node_work(g, n)
+        c = classes.setdefault(op, {"ms": 0.0, "launches": 0, "work": 0.0, "kind": kind})
+        c["ms"] += ms[n] / 2
+        c["launches"] += cnt[n] // 2
+        c["work"] += work
+    op_classes = {}
+    for op, c in sorted(classes.items(), key=lambda kv: -kv[1]["ms"]):
+        if c["kind"] == "flop":
+            rate = c["work"] / (c["ms"] * 1e-3) / 1e12
+            peak, unit = PEAK_TFLOPS[g.dtype], "TFLOP/s"
+        else:
+            rate = c["work"] / (c["ms"] * 1e-3) / 1e9
+            peak, unit = PEAK_HBM_GBS, "GB/s"
+        op_classes[op] = {"ms_per_step": round(c["ms"], 4), "launches_per_step": c["launches"],
+                          "achieved": round(rate, 2), "unit": unit, "frac": round(rate / peak, 4)}
     dom_nodes = by_sig[dom_key]
     mask = [0] * g.n_nodes
     for n in dom_nodes:
@@ -138,7 +207,9 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     # timed region 1: K eager steps, HIP events around every launch of the
     # dominant kernel (on the stream it is launched on) -> its duration
     F.fluid_trace_enable(g.h, mask, len(dom_nodes) * steps + 8)
-    ms_eager = time_steps(ex, steps, stream, torch)
+    MARK.push(f"{wl}/eager_timed")
+    ms_eager, per_step = time_steps(ex, steps, stream, torch)
+    MARK.pop()
     tms, tcnt = F.fluid_trace_collect(g.h, g.n_nodes)
     # timed region 2 (the reported latency): the same K steps captured into
     # one HIP graph; one warm-up replay, then one timed replay
@@ -146,25 +217,30 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     hg.replay()
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    MARK.push(f"{wl}/graph_timed")
     ev0.record()
     hg.replay()
     ev1.record()
     torch.cuda.synchronize()
+    MARK.pop()
     ms_step = ev0.elapsed_time(ev1) / steps
     del hg
     hg_naive = ex_naive.capture(steps=steps)
     hg_naive.replay()
     torch.cuda.synchronize()
+    MARK.push(f"{wl}/naive_graph_timed")
     ev0.record()
     hg_naive.replay()
     ev1.record()
     torch.cuda.synchronize()
+    MARK.pop()
     ms_naive = ev0.elapsed_time(ev1) / steps
     del hg_naive
-    ms_naive_eager = time_steps(ex_naive, steps, stream, torch)
+    ms_naive_eager, _ = time_steps(ex_naive, steps, stream, torch)
 
     kind, work = node_work(g, dom_nodes[0])
     launches = sum(tcnt[n] for n in dom_nodes)
+    order = [n for n in range(g.n_nodes) if lp.variant[n] >= 0]    # fluid_run's launch order
     avg_ms = sum(tms[n] for n in dom_nodes) / max(launches, 1)
     if kind == "flop":
         achieved = work / (avg_ms * 1e-3) / 1e12
@@ -177,6 +253,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
     roof.update({"kernel": dom_key[0], "node_op": dom_key[1], "out_shape": list(dom_key[2]),
                  "avg_launch_us": round(avg_ms * 1e3, 3), "launches": launches,
+                 "positions_in_step": [order.index(n) for n in dom_nodes],
                  "work_per_launch": work, "work_unit": "flop" if kind == "flop" else "byte"})
 
     # planned vs naive outputs (same inputs, different layouts and kernels)
@@ -186,6 +263,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     agree = float((out - out_n).abs().max().item())
     res = {
         "ms_per_step": round(ms_step, 4), "eager_ms": round(ms_eager, 4),
+        "eager_step_ms_p10_p50_p90": [round(float(np.percentile(per_step, q)), 4) for q in (10, 50, 90)],
         "naive_ms": round(ms_naive, 4), "naive_eager_ms": round(ms_naive_eager, 4),
         "speedup_vs_naive": round(ms_naive / ms_step, 3),
         "peak_arena_mb": round(apl.peak / 2**20, 3), "naive_arena_mb": round(ap_naive.peak / 2**20, 3),
@@ -194,6 +272,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         "plan_table_ns": lp.total_ns, "naive_table_ns": lp_naive.total_ns, "guard_used": lp.guard_used,
         "planned_vs_naive_max_abs_diff": agree, "cost_table_s": round(t_measure, 1),
         "roofline": roof,
+        "op_classes": op_classes,
     }
     del ex, ex_naive
     torch.cuda.empty_cache()
@@ -249,6 +328,7 @@ def main():
 
     F.load()
     torch.cuda.init()
+    calibration_copy(torch)
     cfg = synth_inputs.config(a.config)
     log(f"workload {cfg['name']}")
     x, consts = synth_inputs.make_inputs(cfg, F.Graph.transformer(cfg).const_specs(), a.config)

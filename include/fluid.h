@@ -171,8 +171,11 @@ fluid_status fluid_measure_scratch_bytes(const fluid_graph* g, uint64_t* bytes);
 
 /* Measures the cost table on the GPU (Alg. 3's eval: real kernel time).
  * For every operator signature, every candidate layout combination and
- * every kernel variant: warm-up launches, then `reps` launches timed with
- * HIP events; the median is rounded to integer nanoseconds.  View
+ * every kernel variant: one warm-up launch timed on its own (a combination
+ * more than 8x slower than the best so far of its signature keeps that
+ * time), then three batches of `reps` back-to-back launches, each batch
+ * between two HIP events; the cost is the median per-launch time of the
+ * batches, rounded to integer nanoseconds.  View
  * combinations of Transpose/Reshape cost 0.  Candidate lists: all
  * dimension permutations (deduplicated), trimmed for tensors with more than
  * six candidates to those whose innermost dim is one of the last two

@@ -3,7 +3,10 @@
 //  * row (variant 0): one 64-lane wavefront per row; the row is held in
 //    registers (up to 4096 values), reduced with cross-lane butterflies, and
 //    written once -- one HBM read and one write per element.  Coalesced when
-//    the reduced dim is unit-stride.
+//    the reduced dim is unit-stride; when in addition rows start on 16-byte
+//    boundaries, each lane moves 16-byte pieces (lane l takes pieces
+//    l, l + 64, ...), so a wavefront load covers 1 KiB of contiguous row,
+//    and a causal softmax skips the pieces that lie wholly past the mask.
 //  * column (variant 1): one lane per row, consecutive lanes on consecutive
 //    rows, so a layout whose unit-stride dim is a row dim still reads and
 //    writes coalesced; the row is streamed twice (three times for
@@ -105,6 +108,136 @@ __global__ __launch_bounds__(256) void red_row_kernel(RedParams p) {
   }
 }
 
+// 16-byte piece <-> VEC floats
+template <typename T>
+struct Piece;
+template <>
+struct Piece<float> {
+  static constexpr int VEC = 4;
+  __device__ static __forceinline__ void unpack(const uint4& u, float* f) {
+    f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y); f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
+  }
+  __device__ static __forceinline__ uint4 pack(const float* f) {
+    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]), __float_as_uint(f[3]));
+  }
+};
+template <>
+struct Piece<uint16_t> {
+  static constexpr int VEC = 8;
+  __device__ static __forceinline__ void unpack(const uint4& u, float* f) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+  __device__ static __forceinline__ uint4 pack(const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_to_bf16(f[2 * i]) | ((uint32_t)f32_to_bf16(f[2 * i + 1]) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+
+// Row family with 16-byte pieces (unit-stride rows, 16-byte aligned): NC
+// pieces per lane, piece c of lane l at l + 64 c.
+template <typename T, int NC, int OP>
+__global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
+  constexpr int VEC = Piece<T>::VEC;
+  const uint32_t row = blockIdx.x * 4u + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= p.nrows) return;  // uniform per wavefront
+  int32_t io, oo;
+  uint32_t qi;
+  row_offsets(p, row, io, oo, qi);
+  const uint32_t R = p.R;
+  const uint32_t valid = (OP == RED_SOFTMAX && p.causal) ? min(R, qi + 1u) : R;
+  const T* x = (const T*)p.x + io;
+  T* y = (T*)p.y + oo;
+  float v[NC][VEC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const uint32_t e0 = (uint32_t)(lane + 64 * c) * VEC;
+    uint4 u = make_uint4(0, 0, 0, 0);
+    if (e0 < valid) u = *(const uint4*)(x + e0);
+    Piece<T>::unpack(u, v[c]);
+  }
+  if constexpr (OP == RED_SOFTMAX) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const uint32_t k = (uint32_t)(lane + 64 * c) * VEC + i;
+        v[c][i] *= p.attr;
+        if (k < valid) m = fmaxf(m, v[c][i]);
+      }
+    m = wave_max(m);
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const uint32_t k = (uint32_t)(lane + 64 * c) * VEC + i;
+        v[c][i] = k < valid ? expf(v[c][i] - m) : 0.f;
+        s += v[c][i];
+      }
+    s = wave_sum(s);
+    const float inv = 1.0f / s;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const uint32_t e0 = (uint32_t)(lane + 64 * c) * VEC;
+      if (e0 < R) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[c][i] *= inv;
+        *(uint4*)(y + e0) = Piece<T>::pack(v[c]);
+      }
+    }
+  } else {
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) s += (OP == RED_LAYERNORM) ? v[c][i] : v[c][i] * v[c][i];
+    s = wave_sum(s);
+    const float invR = 1.0f / (float)R;
+    float mean = 0.f, rstd;
+    if constexpr (OP == RED_LAYERNORM) {
+      mean = s * invR;
+      float q = 0.f;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const uint32_t e0 = (uint32_t)(lane + 64 * c) * VEC;
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+          const float d = v[c][i] - mean;
+          q += e0 < R ? d * d : 0.f;
+        }
+      }
+      q = wave_sum(q);
+      rstd = 1.0f / sqrtf(q * invR + p.attr);
+    } else {
+      rstd = 1.0f / sqrtf(s * invR + p.attr);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const uint32_t e0 = (uint32_t)(lane + 64 * c) * VEC;
+      if (e0 < R) {
+        float g[VEC], b[VEC];
+        Piece<T>::unpack(*(const uint4*)((const T*)p.gamma + e0), g);
+        if constexpr (OP == RED_LAYERNORM) Piece<T>::unpack(*(const uint4*)((const T*)p.beta + e0), b);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+          v[c][i] = (v[c][i] - mean) * rstd * g[i];
+          if constexpr (OP == RED_LAYERNORM) v[c][i] += b[i];
+        }
+        *(uint4*)(y + e0) = Piece<T>::pack(v[c]);
+      }
+    }
+  }
+}
+
 template <typename T, int OP>
 __global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
   const uint32_t row = blockIdx.x * 256u + threadIdx.x;
@@ -170,6 +303,16 @@ hipError_t red_dispatch_op(const NodeKernel& k, hipStream_t s) {
     return hipGetLastError();
   }
   const dim3 grid((p.nrows + 3u) / 4u);
+  if (k.vec > 1) {
+    const uint32_t nc = (p.R / Piece<T>::VEC + 63u) / 64u;
+    if (nc <= 1) hipLaunchKernelGGL((red_rowv_kernel<T, 1, OP>), grid, dim3(256), 0, s, p);
+    else if (nc <= 2) hipLaunchKernelGGL((red_rowv_kernel<T, 2, OP>), grid, dim3(256), 0, s, p);
+    else if (nc <= 4) hipLaunchKernelGGL((red_rowv_kernel<T, 4, OP>), grid, dim3(256), 0, s, p);
+    else if (nc <= 8) hipLaunchKernelGGL((red_rowv_kernel<T, 8, OP>), grid, dim3(256), 0, s, p);
+    else if (nc <= 16) hipLaunchKernelGGL((red_rowv_kernel<T, 16, OP>), grid, dim3(256), 0, s, p);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   const uint32_t npl = (p.R + 63u) / 64u;
   if (npl <= 1) hipLaunchKernelGGL((red_row_kernel<T, 1, OP>), grid, dim3(256), 0, s, p);
   else if (npl <= 2) hipLaunchKernelGGL((red_row_kernel<T, 2, OP>), grid, dim3(256), 0, s, p);

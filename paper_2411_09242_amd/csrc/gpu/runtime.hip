@@ -413,27 +413,31 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
           for (int v = 0; v < num_variants(nd.op); ++v) {
             NodeKernel k = prepare_node(nd, v, g.dtype, ins, ou);
             if (!k.available) { en.costs.push_back(-1); continue; }
-            hip_check(launch_node_kernel(k, s), "warm-up launch");
+            // a warm-up launch, timed on its own: clearly losing
+            // combinations get no more launches
             hip_check(hipEventRecord(ev[0], s), "hipEventRecord");
-            hip_check(launch_node_kernel(k, s), "timed launch");
+            hip_check(launch_node_kernel(k, s), "warm-up launch");
             hip_check(hipEventRecord(ev[1], s), "hipEventRecord");
             hip_check(hipEventSynchronize(ev[1]), "hipEventSynchronize");
             float first = 0.f;
             hip_check(hipEventElapsedTime(&first, ev[0], ev[1]), "hipEventElapsedTime");
             std::vector<float> times = {first};
             const int64_t first_ns = (int64_t)std::llround((double)first * 1e6);
-            // clearly losing combinations are not worth more launches
-            if (!(best_so_far >= 0 && first_ns > 8 * best_so_far) && R > 1) {
-              for (uint32_t r = 1; r < R; ++r) {
-                hip_check(hipEventRecord(ev[2 * r], s), "hipEventRecord");
-                hip_check(launch_node_kernel(k, s), "timed launch");
-                hip_check(hipEventRecord(ev[2 * r + 1], s), "hipEventRecord");
+            if (!(best_so_far >= 0 && first_ns > 8 * best_so_far)) {
+              // three batches of R back-to-back launches between two events:
+              // the per-launch time includes the kernel's start-up and the
+              // gap to the next launch, as in a run, and no event overhead
+              times.clear();
+              for (int b = 0; b < 3; ++b) {
+                hip_check(hipEventRecord(ev[2 + 2 * b], s), "hipEventRecord");
+                for (uint32_t r = 0; r < R; ++r) hip_check(launch_node_kernel(k, s), "timed launch");
+                hip_check(hipEventRecord(ev[3 + 2 * b], s), "hipEventRecord");
               }
-              hip_check(hipEventSynchronize(ev[2 * R - 1]), "hipEventSynchronize");
-              for (uint32_t r = 1; r < R; ++r) {
+              hip_check(hipEventSynchronize(ev[7]), "hipEventSynchronize");
+              for (int b = 0; b < 3; ++b) {
                 float ms = 0.f;
-                hip_check(hipEventElapsedTime(&ms, ev[2 * r], ev[2 * r + 1]), "hipEventElapsedTime");
-                times.push_back(ms);
+                hip_check(hipEventElapsedTime(&ms, ev[2 + 2 * b], ev[3 + 2 * b]), "hipEventElapsedTime");
+                times.push_back(ms / (float)R);
               }
             }
             std::sort(times.begin(), times.end());

@@ -259,6 +259,14 @@ NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector
   p.gamma = ins.size() > 1 ? ins[1].ptr : nullptr;
   p.beta = ins.size() > 2 ? ins[2].ptr : nullptr;
   if (variant == 0 && p.R > 4096) { k.why = "row variant holds at most 4096 values per row"; return k; }
+  if (variant == 0) {
+    // 16-byte pieces: unit-stride rows starting on 16-byte boundaries
+    const int VEC = k.dtype == DT_BF16 ? 8 : 4;
+    bool ok = p.irs == 1 && p.ors == 1 && p.R % VEC == 0 && aligned16(p.x) && aligned16(p.y);
+    for (int i = 0; i < p.nrd; ++i) ok = ok && p.ris[i] % VEC == 0 && p.ros[i] % VEC == 0;
+    if (p.op != RED_SOFTMAX) ok = ok && aligned16(p.gamma) && (p.op != RED_LAYERNORM || aligned16(p.beta));
+    if (ok) k.vec = VEC;
+  }
   k.available = true;
   return k;
 }
@@ -360,21 +368,28 @@ NodeKernel prepare_gemm(const Node&, int variant, int dtype, const std::vector<O
   k.gemm_tile = variant;
   // tile sizes: 0: 128x128, 1: 64x64 (LDS-staged); 2, 3: 32x32 and 4: 64x32
   // with the K range split over the workgroup's wavefronts
-  // 6: 256x128 and 7: 128x128, loads two K-tiles ahead (bf16 only)
+  // bf16 6: 256x128 and 7: 128x128, loads two or more K-tiles ahead;
+  // fp32 6: 16x32 with K split over 8 wavefronts, 7: 32x32 over 4, operands
+  // loaded straight into MFMA registers
   static const uint32_t TM[] = {128, 64, 32, 32, 64, 32, 256, 128};
   static const uint32_t TN[] = {128, 64, 32, 32, 32, 32, 128, 128};
+  uint32_t tm = TM[variant], tn = TN[variant];
   if (variant >= 6 && k.dtype != DT_BF16) {
-    k.available = false;
-    k.why = "the deep-pipeline tiles are bf16 only";
-    return k;
+    tm = variant == 6 ? 16 : 32;
+    tn = 32;
+    if ((k.amode != GM_K && k.amode != GM_MN) || (k.bmode != GM_K && k.bmode != GM_MN)) {
+      k.available = false;
+      k.why = "the direct-load tiles need unit-stride K or M/N operands";
+      return k;
+    }
   }
   if (variant >= 6 && (sa >= 0x7fffffff || sb >= 0x7fffffff)) {
     k.available = false;
     k.why = "buffer-load tiles address at most 2 GiB per operand";
     return k;
   }
-  p.tiles_m = (p.M + TM[variant] - 1) / TM[variant];
-  p.tiles_n = (p.N + TN[variant] - 1) / TN[variant];
+  p.tiles_m = (p.M + tm - 1) / tm;
+  p.tiles_n = (p.N + tn - 1) / tn;
   k.available = true;
   return k;
 }
@@ -407,11 +422,12 @@ std::string NodeKernel::name() const {
     case KF_EW: return "ew_" + std::string(ew_names[ew.op]) + "_" + dt + "_v" + std::to_string(vec);
     case KF_EW_TILED: return "ew_tiled_" + std::string(ew_names[ew.op]) + "_" + dt;
     case KF_ROPE: return "rope_" + dt;
-    case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt;
+    case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
     case KF_GEMM: {
       static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "p256x128", "p128"};
-      return "gemm_" + dt + "_" + tiles[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
+      static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4"};
+      return "gemm_" + dt + "_" + (dtype == DT_BF16 ? tiles : tiles_f32)[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
              (cmode == 1 ? "n" : cmode == 2 ? "m" : "g");
     }
   }

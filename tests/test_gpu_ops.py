@@ -18,6 +18,18 @@ from oracle.graph import Graph
 pytestmark = pytest.mark.gpu
 
 
+def _check_gemm(og, want, variants, tmp_path, seed, dtype):
+    """_check for a forced GEMM variant; the fp32 direct-load variants (6, 7)
+    need unit-stride K or M/N operands and are skipped where they cannot
+    run."""
+    try:
+        return _check(og, want, variants, tmp_path, seed=seed)
+    except Exception as ex:  # noqa: BLE001
+        if dtype == "f32" and max(variants.values()) >= 6 and "cannot run with these layouts" in str(ex):
+            return None
+        raise
+
+
 def _check(og, want, variants, tmp_path, seed=0, scale=1.0):
     xs, cs = random_inputs(og, seed, scale)
     ref = execute.run_canonical(og, xs, cs)
@@ -48,8 +60,6 @@ PROJ_SHAPES = [(1, 37, 29, 53), (1, 130, 64, 70), (2, 65, 96, 40), (1, 256, 128,
 @pytest.mark.parametrize("shape", PROJ_SHAPES, ids=str)
 @pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5, 6, 7])
 def test_projection_gemm_all_layouts(dtype, shape, variant, tmp_path):
-    if variant >= 6 and dtype == "f32":
-        pytest.skip("the deep-pipeline tile variants are bf16 only")
     B, S, K, N = shape
     og, a, c = proj_graph(B, S, K, N, dtype)
     mm = 1
@@ -57,7 +67,7 @@ def test_projection_gemm_all_layouts(dtype, shape, variant, tmp_path):
     Lc = layouts.layout_list((B, S, N))
     for pa, pc in itertools.product(La, Lc):
         say(f"gemm proj {dtype} {shape} v{variant} A{pa} C{pc}")
-        _check(og, {a: pa, c: pc}, {mm: variant}, tmp_path, seed=B * S + K)
+        _check_gemm(og, {a: pa, c: pc}, {mm: variant}, tmp_path, B * S + K, dtype)
 
 
 def attn_graph(B, NH, S, D, dtype, pv=False):
@@ -93,9 +103,9 @@ def test_attention_gemm_sampled_layouts(dtype, shape, pv, tmp_path):
     combos = list(itertools.product(range(len(Lq)), range(len(Lk)), range(len(Ls))))
     pick = [combos[0]] + [combos[i] for i in rng.choice(len(combos), size=min(10, len(combos)), replace=False)]
     for iq, ik, is_ in pick:
-        for v in (0, 1, 2, 3, 4, 5, 6, 7) if dtype == "bf16" else (0, 1, 2, 3, 4, 5):
+        for v in (0, 1, 2, 3, 4, 5, 6, 7):
             say(f"gemm attn {dtype} {shape} pv={pv} v{v} {Lq[iq]} {Lk[ik]} {Ls[is_]}")
-            _check(og, {q: Lq[iq], k: Lk[ik], s: Ls[is_]}, {2: v}, tmp_path, seed=iq + ik + is_)
+            _check_gemm(og, {q: Lq[iq], k: Lk[ik], s: Ls[is_]}, {2: v}, tmp_path, iq + ik + is_, dtype)
 
 
 # ------------------------------------------------------------------ elementwise
