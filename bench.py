@@ -96,6 +96,35 @@ def time_steps(ex, steps, stream, torch):
     return ev[0].elapsed_time(ev[-1]) / steps, per
 
 
+def time_nodes(ex, nodes, repeat, torch, marker=None):
+    """ms per pass of the given nodes' kernels launched back to back:
+    `repeat` passes captured in one HIP graph (so that host launch cost does
+    not pace small kernels), one warm-up replay, then one replay between two
+    events on the replay stream."""
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        ex.run_nodes(nodes, 1, s.cuda_stream)
+        s.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            ex.run_nodes(nodes, repeat, s.cuda_stream)
+        g.replay()
+        s.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if marker:
+            MARK.push(marker)
+        e0.record(s)
+        g.replay()
+        e1.record(s)
+        s.synchronize()
+        if marker:
+            MARK.pop()
+    torch.cuda.current_stream().wait_stream(s)
+    del g
+    return e0.elapsed_time(e1) / repeat
+
+
 def calibration_copy(torch, mib=256):
     """A plain device-to-device copy of known size, inside its own marker
     range: HBM counters of the kernels are scaled by what the same counters
@@ -158,65 +187,59 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     n_launch = sum(1 for v in lp.variant if v >= 0)
     n_launch_naive = sum(1 for v in lp_naive.variant if v >= 0)
 
-    # warm-up, then find the dominant kernel (largest summed time) untimed
+    # warm-up; then, untimed for the result, each node signature's launches
+    # back to back (a few passes) to find the dominant kernel, and each
+    # operator class's launches back to back for the per-class rates
     for _ in range(warmup):
         ex.run(stream)
         ex_naive.run(stream)
     torch.cuda.synchronize()
-    F.fluid_trace_enable(g.h, None, 4 * g.n_nodes)
-    for _ in range(2):
-        ex.run(stream)
-    torch.cuda.synchronize()
-    ms, cnt = F.fluid_trace_collect(g.h, g.n_nodes)
+    launched = [n for n in range(g.n_nodes) if lp.variant[n] >= 0]    # fluid_run's launch order
     by_sig = {}
-    for n in range(g.n_nodes):
-        if cnt[n] == 0:
-            continue
+    for n in launched:
         nd = g.desc["nodes"][n]
         key = (lp.kernel(n), nd["op"], tuple(nd["out_shape"]),
                tuple(tuple(g.edge_shape(v)) if v >= 0 else ("c",) + tuple(g.desc["consts"][~v]["shape"])
                      for v in nd["ins"]))
         by_sig.setdefault(key, []).append(n)
-    dom_key = max(by_sig, key=lambda k: sum(ms[n] for n in by_sig[k]))
+    sig_ms = {k: time_nodes(ex, v, 3, torch) for k, v in by_sig.items()}
+    dom_key = max(by_sig, key=lambda k: sig_ms[k])
+    dom_nodes = by_sig[dom_key]
     # per operator class: time per step and achieved rate against its bound
-    classes = {}
-    for n in range(g.n_nodes):
-        if cnt[n] == 0:
-            continue
-        op = g.desc["nodes"][n]["op"]
-        kind, work = node_work(g, n)
-        c = classes.setdefault(op, {"ms": 0.0, "launches": 0, "work": 0.0, "kind": kind})
-        c["ms"] += ms[n] / 2
-        c["launches"] += cnt[n] // 2
-        c["work"] += work
+    by_op = {}
+    for n in launched:
+        by_op.setdefault(g.desc["nodes"][n]["op"], []).append(n)
     op_classes = {}
-    for op, c in sorted(classes.items(), key=lambda kv: -kv[1]["ms"]):
-        if c["kind"] == "flop":
-            rate = c["work"] / (c["ms"] * 1e-3) / 1e12
+    for op, nodes in by_op.items():
+        ms_c = time_nodes(ex, nodes, max(3, min(steps, 20)), torch)
+        kind = node_work(g, nodes[0])[0]
+        work = sum(node_work(g, n)[1] for n in nodes)
+        if kind == "flop":
+            rate = work / (ms_c * 1e-3) / 1e12
             peak, unit = PEAK_TFLOPS[g.dtype], "TFLOP/s"
         else:
-            rate = c["work"] / (c["ms"] * 1e-3) / 1e9
+            rate = work / (ms_c * 1e-3) / 1e9
             peak, unit = PEAK_HBM_GBS, "GB/s"
-        op_classes[op] = {"ms_per_step": round(c["ms"], 4), "launches_per_step": c["launches"],
+        op_classes[op] = {"ms_per_step": round(ms_c, 4), "launches_per_step": len(nodes),
                           "achieved": round(rate, 2), "unit": unit, "frac": round(rate / peak, 4)}
-    dom_nodes = by_sig[dom_key]
-    mask = [0] * g.n_nodes
-    for n in dom_nodes:
-        mask[n] = 1
+    op_classes = dict(sorted(op_classes.items(), key=lambda kv: -kv[1]["ms_per_step"]))
 
-    # timed region 1: K eager steps, HIP events around every launch of the
-    # dominant kernel (on the stream it is launched on) -> its duration
-    F.fluid_trace_enable(g.h, mask, len(dom_nodes) * steps + 8)
+    # timed region 1: K eager steps (whole graph, no per-launch events)
     MARK.push(f"{wl}/eager_timed")
     ms_eager, per_step = time_steps(ex, steps, stream, torch)
     MARK.pop()
-    tms, tcnt = F.fluid_trace_collect(g.h, g.n_nodes)
+    # timed region 1b: the dominant kernel alone -- the launches of its nodes
+    # back to back, K times over, with the bindings of a run (the arena holds
+    # the data of the last step), replayed as one HIP graph between two
+    # events on the replay stream
+    launches = steps * len(dom_nodes)
+    avg_ms = time_nodes(ex, dom_nodes, steps, torch, marker=f"{wl}/kernel_timed") / len(dom_nodes)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     # timed region 2 (the reported latency): the same K steps captured into
     # one HIP graph; one warm-up replay, then one timed replay
     hg = ex.capture(steps=steps)
     hg.replay()
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     MARK.push(f"{wl}/graph_timed")
     ev0.record()
     hg.replay()
@@ -239,9 +262,6 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     ms_naive_eager, _ = time_steps(ex_naive, steps, stream, torch)
 
     kind, work = node_work(g, dom_nodes[0])
-    launches = sum(tcnt[n] for n in dom_nodes)
-    order = [n for n in range(g.n_nodes) if lp.variant[n] >= 0]    # fluid_run's launch order
-    avg_ms = sum(tms[n] for n in dom_nodes) / max(launches, 1)
     if kind == "flop":
         achieved = work / (avg_ms * 1e-3) / 1e12
         peak = PEAK_TFLOPS[g.dtype]
@@ -253,7 +273,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
     roof.update({"kernel": dom_key[0], "node_op": dom_key[1], "out_shape": list(dom_key[2]),
                  "avg_launch_us": round(avg_ms * 1e3, 3), "launches": launches,
-                 "positions_in_step": [order.index(n) for n in dom_nodes],
+                 "positions_in_step": [launched.index(n) for n in dom_nodes],
                  "work_per_launch": work, "work_unit": "flop" if kind == "flop" else "byte"})
 
     # planned vs naive outputs (same inputs, different layouts and kernels)
@@ -341,8 +361,9 @@ def main():
         "config": {"workload": cfg["name"], "arch": cfg["arch"], "layers": cfg["layers"],
                    "batch": cfg["batch"], "seq": cfg["seq"], "hidden": cfg["hidden"],
                    "heads": cfg["heads"], "ffn": cfg["ffn"], "parallelism": "none (1 GPU)"},
-        "timing": "value: K steps captured in one HIP graph, one timed replay; roofline kernel "
-                  "durations: HIP events around each dominant-kernel launch in a K-step eager region",
+        "timing": "value: K steps captured in one HIP graph, one timed replay; roofline: the "
+                  "dominant kernel's launches (all nodes of its signature) back to back K times over, "
+                  "replayed as one HIP graph between two HIP events, per-launch mean",
     }
     res.update({k: v for k, v in r.items() if k != "ms_per_step"})
     extras = {}

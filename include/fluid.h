@@ -239,6 +239,19 @@ fluid_status fluid_run(const fluid_graph* g, const fluid_layout_plan* lp, const 
                        void* arena, uint64_t arena_bytes, const void* const* consts,
                        const void* const* inputs, void* const* outputs, void* hip_stream);
 
+/* Launches only the kernels of the listed nodes, in list order, the whole
+ * list `repeat` times over, with exactly the bindings and kernels fluid_run
+ * uses for them (profiling aid: the time of chosen kernels back to back,
+ * without the rest of the graph).  Same argument rules and errors as
+ * fluid_run; nodes: n_nodes node ids, each a non-view node under the plan
+ * (else FLUID_E_INVALID); repeat >= 1.  Reads and writes the arena like a
+ * run would, so it leaves the arena contents of a partial run.  GPU build
+ * only. */
+fluid_status fluid_run_nodes(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
+                             void* arena, uint64_t arena_bytes, const void* const* consts,
+                             const void* const* inputs, void* const* outputs, const int32_t* nodes,
+                             int32_t n_nodes, int32_t repeat, void* hip_stream);
+
 /* Per-node timing of later fluid_run calls (profiling aid).  While enabled,
  * fluid_run records a HIP event pair around every launch of a node whose
  * node_mask entry is nonzero (NULL mask = all nodes), for at most

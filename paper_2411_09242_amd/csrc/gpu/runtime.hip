@@ -220,46 +220,56 @@ uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
 
 using namespace fluid;
 
+namespace {
+
+// Argument checks shared by fluid_run and fluid_run_nodes, then the cached
+// launch parameters of the (layout plan, arena plan) pair.
+std::shared_ptr<Prepared> checked_prepared(const fluid_graph* gh, const fluid_layout_plan* lh,
+                                           const fluid_arena_plan* ah, void* arena, uint64_t arena_bytes,
+                                           const void* const* consts, const void* const* inputs,
+                                           void* const* outputs, const char* fn) {
+  const std::string f(fn);
+  require(gh && lh && ah, f + ": NULL graph or plan");
+  const Graph& g = gh->g;
+  require(lh->p.graph_serial == gh->serial && ah->a.graph_serial == gh->serial, f + ": plans belong to another graph");
+  require(ah->a.root.size() == (size_t)g.n_edges(), f + ": arena plan size mismatch");
+  if (ah->a.peak > 0) {
+    require(arena != nullptr, f + ": NULL arena");
+    require(aligned(arena, 256), f + ": arena must be 256-byte aligned");
+  }
+  if (arena_bytes < ah->a.peak)
+    fail(FLUID_E_ARENA_TOO_SMALL, f + ": arena has " + std::to_string(arena_bytes) + " bytes, plan needs " +
+                                      std::to_string(ah->a.peak));
+  require(inputs && outputs, f + ": NULL inputs/outputs array");
+  require(consts || g.consts.empty(), f + ": NULL consts array");
+  for (int i = 0; i < g.n_inputs(); ++i)
+    require(inputs[i] && aligned(inputs[i], 16), f + ": input " + std::to_string(i) + " is NULL or not 16-byte aligned");
+  for (size_t i = 0; i < g.outputs.size(); ++i)
+    require(outputs[i] && aligned(outputs[i], 16), f + ": output " + std::to_string(i) + " is NULL or not 16-byte aligned");
+  for (size_t i = 0; i < g.consts.size(); ++i)
+    require(consts[i] && aligned(consts[i], 16), f + ": const " + std::to_string(i) + " is NULL or not 16-byte aligned");
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  // plan serials are never reused, so a stale entry can never match
+  static std::map<std::pair<uint64_t, uint64_t>, std::shared_ptr<Prepared>> cache;
+  auto key = std::make_pair(lh->serial, ah->serial);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  auto prep = prepare(gh, lh, ah);
+  if (cache.size() > 256) cache.clear();
+  cache[key] = prep;
+  return prep;
+}
+
+}  // namespace
+
 extern "C" {
 
 fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah, void* arena,
                        uint64_t arena_bytes, const void* const* consts, const void* const* inputs,
                        void* const* outputs, void* hip_stream) {
   return call_guarded([&] {
-    require(gh && lh && ah, "fluid_run: NULL graph or plan");
-    const Graph& g = gh->g;
-    require(lh->p.graph_serial == gh->serial && ah->a.graph_serial == gh->serial, "fluid_run: plans belong to another graph");
-    require(ah->a.root.size() == (size_t)g.n_edges(), "fluid_run: arena plan size mismatch");
-    if (ah->a.peak > 0) {
-      require(arena != nullptr, "fluid_run: NULL arena");
-      require(aligned(arena, 256), "fluid_run: arena must be 256-byte aligned");
-    }
-    if (arena_bytes < ah->a.peak)
-      fail(FLUID_E_ARENA_TOO_SMALL, "fluid_run: arena has " + std::to_string(arena_bytes) + " bytes, plan needs " +
-                                        std::to_string(ah->a.peak));
-    require(inputs && outputs, "fluid_run: NULL inputs/outputs array");
-    require(consts || g.consts.empty(), "fluid_run: NULL consts array");
-    for (int i = 0; i < g.n_inputs(); ++i)
-      require(inputs[i] && aligned(inputs[i], 16), "fluid_run: input " + std::to_string(i) + " is NULL or not 16-byte aligned");
-    for (size_t i = 0; i < g.outputs.size(); ++i)
-      require(outputs[i] && aligned(outputs[i], 16), "fluid_run: output " + std::to_string(i) + " is NULL or not 16-byte aligned");
-    for (size_t i = 0; i < g.consts.size(); ++i)
-      require(consts[i] && aligned(consts[i], 16), "fluid_run: const " + std::to_string(i) + " is NULL or not 16-byte aligned");
-    std::shared_ptr<Prepared> prep = nullptr;
-    {
-      std::lock_guard<std::mutex> lk(g_cache_mu);
-      // plan serials are never reused, so a stale entry can never match
-      static std::map<std::pair<uint64_t, uint64_t>, std::shared_ptr<Prepared>> cache;
-      auto key = std::make_pair(lh->serial, ah->serial);
-      auto it = cache.find(key);
-      if (it != cache.end()) {
-        prep = it->second;
-      } else {
-        prep = prepare(gh, lh, ah);
-        if (cache.size() > 256) cache.clear();
-        cache[key] = prep;
-      }
-    }
+    std::shared_ptr<Prepared> prep =
+        checked_prepared(gh, lh, ah, arena, arena_bytes, consts, inputs, outputs, "fluid_run");
     Bases B{(char*)arena, inputs, outputs, consts};
     hipStream_t s = (hipStream_t)hip_stream;
     std::unique_lock<std::mutex> tl(g_trace_mu);
@@ -279,6 +289,37 @@ fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const
         fail(FLUID_E_HIP, "node " + std::to_string(pn.node) + " (" + k.name() + "): " + hipGetErrorString(e));
       if (rec >= 0) hip_check(hipEventRecord(g_trace.ev[2 * rec + 1], s), "hipEventRecord");
     }
+  });
+}
+
+fluid_status fluid_run_nodes(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah,
+                             void* arena, uint64_t arena_bytes, const void* const* consts, const void* const* inputs,
+                             void* const* outputs, const int32_t* nodes, int32_t n_nodes, int32_t repeat,
+                             void* hip_stream) {
+  return call_guarded([&] {
+    std::shared_ptr<Prepared> prep =
+        checked_prepared(gh, lh, ah, arena, arena_bytes, consts, inputs, outputs, "fluid_run_nodes");
+    require(nodes && n_nodes > 0 && repeat >= 1, "fluid_run_nodes: empty node list or repeat < 1");
+    std::vector<const PreparedNode*> sel;
+    for (int32_t i = 0; i < n_nodes; ++i) {
+      const int n = nodes[i];
+      require(n >= 0 && n < gh->g.n_nodes(), "fluid_run_nodes: node out of range");
+      const PreparedNode* found = nullptr;
+      for (const PreparedNode& pn : prep->nodes)
+        if (pn.node == n) found = &pn;
+      require(found != nullptr, "fluid_run_nodes: node " + std::to_string(n) + " is a view under this plan");
+      sel.push_back(found);
+    }
+    Bases B{(char*)arena, inputs, outputs, consts};
+    hipStream_t s = (hipStream_t)hip_stream;
+    for (int32_t r = 0; r < repeat; ++r)
+      for (const PreparedNode* pn : sel) {
+        NodeKernel k = pn->k;
+        patch(k, *pn, B);
+        hipError_t e = launch_node_kernel(k, s);
+        if (e != hipSuccess)
+          fail(FLUID_E_HIP, "node " + std::to_string(pn->node) + " (" + k.name() + "): " + hipGetErrorString(e));
+      }
   });
 }
 

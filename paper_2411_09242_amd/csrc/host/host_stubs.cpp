@@ -19,6 +19,12 @@ fluid_status fluid_run(const fluid_graph*, const fluid_layout_plan*, const fluid
   return unsupported("fluid_run");
 }
 
+fluid_status fluid_run_nodes(const fluid_graph*, const fluid_layout_plan*, const fluid_arena_plan*, void*, uint64_t,
+                             const void* const*, const void* const*, void* const*, const int32_t*, int32_t, int32_t,
+                             void*) {
+  return unsupported("fluid_run_nodes");
+}
+
 fluid_status fluid_measure_costs(const fluid_graph*, uint32_t, void*, uint64_t, void*, fluid_cost_table**) {
   return unsupported("fluid_measure_costs");
 }

@@ -82,6 +82,8 @@ _PROTOS = {
                                        C.POINTER(C.c_uint64), C.POINTER(C.c_int64), C.POINTER(C.c_int32)]),
     "fluid_run": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
                             C.POINTER(_VP), _VP]),
+    "fluid_run_nodes": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
+                                  C.POINTER(_VP), C.POINTER(C.c_int32), C.c_int32, C.c_int32, _VP]),
     "fluid_trace_enable": (C.c_int, [_VP, C.POINTER(C.c_uint8), C.c_int32]),
     "fluid_trace_collect": (C.c_int, [_VP, C.POINTER(C.c_double), C.POINTER(C.c_int32)]),
     "fluid_node_kernel": (C.c_int, [_VP, _VP, C.c_int32, C.c_char_p, C.c_uint64]),
@@ -257,6 +259,14 @@ def fluid_run(g, lp, ap, arena_ptr, arena_bytes, const_ptrs, input_ptrs, output_
                           _ptr_array(input_ptrs), _ptr_array(output_ptrs), stream))
 
 
+def fluid_run_nodes(g, lp, ap, arena_ptr, arena_bytes, const_ptrs, input_ptrs, output_ptrs, nodes, repeat,
+                    stream):
+    arr = (C.c_int32 * len(nodes))(*nodes)
+    _check(_L().fluid_run_nodes(g, lp, ap, arena_ptr, arena_bytes, _ptr_array(const_ptrs),
+                                _ptr_array(input_ptrs), _ptr_array(output_ptrs), arr, len(nodes), repeat,
+                                stream))
+
+
 def fluid_trace_enable(g, mask, max_records):
     m = None
     if mask is not None:
@@ -392,6 +402,13 @@ class Executor:
         fluid_run(self.graph.h, self.lplan.h, self.aplan.h, self.arena_ptr, self.aplan.peak,
                   self._cp, self._ip, self._op, s)
         return self.outputs
+
+    def run_nodes(self, nodes, repeat=1, stream=None):
+        """Launch only the kernels of ``nodes`` (in list order), ``repeat``
+        times over, with the bindings of a full run (profiling aid)."""
+        s = stream if stream is not None else self.torch.cuda.current_stream().cuda_stream
+        fluid_run_nodes(self.graph.h, self.lplan.h, self.aplan.h, self.arena_ptr, self.aplan.peak,
+                        self._cp, self._ip, self._op, list(nodes), repeat, s)
 
     def capture(self, steps=1):
         """Record ``steps`` consecutive fluid_run calls into one HIP graph

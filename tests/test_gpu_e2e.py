@@ -103,3 +103,32 @@ def test_random_forced_layouts_on_one_layer(tmp_path):
         say(f"forced trial {trial}")
         out, *_ = _device_run(cfg, x, consts, table=lambda gg: F.CostTable.load(str(path), gg))
         assert_close(out, ref, "f32", f"trial {trial}")
+
+
+def test_run_nodes_replays_the_run_bit_for_bit():
+    """fluid_run_nodes over every launched node, in launch order, is the same
+    computation as fluid_run: the output matches bit for bit; a view node or
+    an empty list is rejected before any launch."""
+    import torch
+    from paper_2411_09242_amd import fluid as F
+    cfg = synth_inputs.config(1)
+    g = F.Graph.transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, g.const_specs(), 1)
+    t = F.CostTable.measure(g, reps=2)
+    lp = F.LayoutPlan(g, t)
+    ap = F.ArenaPlan(g, lp)
+    ex = F.Executor(g, lp, ap, consts, [x])
+    ref = ex.run()[0].clone()
+    torch.cuda.synchronize()
+    launched = [n for n in range(g.n_nodes) if lp.variant[n] >= 0]
+    ex.arena.fill_(0xFF)
+    ex.outputs[0].fill_(float("nan"))
+    ex.run_nodes(launched, repeat=2)
+    torch.cuda.synchronize()
+    assert torch.equal(ex.outputs[0], ref)
+    views = [n for n in range(g.n_nodes) if lp.variant[n] < 0]
+    if views:
+        with pytest.raises(F.FluidError, match="view"):
+            ex.run_nodes([views[0]])
+    with pytest.raises(F.FluidError):
+        ex.run_nodes([])
