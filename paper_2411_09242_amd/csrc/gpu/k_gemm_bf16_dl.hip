@@ -1,30 +1,31 @@
 // bf16 GEMM for a K-contiguous A and an N-contiguous B (the projection
-// shape: activations times a row-major weight), MFMA 16x16x32 bf16 with fp32
-// accumulate, written around two gfx950 features:
+// shape: activations times a row-major weight), MFMA 32x32x16 bf16 with fp32
+// accumulate, written around three gfx950 features:
 //
-//  * A never passes through LDS.  The workgroup tile is 256 x 128 with four
-//    wavefronts stacked along M, so each wavefront owns 64 rows of A and no
-//    other wavefront needs them.  Lane l loads its MFMA operand (8
-//    consecutive k of row l % 16) straight from HBM with one 16-byte buffer
-//    load; the 16 x 32 operand shape puts four lanes on each row, so one
-//    load instruction touches 16 rows of 64 bytes rather than 32 rows of 32.
-//  * B goes from HBM to LDS by direct buffer loads (no registers, no VALU),
-//    in its natural [k][n] form, and is read back with ds_read_b64_tr_b16,
-//    which hands each lane four k-consecutive values of one column n.  Two
-//    such reads make one 8-k MFMA operand.
+//  * both operands go from HBM to LDS by direct buffer loads
+//    (`buffer_load ... lds`: no registers, no VALU work), each in its
+//    natural layout -- A as [m][k] rows of 32 k, B as [k][n] rows of 128 n;
+//  * B is read back with ds_read_b64_tr_b16, which hands each lane four
+//    k-consecutive values of one column n; two such reads make one 8-k MFMA
+//    operand, so the N-contiguous weight never needs a VALU transpose;
+//  * MFMA 32x32x16 bf16, which a single wavefront per SIMD issues at close
+//    to the matrix cores' full rate (the 16x16x32 form reaches about 60%).
 //
-// B lives in a four-stage LDS ring of 32 x 128 tiles; both operands are
-// fetched three K-tiles ahead.  One barrier per K-tile: after a wavefront has
-// waited for its own loads of tile t, the barrier makes every wavefront's
-// part of tile t visible and frees the stage that tile t+3 overwrites.  The
-// barrier is a bare s_barrier behind an explicit counter wait: a workgroup
-// fence would wait for every load in flight, tiles t+1 and t+2 included.
+// Workgroup tile 256 x 128, four wavefronts stacked along M (64 x 128 each).
+// Both tiles live in a four-stage LDS ring (24 KiB per stage) and are loaded
+// three K-tiles ahead.  One barrier per K-tile, a bare s_barrier behind an
+// explicit counter wait: after a wavefront has waited for its own loads of
+// tile t, the barrier makes every wavefront's part of tile t visible and
+// frees the stage that tile t+3 overwrites (a workgroup fence would wait for
+// the later tiles' loads too).
 //
-// LDS tile rows are 256 bytes (128 bf16) with no padding.  The 16-byte
-// chunk c of row r is stored at chunk c ^ (2 (r % 4) + 8 ((r / 8) % 2)): a
-// transpose read by half a wavefront touches rows {0..3, 8..11} (+4 h) at
-// the same two chunks, and the swizzle gives the eight rows eight different
-// 32-byte bank groups.
+// The DMA writes 64 lanes x 16 bytes contiguously, so the bank-conflict
+// swizzles are applied by choosing which 16-byte chunk each lane fetches:
+//  * A row r (64 bytes) stores chunk c at c ^ (((r >> 1) ^ (r >> 3)) & 3):
+//    the 32 rows one A-operand read touches then cover every bank once;
+//  * B row r (256 bytes) stores chunk c at c ^ 4 (r % 4): a transpose read
+//    touches four consecutive rows at the same columns, which the swizzle
+//    puts in four different 64-byte bank groups.
 #include "gemm_common.h"
 #include "launch.h"
 
@@ -34,6 +35,7 @@ namespace {
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) uint4 lds_uint4;
 typedef __attribute__((address_space(3))) void lds_void;
 
 // s_waitcnt immediate (gfx9 encoding) waiting until at most n vector-memory
@@ -41,130 +43,145 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 constexpr int DL_BM = 256, DL_BN = 128, DL_BK = 32, DL_NS = 4;
-constexpr int DL_ROWB = DL_BN * 2;               // bytes per LDS row (one k)
-constexpr int DL_STAGEB = DL_BK * DL_ROWB;       // 8 KiB per stage
+constexpr int DL_AROWB = DL_BK * 2;              // bytes per A row in LDS (one m)
+constexpr int DL_BROWB = DL_BN * 2;              // bytes per B row in LDS (one k)
+constexpr int DL_ASTAGE = DL_BM * DL_AROWB;      // 16 KiB
+constexpr int DL_BSTAGE = DL_BK * DL_BROWB;      // 8 KiB
+
+__device__ __forceinline__ int a_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
 
 }  // namespace
 
 __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
   constexpr int BK = DL_BK, NS = DL_NS;
-  constexpr int FM = 4, FN = 8;  // wavefront tile 64 x 128 in 16 x 16 blocks
-  // one LDS object per stage, so that the compiler can tell a DMA into one
-  // stage from reads of another and does not wait for every load in flight
-  __shared__ __attribute__((aligned(1024))) uint8_t Bs0[DL_STAGEB];
-  __shared__ __attribute__((aligned(1024))) uint8_t Bs1[DL_STAGEB];
-  __shared__ __attribute__((aligned(1024))) uint8_t Bs2[DL_STAGEB];
-  __shared__ __attribute__((aligned(1024))) uint8_t Bs3[DL_STAGEB];
-  auto stage = [&](int st) -> uint8_t* { return st == 0 ? Bs0 : st == 1 ? Bs1 : st == 2 ? Bs2 : Bs3; };
+  constexpr int FM = 2, FN = 4;  // wavefront tile 64 x 128 in 32 x 32 blocks
+  // one LDS object per stage and operand, so that the compiler can tell a
+  // DMA into one stage from reads of another and does not wait for every
+  // load in flight
+  __shared__ __attribute__((aligned(1024))) uint8_t As0[DL_ASTAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t As1[DL_ASTAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t As2[DL_ASTAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t As3[DL_ASTAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t Bs0[DL_BSTAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t Bs1[DL_BSTAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t Bs2[DL_BSTAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t Bs3[DL_BSTAGE];
+  auto astage = [&](int st) -> uint8_t* { return st == 0 ? As0 : st == 1 ? As1 : st == 2 ? As2 : As3; };
+  auto bstage = [&](int st) -> uint8_t* { return st == 0 ? Bs0 : st == 1 ? Bs1 : st == 2 ? Bs2 : Bs3; };
   const TileCoord tc = tile_coord(p, DL_BM, DL_BN);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: DMA base in M0
-  const int lr = lane & 15, lq = lane >> 4;
+  const int lr = lane & 31, lh = lane >> 5;
   const Rsrc ra = make_rsrc(p.A, p.a_bytes);
   const Rsrc rb = make_rsrc(p.B, p.b_bytes);
 
   // Rows of A past M and columns of B past N only feed outputs that are
   // never stored, so they are clamped onto row / column 0 instead of being
   // masked; only k past K has to read as zero.
-  // A: row of fragment i for this lane; 8 k at k0 + 8 lq
-  int32_t a_row[FM];
+  // A DMA: round q of wavefront w fills tile rows 16 (4q + w) .. +15; lane l
+  // writes chunk position l % 4 of row l / 4, holding logical chunk
+  // (l % 4) ^ swizzle(row).
+  int32_t a_src[4];
+  int a_chunk[4];
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const uint32_t m = tc.m0 + wave * 64 + i * 16 + lr;
-    a_row[i] = tc.a_base + (m < p.M ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+  for (int q = 0; q < 4; ++q) {
+    const int row = 16 * (4 * q + wave) + (lane >> 2);
+    const uint32_t m = tc.m0 + row;
+    a_src[q] = tc.a_base + (m < p.M ? row_off(p, m, p.a_m1, p.a_m2) : 0);
+    a_chunk[q] = (lane & 3) ^ a_swz(row);
   }
-  // B: each wavefront DMA instruction fills four 256-byte rows; lane l
-  // writes chunk position l % 16 of row l / 16 of the instruction, which
-  // holds the swizzled logical chunk of that row.  Round q covers rows
-  // 16 q + 4 wave .. +3, so row % 4 = l / 16 and (row / 8) % 2 = wave / 2.
-  const int b_rsub = lane >> 4;                               // row within the instruction
-  const int b_chunk = (lane & 15) ^ (2 * b_rsub + 8 * (wave >> 1));  // logical 16-byte chunk
+  // B DMA: round q fills rows 16 q + 4 w .. +3; lane l writes chunk position
+  // l % 16 of row l / 16, holding logical chunk (l % 16) ^ 4 (row % 4).
+  const int b_rsub = lane >> 4;
+  const int b_chunk = (lane & 15) ^ (4 * b_rsub);
   const uint32_t b_n = tc.n0 + 8 * b_chunk;
   const int32_t b_col = tc.b_base + (int32_t)(b_n < p.N ? b_n : 0);
 
-  auto load_a = [&](uint4 (&R)[FM], uint32_t k0) {
+  auto load = [&](int st, uint32_t k0) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const uint32_t k = k0 + 8 * lq;
-      R[i] = bload16(ra, k < p.K ? 2u * (uint32_t)(a_row[i] + (int32_t)k) : kOOB);
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t k = k0 + 8 * a_chunk[q];
+      const uint32_t off = k < p.K ? 2u * (uint32_t)(a_src[q] + (int32_t)k) : kOOB;
+      lds_void* dst = (lds_void*)(astage(st) + 16 * (4 * q + wave) * DL_AROWB);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, dst, 16, off, 0, 0, 0);
     }
-  };
-  auto load_b = [&](int st, uint32_t k0) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const int row = 16 * q + 4 * wave + b_rsub;
       const uint32_t k = k0 + row;
       const uint32_t off = k < p.K ? 2u * (uint32_t)(b_col + (int32_t)k * p.b_k) : kOOB;
-      lds_void* dst = (lds_void*)(stage(st) + (16 * q + 4 * wave) * DL_ROWB);
+      lds_void* dst = (lds_void*)(bstage(st) + (16 * q + 4 * wave) * DL_BROWB);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst, 16, off, 0, 0, 0);
     }
   };
+  constexpr int kTile = 6;  // DMA instructions per tile and wavefront
 
+  // A operand of block i, k-step kk: row 64 w + 32 i + l % 32, logical chunk
+  // 2 kk + l / 32
+  auto a_addr = [&](int st, int i, int kk) {
+    const int row = wave * 64 + 32 * i + lr;
+    const int chunk = (2 * kk + lh) ^ a_swz(row);
+    return (const lds_uint4*)(astage(st) + row * DL_AROWB + chunk * 16);
+  };
   // transpose-read addressing: lane l (group g = l / 16, s = l % 16) points
-  // at row 8 g + 4 h + s / 4 of the tile, columns 16 j + 4 (s % 4) .. +3;
-  // the read returns column 16 j + l % 16, rows 8 (l / 16) + 4 h .. +3,
-  // which is half of the lane's MFMA operand.
+  // at row 8 (g / 2) + 4 h + s / 4 of the 16-k slice, columns
+  // 32 j + 16 (g % 2) + 4 (s % 4) .. +3; the read returns column
+  // 32 j + (l % 32), rows 8 (l / 32) + 4 h .. +3.
   const int tg = lane >> 4, ts = lane & 15;
-  const int t_row = 8 * tg + (ts >> 2);                        // + 4 h
-  const int t_col = 4 * (ts & 3);                              // + 16 j (elements)
-  auto b_addr = [&](int st, int h, int j) {
-    const int row = 4 * h + t_row;
-    const int col = 16 * j + t_col;
-    const int chunk = (col >> 3) ^ (2 * (row & 3) + 8 * ((row >> 3) & 1));
-    return (lds_v4i16*)(stage(st) + row * DL_ROWB + chunk * 16 + (col & 7) * 2);
+  const int t_row = 8 * (tg >> 1) + (ts >> 2);
+  const int t_col = 16 * (tg & 1) + 4 * (ts & 3);
+  auto b_addr = [&](int st, int kk, int h, int j) {
+    const int row = 16 * kk + 4 * h + t_row;  // row % 4 == ts / 4
+    const int col = 32 * j + t_col;
+    const int chunk = (col >> 3) ^ (4 * (row & 3));
+    return (lds_v4i16*)(bstage(st) + row * DL_BROWB + chunk * 16 + (col & 7) * 2);
   };
 
-  f32x4 acc[FM][FN];
+  f32x16 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  auto compute = [&](int st, const uint4 (&R)[FM]) {
-    bf16x8 b[FN];
+  auto compute = [&](int st) {
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(b_addr(st, 0, j));
-      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(b_addr(st, 1, j));
-      b[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    }
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      bf16x8 a[FM], b[FN];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const bf16x8 a = __builtin_bit_cast(bf16x8, R[i]);
+      for (int i = 0; i < FM; ++i) a[i] = __builtin_bit_cast(bf16x8, *a_addr(st, i, kk));
 #pragma unroll
-      for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < FN; ++j) {
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(b_addr(st, kk, 0, j));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(b_addr(st, kk, 1, j));
+        b[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
   };
 
-  // Tile t: A in register set t % 4, B in stage t % 4.  Loads are issued in
-  // the order A(t), B(t) and past the end of K they read zeros, so the loop
-  // runs whole groups of four tiles and skips the MFMAs of the padding.
+  // Tile t lives in stage t % 4.  Loads past the end of K read zeros, so
+  // the loop runs whole groups of four tiles (padding tiles add zeros).
   const uint32_t nt = (p.K + BK - 1) / BK;
-  uint4 RA0[FM], RA1[FM], RA2[FM], RA3[FM];
-  load_a(RA0, 0);
-  load_b(0, 0);
-  load_a(RA1, BK);
-  load_b(1, BK);
-  load_a(RA2, 2 * BK);
-  load_b(2, 2 * BK);
-  // After the loads of tile t, tiles t+1 and t+2 (2 x (FM + 2) loads) may
-  // still be in flight.
-  constexpr int kAhead = 2 * (FM + 2);
+  load(0, 0);
+  load(1, BK);
+  load(2, 2 * BK);
   for (uint32_t t = 0; t < nt; t += 4) {
-#define FLUID_DL_STEP(U, RCUR, RNEXT)                                \
-  asm volatile("" ::: "memory");                                     \
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(kAhead));                     \
-  __builtin_amdgcn_s_barrier();                                      \
-  asm volatile("" ::: "memory");                                     \
-  load_a(RNEXT, (t + U + 3) * BK);                                   \
-  load_b((U + 3) % NS, (t + U + 3) * BK);                            \
-  if (t + U < nt) compute(U, RCUR);
-    FLUID_DL_STEP(0, RA0, RA3)
-    FLUID_DL_STEP(1, RA1, RA0)
-    FLUID_DL_STEP(2, RA2, RA1)
-    FLUID_DL_STEP(3, RA3, RA2)
+#define FLUID_DL_STEP(U)                                            \
+  asm volatile("" ::: "memory");                                    \
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kTile));                 \
+  __builtin_amdgcn_s_barrier();                                     \
+  asm volatile("" ::: "memory");                                    \
+  load((U + 3) % NS, (t + U + 3) * BK);                             \
+  compute(U);
+    FLUID_DL_STEP(0)
+    FLUID_DL_STEP(1)
+    FLUID_DL_STEP(2)
+    FLUID_DL_STEP(3)
 #undef FLUID_DL_STEP
   }
 
@@ -173,11 +190,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const uint32_t n = tc.n0 + j * 16 + lr;
+      const uint32_t n = tc.n0 + j * 32 + lr;
       if (n >= p.N) continue;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const uint32_t m = tc.m0 + wave * 64 + i * 16 + 4 * lq + v;
+      for (int v = 0; v < 16; ++v) {
+        const uint32_t m = tc.m0 + wave * 64 + i * 32 + 8 * (v / 4) + 4 * lh + (v % 4);
         if (m < p.M) C[tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n * p.c_n] = f32_to_bf16(acc[i][j][v]);
       }
     }
