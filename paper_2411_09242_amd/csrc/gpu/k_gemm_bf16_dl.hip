@@ -1,10 +1,12 @@
 // bf16 GEMM for a K-contiguous A and an N-contiguous B (the projection
-// shape: activations times a row-major weight), MFMA 32x32x16 bf16 with fp32
-// accumulate, written around three gfx950 features:
+// shape: activations times a row-major weight) or a K-contiguous B (Q K^T
+// with K stored [S, D]), MFMA 32x32x16 bf16 with fp32 accumulate, written
+// around three gfx950 features:
 //
 //  * both operands go from HBM to LDS by direct buffer loads
 //    (`buffer_load ... lds`: no registers, no VALU work), each in its
-//    natural layout -- A as [m][k] rows of 32 k, B as [k][n] rows of 128 n;
+//    natural layout -- A as [m][k] rows of 32 k, an N-contiguous B as [k][n]
+//    rows of 128 n, a K-contiguous B as [n][k] rows of 32 k;
 //  * B is read back with ds_read_b64_tr_b16, which hands each lane four
 //    k-consecutive values of one column n; two such reads make one 8-k MFMA
 //    operand, so the N-contiguous weight never needs a VALU transpose;
@@ -23,9 +25,16 @@
 // swizzles are applied by choosing which 16-byte chunk each lane fetches:
 //  * A row r (64 bytes) stores chunk c at c ^ (((r >> 1) ^ (r >> 3)) & 3):
 //    the 32 rows one A-operand read touches then cover every bank once;
-//  * B row r (256 bytes) stores chunk c at c ^ 4 (r % 4): a transpose read
-//    touches four consecutive rows at the same columns, which the swizzle
-//    puts in four different 64-byte bank groups.
+//  * an N-contiguous B row r (256 bytes) stores chunk c at c ^ 4 (r % 4): a
+//    transpose read touches four consecutive rows at the same columns,
+//    which the swizzle puts in four different 64-byte bank groups; a
+//    K-contiguous B is laid out and read like A.
+//
+// The output tile leaves through LDS when C is N- or M-contiguous, so that
+// every lane writes 16 contiguous bytes (an S x S score matrix is mostly
+// store traffic): each wavefront parks its 64 x 128 bf16 tile in its own
+// 16 KiB of the ring, swizzled so that both the parking writes and the
+// 16-byte reads are conflict-free.
 #include "gemm_common.h"
 #include "launch.h"
 
@@ -52,6 +61,7 @@ __device__ __forceinline__ int a_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; 
 
 }  // namespace
 
+template <int BMD>
 __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
   constexpr int BK = DL_BK, NS = DL_NS;
   constexpr int FM = 2, FN = 4;  // wavefront tile 64 x 128 in 32 x 32 blocks
@@ -90,12 +100,23 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
     a_src[q] = tc.a_base + (m < p.M ? row_off(p, m, p.a_m1, p.a_m2) : 0);
     a_chunk[q] = (lane & 3) ^ a_swz(row);
   }
-  // B DMA: round q fills rows 16 q + 4 w .. +3; lane l writes chunk position
-  // l % 16 of row l / 16, holding logical chunk (l % 16) ^ 4 (row % 4).
+  // N-contiguous B DMA: round q fills rows 16 q + 4 w .. +3; lane l writes
+  // chunk position l % 16 of row l / 16, holding logical chunk
+  // (l % 16) ^ 4 (row % 4).  K-contiguous B DMA: like A, round q of
+  // wavefront w fills rows (n) 16 (4q + w) .. +15.
   const int b_rsub = lane >> 4;
   const int b_chunk = (lane & 15) ^ (4 * b_rsub);
   const uint32_t b_n = tc.n0 + 8 * b_chunk;
   const int32_t b_col = tc.b_base + (int32_t)(b_n < p.N ? b_n : 0);
+  int32_t bk_src[2];
+  int bk_chunk[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int row = 16 * (4 * q + wave) + (lane >> 2);
+    const uint32_t n = tc.n0 + row;
+    bk_src[q] = tc.b_base + (int32_t)(n < p.N ? n : 0) * p.b_n;
+    bk_chunk[q] = (lane & 3) ^ a_swz(row);
+  }
 
   auto load = [&](int st, uint32_t k0) {
 #pragma unroll
@@ -107,11 +128,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
     }
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int row = 16 * q + 4 * wave + b_rsub;
-      const uint32_t k = k0 + row;
-      const uint32_t off = k < p.K ? 2u * (uint32_t)(b_col + (int32_t)k * p.b_k) : kOOB;
-      lds_void* dst = (lds_void*)(bstage(st) + (16 * q + 4 * wave) * DL_BROWB);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst, 16, off, 0, 0, 0);
+      if constexpr (BMD == GM_MN) {
+        const int row = 16 * q + 4 * wave + b_rsub;
+        const uint32_t k = k0 + row;
+        const uint32_t off = k < p.K ? 2u * (uint32_t)(b_col + (int32_t)k * p.b_k) : kOOB;
+        lds_void* dst = (lds_void*)(bstage(st) + (16 * q + 4 * wave) * DL_BROWB);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst, 16, off, 0, 0, 0);
+      } else {
+        const uint32_t k = k0 + 8 * bk_chunk[q];
+        const uint32_t off = k < p.K ? 2u * (uint32_t)(bk_src[q] + (int32_t)k) : kOOB;
+        lds_void* dst = (lds_void*)(bstage(st) + 16 * (4 * q + wave) * DL_AROWB);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst, 16, off, 0, 0, 0);
+      }
     }
   };
   constexpr int kTile = 6;  // DMA instructions per tile and wavefront
@@ -153,9 +181,16 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
       for (int i = 0; i < FM; ++i) a[i] = __builtin_bit_cast(bf16x8, *a_addr(st, i, kk));
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(b_addr(st, kk, 0, j));
-        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(b_addr(st, kk, 1, j));
-        b[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        if constexpr (BMD == GM_MN) {
+          const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(b_addr(st, kk, 0, j));
+          const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(b_addr(st, kk, 1, j));
+          b[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        } else {
+          // [n][k] rows like A: row 32 j + l % 32, logical chunk 2 kk + l / 32
+          const int row = 32 * j + lr;
+          const int chunk = (2 * kk + lh) ^ a_swz(row);
+          b[j] = __builtin_bit_cast(bf16x8, *(const lds_uint4*)(bstage(st) + row * DL_AROWB + chunk * 16));
+        }
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -186,6 +221,73 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
   }
 
   uint16_t* C = (uint16_t*)p.C;
+  const uint32_t wm0 = tc.m0 + wave * 64;  // first row of this wavefront's tile
+  if (p.cmode == 1 || p.cmode == 2) {
+    // the padding tiles' loads land in the ring: drain them, and let every
+    // wavefront finish its last tile, before the ring is reused
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __syncthreads();
+    uint16_t* cs = (uint16_t*)astage(wave);  // 16 KiB: this wavefront's 64 x 128 tile
+    if (p.cmode == 1) {
+      // row-major [64][128], 16-byte chunk c of row r at c ^ (r % 16)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int r = i * 32 + 8 * (v / 4) + 4 * lh + (v % 4), c = j * 32 + lr;
+            cs[r * 128 + (((c >> 3) ^ (r & 15)) << 3) + (c & 7)] = f32_to_bf16(acc[i][j][v]);
+          }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own parking writes done
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int r = 4 * u + (lane >> 4), ch = lane & 15;
+        const uint4 val = *(const uint4*)&cs[r * 128 + ((ch ^ (r & 15)) << 3)];
+        const uint32_t m = wm0 + r, n0 = tc.n0 + 8 * ch;
+        if (m >= p.M || n0 >= p.N) continue;
+        uint16_t* dst = C + tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n0;
+        if (n0 + 8 <= p.N && ((uintptr_t)dst & 15u) == 0) {
+          *(uint4*)dst = val;
+        } else {
+          const uint32_t w[4] = {val.x, val.y, val.z, val.w};
+          for (int e = 0; e < 8 && n0 + e < p.N; ++e) dst[e] = (uint16_t)(w[e / 2] >> (16 * (e & 1)));
+        }
+      }
+    } else {
+      // column-major [128][64] (rows contiguous), 16-byte chunk c of column
+      // n at c ^ ((n / 2) % 8); a lane parks 4 consecutive rows (8 bytes)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int vg = 0; vg < 4; ++vg) {
+            const int r0 = i * 32 + 8 * vg + 4 * lh, c = j * 32 + lr;
+            const uint32_t lo = (uint32_t)f32_to_bf16(acc[i][j][4 * vg]) | ((uint32_t)f32_to_bf16(acc[i][j][4 * vg + 1]) << 16);
+            const uint32_t hi = (uint32_t)f32_to_bf16(acc[i][j][4 * vg + 2]) | ((uint32_t)f32_to_bf16(acc[i][j][4 * vg + 3]) << 16);
+            *(uint2*)&cs[c * 64 + ((((r0 >> 3) ^ ((c >> 1) & 7))) << 3) + (r0 & 7)] = make_uint2(lo, hi);
+          }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int c = 8 * u + (lane >> 3), ch = lane & 7;
+        const uint4 val = *(const uint4*)&cs[c * 64 + ((ch ^ ((c >> 1) & 7)) << 3)];
+        const uint32_t n = tc.n0 + c, m0 = wm0 + 8 * ch;
+        if (n >= p.N || m0 >= p.M) continue;
+        const uint32_t m2 = m0 - fdiv(m0, p.m2div) * p.M2;  // position within the M2 run
+        uint16_t* dst = C + tc.c_base + row_off(p, m0, p.c_m1, p.c_m2) + (int32_t)n * p.c_n;
+        if (m0 + 8 <= p.M && m2 + 8 <= p.M2 && ((uintptr_t)dst & 15u) == 0) {
+          *(uint4*)dst = val;
+        } else {
+          const uint32_t w[4] = {val.x, val.y, val.z, val.w};
+          for (int e = 0; e < 8 && m0 + e < p.M; ++e)
+            C[tc.c_base + row_off(p, m0 + e, p.c_m1, p.c_m2) + (int32_t)n * p.c_n] = (uint16_t)(w[e / 2] >> (16 * (e & 1)));
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -194,7 +296,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
       if (n >= p.N) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const uint32_t m = tc.m0 + wave * 64 + i * 32 + 8 * (v / 4) + 4 * lh + (v % 4);
+        const uint32_t m = wm0 + i * 32 + 8 * (v / 4) + 4 * lh + (v % 4);
         if (m < p.M) C[tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n * p.c_n] = f32_to_bf16(acc[i][j][v]);
       }
     }
@@ -202,8 +304,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
 
 hipError_t launch_gemm_bf16_dl(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
-  if (k.dtype != DT_BF16 || k.amode != GM_K || k.bmode != GM_MN) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gemm_bf16_dl_kernel, dim3(p.tiles_m * p.tiles_n * p.G), dim3(256), 0, s, p);
+  if (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_MN && k.bmode != GM_K)) return hipErrorInvalidValue;
+  const dim3 grid(p.tiles_m * p.tiles_n * p.G);
+  if (k.bmode == GM_MN) hipLaunchKernelGGL((gemm_bf16_dl_kernel<GM_MN>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((gemm_bf16_dl_kernel<GM_K>), grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
