@@ -138,6 +138,45 @@ __global__ __launch_bounds__(256) void ew_tiled_kernel(EwParams p) {
   }
 }
 
+// VEC > 1: each thread rotates VEC consecutive pairs (D unit-stride in x and
+// y; the host scaled the innermost extent and strides to pieces).
+template <typename T, int VEC>
+__global__ __launch_bounds__(256) void rope_vec_kernel(RopeParams p) {
+  const uint32_t step = gridDim.x * 256u;
+  for (uint32_t v = blockIdx.x * 256u + threadIdx.x; v < p.total; v += step) {
+    uint32_t rest = v;
+    int32_t xo = 0, yo = 0;
+    uint32_t pos = 0, i = 0;
+#pragma unroll
+    for (int d = 3; d >= 0; --d) {
+      const uint32_t q = fdiv(rest, p.div[d]);
+      const uint32_t id = rest - q * p.ext[d];
+      rest = q;
+      xo += (int32_t)id * p.xs[d];
+      yo += (int32_t)id * p.ys[d];
+      if (d == p.pos_dim) pos = id;
+      if (d == p.half_dim) i = id * VEC;
+    }
+    float c[VEC], s[VEC], x1[VEC], x2[VEC], y1[VEC], y2[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; e += 4) {
+      const float4 cc = *(const float4*)(p.cos_t + pos * p.half + i + e);
+      const float4 ss = *(const float4*)(p.sin_t + pos * p.half + i + e);
+      c[e] = cc.x; c[e + 1] = cc.y; c[e + 2] = cc.z; c[e + 3] = cc.w;
+      s[e] = ss.x; s[e + 1] = ss.y; s[e + 2] = ss.z; s[e + 3] = ss.w;
+    }
+    load_vec<T, VEC>(p.x, xo, x1);
+    load_vec<T, VEC>(p.x, xo + p.x_half, x2);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      y1[e] = x1[e] * c[e] - x2[e] * s[e];
+      y2[e] = x2[e] * c[e] + x1[e] * s[e];
+    }
+    store_vec<T, VEC>(p.y, yo, y1);
+    store_vec<T, VEC>(p.y, yo + p.y_half, y2);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kernel(RopeParams p) {
   const uint32_t step = gridDim.x * 256u;
@@ -218,8 +257,14 @@ hipError_t launch_elementwise(const NodeKernel& k, hipStream_t s) {
 
 hipError_t launch_rope(const NodeKernel& k, hipStream_t s) {
   const uint32_t g = grid_for(k.rope.total);
-  if (k.dtype == DT_BF16) hipLaunchKernelGGL(rope_kernel<uint16_t>, dim3(g), dim3(256), 0, s, k.rope);
-  else hipLaunchKernelGGL(rope_kernel<float>, dim3(g), dim3(256), 0, s, k.rope);
+  if (k.vec > 1) {
+    if (k.dtype == DT_BF16) hipLaunchKernelGGL((rope_vec_kernel<uint16_t, 8>), dim3(g), dim3(256), 0, s, k.rope);
+    else hipLaunchKernelGGL((rope_vec_kernel<float, 4>), dim3(g), dim3(256), 0, s, k.rope);
+  } else if (k.dtype == DT_BF16) {
+    hipLaunchKernelGGL(rope_kernel<uint16_t>, dim3(g), dim3(256), 0, s, k.rope);
+  } else {
+    hipLaunchKernelGGL(rope_kernel<float>, dim3(g), dim3(256), 0, s, k.rope);
+  }
   return hipGetLastError();
 }
 

@@ -163,6 +163,17 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
     if (e0 < valid) u = *(const uint4*)(x + e0);
     Piece<T>::unpack(u, v[c]);
   }
+  // gamma / beta pieces are fetched with the row, not after the reduction,
+  // so the row costs one memory round trip
+  uint4 gq[OP == RED_SOFTMAX ? 1 : NC], bq[OP == RED_LAYERNORM ? NC : 1];
+  if constexpr (OP != RED_SOFTMAX) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const uint32_t e0 = (uint32_t)(lane + 64 * c) * VEC;
+      gq[c] = e0 < R ? *(const uint4*)((const T*)p.gamma + e0) : make_uint4(0, 0, 0, 0);
+      if constexpr (OP == RED_LAYERNORM) bq[c] = e0 < R ? *(const uint4*)((const T*)p.beta + e0) : make_uint4(0, 0, 0, 0);
+    }
+  }
   if constexpr (OP == RED_SOFTMAX) {
     float m = -INFINITY;
 #pragma unroll
@@ -225,8 +236,8 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
       const uint32_t e0 = (uint32_t)(lane + 64 * c) * VEC;
       if (e0 < R) {
         float g[VEC], b[VEC];
-        Piece<T>::unpack(*(const uint4*)((const T*)p.gamma + e0), g);
-        if constexpr (OP == RED_LAYERNORM) Piece<T>::unpack(*(const uint4*)((const T*)p.beta + e0), b);
+        Piece<T>::unpack(gq[c], g);
+        if constexpr (OP == RED_LAYERNORM) Piece<T>::unpack(bq[c], b);
 #pragma unroll
         for (int i = 0; i < VEC; ++i) {
           v[c][i] = (v[c][i] - mean) * rstd * g[i];

@@ -216,6 +216,18 @@ NodeKernel prepare_rope(const Node&, int dtype, const std::vector<Operand>& ins,
   p.y = const_cast<void*>(out.ptr);
   p.cos_t = (const float*)ins[1].ptr;
   p.sin_t = (const float*)ins[2].ptr;
+  // 16-byte pieces along D/2 when D is unit-stride in x and y
+  const int VEC = k.dtype == DT_BF16 ? 8 : 4;
+  bool vec_ok = p.half_dim == 3 && p.xs[3] == 1 && p.ys[3] == 1 && half % VEC == 0 && aligned16(p.x) &&
+                aligned16(p.y) && aligned16(p.cos_t) && aligned16(p.sin_t) && p.x_half % VEC == 0 && p.y_half % VEC == 0;
+  for (int i = 0; i < 3; ++i) vec_ok = vec_ok && p.xs[i] % VEC == 0 && p.ys[i] % VEC == 0;
+  if (vec_ok) {
+    k.vec = VEC;
+    p.ext[3] = (uint32_t)(half / VEC);
+    p.div[3] = make_fastdiv(p.ext[3]);
+    p.xs[3] = p.ys[3] = VEC;
+    p.total /= (uint32_t)VEC;
+  }
   k.available = true;
   return k;
 }
@@ -421,7 +433,7 @@ std::string NodeKernel::name() const {
     case KF_VIEW: return "view";
     case KF_EW: return "ew_" + std::string(ew_names[ew.op]) + "_" + dt + "_v" + std::to_string(vec);
     case KF_EW_TILED: return "ew_tiled_" + std::string(ew_names[ew.op]) + "_" + dt;
-    case KF_ROPE: return "rope_" + dt;
+    case KF_ROPE: return "rope_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
     case KF_GEMM: {
