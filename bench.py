@@ -125,6 +125,72 @@ def time_nodes(ex, nodes, repeat, torch, marker=None):
     return e0.elapsed_time(e1) / repeat
 
 
+def op_class_rates(F, g, lp, ex, steps, torch):
+    """Per operator class: ms per step of its launches back to back (one
+    HIP graph), and the rate against the class's bound."""
+    by_op = {}
+    for n in range(g.n_nodes):
+        if lp.variant[n] >= 0:
+            by_op.setdefault(g.desc["nodes"][n]["op"], []).append(n)
+    out = {}
+    for op, nodes in by_op.items():
+        ms_c = time_nodes(ex, nodes, max(3, min(steps, 20)), torch)
+        kind = node_work(g, nodes[0])[0]
+        work = sum(node_work(g, n)[1] for n in nodes)
+        if kind == "flop":
+            rate = work / (ms_c * 1e-3) / 1e12
+            peak, unit = PEAK_TFLOPS[g.dtype], "TFLOP/s"
+        else:
+            rate = work / (ms_c * 1e-3) / 1e9
+            peak, unit = PEAK_HBM_GBS, "GB/s"
+        out[op] = {"ms_per_step": round(ms_c, 4), "launches_per_step": len(nodes),
+                   "achieved": round(rate, 2), "unit": unit, "frac": round(rate / peak, 4)}
+    return dict(sorted(out.items(), key=lambda kv: -kv[1]["ms_per_step"]))
+
+
+def graph_ms(ex, steps, torch, marker=None):
+    """ms per step: `steps` runs captured in one HIP graph, one warm-up
+    replay, one replay between two events."""
+    hg = ex.capture(steps=steps)
+    hg.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if marker:
+        MARK.push(marker)
+    e0.record()
+    hg.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    if marker:
+        MARK.pop()
+    del hg
+    return e0.elapsed_time(e1) / steps
+
+
+def ablation(F, g, table, ex, steps, torch):
+    """Layout DP and kernel variants switched on one at a time (same cost
+    table, same Greedy-by-Size arena planner): graph latency, planned table
+    total and per-operator-class times of each plan."""
+    out = {}
+    for name, flags in (("identity_layouts_variant0", F.NO_DP | F.NO_VARIANTS),
+                        ("identity_layouts_best_variant", F.NO_DP),
+                        ("dp_layouts_variant0", F.NO_VARIANTS),
+                        ("dp_layouts_best_variant", 0)):
+        lp_a = F.LayoutPlan(g, table, flags)
+        ap_a = F.ArenaPlan(g, lp_a)
+        ex_a = F.Executor(g, lp_a, ap_a, ex.consts, ex.inputs)
+        for _ in range(2):
+            ex_a.run()
+        torch.cuda.synchronize()
+        out[name] = {"ms_per_step": round(graph_ms(ex_a, steps, torch), 4), "table_ns": lp_a.total_ns,
+                     "launches_per_step": sum(1 for v in lp_a.variant if v >= 0),
+                     "peak_arena_mb": round(ap_a.peak / 2**20, 3),
+                     "op_ms": {op: c["ms_per_step"] for op, c in op_class_rates(F, g, lp_a, ex_a, steps, torch).items()}}
+        del ex_a
+        torch.cuda.empty_cache()
+    return out
+
+
 def calibration_copy(torch, mib=256):
     """A plain device-to-device copy of known size, inside its own marker
     range: HBM counters of the kernels are scaled by what the same counters
@@ -205,24 +271,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     sig_ms = {k: time_nodes(ex, v, 3, torch) for k, v in by_sig.items()}
     dom_key = max(by_sig, key=lambda k: sig_ms[k])
     dom_nodes = by_sig[dom_key]
-    # per operator class: time per step and achieved rate against its bound
-    by_op = {}
-    for n in launched:
-        by_op.setdefault(g.desc["nodes"][n]["op"], []).append(n)
-    op_classes = {}
-    for op, nodes in by_op.items():
-        ms_c = time_nodes(ex, nodes, max(3, min(steps, 20)), torch)
-        kind = node_work(g, nodes[0])[0]
-        work = sum(node_work(g, n)[1] for n in nodes)
-        if kind == "flop":
-            rate = work / (ms_c * 1e-3) / 1e12
-            peak, unit = PEAK_TFLOPS[g.dtype], "TFLOP/s"
-        else:
-            rate = work / (ms_c * 1e-3) / 1e9
-            peak, unit = PEAK_HBM_GBS, "GB/s"
-        op_classes[op] = {"ms_per_step": round(ms_c, 4), "launches_per_step": len(nodes),
-                          "achieved": round(rate, 2), "unit": unit, "frac": round(rate / peak, 4)}
-    op_classes = dict(sorted(op_classes.items(), key=lambda kv: -kv[1]["ms_per_step"]))
+    op_classes = op_class_rates(F, g, lp, ex, steps, torch)
 
     # timed region 1: K eager steps (whole graph, no per-launch events)
     MARK.push(f"{wl}/eager_timed")
@@ -276,6 +325,8 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
                  "positions_in_step": [launched.index(n) for n in dom_nodes],
                  "work_per_launch": work, "work_unit": "flop" if kind == "flop" else "byte"})
 
+    abl = ablation(F, g, table, ex, steps, torch)
+
     # planned vs naive outputs (same inputs, different layouts and kernels)
     out = ex.run(stream)[0].float()
     out_n = ex_naive.run(stream)[0].float()
@@ -293,6 +344,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         "planned_vs_naive_max_abs_diff": agree, "cost_table_s": round(t_measure, 1),
         "roofline": roof,
         "op_classes": op_classes,
+        "ablation": abl,
     }
     del ex, ex_naive
     torch.cuda.empty_cache()

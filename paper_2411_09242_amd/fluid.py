@@ -108,6 +108,11 @@ def load(host_only=False):
     path = os.path.join(LIBDIR, name)
     if not os.path.exists(path):
         raise FileNotFoundError(f"{path} is not built; run `python -m paper_2411_09242_amd.build`")
+    if not host_only:
+        # torch carries its own HIP runtime; loading it first makes the
+        # library bind to that same runtime instead of bringing a second one
+        # into the process (two runtimes do not share devices or memory)
+        import torch  # noqa: F401
     lib = C.CDLL(path)
     for sym, (res, args) in _PROTOS.items():
         f = getattr(lib, sym)
