@@ -30,6 +30,34 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 
+# HBM bytes per launch of each workload's dominant kernel: two rocprofv3
+# --pmc passes (FETCH_SIZE, then WRITE_SIZE) over that kernel, each scaled by
+# what the same counter read for the 256 MiB calibration copy (FETCH_SIZE
+# 0.5001x, WRITE_SIZE 1.0000x).  Reported as `traffic` only for the same
+# (workload, kernel, output shape) and only while the kernel sources hash to
+# TRAFFIC_SRC -- a changed kernel makes the figure stale, and then null.
+TRAFFIC_SRC = "f6ed162e81e8d3ce"
+TRAFFIC = {
+    ("bert-base-12l-b1-s128-h768", "gemm_f32_dl32w4_amn_bmn_cn", (1, 128, 3072)): 14281158,
+    ("gpt2-small-12l-b1-s512-h768-prefill", "gemm_f32_dl32w4_ak_bmn_cm", (1, 512, 3072)): 28415210,
+    ("bert-large-24l-b8-s512-h1024", "gemm_f32_t128_ak_bmn_cm", (8, 512, 4096)): 230888216,
+    ("llama-8l-b1-s2048-h4096-prefill", "gemm_bf16_p256x128_ak_bmn_cn", (1, 2048, 11008)): 913730701,
+}
+
+
+def kernel_source_hash():
+    import glob
+    import hashlib
+    d = os.path.join(ROOT, "paper_2411_09242_amd", "csrc")
+    files = sorted(glob.glob(os.path.join(d, "gpu", "*.hip")) + glob.glob(os.path.join(d, "gpu", "*.h")) +
+                   [os.path.join(d, "host", "dispatch.cpp"), os.path.join(d, "host", "kparams.h")])
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -230,17 +258,29 @@ def cpu_baseline(cfg, budget_s=20.0):
             "sample": f"whole {cfg['layers']}-layer graph, {len(times)} run(s), median; float64 NumPy"}
 
 
-def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=None):
-    """Cost table (untimed), plans, then the two timed regions; returns a dict."""
+def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=None, tables=None,
+                     kernel_only=False):
+    """Cost table (untimed), plans, then the timed regions; returns a dict.
+    tables: (directory, "save" | "load") -- keep each workload's measured
+    table, or plan from a kept one instead of measuring (same plan, e.g. for
+    counter runs).  kernel_only: after planning, launch only the dominant
+    kernel's nodes K times (eagerly) and return which kernel that was."""
     g = F.Graph.transformer(cfg)
     wl = cfg["name"]
     stream = torch.cuda.current_stream().cuda_stream
     t = time.time()
-    MARK.push(f"{wl}/cost_table")
-    table = F.CostTable.measure(g, reps=reps)
-    MARK.pop()
+    tpath = os.path.join(tables[0], wl + ".json") if tables else None
+    if tables and tables[1] == "load":
+        table = F.CostTable.load(tpath, g)
+    else:
+        MARK.push(f"{wl}/cost_table")
+        table = F.CostTable.measure(g, reps=reps)
+        MARK.pop()
+        if tables:
+            os.makedirs(tables[0], exist_ok=True)
+            table.save(tpath)
     t_measure = time.time() - t
-    log(f"{cfg['name']}: cost table measured in {t_measure:.1f} s")
+    log(f"{cfg['name']}: cost table ready in {t_measure:.1f} s")
     if save_table:
         table.save(save_table)
     lp = F.LayoutPlan(g, table)
@@ -268,9 +308,20 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
                tuple(tuple(g.edge_shape(v)) if v >= 0 else ("c",) + tuple(g.desc["consts"][~v]["shape"])
                      for v in nd["ins"]))
         by_sig.setdefault(key, []).append(n)
-    sig_ms = {k: time_nodes(ex, v, 3, torch) for k, v in by_sig.items()}
-    dom_key = max(by_sig, key=lambda k: sig_ms[k])
+    # dominant kernel: the signature with the largest summed algorithmic
+    # time at its bound's peak (flops / MFMA peak or bytes / HBM peak) --
+    # fixed by the graph and the plan, not by timing noise or by the
+    # per-dispatch overhead a tracer adds
+    def ideal_ms(nodes):
+        kind, work = node_work(g, nodes[0])
+        return len(nodes) * work / ((PEAK_TFLOPS[g.dtype] * 1e12) if kind == "flop" else (PEAK_HBM_GBS * 1e9))
+    dom_key = max(by_sig, key=lambda k: (ideal_ms(by_sig[k]), -by_sig[k][0]))
     dom_nodes = by_sig[dom_key]
+    if kernel_only:
+        ex.run_nodes(dom_nodes, steps, stream)
+        torch.cuda.synchronize()
+        return {"kernel": dom_key[0], "node_op": dom_key[1], "out_shape": list(dom_key[2]),
+                "launches": steps * len(dom_nodes)}
     op_classes = op_class_rates(F, g, lp, ex, steps, torch)
 
     # timed region 1: K eager steps (whole graph, no per-launch events)
@@ -316,10 +367,14 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         peak = PEAK_TFLOPS[g.dtype]
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": None}
+        if kernel_source_hash() == TRAFFIC_SRC:
+            roof["traffic"] = TRAFFIC.get((wl, dom_key[0], tuple(dom_key[2])))
     else:
         achieved = work / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+        if kernel_source_hash() == TRAFFIC_SRC:
+            roof["traffic"] = TRAFFIC.get((wl, dom_key[0], tuple(dom_key[2])))
     roof.update({"kernel": dom_key[0], "node_op": dom_key[1], "out_shape": list(dom_key[2]),
                  "avg_launch_us": round(avg_ms * 1e3, 3), "launches": launches,
                  "positions_in_step": [launched.index(n) for n in dom_nodes],
@@ -388,6 +443,10 @@ def main():
     ap.add_argument("--reps", type=int, default=7, help="timed launches per cost-table entry")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--save-table", default=None)
+    ap.add_argument("--tables-dir", default=None, help="directory for every workload's cost table")
+    ap.add_argument("--tables-mode", choices=("save", "load"), default="save")
+    ap.add_argument("--kernel-only", action="store_true",
+                    help="launch only each workload's dominant kernel (for counter runs); prints what ran")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
@@ -403,8 +462,15 @@ def main():
     calibration_copy(torch)
     cfg = synth_inputs.config(a.config)
     log(f"workload {cfg['name']}")
-    x, consts = synth_inputs.make_inputs(cfg, F.Graph.transformer(cfg).const_specs(), a.config)
-    r = measure_workload(F, torch, cfg, x, consts, a.steps, a.warmup, a.reps, a.save_table)
+    if a.kernel_only:   # values do not matter for which kernel runs or the bytes it moves
+        x, consts = device_inputs(torch, F, cfg, a.config)
+    else:
+        x, consts = synth_inputs.make_inputs(cfg, F.Graph.transformer(cfg).const_specs(), a.config)
+    tables = (a.tables_dir, a.tables_mode) if a.tables_dir else None
+    r = measure_workload(F, torch, cfg, x, consts, a.steps, a.warmup, a.reps, a.save_table, tables, a.kernel_only)
+    if a.kernel_only:
+        print(json.dumps({"kernel_only": True, "workload": cfg["name"], **r}), flush=True)
+        return
     res = {
         "metric": "graph latency (ms) + peak arena MB vs naive plan; kernel % of roofline",
         "value": r["ms_per_step"], "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
@@ -426,7 +492,7 @@ def main():
         log(f"extra workload {c['name']}")
         xe, ce = device_inputs(torch, F, c, idx)
         st = max(5, a.steps // 5) if idx in (4, 5) else a.steps
-        e = measure_workload(F, torch, c, xe, ce, st, max(2, a.warmup // 5), max(2, a.reps // 2))
+        e = measure_workload(F, torch, c, xe, ce, st, max(2, a.warmup // 5), max(2, a.reps // 2), None, tables)
         e.update({"workload": c["name"], "dtype": c["dtype"], "steps": st,
                   "data": "synthetic, drawn on the GPU"})
         extras[f"cfg{idx}"] = e
