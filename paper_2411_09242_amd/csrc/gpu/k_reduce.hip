@@ -249,6 +249,128 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
   }
 }
 
+// Row family with 16-byte pieces, one 256-thread workgroup per row (for
+// long rows when there are too few rows to keep one wavefront per row busy:
+// four times the wavefronts, a quarter of the pieces each).  NC pieces per
+// thread, piece c of thread t at t + 256 c; reductions through LDS.
+template <typename T, int NC, int OP>
+__global__ __launch_bounds__(256) void red_rowb_kernel(RedParams p) {
+  constexpr int VEC = Piece<T>::VEC;
+  __shared__ float part[4];
+  const uint32_t row = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int32_t io, oo;
+  uint32_t qi;
+  row_offsets(p, row, io, oo, qi);
+  const uint32_t R = p.R;
+  const uint32_t valid = (OP == RED_SOFTMAX && p.causal) ? min(R, qi + 1u) : R;
+  const T* x = (const T*)p.x + io;
+  T* y = (T*)p.y + oo;
+  float v[NC][VEC];
+  uint4 gq[OP == RED_SOFTMAX ? 1 : NC], bq[OP == RED_LAYERNORM ? NC : 1];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const uint32_t e0 = (uint32_t)(tid + 256 * c) * VEC;
+    uint4 u = make_uint4(0, 0, 0, 0);
+    if (e0 < valid) u = *(const uint4*)(x + e0);
+    Piece<T>::unpack(u, v[c]);
+    if constexpr (OP != RED_SOFTMAX) {
+      gq[c] = e0 < R ? *(const uint4*)((const T*)p.gamma + e0) : make_uint4(0, 0, 0, 0);
+      if constexpr (OP == RED_LAYERNORM) bq[c] = e0 < R ? *(const uint4*)((const T*)p.beta + e0) : make_uint4(0, 0, 0, 0);
+    }
+  }
+  // block-wide sum / max: wavefront butterflies, then the four partials
+  auto block_sum = [&](float a) {
+    a = wave_sum(a);
+    if (lane == 0) part[wave] = a;
+    __syncthreads();
+    const float r = part[0] + part[1] + part[2] + part[3];
+    __syncthreads();
+    return r;
+  };
+  auto block_max = [&](float a) {
+    a = wave_max(a);
+    if (lane == 0) part[wave] = a;
+    __syncthreads();
+    const float r = fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3]));
+    __syncthreads();
+    return r;
+  };
+  if constexpr (OP == RED_SOFTMAX) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const uint32_t k = (uint32_t)(tid + 256 * c) * VEC + i;
+        v[c][i] *= p.attr;
+        if (k < valid) m = fmaxf(m, v[c][i]);
+      }
+    m = block_max(m);
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const uint32_t k = (uint32_t)(tid + 256 * c) * VEC + i;
+        v[c][i] = k < valid ? expf(v[c][i] - m) : 0.f;
+        s += v[c][i];
+      }
+    s = block_sum(s);
+    const float inv = 1.0f / s;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const uint32_t e0 = (uint32_t)(tid + 256 * c) * VEC;
+      if (e0 < R) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[c][i] *= inv;
+        *(uint4*)(y + e0) = Piece<T>::pack(v[c]);
+      }
+    }
+  } else {
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) s += (OP == RED_LAYERNORM) ? v[c][i] : v[c][i] * v[c][i];
+    s = block_sum(s);
+    const float invR = 1.0f / (float)R;
+    float mean = 0.f, rstd;
+    if constexpr (OP == RED_LAYERNORM) {
+      mean = s * invR;
+      float q = 0.f;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const uint32_t e0 = (uint32_t)(tid + 256 * c) * VEC;
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+          const float d = v[c][i] - mean;
+          q += e0 < R ? d * d : 0.f;
+        }
+      }
+      q = block_sum(q);
+      rstd = 1.0f / sqrtf(q * invR + p.attr);
+    } else {
+      rstd = 1.0f / sqrtf(s * invR + p.attr);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const uint32_t e0 = (uint32_t)(tid + 256 * c) * VEC;
+      if (e0 < R) {
+        float g[VEC], b[VEC];
+        Piece<T>::unpack(gq[c], g);
+        if constexpr (OP == RED_LAYERNORM) Piece<T>::unpack(bq[c], b);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+          v[c][i] = (v[c][i] - mean) * rstd * g[i];
+          if constexpr (OP == RED_LAYERNORM) v[c][i] += b[i];
+        }
+        *(uint4*)(y + e0) = Piece<T>::pack(v[c]);
+      }
+    }
+  }
+}
+
 template <typename T, int OP>
 __global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
   const uint32_t row = blockIdx.x * 256u + threadIdx.x;
@@ -304,18 +426,193 @@ __global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
   }
 }
 
+// Column family with the row held in registers: a workgroup of 16
+// wavefronts owns RT consecutive rows.  Lane l of a wavefront works on row
+// RT b + l % RT at the k phase q = l / RT (one of KQ = 64 / RT), so one load
+// by a wavefront reads KQ runs of RT neighbouring rows.  Wavefront w holds the
+// k in [w KQ KPL, (w + 1) KQ KPL) with k = w KQ KPL + q + KQ j.  The input is
+// read once; per-row sums and maxima are combined over the KQ phases with
+// lane shuffles and over the 16 wavefronts through LDS, in a fixed order.
+template <typename T, int RT, int KPL, int OP>
+__global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
+  constexpr int KQ = 64 / RT;
+  __shared__ float part[16][RT];
+  // the wavefront index is uniform: keep it in a scalar register
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane % RT, q = lane / RT;
+  // Consecutive workgroups go to the 8 XCDs in turn.  A tile's run of RT
+  // rows covers RT * sizeof(T) bytes, so G = 128 / (RT sizeof(T)) tiles share
+  // one 128-byte line: place runs of G consecutive tiles on one XCD (tile t
+  // on XCD (t / G) % 8), so that a line is fetched into, and written back
+  // from, a single L2.
+  constexpr uint32_t G = RT * sizeof(T) >= 128 ? 1u : 128u / (RT * (uint32_t)sizeof(T));
+  uint32_t tile = blockIdx.x;
+  if (G > 1 && gridDim.x % (8u * G) == 0) {
+    const uint32_t x = tile & 7u, i = tile >> 3;
+    tile = ((i / G) * 8u + x) * G + i % G;
+  }
+  const uint32_t row = tile * (uint32_t)RT + (uint32_t)r;
+  // rows past the end compute on the last row and store nothing
+  const bool live = row < p.nrows;
+  int32_t io, oo;
+  uint32_t qi;
+  row_offsets(p, live ? row : p.nrows - 1u, io, oo, qi);
+  const uint32_t R = p.R;
+  const uint32_t valid = (OP == RED_SOFTMAX && p.causal) ? min(R, qi + 1u) : R;
+  const uint32_t kb = (uint32_t)wave * (KQ * KPL);  // uniform
+  const uint32_t kl = kb + (uint32_t)q;             // this lane's first k
+  // Only a wavefront whose k range runs past R, or a causal softmax, masks
+  // single loads and stores; the test is uniform across the wavefront.
+  const bool masked = (OP == RED_SOFTMAX && p.causal) || kb + KQ * KPL > R;
+  // Buffer loads and stores: the lane's row offset plus its phase is the one
+  // per-lane address register, the uniform part of k a scalar offset.  Byte
+  // offsets stay below 2^31 (the launcher checks), so a lane that must not
+  // load or store points at offset 2^31, which the buffer range check turns
+  // into a zero load or a dropped store.
+  constexpr uint32_t ES = sizeof(T);
+  constexpr uint32_t OOB = 0x80000000u;
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.x), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(p.y, 0, 0x7fffffff, 0x00020000);
+  const uint32_t xstep = (uint32_t)p.irs * ES, ystep = (uint32_t)p.ors * ES;
+  const uint32_t xo = (uint32_t)io * ES + (uint32_t)q * xstep;
+  const uint32_t yo = live ? (uint32_t)oo * ES + (uint32_t)q * ystep : OOB;
+  auto ld = [&](int j, uint32_t vo) {
+    const uint32_t so = (kb + (uint32_t)(KQ * j)) * xstep;
+    if constexpr (ES == 4) return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rx, vo, so, 0));
+    else return bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rx, vo, so, 0));
+  };
+  auto st1 = [&](int j, uint32_t vo, float y) {
+    const uint32_t so = (kb + (uint32_t)(KQ * j)) * ystep;
+    if constexpr (ES == 4) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, y), ry, vo, so, 0);
+    else __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(y), ry, vo, so, 0);
+  };
+  float v[KPL];
+  if (masked) {
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) v[j] = ld(j, kl + KQ * j < valid ? xo : OOB);
+  } else {
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) v[j] = ld(j, xo);
+  }
+  // y[j] for every j, stored where k < R
+  auto store_all = [&](auto&& yfun) {
+    if (masked) {
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) st1(j, kl + KQ * j < R ? yo : OOB, yfun(j));
+    } else {
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) st1(j, yo, yfun(j));
+    }
+  };
+  auto combine = [&](float a, bool take_max) {
+#pragma unroll
+    for (int o = RT; o < 64; o <<= 1) {
+      const float b = __shfl_xor(a, o, 64);
+      a = take_max ? fmaxf(a, b) : a + b;
+    }
+    if (q == 0) part[wave][r] = a;
+    __syncthreads();
+    float t = part[0][r];
+#pragma unroll
+    for (int w = 1; w < 16; ++w) t = take_max ? fmaxf(t, part[w][r]) : t + part[w][r];
+    __syncthreads();
+    return t;
+  };
+  if constexpr (OP == RED_SOFTMAX) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      v[j] *= p.attr;
+      if (kl + KQ * j < valid) m = fmaxf(m, v[j]);
+    }
+    m = combine(m, true);
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      v[j] = kl + KQ * j < valid ? expf(v[j] - m) : 0.f;
+      sum += v[j];
+    }
+    sum = combine(sum, false);
+    const float inv = 1.0f / sum;
+    store_all([&](int j) { return v[j] * inv; });
+  } else {
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) sum += (OP == RED_LAYERNORM) ? v[j] : v[j] * v[j];
+    sum = combine(sum, false);
+    const float invR = 1.0f / (float)R;
+    float mean = 0.f, rstd;
+    if constexpr (OP == RED_LAYERNORM) {
+      mean = sum * invR;
+      float qs = 0.f;
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) {
+        const float d = v[j] - mean;
+        qs += kl + KQ * j < R ? d * d : 0.f;
+      }
+      qs = combine(qs, false);
+      rstd = 1.0f / sqrtf(qs * invR + p.attr);
+    } else {
+      rstd = 1.0f / sqrtf(sum * invR + p.attr);
+    }
+    // gamma and beta are read at min(k, R - 1): in bounds for k past the row
+    store_all([&](int j) {
+      const uint32_t kc = min(kl + KQ * j, R - 1u);
+      float y = (v[j] - mean) * rstd * Elem<T>::load(p.gamma, kc);
+      if constexpr (OP == RED_LAYERNORM) y += Elem<T>::load(p.beta, kc);
+      return y;
+    });
+  }
+}
+
 namespace {
 
 template <typename T, int OP>
 hipError_t red_dispatch_op(const NodeKernel& k, hipStream_t s) {
   const RedParams& p = k.red;
   if (k.family == KF_RED_COL) {
-    hipLaunchKernelGGL((red_col_kernel<T, OP>), dim3((p.nrows + 255u) / 256u), dim3(256), 0, s, p);
+    // register-resident variant: byte offsets below 2^31, at most 32 values
+    // per lane; 64-row tiles where they still give 512 workgroups, else 16-
+    // or (for rows longer than 2048) 8-row tiles
+    const bool fits = (uint64_t)p.nrows * p.R * sizeof(T) < (uint64_t(1) << 31);
+    const int rt = ((p.nrows + 63u) / 64u >= 512u && p.R <= 512u) ? 64 : p.R <= 2048u ? 16 : 8;
+    const uint32_t kpl = (p.R + 16u * (64 / rt) - 1u) / (16u * (64 / rt));
+#define FLUID_COLB(RTv, K) \
+  hipLaunchKernelGGL((red_colb_kernel<T, RTv, K, OP>), dim3((p.nrows + RTv - 1u) / RTv), dim3(1024), 0, s, p)
+#define FLUID_COLB_RT(RTv)                \
+  if (kpl <= 1) FLUID_COLB(RTv, 1);       \
+  else if (kpl <= 2) FLUID_COLB(RTv, 2);  \
+  else if (kpl <= 4) FLUID_COLB(RTv, 4);  \
+  else if (kpl <= 8) FLUID_COLB(RTv, 8);  \
+  else if (kpl <= 16) FLUID_COLB(RTv, 16); \
+  else FLUID_COLB(RTv, 32);
+    if (!fits || kpl > 32) {
+      hipLaunchKernelGGL((red_col_kernel<T, OP>), dim3((p.nrows + 255u) / 256u), dim3(256), 0, s, p);
+    } else if (rt == 64) {
+      FLUID_COLB_RT(64)
+    } else if (rt == 16) {
+      FLUID_COLB_RT(16)
+    } else {
+      FLUID_COLB_RT(8)
+    }
+#undef FLUID_COLB_RT
+#undef FLUID_COLB
     return hipGetLastError();
   }
   const dim3 grid((p.nrows + 3u) / 4u);
   if (k.vec > 1) {
-    const uint32_t nc = (p.R / Piece<T>::VEC + 63u) / 64u;
+    const uint32_t pieces = p.R / Piece<T>::VEC;
+    // long rows and few of them: a workgroup per row
+    if (pieces >= 256 && p.nrows < 16384) {
+      const uint32_t ncb = (pieces + 255u) / 256u;
+      const dim3 gb(p.nrows);
+      if (ncb <= 1) hipLaunchKernelGGL((red_rowb_kernel<T, 1, OP>), gb, dim3(256), 0, s, p);
+      else if (ncb <= 2) hipLaunchKernelGGL((red_rowb_kernel<T, 2, OP>), gb, dim3(256), 0, s, p);
+      else if (ncb <= 4) hipLaunchKernelGGL((red_rowb_kernel<T, 4, OP>), gb, dim3(256), 0, s, p);
+      else return hipErrorInvalidValue;
+      return hipGetLastError();
+    }
+    const uint32_t nc = (pieces + 63u) / 64u;
     if (nc <= 1) hipLaunchKernelGGL((red_rowv_kernel<T, 1, OP>), grid, dim3(256), 0, s, p);
     else if (nc <= 2) hipLaunchKernelGGL((red_rowv_kernel<T, 2, OP>), grid, dim3(256), 0, s, p);
     else if (nc <= 4) hipLaunchKernelGGL((red_rowv_kernel<T, 4, OP>), grid, dim3(256), 0, s, p);

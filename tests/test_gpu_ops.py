@@ -190,7 +190,7 @@ def softmax_graph(B, NH, S, T, dtype, causal, scale):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("shape", [(1, 2, 37, 37), (2, 3, 64, 64), (1, 2, 130, 130), (1, 1, 5, 300)], ids=str)
+@pytest.mark.parametrize("shape", [(1, 2, 37, 37), (2, 3, 64, 64), (1, 2, 130, 130), (1, 1, 5, 300), (1, 1, 9, 1024)], ids=str)
 @pytest.mark.parametrize("causal", [0, 1])
 def test_softmax_layouts_and_variants(dtype, shape, causal, tmp_path):
     og, a, p = softmax_graph(*shape, dtype, causal, 0.125)
@@ -220,7 +220,7 @@ def norm_graph(B, S, H, dtype, op):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("op", ["layernorm", "rmsnorm"])
-@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (1, 8, 768), (1, 3, 4096)], ids=str)
+@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (1, 8, 768), (2, 5, 1024), (1, 5, 3000), (1, 3, 4096)], ids=str)
 def test_norm_layouts_and_variants(dtype, op, shape, tmp_path):
     og, a, n = norm_graph(*shape, dtype, op)
     L = layouts.layout_list(shape)
@@ -228,6 +228,28 @@ def test_norm_layouts_and_variants(dtype, op, shape, tmp_path):
         for v in (0, 1):
             say(f"{op} {dtype} {shape} v{v} {L[ia]} {L[ib]}")
             _check(og, {a: L[ia], n: L[ib]}, {1: v}, tmp_path, seed=ia + 3 * ib, scale=2.0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("op", ["layernorm", "rmsnorm", "softmax"])
+def test_column_reduction_many_rows(dtype, op, tmp_path):
+    """More than 32704 short rows: the column variant's 64-row tiles (fewer
+    rows take 16- or 8-row tiles), with a row length that leaves masked k."""
+    if op == "softmax":
+        shape = (1, 1, 32775, 40)
+        L = layouts.layout_list(shape)
+        for causal in (0, 1):
+            og, a, n = softmax_graph(*shape, dtype, causal, 0.5)
+            for ia, ib in ((0, 0), (1, 1), (0, 1)):
+                say(f"{op} {dtype} {shape} causal={causal} v1 {L[ia]} {L[ib]}")
+                _check(og, {a: L[ia], n: L[ib]}, {1: 1}, tmp_path, seed=ia + 3 * ib, scale=3.0)
+        return
+    shape = (1, 32775, 40)
+    og, a, n = norm_graph(*shape, dtype, op)
+    L = layouts.layout_list(shape)
+    for ia, ib in ((0, 0), (1, 1), (0, 1), (1, 0)):
+        say(f"{op} {dtype} {shape} v1 {L[ia]} {L[ib]}")
+        _check(og, {a: L[ia], n: L[ib]}, {1: 1}, tmp_path, seed=ia + 3 * ib, scale=2.0)
 
 
 # ------------------------------------------------------------------ RoPE
