@@ -51,7 +51,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 // operations are outstanding; export and LDS counters left unconstrained.
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-constexpr int DL_BM = 256, DL_BN = 128, DL_BK = 32, DL_NS = 4;
+constexpr int DL_BM = 256, DL_BN = 128, DL_BK = 32;
 constexpr int DL_AROWB = DL_BK * 2;              // bytes per A row in LDS (one m)
 constexpr int DL_BROWB = DL_BN * 2;              // bytes per B row in LDS (one k)
 constexpr int DL_ASTAGE = DL_BM * DL_AROWB;      // 16 KiB
@@ -61,9 +61,16 @@ __device__ __forceinline__ int a_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; 
 
 }  // namespace
 
-template <int BMD>
-__global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
-  constexpr int BK = DL_BK, NS = DL_NS;
+// NS = 4: the ring above, one workgroup per CU.  NS = 3: a three-stage ring
+// (72 KiB, tiles loaded two ahead) and at most 256 registers per lane
+// (VGPRs and AGPRs together), so that two workgroups share a CU and one's
+// loads, barrier waits and epilogue overlap the other's MFMAs: faster where
+// there are many tiles or K is short (Q K^T, the 11008-wide FFN GEMMs).
+template <int BMD, int NS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NS == 3 ? 2 : 1, NS == 3 ? 2 : 1)))
+void gemm_bf16_dl_kernel(GemmParams p) {
+  static_assert(NS == 3 || NS == 4, "three or four stages");
+  constexpr int BK = DL_BK;
   constexpr int FM = 2, FN = 4;  // wavefront tile 64 x 128 in 32 x 32 blocks
   // one LDS object per stage and operand, so that the compiler can tell a
   // DMA into one stage from reads of another and does not wait for every
@@ -71,11 +78,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t As0[DL_ASTAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t As1[DL_ASTAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t As2[DL_ASTAGE];
-  __shared__ __attribute__((aligned(1024))) uint8_t As3[DL_ASTAGE];
+  __shared__ __attribute__((aligned(NS > 3 ? 1024 : 16))) uint8_t As3[NS > 3 ? DL_ASTAGE : 16];
   __shared__ __attribute__((aligned(1024))) uint8_t Bs0[DL_BSTAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t Bs1[DL_BSTAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t Bs2[DL_BSTAGE];
-  __shared__ __attribute__((aligned(1024))) uint8_t Bs3[DL_BSTAGE];
+  __shared__ __attribute__((aligned(NS > 3 ? 1024 : 16))) uint8_t Bs3[NS > 3 ? DL_BSTAGE : 16];
+  // stage indices are compile-time constants in the loop; only the epilogue
+  // selects an A stage (its own wavefront's, < 4) at run time
   auto astage = [&](int st) -> uint8_t* { return st == 0 ? As0 : st == 1 ? As1 : st == 2 ? As2 : As3; };
   auto bstage = [&](int st) -> uint8_t* { return st == 0 ? Bs0 : st == 1 ? Bs1 : st == 2 ? Bs2 : Bs3; };
   const TileCoord tc = tile_coord(p, DL_BM, DL_BN);
@@ -199,24 +208,26 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
     }
   };
 
-  // Tile t lives in stage t % 4.  Loads past the end of K read zeros, so
-  // the loop runs whole groups of four tiles (padding tiles add zeros).
+  // Tile t lives in stage t % NS and is loaded NS - 1 tiles ahead.  Loads
+  // past the end of K read zeros, so the loop runs whole groups of NS tiles
+  // (padding tiles add zeros).
   const uint32_t nt = (p.K + BK - 1) / BK;
-  load(0, 0);
-  load(1, BK);
-  load(2, 2 * BK);
-  for (uint32_t t = 0; t < nt; t += 4) {
+#pragma unroll
+  for (int u = 0; u < NS - 1; ++u) load(u, u * BK);
+  for (uint32_t t = 0; t < nt; t += NS) {
 #define FLUID_DL_STEP(U)                                            \
   asm volatile("" ::: "memory");                                    \
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kTile));                 \
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * kTile));          \
   __builtin_amdgcn_s_barrier();                                     \
   asm volatile("" ::: "memory");                                    \
-  load((U + 3) % NS, (t + U + 3) * BK);                             \
+  load((U + NS - 1) % NS, (t + U + NS - 1) * BK);                   \
   compute(U);
     FLUID_DL_STEP(0)
     FLUID_DL_STEP(1)
     FLUID_DL_STEP(2)
-    FLUID_DL_STEP(3)
+    if constexpr (NS > 3) {
+      FLUID_DL_STEP(3)
+    }
 #undef FLUID_DL_STEP
   }
 
@@ -227,7 +238,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
     // wavefront finish its last tile, before the ring is reused
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     __syncthreads();
-    uint16_t* cs = (uint16_t*)astage(wave);  // 16 KiB: this wavefront's 64 x 128 tile
+    // 16 KiB for this wavefront's 64 x 128 tile, as two 8 KiB halves: its
+    // own A stage, or with three stages, for wavefront 3, two B stages
+    auto half = [&](int h) -> uint16_t* {
+      if (NS == 3 && wave == 3) return (uint16_t*)(h ? Bs1 : Bs0);
+      return (uint16_t*)(astage(wave) + 8192 * h);
+    };
     if (p.cmode == 1) {
       // row-major [64][128], 16-byte chunk c of row r at c ^ (r % 16)
 #pragma unroll
@@ -237,13 +253,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int r = i * 32 + 8 * (v / 4) + 4 * lh + (v % 4), c = j * 32 + lr;
-            cs[r * 128 + (((c >> 3) ^ (r & 15)) << 3) + (c & 7)] = f32_to_bf16(acc[i][j][v]);
+            half(r >> 5)[(r & 31) * 128 + (((c >> 3) ^ (r & 15)) << 3) + (c & 7)] = f32_to_bf16(acc[i][j][v]);
           }
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own parking writes done
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const int r = 4 * u + (lane >> 4), ch = lane & 15;
-        const uint4 val = *(const uint4*)&cs[r * 128 + ((ch ^ (r & 15)) << 3)];
+        const uint4 val = *(const uint4*)&half(r >> 5)[(r & 31) * 128 + ((ch ^ (r & 15)) << 3)];
         const uint32_t m = wm0 + r, n0 = tc.n0 + 8 * ch;
         if (m >= p.M || n0 >= p.N) continue;
         uint16_t* dst = C + tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n0;
@@ -266,13 +282,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_dl_kernel(GemmParams p) {
             const int r0 = i * 32 + 8 * vg + 4 * lh, c = j * 32 + lr;
             const uint32_t lo = (uint32_t)f32_to_bf16(acc[i][j][4 * vg]) | ((uint32_t)f32_to_bf16(acc[i][j][4 * vg + 1]) << 16);
             const uint32_t hi = (uint32_t)f32_to_bf16(acc[i][j][4 * vg + 2]) | ((uint32_t)f32_to_bf16(acc[i][j][4 * vg + 3]) << 16);
-            *(uint2*)&cs[c * 64 + ((((r0 >> 3) ^ ((c >> 1) & 7))) << 3) + (r0 & 7)] = make_uint2(lo, hi);
+            *(uint2*)&half(c >> 6)[(c & 63) * 64 + ((((r0 >> 3) ^ ((c >> 1) & 7))) << 3) + (r0 & 7)] = make_uint2(lo, hi);
           }
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const int c = 8 * u + (lane >> 3), ch = lane & 7;
-        const uint4 val = *(const uint4*)&cs[c * 64 + ((ch ^ ((c >> 1) & 7)) << 3)];
+        const uint4 val = *(const uint4*)&half(c >> 6)[(c & 63) * 64 + ((ch ^ ((c >> 1) & 7)) << 3)];
         const uint32_t n = tc.n0 + c, m0 = wm0 + 8 * ch;
         if (n >= p.N || m0 >= p.M) continue;
         const uint32_t m2 = m0 - fdiv(m0, p.m2div) * p.M2;  // position within the M2 run
@@ -306,8 +322,14 @@ hipError_t launch_gemm_bf16_dl(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   if (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_MN && k.bmode != GM_K)) return hipErrorInvalidValue;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
-  if (k.bmode == GM_MN) hipLaunchKernelGGL((gemm_bf16_dl_kernel<GM_MN>), grid, dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((gemm_bf16_dl_kernel<GM_K>), grid, dim3(256), 0, s, p);
+  // tile 8: the three-stage ring, two workgroups per CU
+  if (k.gemm_tile == 8) {
+    if (k.bmode == GM_MN) hipLaunchKernelGGL((gemm_bf16_dl_kernel<GM_MN, 3>), grid, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((gemm_bf16_dl_kernel<GM_K, 3>), grid, dim3(256), 0, s, p);
+  } else {
+    if (k.bmode == GM_MN) hipLaunchKernelGGL((gemm_bf16_dl_kernel<GM_MN, 4>), grid, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((gemm_bf16_dl_kernel<GM_K, 4>), grid, dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 
