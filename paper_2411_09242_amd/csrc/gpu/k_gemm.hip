@@ -30,6 +30,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
   __shared__ float As[BK * AP];
   __shared__ float Bs[BK * BP];
   const TileCoord tc = tile_coord(p, BM, BN);
+  // causal attention: a tile entirely above the diagonal is never read; a
+  // row block's A is zero past its last row, so K stops there
+  if ((p.causal & 1u) && tc.n0 > tc.m0 + BM - 1) return;
+  const uint32_t Kc = (p.causal & 2u) ? min(p.K, tc.m0 + BM) : p.K;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 
@@ -109,7 +113,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
       for (int r = 0; r < A_VECS; ++r) {
         const uint32_t k = k0 + a_k[r];
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (a_ok[r] && k < p.K) v = *(const float4*)(A + a_off[r] + (int32_t)k);
+        if (a_ok[r] && k < Kc) v = *(const float4*)(A + a_off[r] + (int32_t)k);
         ra[4 * r] = v.x; ra[4 * r + 1] = v.y; ra[4 * r + 2] = v.z; ra[4 * r + 3] = v.w;
       }
     } else if constexpr (AM == GM_MN) {
@@ -117,14 +121,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
       for (int r = 0; r < A_VECS; ++r) {
         const uint32_t k = k0 + a_k[r];
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (a_ok[r] && k < p.K) v = *(const float4*)(A + a_off[r] + (int32_t)k * p.a_k);
+        if (a_ok[r] && k < Kc) v = *(const float4*)(A + a_off[r] + (int32_t)k * p.a_k);
         ra[4 * r] = v.x; ra[4 * r + 1] = v.y; ra[4 * r + 2] = v.z; ra[4 * r + 3] = v.w;
       }
     } else {
 #pragma unroll
       for (int r = 0; r < A_ELEMS; ++r) {
         const uint32_t k = k0 + a_k[r];
-        ra[r] = (a_ok[r] && k < p.K) ? A[a_off[r] + (int32_t)k * p.a_k] : 0.f;
+        ra[r] = (a_ok[r] && k < Kc) ? A[a_off[r] + (int32_t)k * p.a_k] : 0.f;
       }
     }
     if constexpr (BMD == GM_MN) {
@@ -132,7 +136,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
       for (int r = 0; r < B_VECS; ++r) {
         const uint32_t k = k0 + b_k[r];
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (b_ok[r] && k < p.K) v = *(const float4*)(B + tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]));
+        if (b_ok[r] && k < Kc) v = *(const float4*)(B + tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]));
         rb[4 * r] = v.x; rb[4 * r + 1] = v.y; rb[4 * r + 2] = v.z; rb[4 * r + 3] = v.w;
       }
     } else if constexpr (BMD == GM_K) {
@@ -140,14 +144,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
       for (int r = 0; r < B_VECS; ++r) {
         const uint32_t k = k0 + b_k[r];
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (b_ok[r] && k < p.K) v = *(const float4*)(B + tc.b_base + (int32_t)k + (int32_t)(tc.n0 + b_n[r]) * p.b_n);
+        if (b_ok[r] && k < Kc) v = *(const float4*)(B + tc.b_base + (int32_t)k + (int32_t)(tc.n0 + b_n[r]) * p.b_n);
         rb[4 * r] = v.x; rb[4 * r + 1] = v.y; rb[4 * r + 2] = v.z; rb[4 * r + 3] = v.w;
       }
     } else {
 #pragma unroll
       for (int r = 0; r < B_ELEMS; ++r) {
         const uint32_t k = k0 + b_k[r];
-        rb[r] = (b_ok[r] && k < p.K) ? B[tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]) * p.b_n] : 0.f;
+        rb[r] = (b_ok[r] && k < Kc) ? B[tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]) * p.b_n] : 0.f;
       }
     }
   };
@@ -190,11 +194,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 
   const int lr = lane & 31, lk = lane >> 5;
   gload(0);
-  for (uint32_t k0 = 0; k0 < p.K; k0 += BK) {
+  for (uint32_t k0 = 0; k0 < Kc; k0 += BK) {
     __syncthreads();
     lstore();
     __syncthreads();
-    if (k0 + BK < p.K) gload(k0 + BK);
+    if (k0 + BK < Kc) gload(k0 + BK);
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 2) {
       float a[FM], b[FN];
@@ -248,6 +252,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
   __shared__ uint16_t As[BM * KP];
   __shared__ uint16_t Bs[BN * KP];
   const TileCoord tc = tile_coord(p, BM, BN);
+  // causal attention: a tile entirely above the diagonal is never read; a
+  // row block's A is zero past its last row, so K stops there
+  if ((p.causal & 1u) && tc.n0 > tc.m0 + BM - 1) return;
+  const uint32_t Kc = (p.causal & 2u) ? min(p.K, tc.m0 + BM) : p.K;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const uint16_t* A = (const uint16_t*)p.A;
@@ -334,7 +342,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < A_CH; ++r) {
         const uint32_t k = k0 + a_k[r];
-        ca[r] = (a_ok[r] && k < p.K) ? *(const uint4*)(A + a_off[r] + (int32_t)k) : make_uint4(0, 0, 0, 0);
+        ca[r] = (a_ok[r] && k < Kc) ? *(const uint4*)(A + a_off[r] + (int32_t)k) : make_uint4(0, 0, 0, 0);
       }
     } else if constexpr (A_VEC_MN) {
 #pragma unroll
@@ -342,20 +350,20 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const uint32_t k = k0 + a_k[r] + t;
-          ba[4 * r + t] = (a_ok[r] && k < p.K) ? *(const uint2*)(A + a_off[r] + (int32_t)k * p.a_k) : make_uint2(0, 0);
+          ba[4 * r + t] = (a_ok[r] && k < Kc) ? *(const uint2*)(A + a_off[r] + (int32_t)k * p.a_k) : make_uint2(0, 0);
         }
     } else {
 #pragma unroll
       for (int r = 0; r < A_ELEMS; ++r) {
         const uint32_t k = k0 + a_k[r];
-        sa[r] = (a_ok[r] && k < p.K) ? A[a_off[r] + (int32_t)k * p.a_k] : (uint16_t)0;
+        sa[r] = (a_ok[r] && k < Kc) ? A[a_off[r] + (int32_t)k * p.a_k] : (uint16_t)0;
       }
     }
     if constexpr (B_VEC_K) {
 #pragma unroll
       for (int r = 0; r < B_CH; ++r) {
         const uint32_t k = k0 + b_k[r];
-        cb[r] = (b_ok[r] && k < p.K) ? *(const uint4*)(B + tc.b_base + (int32_t)k + (int32_t)(tc.n0 + b_n[r]) * p.b_n)
+        cb[r] = (b_ok[r] && k < Kc) ? *(const uint4*)(B + tc.b_base + (int32_t)k + (int32_t)(tc.n0 + b_n[r]) * p.b_n)
                                      : make_uint4(0, 0, 0, 0);
       }
     } else if constexpr (B_VEC_MN) {
@@ -364,7 +372,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const uint32_t k = k0 + b_k[r] + t;
-          bb[4 * r + t] = (b_ok[r] && k < p.K)
+          bb[4 * r + t] = (b_ok[r] && k < Kc)
                               ? *(const uint2*)(B + tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]))
                               : make_uint2(0, 0);
         }
@@ -372,7 +380,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < B_ELEMS; ++r) {
         const uint32_t k = k0 + b_k[r];
-        sb[r] = (b_ok[r] && k < p.K) ? B[tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]) * p.b_n] : (uint16_t)0;
+        sb[r] = (b_ok[r] && k < Kc) ? B[tc.b_base + (int32_t)k * p.b_k + (int32_t)(tc.n0 + b_n[r]) * p.b_n] : (uint16_t)0;
       }
     }
   };
@@ -417,11 +425,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 
   const int lr = lane & 31, lk = (lane >> 5) * 8;
   gload(0);
-  for (uint32_t k0 = 0; k0 < p.K; k0 += BK) {
+  for (uint32_t k0 = 0; k0 < Kc; k0 += BK) {
     __syncthreads();
     lstore();
     __syncthreads();
-    if (k0 + BK < p.K) gload(k0 + BK);
+    if (k0 + BK < Kc) gload(k0 + BK);
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
       bf16x8 a[FM], b[FN];
@@ -479,14 +487,18 @@ __global__ __launch_bounds__(64 * W) void gemm_sk_kernel(GemmParams p) {
   constexpr bool BF = sizeof(T) == 2;
   __shared__ float red[W * TM * RP];
   const TileCoord tc = tile_coord(p, TM, TN);
+  // causal attention: a tile entirely above the diagonal is never read; a
+  // row block's A is zero past its last row, so K stops there
+  if ((p.causal & 1u) && tc.n0 > tc.m0 + TM - 1) return;
+  const uint32_t Kc = (p.causal & 2u) ? min(p.K, tc.m0 + TM) : p.K;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, r = lane & 31;
   const T* A = (const T*)p.A;
   const T* B = (const T*)p.B;
   // K slice of this wavefront (multiple of 16 wide)
-  const uint32_t kc = ((p.K + W - 1) / W + 15u) & ~15u;
+  const uint32_t kc = ((Kc + W - 1) / W + 15u) & ~15u;
   const uint32_t kb = (uint32_t)w * kc;
-  const uint32_t ke = min(p.K, kb + kc);
+  const uint32_t ke = min(Kc, kb + kc);
   int32_t arow[FM];
   bool aok[FM];
 #pragma unroll

@@ -22,6 +22,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
   __shared__ uint16_t As[2 * BM * KP];
   __shared__ uint16_t Bs[2 * BN * KP];
   const TileCoord tc = tile_coord(p, BM, BN);
+  // causal attention: a tile entirely above the diagonal is never read; a
+  // row block's A is zero past its last row, so K stops there
+  if ((p.causal & 1u) && tc.n0 > tc.m0 + BM - 1) return;
+  const uint32_t Kc = (p.causal & 2u) ? min(p.K, tc.m0 + BM) : p.K;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const Rsrc ra = make_rsrc(p.A, p.a_bytes);
@@ -75,32 +79,32 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
     for (int r = 0; r < AN; ++r) {
       if constexpr (AM == GM_K) {
         const uint32_t k = k0 + a_k[r];
-        R.ca[r] = bload16(ra, (a_ok[r] && k < p.K) ? 2u * (uint32_t)(a_off[r] + (int32_t)k) : kOOB);
+        R.ca[r] = bload16(ra, (a_ok[r] && k < Kc) ? 2u * (uint32_t)(a_off[r] + (int32_t)k) : kOOB);
       } else if constexpr (AM == GM_MN) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const uint32_t k = k0 + a_k[r] + t;
-          R.ba[4 * r + t] = bload8(ra, (a_ok[r] && k < p.K) ? 2u * (uint32_t)(a_off[r] + (int32_t)k * p.a_k) : kOOB);
+          R.ba[4 * r + t] = bload8(ra, (a_ok[r] && k < Kc) ? 2u * (uint32_t)(a_off[r] + (int32_t)k * p.a_k) : kOOB);
         }
       } else {
         const uint32_t k = k0 + a_k[r];
-        R.sa[r] = bload2(ra, (a_ok[r] && k < p.K) ? 2u * (uint32_t)(a_off[r] + (int32_t)k * p.a_k) : kOOB);
+        R.sa[r] = bload2(ra, (a_ok[r] && k < Kc) ? 2u * (uint32_t)(a_off[r] + (int32_t)k * p.a_k) : kOOB);
       }
     }
 #pragma unroll
     for (int r = 0; r < BNN; ++r) {
       if constexpr (BMD == GM_K) {
         const uint32_t k = k0 + b_k[r];
-        R.cb[r] = bload16(rb, (b_ok[r] && k < p.K) ? 2u * (uint32_t)(b_off[r] + (int32_t)k) : kOOB);
+        R.cb[r] = bload16(rb, (b_ok[r] && k < Kc) ? 2u * (uint32_t)(b_off[r] + (int32_t)k) : kOOB);
       } else if constexpr (BMD == GM_MN) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const uint32_t k = k0 + b_k[r] + t;
-          R.bb[4 * r + t] = bload8(rb, (b_ok[r] && k < p.K) ? 2u * (uint32_t)(b_off[r] + (int32_t)k * p.b_k) : kOOB);
+          R.bb[4 * r + t] = bload8(rb, (b_ok[r] && k < Kc) ? 2u * (uint32_t)(b_off[r] + (int32_t)k * p.b_k) : kOOB);
         }
       } else {
         const uint32_t k = k0 + b_k[r];
-        R.sb[r] = bload2(rb, (b_ok[r] && k < p.K) ? 2u * (uint32_t)(b_off[r] + (int32_t)k * p.b_k) : kOOB);
+        R.sb[r] = bload2(rb, (b_ok[r] && k < Kc) ? 2u * (uint32_t)(b_off[r] + (int32_t)k * p.b_k) : kOOB);
       }
     }
   };
@@ -165,7 +169,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
   // global memory, issued two tiles before it is stored.  Loads past the
   // last tile read zeros (k >= K) and are never stored, so the loop body
   // has no data-dependent branches and the memory counters stay exact.
-  const uint32_t nt = (p.K + BK - 1) / BK;
+  const uint32_t nt = (Kc + BK - 1) / BK;
   gload(R0, 0);
   gload(R1, BK);
   lstore(R0, 0);

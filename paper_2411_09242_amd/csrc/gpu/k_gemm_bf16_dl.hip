@@ -88,6 +88,10 @@ void gemm_bf16_dl_kernel(GemmParams p) {
   auto astage = [&](int st) -> uint8_t* { return st == 0 ? As0 : st == 1 ? As1 : st == 2 ? As2 : As3; };
   auto bstage = [&](int st) -> uint8_t* { return st == 0 ? Bs0 : st == 1 ? Bs1 : st == 2 ? Bs2 : Bs3; };
   const TileCoord tc = tile_coord(p, DL_BM, DL_BN);
+  // causal attention: a tile entirely above the diagonal is never read; a
+  // row block's A is zero past its last row, so K stops there
+  if ((p.causal & 1u) && tc.n0 > tc.m0 + DL_BM - 1) return;
+  const uint32_t kend = (p.causal & 2u) ? min(p.K, tc.m0 + DL_BM) : p.K;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: DMA base in M0
   const int lr = lane & 31, lh = lane >> 5;
@@ -131,7 +135,7 @@ void gemm_bf16_dl_kernel(GemmParams p) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint32_t k = k0 + 8 * a_chunk[q];
-      const uint32_t off = k < p.K ? 2u * (uint32_t)(a_src[q] + (int32_t)k) : kOOB;
+      const uint32_t off = k < kend ? 2u * (uint32_t)(a_src[q] + (int32_t)k) : kOOB;
       lds_void* dst = (lds_void*)(astage(st) + 16 * (4 * q + wave) * DL_AROWB);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, dst, 16, off, 0, 0, 0);
     }
@@ -140,12 +144,12 @@ void gemm_bf16_dl_kernel(GemmParams p) {
       if constexpr (BMD == GM_MN) {
         const int row = 16 * q + 4 * wave + b_rsub;
         const uint32_t k = k0 + row;
-        const uint32_t off = k < p.K ? 2u * (uint32_t)(b_col + (int32_t)k * p.b_k) : kOOB;
+        const uint32_t off = k < kend ? 2u * (uint32_t)(b_col + (int32_t)k * p.b_k) : kOOB;
         lds_void* dst = (lds_void*)(bstage(st) + (16 * q + 4 * wave) * DL_BROWB);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst, 16, off, 0, 0, 0);
       } else {
         const uint32_t k = k0 + 8 * bk_chunk[q];
-        const uint32_t off = k < p.K ? 2u * (uint32_t)(bk_src[q] + (int32_t)k) : kOOB;
+        const uint32_t off = k < kend ? 2u * (uint32_t)(bk_src[q] + (int32_t)k) : kOOB;
         lds_void* dst = (lds_void*)(bstage(st) + 16 * (4 * q + wave) * DL_AROWB);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst, 16, off, 0, 0, 0);
       }
@@ -211,7 +215,7 @@ void gemm_bf16_dl_kernel(GemmParams p) {
   // Tile t lives in stage t % NS and is loaded NS - 1 tiles ahead.  Loads
   // past the end of K read zeros, so the loop runs whole groups of NS tiles
   // (padding tiles add zeros).
-  const uint32_t nt = (p.K + BK - 1) / BK;
+  const uint32_t nt = (kend + BK - 1) / BK;
 #pragma unroll
   for (int u = 0; u < NS - 1; ++u) load(u, u * BK);
   for (uint32_t t = 0; t < nt; t += NS) {

@@ -36,15 +36,19 @@ __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
   constexpr int SK_TM = 16 * SK_FM;
   __shared__ float red[W * SK_TM * SK_RP];
   const TileCoord tc = tile_coord(p, SK_TM, SK_TN);
+  // causal attention: a tile entirely above the diagonal is never read; a
+  // row block's A is zero past its last row, so K stops there
+  if ((p.causal & 1u) && tc.n0 > tc.m0 + SK_TM - 1) return;
+  const uint32_t Kc = (p.causal & 2u) ? min(p.K, tc.m0 + SK_TM) : p.K;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lq = lane >> 4;
   const Rsrc ra = make_rsrc(p.A, p.a_bytes);
   const Rsrc rb = make_rsrc(p.B, p.b_bytes);
 
   // this wavefront's K slice [kbeg, kend), a multiple of 16 long
-  const uint32_t kw = ((p.K + 16u * W - 1u) / (16u * W)) * 16u;
+  const uint32_t kw = ((Kc + 16u * W - 1u) / (16u * W)) * 16u;
   const uint32_t kbeg = wave * kw;
-  const uint32_t kend = min(p.K, kbeg + kw);
+  const uint32_t kend = min(Kc, kbeg + kw);
   const uint32_t ngroups = kend > kbeg ? (kend - kbeg + 15u) / 16u : 0u;
 
   // Rows past M and columns past N only feed outputs that are never

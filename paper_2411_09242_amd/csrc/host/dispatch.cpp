@@ -283,7 +283,7 @@ NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector
   return k;
 }
 
-NodeKernel prepare_gemm(const Node&, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
   NodeKernel k;
   k.family = KF_GEMM;
   k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
@@ -341,6 +341,8 @@ NodeKernel prepare_gemm(const Node&, int variant, int dtype, const std::vector<O
   p.G2 = G2;
   p.M2 = M2;
   p.M = M1 * M2;
+  // batched products only: rows are then the query dim, unmerged
+  p.causal = rB >= 3 ? (uint32_t)nd.causal : 0u;
   p.g2div = make_fastdiv(G2);
   p.m2div = make_fastdiv(M2);
   const int VEC = k.dtype == DT_F32 ? 4 : 8;
@@ -446,7 +448,7 @@ std::string NodeKernel::name() const {
       static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "p256x128", "p128", "p256x128s3"};
       static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4", "-"};
       return "gemm_" + dt + "_" + (dtype == DT_BF16 ? tiles : tiles_f32)[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
-             (cmode == 1 ? "n" : cmode == 2 ? "m" : "g");
+             (cmode == 1 ? "n" : cmode == 2 ? "m" : "g") + (gemm.causal ? "_causal" + std::to_string(gemm.causal) : "");
     }
   }
   return "?";

@@ -198,6 +198,18 @@ void Graph::finalize() {
   cand.assign(E, {});
   for (int e = 0; e < E; ++e)
     cand[e] = pinned(e) ? std::vector<Perm>{identity_perm((int)edge_shape(e).size())} : layout_list(edge_shape(e));
+  // Causal attention products.  A causal softmax reads only the entries of
+  // its input on or below the diagonal (key <= query, the last two dims),
+  // and writes exact zeros above it.
+  auto causal_softmax = [&](int m) { return m >= 0 && nodes[m].op == FLUID_OP_SOFTMAX && nodes[m].iattr != 0; };
+  for (size_t n = 0; n < nodes.size(); ++n) {
+    Node& nd = nodes[n];
+    nd.causal = 0;
+    if (nd.op != FLUID_OP_MATMUL || nd.ins[0] < 0 || nd.ins[1] < 0 || edge_shape(nd.ins[1]).size() < 3) continue;
+    const int e = out_edge((int)n);
+    if (!is_output[e] && readers[e].size() == 1 && causal_softmax(readers[e][0])) nd.causal |= 1;
+    if (causal_softmax(producer(nd.ins[0]))) nd.causal |= 2;
+  }
 }
 
 // ------------------------------------------------------------ transformers

@@ -16,6 +16,11 @@ struct Node {
   Perm perm;             // TRANSPOSE
   float fattr = 0.f;
   int iattr = 0;
+  // derived by Graph::finalize, for a batched MatMul: bit 0, a causal
+  // Softmax is the only reader of the output (entries above its diagonal
+  // are never read); bit 1, input A is a causal Softmax's output (exactly
+  // zero above the diagonal)
+  int causal = 0;
 };
 
 struct Const {

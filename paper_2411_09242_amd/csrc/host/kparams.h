@@ -95,6 +95,11 @@ struct GemmParams {
   int32_t cmode;              // 0 scalar stores, 1 N-contiguous, 2 M-contiguous (4 rows)
   uint32_t tiles_m, tiles_n;
   uint32_t a_bytes, b_bytes;  // byte span of A and B from their base pointers
+  // Causal attention (rows m are query positions, columns or k key
+  // positions): bit 0, only C[m][n] with n <= m is ever read, so tiles with
+  // every n > m may be skipped; bit 1, A[m][k] = 0 for k > m, so the K loop
+  // of rows m0 .. m0 + BM - 1 may stop at m0 + BM.
+  uint32_t causal;
 };
 
 }  // namespace fluid

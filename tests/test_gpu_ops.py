@@ -110,6 +110,38 @@ def test_attention_gemm_sampled_layouts(dtype, shape, pv, tmp_path):
             _check_gemm(og, {q: Lq[iq], k: Lk[ik], s: Ls[is_]}, {2: v}, tmp_path, iq + ik + is_, dtype)
 
 
+def causal_attn_graph(B, NH, S, D, dtype):
+    g = Graph(dtype=dtype)
+    x1 = g.add_input((B, NH, S, D))
+    x2 = g.add_input((B, NH, D, S))
+    x3 = g.add_input((B, NH, S, D))
+    q = g.add_node("gelu", [x1], (B, NH, S, D))
+    k = g.add_node("silu", [x2], (B, NH, D, S))
+    s = g.add_node("matmul", [q, k], (B, NH, S, S))
+    p = g.add_node("softmax", [s], (B, NH, S, S), fattr=0.3, iattr=1)
+    o = g.add_node("matmul", [p, x3], (B, NH, S, D))
+    y = g.add_node("gelu", [o], (B, NH, S, D))
+    g.outputs = [y]
+    return g, q, k, s, p, o
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(1, 2, 37, 16), (1, 2, 300, 64), (2, 1, 520, 32)], ids=str)
+def test_causal_attention_skips(dtype, shape, tmp_path):
+    """Q K^T read only by a causal softmax (tiles above the diagonal are
+    skipped) and P V with P from it (K stops at the tile's last row), every
+    GEMM variant on both, a few layouts of S and P: same output as the
+    oracle's full products."""
+    og, q, k, s, p, o = causal_attn_graph(*shape, dtype)
+    Ls = layouts.layout_list(og.edge_shape(s))
+    rng = np.random.default_rng(sum(shape))
+    picks = [(0, 0)] + [tuple(int(v) for v in rng.integers(0, len(Ls), 2)) for _ in range(2)]
+    for i_s, i_p in picks:
+        for v in range(9):
+            say(f"causal attn {dtype} {shape} v{v} S{Ls[i_s]} P{Ls[i_p]}")
+            _check_gemm(og, {s: Ls[i_s], p: Ls[i_p]}, {2: v, 4: v}, tmp_path, i_s + i_p, dtype)
+
+
 # ------------------------------------------------------------------ elementwise
 def ew_graph(B, S, H, dtype):
     g = Graph(dtype=dtype)
