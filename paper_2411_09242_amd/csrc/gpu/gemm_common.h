@@ -34,10 +34,13 @@ __device__ __forceinline__ uint16_t bload2(Rsrc r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
 
-// Workgroup -> (batch, tile row, tile column), row-major over tiles.
-__device__ __forceinline__ TileCoord tile_coord(const GemmParams& p, uint32_t BM, uint32_t BN) {
+// s_waitcnt immediate (gfx9 encoding) waiting until at most n vector-memory
+// operations are outstanding; export and LDS counters left unconstrained.
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// Tile index -> (batch, tile row, tile column), row-major over tiles.
+__device__ __forceinline__ TileCoord tile_coord_at(const GemmParams& p, uint32_t bid, uint32_t BM, uint32_t BN) {
   const uint32_t per_g = p.tiles_m * p.tiles_n;
-  const uint32_t bid = blockIdx.x;
   const uint32_t g = bid / per_g;
   const uint32_t r = bid - g * per_g;
   const uint32_t tm = r / p.tiles_n;
@@ -51,6 +54,10 @@ __device__ __forceinline__ TileCoord tile_coord(const GemmParams& p, uint32_t BM
   t.b_base = (int32_t)g1 * p.b_g1 + (int32_t)g2 * p.b_g2;
   t.c_base = (int32_t)g1 * p.c_g1 + (int32_t)g2 * p.c_g2;
   return t;
+}
+// One workgroup per tile.
+__device__ __forceinline__ TileCoord tile_coord(const GemmParams& p, uint32_t BM, uint32_t BN) {
+  return tile_coord_at(p, blockIdx.x, BM, BN);
 }
 
 // Offset of row m of A (or C) given the two-level row decomposition.

@@ -229,6 +229,7 @@ hipError_t launch_gemm_bf16_pipe(const NodeKernel& k, hipStream_t s) {
   if (k.dtype != DT_BF16) return hipErrorInvalidValue;
   if ((k.gemm_tile == 6 || k.gemm_tile == 8) && k.amode == GM_K && (k.bmode == GM_MN || k.bmode == GM_K))
     return launch_gemm_bf16_dl(k, s);
+  if (k.gemm_tile == 9) return launch_gemm_bf16_qk(k, s);
   if (k.gemm_tile >= 8) return hipErrorInvalidValue;
   return k.gemm_tile == 6 ? pipe_go<256>(k, s) : pipe_go<128>(k, s);
 }

@@ -47,10 +47,6 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __attribute__((address_space(3))) uint4 lds_uint4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-// s_waitcnt immediate (gfx9 encoding) waiting until at most n vector-memory
-// operations are outstanding; export and LDS counters left unconstrained.
-constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-
 constexpr int DL_BM = 256, DL_BN = 128, DL_BK = 32;
 constexpr int DL_AROWB = DL_BK * 2;              // bytes per A row in LDS (one m)
 constexpr int DL_BROWB = DL_BN * 2;              // bytes per B row in LDS (one k)

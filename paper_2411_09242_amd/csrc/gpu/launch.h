@@ -13,6 +13,7 @@ hipError_t launch_reduce(const NodeKernel& k, hipStream_t s);
 hipError_t launch_gemm(const NodeKernel& k, hipStream_t s);
 hipError_t launch_gemm_bf16_pipe(const NodeKernel& k, hipStream_t s);
 hipError_t launch_gemm_bf16_dl(const NodeKernel& k, hipStream_t s);
+hipError_t launch_gemm_bf16_qk(const NodeKernel& k, hipStream_t s);
 hipError_t launch_gemm_f32_dl(const NodeKernel& k, hipStream_t s);
 hipError_t launch_fill(void* p, uint64_t bytes, uint32_t seed, hipStream_t s);
 

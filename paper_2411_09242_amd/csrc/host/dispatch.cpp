@@ -22,7 +22,7 @@ std::vector<int64_t> row_major_strides(const Shape& s) {
 
 int num_variants(int op) {
   switch (op) {
-    case FLUID_OP_MATMUL: return 9;
+    case FLUID_OP_MATMUL: return 10;
     case FLUID_OP_GELU:
     case FLUID_OP_SILU:
     case FLUID_OP_TRANSPOSE:
@@ -383,15 +383,21 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   // tile sizes: 0: 128x128, 1: 64x64 (LDS-staged); 2, 3: 32x32 and 4: 64x32
   // with the K range split over the workgroup's wavefronts
   // bf16 6: 256x128 and 7: 128x128, loads two or more K-tiles ahead, 8:
-  // 256x128 with a three-stage ring, two workgroups per CU;
+  // 256x128 with a three-stage ring, two workgroups per CU, 9: 128x128
+  // persistent with the whole K (at most 128) in LDS;
   // fp32 6: 16x32 with K split over 8 wavefronts, 7: 32x32 over 4, operands
   // loaded straight into MFMA registers
-  static const uint32_t TM[] = {128, 64, 32, 32, 64, 32, 256, 128, 256};
-  static const uint32_t TN[] = {128, 64, 32, 32, 32, 32, 128, 128, 128};
+  static const uint32_t TM[] = {128, 64, 32, 32, 64, 32, 256, 128, 256, 128};
+  static const uint32_t TN[] = {128, 64, 32, 32, 32, 32, 128, 128, 128, 128};
   uint32_t tm = TM[variant], tn = TN[variant];
-  if (variant == 8 && (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_K && k.bmode != GM_MN))) {
+  if (variant >= 8 && (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_K && k.bmode != GM_MN))) {
     k.available = false;
-    k.why = "the three-stage tile is bf16 with a K-contiguous A and a K- or N-contiguous B";
+    k.why = "tiles 8 and 9 are bf16 with a K-contiguous A and a K- or N-contiguous B";
+    return k;
+  }
+  if (variant == 9 && p.K > 128) {
+    k.available = false;
+    k.why = "tile 9 holds the whole K (at most 128) in LDS";
     return k;
   }
   if (variant >= 6 && k.dtype != DT_BF16) {
@@ -445,8 +451,8 @@ std::string NodeKernel::name() const {
     case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
     case KF_GEMM: {
-      static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "p256x128", "p128", "p256x128s3"};
-      static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4", "-"};
+      static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "p256x128", "p128", "p256x128s3", "q128"};
+      static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4", "-", "-"};
       return "gemm_" + dt + "_" + (dtype == DT_BF16 ? tiles : tiles_f32)[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
              (cmode == 1 ? "n" : cmode == 2 ? "m" : "g") + (gemm.causal ? "_causal" + std::to_string(gemm.causal) : "");
     }
