@@ -34,14 +34,31 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 # --pmc passes (FETCH_SIZE, then WRITE_SIZE) over that kernel, each scaled by
 # what the same counter read for the 256 MiB calibration copy (FETCH_SIZE
 # 0.5001x, WRITE_SIZE 1.0000x).  Reported as `traffic` only for the same
-# (workload, kernel, output shape) and only while the kernel sources hash to
-# TRAFFIC_SRC -- a changed kernel makes the figure stale, and then null.
-TRAFFIC_SRC = "f6ed162e81e8d3ce"
+# (workload, kernel, output shape, input shapes) and only while the kernel
+# sources hash to TRAFFIC_SRC -- a changed kernel makes the figure stale, and
+# then null.
+TRAFFIC_SRC = "03d3722195f168b9"
 TRAFFIC = {
-    ("bert-base-12l-b1-s128-h768", "gemm_f32_dl32w4_amn_bmn_cn", (1, 128, 3072)): 14281158,
-    ("gpt2-small-12l-b1-s512-h768-prefill", "gemm_f32_dl32w4_ak_bmn_cm", (1, 512, 3072)): 28415210,
-    ("bert-large-24l-b8-s512-h1024", "gemm_f32_t128_ak_bmn_cm", (8, 512, 4096)): 230888216,
-    ("llama-8l-b1-s2048-h4096-prefill", "gemm_bf16_p256x128_ak_bmn_cn", (1, 2048, 11008)): 913730701,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6004029,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14269889,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155491201,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 229547587,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 225652680,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 594951228,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16651399,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28424446,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16628910,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 913797883,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185039712,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 893977536,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14289331,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_amn_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14277026,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 768), ((1, 128, 3072), ('c', 3072, 768))): 22512906,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_amn_bmn_cn', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6020398,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16628845,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16648284,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28446950,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28424477,
 }
 
 
@@ -321,7 +338,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         ex.run_nodes(dom_nodes, steps, stream)
         torch.cuda.synchronize()
         return {"kernel": dom_key[0], "node_op": dom_key[1], "out_shape": list(dom_key[2]),
-                "launches": steps * len(dom_nodes)}
+                "in_shapes": [list(s) for s in dom_key[3]], "launches": steps * len(dom_nodes)}
     op_classes = op_class_rates(F, g, lp, ex, steps, torch)
 
     # timed region 1: K eager steps (whole graph, no per-launch events)
@@ -368,13 +385,13 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": None}
         if kernel_source_hash() == TRAFFIC_SRC:
-            roof["traffic"] = TRAFFIC.get((wl, dom_key[0], tuple(dom_key[2])))
+            roof["traffic"] = TRAFFIC.get((wl, dom_key[0], tuple(dom_key[2]), dom_key[3]))
     else:
         achieved = work / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
         if kernel_source_hash() == TRAFFIC_SRC:
-            roof["traffic"] = TRAFFIC.get((wl, dom_key[0], tuple(dom_key[2])))
+            roof["traffic"] = TRAFFIC.get((wl, dom_key[0], tuple(dom_key[2]), dom_key[3]))
     roof.update({"kernel": dom_key[0], "node_op": dom_key[1], "out_shape": list(dom_key[2]),
                  "avg_launch_us": round(avg_ms * 1e3, 3), "launches": launches,
                  "positions_in_step": [launched.index(n) for n in dom_nodes],
