@@ -228,7 +228,7 @@ def ablation(F, g, table, ex, steps, torch):
             ex_a.run()
         torch.cuda.synchronize()
         out[name] = {"ms_per_step": round(graph_ms(ex_a, steps, torch), 4), "table_ns": lp_a.total_ns,
-                     "launches_per_step": sum(1 for v in lp_a.variant if v >= 0),
+                     "launches_per_step": ex_a.launches(),
                      "peak_arena_mb": round(ap_a.peak / 2**20, 3),
                      "op_ms": {op: c["ms_per_step"] for op, c in op_class_rates(F, g, lp_a, ex_a, steps, torch).items()}}
         del ex_a
@@ -307,8 +307,8 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     ex = F.Executor(g, lp, apl, consts, [x])
     ex_naive = F.Executor(g, lp_naive, ap_naive, consts, [x])
     del consts
-    n_launch = sum(1 for v in lp.variant if v >= 0)
-    n_launch_naive = sum(1 for v in lp_naive.variant if v >= 0)
+    n_launch = ex.launches()
+    n_launch_naive = ex_naive.launches()
 
     # warm-up; then, untimed for the result, each node signature's launches
     # back to back (a few passes) to find the dominant kernel, and each

@@ -228,7 +228,11 @@ fluid_status fluid_arena_plan_get(const fluid_arena_plan* ap, uint64_t* peak_byt
 
 /* Executes the graph (Section 4 "Virtual Machine": the invoke interface):
  * enqueues one kernel per non-view node, in node order, on hip_stream; the
- * caller synchronises.  arena: device memory of at least the plan's peak,
+ * caller synchronises.  One exception: a MatMul directly followed (in node
+ * order, views aside) by the Add of a bias constant [N] to its output, that
+ * output being read by nothing else and not a graph output, runs as one
+ * kernel that writes the Add's output with the bias added before rounding
+ * (unless the Add's output shares arena bytes with a MatMul operand).  arena: device memory of at least the plan's peak,
  * 256-B aligned; consts[i], inputs[i], outputs[i]: device pointers to dense
  * row-major tensors of the graph's dtype (RoPE tables fp32).  No device
  * allocation.  Errors before any launch: FLUID_E_INVALID (NULL pointer,
@@ -244,13 +248,21 @@ fluid_status fluid_run(const fluid_graph* g, const fluid_layout_plan* lp, const 
  * uses for them (profiling aid: the time of chosen kernels back to back,
  * without the rest of the graph).  Same argument rules and errors as
  * fluid_run; nodes: n_nodes node ids, each a non-view node under the plan
- * (else FLUID_E_INVALID); repeat >= 1.  Reads and writes the arena like a
+ * (else FLUID_E_INVALID); repeat >= 1.  A MatMul whose bias Add fluid_run
+ * performs in the same launch does so here too when the Add follows it in
+ * the list; listed alone, each runs its own kernel.  Reads and writes the arena like a
  * run would, so it leaves the arena contents of a partial run.  GPU build
  * only. */
 fluid_status fluid_run_nodes(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
                              void* arena, uint64_t arena_bytes, const void* const* consts,
                              const void* const* inputs, void* const* outputs, const int32_t* nodes,
                              int32_t n_nodes, int32_t repeat, void* hip_stream);
+
+/* Number of kernel launches one fluid_run of these plans enqueues (the
+ * non-view nodes, less the bias Adds performed by their MatMul).  Errors:
+ * FLUID_E_INVALID (NULL argument, plans of another graph).  GPU build only. */
+fluid_status fluid_run_launches(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
+                                int32_t* launches);
 
 /* Per-node timing of later fluid_run calls (profiling aid).  While enabled,
  * fluid_run records a HIP event pair around every launch of a node whose

@@ -34,6 +34,20 @@ __device__ __forceinline__ uint16_t bload2(Rsrc r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
 
+// Bias of output column n (0 when the product has none).
+__device__ __forceinline__ float gemm_bias(const GemmParams& p, uint32_t n) {
+  return p.bias_bf16 ? bf16_to_f32(((const uint16_t*)p.bias)[n]) : ((const float*)p.bias)[n];
+}
+// Adds the bias to the 16 accumulators of a 32 x 32 MFMA block whose lane
+// holds output column n (the 32x32 layouts: column l % 32 of the block).
+__device__ __forceinline__ void add_bias16(const GemmParams& p, uint32_t n, f32x16& v) {
+  if (p.bias && n < p.N) {
+    const float b = gemm_bias(p, n);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] += b;
+  }
+}
+
 // s_waitcnt immediate (gfx9 encoding) waiting until at most n vector-memory
 // operations are outstanding; export and LDS counters left unconstrained.
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }

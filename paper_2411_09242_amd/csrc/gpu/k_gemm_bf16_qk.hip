@@ -203,6 +203,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
 
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) add_bias16(p, cur.n0 + wn * 64 + 32 * j + lr, acc[i][j]);
     if (p.cmode == 1 || p.cmode == 2) {
       // every wavefront is done with the A tile: park the output there
       lds_barrier();

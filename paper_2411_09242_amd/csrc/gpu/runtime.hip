@@ -37,6 +37,15 @@ struct PreparedNode {
   NodeKernel k;
   std::vector<Bind> in;  // one per node input (activations and constants)
   Bind out;
+  std::vector<Operand> ops;  // the inputs as prepared (for re-preparing a fused launch)
+  // Bias epilogue: this MatMul also performs the next node, an Add of a
+  // bias vector to its output, and writes that Add's output (fout) directly;
+  // the Add is then not launched by fluid_run.
+  bool fuse_bias = false;
+  NodeKernel kf;
+  Bind fout;
+  int fbias = -1;          // constant id of the bias
+  bool fused_away = false;  // this Add is performed by the previous MatMul
 };
 
 struct Prepared {
@@ -64,6 +73,51 @@ Bind bind_edge(const Graph& g, const ArenaPlan& ap, int e) {
     b.off = ap.offset[e];
   }
   return b;
+}
+
+// Bytes [lo, hi) an arena-bound edge occupies (empty for caller tensors).
+std::pair<int64_t, int64_t> arena_range(const Graph& g, const ArenaPlan& ap, int e, const Bind& b) {
+  if (b.kind != BK_ARENA) return {0, 0};
+  const int64_t bytes = numel(g.edge_shape(e)) * (g.dtype == FLUID_BF16 ? 2 : 4);
+  return {b.off, b.off + bytes};
+}
+
+// Bias epilogue: when the Add `add` directly follows the MatMul `mm` in launch
+// order, adds a bias constant [N] to the MatMul's output, and is that
+// output's only reader (which is no graph output), the MatMul is re-prepared
+// to write the Add's output (in the Add's output layout) with the bias added
+// in fp32 before rounding.  Not when the Add's output shares arena bytes with
+// a MatMul operand: the Add's output only becomes live after the MatMul has
+// read its operands, so the arena may have placed it over them.
+void try_fuse_bias(const Graph& g, const LayoutPlan& lp, const ArenaPlan& ap, PreparedNode& mm, PreparedNode& add,
+                   const Operand& add_out) {
+  if (mm.k.family != KF_GEMM) return;
+  const Node& an = g.nodes[add.node];
+  const Node& mn = g.nodes[mm.node];
+  if (an.op != FLUID_OP_ADD || an.ins.size() != 2 || mn.ins.size() != 2) return;
+  const int em = g.out_edge(mm.node);
+  int slot = -1;
+  for (int i = 0; i < 2; ++i)
+    if (an.ins[i] == em) slot = i;
+  if (slot < 0 || an.ins[1 - slot] >= 0) return;
+  const int c = ~an.ins[1 - slot];
+  const Shape& cs = g.consts[c].shape;
+  if (cs.size() != 1 || cs[0] != mn.out_shape.back() || g.consts[c].dtype != g.dtype) return;
+  if (g.is_output[em] || g.readers[em].size() != 1 || g.readers[em][0] != add.node) return;
+  const auto ro = arena_range(g, ap, g.out_edge(add.node), add.out);
+  for (int i = 0; i < 2; ++i) {
+    if (mn.ins[i] < 0) continue;
+    const auto ri = arena_range(g, ap, mn.ins[i], mm.in[i]);
+    if (ro.first < ro.second && ri.first < ri.second && ro.first < ri.second && ri.first < ro.second) return;
+  }
+  NodeKernel kf = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, add_out);
+  if (!kf.available) return;
+  kf.gemm.bias_bf16 = g.dtype == FLUID_BF16 ? 1u : 0u;
+  mm.fuse_bias = true;
+  mm.kf = kf;
+  mm.fout = add.out;
+  mm.fbias = c;
+  add.fused_away = true;
 }
 
 std::shared_ptr<Prepared> prepare(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah) {
@@ -107,6 +161,8 @@ std::shared_ptr<Prepared> prepare(const fluid_graph* gh, const fluid_layout_plan
     if (!pn.k.available)
       fail(FLUID_E_INVALID, "node " + std::to_string(n) + ": variant " + std::to_string(lp.variant[n]) +
                                 " cannot run with these layouts (" + pn.k.why + ")");
+    pn.ops = ins;
+    if (!P->nodes.empty()) try_fuse_bias(g, lp, ap, P->nodes.back(), pn, out);
     P->nodes.push_back(std::move(pn));
   }
   return P;
@@ -151,6 +207,16 @@ void patch(NodeKernel& k, const PreparedNode& pn, const Bases& B) {
     default:
       break;
   }
+}
+
+// The fused MatMul + bias launch of pn (fuse_bias set).
+NodeKernel fused_kernel(const PreparedNode& pn, const Bases& B) {
+  NodeKernel k = pn.kf;
+  k.gemm.A = resolve(pn.in[0], B);
+  k.gemm.B = resolve(pn.in[1], B);
+  k.gemm.C = resolve(pn.fout, B);
+  k.gemm.bias = B.consts[pn.fbias];
+  return k;
 }
 
 // ------------------------------------------------------------ tracing
@@ -222,6 +288,9 @@ using namespace fluid;
 
 namespace {
 
+std::shared_ptr<Prepared> cached_prepared(const fluid_graph* gh, const fluid_layout_plan* lh,
+                                          const fluid_arena_plan* ah);
+
 // Argument checks shared by fluid_run and fluid_run_nodes, then the cached
 // launch parameters of the (layout plan, arena plan) pair.
 std::shared_ptr<Prepared> checked_prepared(const fluid_graph* gh, const fluid_layout_plan* lh,
@@ -248,6 +317,11 @@ std::shared_ptr<Prepared> checked_prepared(const fluid_graph* gh, const fluid_la
     require(outputs[i] && aligned(outputs[i], 16), f + ": output " + std::to_string(i) + " is NULL or not 16-byte aligned");
   for (size_t i = 0; i < g.consts.size(); ++i)
     require(consts[i] && aligned(consts[i], 16), f + ": const " + std::to_string(i) + " is NULL or not 16-byte aligned");
+  return cached_prepared(gh, lh, ah);
+}
+
+std::shared_ptr<Prepared> cached_prepared(const fluid_graph* gh, const fluid_layout_plan* lh,
+                                          const fluid_arena_plan* ah) {
   std::lock_guard<std::mutex> lk(g_cache_mu);
   // plan serials are never reused, so a stale entry can never match
   static std::map<std::pair<uint64_t, uint64_t>, std::shared_ptr<Prepared>> cache;
@@ -276,8 +350,10 @@ fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const
     const bool tracing = g_trace.on && g_trace.graph_serial == gh->serial;
     if (!tracing) tl.unlock();
     for (const PreparedNode& pn : prep->nodes) {
+      if (pn.fused_away) continue;  // performed by the MatMul before it
       NodeKernel k = pn.k;
-      patch(k, pn, B);
+      if (pn.fuse_bias) k = fused_kernel(pn, B);
+      else patch(k, pn, B);
       int rec = -1;
       if (tracing && g_trace.mask[pn.node] && (int)g_trace.node_of.size() < g_trace.max_records) {
         rec = (int)g_trace.node_of.size();
@@ -312,14 +388,35 @@ fluid_status fluid_run_nodes(const fluid_graph* gh, const fluid_layout_plan* lh,
     }
     Bases B{(char*)arena, inputs, outputs, consts};
     hipStream_t s = (hipStream_t)hip_stream;
+    // a fused MatMul followed in the list by its Add runs as in fluid_run;
+    // either one on its own runs its own kernel
     for (int32_t r = 0; r < repeat; ++r)
-      for (const PreparedNode* pn : sel) {
+      for (size_t i = 0; i < sel.size(); ++i) {
+        const PreparedNode* pn = sel[i];
         NodeKernel k = pn->k;
-        patch(k, *pn, B);
+        if (pn->fuse_bias && i + 1 < sel.size() && sel[i + 1] == pn + 1) {
+          k = fused_kernel(*pn, B);
+          ++i;
+        } else {
+          patch(k, *pn, B);
+        }
         hipError_t e = launch_node_kernel(k, s);
         if (e != hipSuccess)
           fail(FLUID_E_HIP, "node " + std::to_string(pn->node) + " (" + k.name() + "): " + hipGetErrorString(e));
       }
+  });
+}
+
+fluid_status fluid_run_launches(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah,
+                                int32_t* launches) {
+  return call_guarded([&] {
+    require(gh && lh && ah && launches, "fluid_run_launches: NULL argument");
+    require(lh->p.graph_serial == gh->serial && ah->a.graph_serial == gh->serial,
+            "fluid_run_launches: plans belong to another graph");
+    std::shared_ptr<Prepared> prep = cached_prepared(gh, lh, ah);
+    int32_t n = 0;
+    for (const PreparedNode& pn : prep->nodes) n += pn.fused_away ? 0 : 1;
+    *launches = n;
   });
 }
 

@@ -295,6 +295,8 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   check_small(C, "matmul");
   const int rA = (int)A.shape.size(), rB = (int)B.shape.size();
   GemmParams& p = k.gemm;
+  p.bias = nullptr;
+  p.bias_bf16 = 0;
   p.A = A.ptr;
   p.B = B.ptr;
   p.C = const_cast<void*>(C.ptr);

@@ -84,6 +84,7 @@ _PROTOS = {
                             C.POINTER(_VP), _VP]),
     "fluid_run_nodes": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
                                   C.POINTER(_VP), C.POINTER(C.c_int32), C.c_int32, C.c_int32, _VP]),
+    "fluid_run_launches": (C.c_int, [_VP, _VP, _VP, C.POINTER(C.c_int32)]),
     "fluid_trace_enable": (C.c_int, [_VP, C.POINTER(C.c_uint8), C.c_int32]),
     "fluid_trace_collect": (C.c_int, [_VP, C.POINTER(C.c_double), C.POINTER(C.c_int32)]),
     "fluid_node_kernel": (C.c_int, [_VP, _VP, C.c_int32, C.c_char_p, C.c_uint64]),
@@ -272,6 +273,12 @@ def fluid_run_nodes(g, lp, ap, arena_ptr, arena_bytes, const_ptrs, input_ptrs, o
                                 stream))
 
 
+def fluid_run_launches(g, lp, ap):
+    n = C.c_int32(0)
+    _check(_L().fluid_run_launches(g, lp, ap, C.byref(n)))
+    return n.value
+
+
 def fluid_trace_enable(g, mask, max_records):
     m = None
     if mask is not None:
@@ -407,6 +414,11 @@ class Executor:
         fluid_run(self.graph.h, self.lplan.h, self.aplan.h, self.arena_ptr, self.aplan.peak,
                   self._cp, self._ip, self._op, s)
         return self.outputs
+
+    def launches(self):
+        """Kernel launches one run enqueues (bias Adds fused into their
+        MatMul are not counted)."""
+        return fluid_run_launches(self.graph.h, self.lplan.h, self.aplan.h)
 
     def run_nodes(self, nodes, repeat=1, stream=None):
         """Launch only the kernels of ``nodes`` (in list order), ``repeat``
