@@ -204,10 +204,10 @@ def build_transformer(cfg: dict) -> Graph:
             gm2 = g.add_const("gamma", (H,))
             h1 = g.add_node("rmsnorm", [r1, gm2], (B, S, H), fattr=eps)
             wg = g.add_const("weight", (H, F))
-            gg = g.add_node("matmul", [h1, wg], (B, S, F))
             wu = g.add_const("weight", (H, F))
-            uu = g.add_node("matmul", [h1, wu], (B, S, F))
+            gg = g.add_node("matmul", [h1, wg], (B, S, F))
             sg = g.add_node("silu", [gg], (B, S, F))
+            uu = g.add_node("matmul", [h1, wu], (B, S, F))
             m = g.add_node("mul", [sg, uu], (B, S, F))
             wd = g.add_const("weight", (F, H))
             d = g.add_node("matmul", [m, wd], (B, S, H))

@@ -34,17 +34,29 @@ __device__ __forceinline__ uint16_t bload2(Rsrc r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
 
-// Bias of output column n (0 when the product has none).
+// Bias of output column n.
 __device__ __forceinline__ float gemm_bias(const GemmParams& p, uint32_t n) {
   return p.bias_bf16 ? bf16_to_f32(((const uint16_t*)p.bias)[n]) : ((const float*)p.bias)[n];
 }
-// Adds the bias to the 16 accumulators of a 32 x 32 MFMA block whose lane
+// The epilogue of one output value of column n (bias, then activation).
+__device__ __forceinline__ float gemm_epi(const GemmParams& p, uint32_t n, float v) {
+  if (p.bias) v += gemm_bias(p, n);
+  if (p.act == 1) v = gelu_erf(v);
+  else if (p.act == 2) v = silu(v);
+  return v;
+}
+// The epilogue of the 16 accumulators of a 32 x 32 MFMA block whose lane
 // holds output column n (the 32x32 layouts: column l % 32 of the block).
-__device__ __forceinline__ void add_bias16(const GemmParams& p, uint32_t n, f32x16& v) {
-  if (p.bias && n < p.N) {
-    const float b = gemm_bias(p, n);
+__device__ __forceinline__ void epi16(const GemmParams& p, uint32_t n, f32x16& v) {
+  if ((p.bias || p.act) && n < p.N) {
+    const float b = p.bias ? gemm_bias(p, n) : 0.f;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) v[i] += b;
+    for (int i = 0; i < 16; ++i) {
+      float x = p.bias ? v[i] + b : v[i];
+      if (p.act == 1) x = gelu_erf(x);
+      else if (p.act == 2) x = silu(x);
+      v[i] = x;
+    }
   }
 }
 

@@ -218,7 +218,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) add_bias16(p, tc.n0 + wn * WN + j * 32 + lr, acc[i][j]);
+    for (int j = 0; j < FN; ++j) epi16(p, tc.n0 + wn * WN + j * 32 + lr, acc[i][j]);
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -460,7 +460,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const uint32_t n = tc.n0 + wn * WN + j * 32 + lr;
-      add_bias16(p, n, acc[i][j]);
+      epi16(p, n, acc[i][j]);
       if (n >= p.N) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -649,7 +649,7 @@ __global__ __launch_bounds__(64 * W) void gemm_sk_kernel(GemmParams p) {
     float sum = 0.f;
 #pragma unroll
     for (int q = 0; q < W; ++q) sum += red[q * TM * RP + ml * RP + nl];
-    if (p.bias) sum += gemm_bias(p, n);
+    sum = gemm_epi(p, n, sum);
     Elem<T>::store(p.C, tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n * p.c_n, sum);
   }
 }

@@ -194,7 +194,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const uint32_t n = tc.n0 + wn * 64 + j * 32 + lr;
-      add_bias16(p, n, acc[i][j]);
+      epi16(p, n, acc[i][j]);
       if (n >= p.N) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {

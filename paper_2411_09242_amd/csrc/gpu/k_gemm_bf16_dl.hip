@@ -236,7 +236,7 @@ void gemm_bf16_dl_kernel(GemmParams p) {
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) add_bias16(p, tc.n0 + j * 32 + lr, acc[i][j]);
+    for (int j = 0; j < FN; ++j) epi16(p, tc.n0 + j * 32 + lr, acc[i][j]);
   if (p.cmode == 1 || p.cmode == 2) {
     // the padding tiles' loads land in the ring: drain them, and let every
     // wavefront finish its last tile, before the ring is reused

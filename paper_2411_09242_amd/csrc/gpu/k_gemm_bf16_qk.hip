@@ -206,7 +206,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) add_bias16(p, cur.n0 + wn * 64 + 32 * j + lr, acc[i][j]);
+      for (int j = 0; j < 2; ++j) epi16(p, cur.n0 + wn * 64 + 32 * j + lr, acc[i][j]);
     if (p.cmode == 1 || p.cmode == 2) {
       // every wavefront is done with the A tile: park the output there
       lds_barrier();

@@ -159,7 +159,7 @@ __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
       for (int t = 0; t < 4; ++t) {
         float sum = 0.f;
         for (int w = 0; w < W; ++w) sum += red[(w * SK_TM + r0 + t) * SK_RP + c];
-        o[t] = p.bias ? sum + gemm_bias(p, n) : sum;
+        o[t] = gemm_epi(p, n, sum);
       }
       // four rows m0..m0+3 lie in one M2 run (M2 % 4 == 0 in this mode)
       if (m0 + 3 < p.M) {
@@ -181,7 +181,7 @@ __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
       for (int t = 0; t < 4; ++t) {
         float sum = 0.f;
         for (int w = 0; w < W; ++w) sum += red[(w * SK_TM + r) * SK_RP + c0 + t];
-        o[t] = (p.bias && n0 + t < p.N) ? sum + gemm_bias(p, n0 + t) : sum;
+        o[t] = n0 + t < p.N ? gemm_epi(p, n0 + t, sum) : sum;
       }
       const int32_t base = tc.c_base + row_off(p, m, p.c_m1, p.c_m2);
       if (p.cmode == 1 && n0 + 3 < p.N && ((uintptr_t)(C + base + (int32_t)n0) & 15u) == 0) {

@@ -38,14 +38,15 @@ struct PreparedNode {
   std::vector<Bind> in;  // one per node input (activations and constants)
   Bind out;
   std::vector<Operand> ops;  // the inputs as prepared (for re-preparing a fused launch)
-  // Bias epilogue: this MatMul also performs the next node, an Add of a
-  // bias vector to its output, and writes that Add's output (fout) directly;
-  // the Add is then not launched by fluid_run.
-  bool fuse_bias = false;
+  // Epilogue fusion: this MatMul also performs the fuse_n nodes after it (a
+  // bias Add, an activation, or a bias Add then an activation) and writes the
+  // last one's output (fout) directly; those nodes are then not launched by
+  // fluid_run.
+  int fuse_n = 0;
   NodeKernel kf;
   Bind fout;
-  int fbias = -1;          // constant id of the bias
-  bool fused_away = false;  // this Add is performed by the previous MatMul
+  int fbias = -1;           // constant id of the bias, -1 when none
+  bool fused_away = false;  // this node is performed by a MatMul before it
 };
 
 struct Prepared {
@@ -82,42 +83,53 @@ std::pair<int64_t, int64_t> arena_range(const Graph& g, const ArenaPlan& ap, int
   return {b.off, b.off + bytes};
 }
 
-// Bias epilogue: when the Add `add` directly follows the MatMul `mm` in launch
-// order, adds a bias constant [N] to the MatMul's output, and is that
-// output's only reader (which is no graph output), the MatMul is re-prepared
-// to write the Add's output (in the Add's output layout) with the bias added
-// in fp32 before rounding.  Not when the Add's output shares arena bytes with
-// a MatMul operand: the Add's output only becomes live after the MatMul has
-// read its operands, so the arena may have placed it over them.
-void try_fuse_bias(const Graph& g, const LayoutPlan& lp, const ArenaPlan& ap, PreparedNode& mm, PreparedNode& add,
-                   const Operand& add_out) {
-  if (mm.k.family != KF_GEMM) return;
-  const Node& an = g.nodes[add.node];
+// Epilogue fusion.  A MatMul absorbs the node `nx` launched right after the
+// chain it already performs (its own product, or product + bias) when nx is
+// the chain output's only reader (which is no graph output) and is either an
+// Add of a bias constant [N] (only as the first step) or a GELU / SiLU (the
+// last step).  The MatMul is then re-prepared to write nx's output, in nx's
+// output layout, with bias and activation applied in fp32 before the one
+// rounding.  Not when nx's output shares arena bytes with a MatMul operand:
+// that output only becomes live after the MatMul has read its operands, so
+// the arena may have placed it over them.
+// `tail` is the output edge of the chain's last node.
+void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan& ap, PreparedNode& mm, int tail,
+                       PreparedNode& nx, const Operand& nx_out) {
+  if (mm.k.family != KF_GEMM || mm.fused_away) return;
+  const Node& xn = g.nodes[nx.node];
   const Node& mn = g.nodes[mm.node];
-  if (an.op != FLUID_OP_ADD || an.ins.size() != 2 || mn.ins.size() != 2) return;
-  const int em = g.out_edge(mm.node);
-  int slot = -1;
-  for (int i = 0; i < 2; ++i)
-    if (an.ins[i] == em) slot = i;
-  if (slot < 0 || an.ins[1 - slot] >= 0) return;
-  const int c = ~an.ins[1 - slot];
-  const Shape& cs = g.consts[c].shape;
-  if (cs.size() != 1 || cs[0] != mn.out_shape.back() || g.consts[c].dtype != g.dtype) return;
-  if (g.is_output[em] || g.readers[em].size() != 1 || g.readers[em][0] != add.node) return;
-  const auto ro = arena_range(g, ap, g.out_edge(add.node), add.out);
+  const uint32_t act_now = mm.fuse_n ? mm.kf.gemm.act : 0u;
+  if (mn.ins.size() != 2) return;
+  if (g.is_output[tail] || g.readers[tail].size() != 1 || g.readers[tail][0] != nx.node) return;
+  int bias = mm.fbias;
+  uint32_t act = 0;
+  if (xn.op == FLUID_OP_ADD && mm.fuse_n == 0 && xn.ins.size() == 2) {
+    const int slot = xn.ins[0] == tail ? 0 : 1;
+    if (xn.ins[1 - slot] >= 0) return;
+    const int c = ~xn.ins[1 - slot];
+    const Shape& cs = g.consts[c].shape;
+    if (cs.size() != 1 || cs[0] != mn.out_shape.back() || g.consts[c].dtype != g.dtype) return;
+    bias = c;
+  } else if ((xn.op == FLUID_OP_GELU || xn.op == FLUID_OP_SILU) && act_now == 0) {
+    act = xn.op == FLUID_OP_GELU ? 1u : 2u;
+  } else {
+    return;
+  }
+  const auto ro = arena_range(g, ap, g.out_edge(nx.node), nx.out);
   for (int i = 0; i < 2; ++i) {
     if (mn.ins[i] < 0) continue;
     const auto ri = arena_range(g, ap, mn.ins[i], mm.in[i]);
     if (ro.first < ro.second && ri.first < ri.second && ro.first < ri.second && ri.first < ro.second) return;
   }
-  NodeKernel kf = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, add_out);
+  NodeKernel kf = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, nx_out);
   if (!kf.available) return;
   kf.gemm.bias_bf16 = g.dtype == FLUID_BF16 ? 1u : 0u;
-  mm.fuse_bias = true;
+  kf.gemm.act = act ? act : act_now;
+  mm.fuse_n += 1;
   mm.kf = kf;
-  mm.fout = add.out;
-  mm.fbias = c;
-  add.fused_away = true;
+  mm.fout = nx.out;
+  mm.fbias = bias;
+  nx.fused_away = true;
 }
 
 std::shared_ptr<Prepared> prepare(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah) {
@@ -162,7 +174,13 @@ std::shared_ptr<Prepared> prepare(const fluid_graph* gh, const fluid_layout_plan
       fail(FLUID_E_INVALID, "node " + std::to_string(n) + ": variant " + std::to_string(lp.variant[n]) +
                                 " cannot run with these layouts (" + pn.k.why + ")");
     pn.ops = ins;
-    if (!P->nodes.empty()) try_fuse_bias(g, lp, ap, P->nodes.back(), pn, out);
+    if (!P->nodes.empty()) {
+      // the MatMul whose fused chain ends at the previous launch, if any
+      size_t j = P->nodes.size() - 1;
+      while (j > 0 && P->nodes[j].fused_away) --j;
+      if (j + P->nodes[j].fuse_n == P->nodes.size() - 1)
+        try_fuse_epilogue(g, lp, ap, P->nodes[j], g.out_edge(P->nodes.back().node), pn, out);
+    }
     P->nodes.push_back(std::move(pn));
   }
   return P;
@@ -209,13 +227,13 @@ void patch(NodeKernel& k, const PreparedNode& pn, const Bases& B) {
   }
 }
 
-// The fused MatMul + bias launch of pn (fuse_bias set).
+// The fused MatMul + epilogue launch of pn (fuse_n > 0).
 NodeKernel fused_kernel(const PreparedNode& pn, const Bases& B) {
   NodeKernel k = pn.kf;
   k.gemm.A = resolve(pn.in[0], B);
   k.gemm.B = resolve(pn.in[1], B);
   k.gemm.C = resolve(pn.fout, B);
-  k.gemm.bias = B.consts[pn.fbias];
+  k.gemm.bias = pn.fbias >= 0 ? B.consts[pn.fbias] : nullptr;
   return k;
 }
 
@@ -350,9 +368,9 @@ fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const
     const bool tracing = g_trace.on && g_trace.graph_serial == gh->serial;
     if (!tracing) tl.unlock();
     for (const PreparedNode& pn : prep->nodes) {
-      if (pn.fused_away) continue;  // performed by the MatMul before it
+      if (pn.fused_away) continue;  // performed by a MatMul before it
       NodeKernel k = pn.k;
-      if (pn.fuse_bias) k = fused_kernel(pn, B);
+      if (pn.fuse_n) k = fused_kernel(pn, B);
       else patch(k, pn, B);
       int rec = -1;
       if (tracing && g_trace.mask[pn.node] && (int)g_trace.node_of.size() < g_trace.max_records) {
@@ -388,15 +406,17 @@ fluid_status fluid_run_nodes(const fluid_graph* gh, const fluid_layout_plan* lh,
     }
     Bases B{(char*)arena, inputs, outputs, consts};
     hipStream_t s = (hipStream_t)hip_stream;
-    // a fused MatMul followed in the list by its Add runs as in fluid_run;
-    // either one on its own runs its own kernel
+    // a fused MatMul followed in the list by every node it absorbs runs as in
+    // fluid_run; otherwise each node runs its own kernel
     for (int32_t r = 0; r < repeat; ++r)
       for (size_t i = 0; i < sel.size(); ++i) {
         const PreparedNode* pn = sel[i];
         NodeKernel k = pn->k;
-        if (pn->fuse_bias && i + 1 < sel.size() && sel[i + 1] == pn + 1) {
+        bool whole = pn->fuse_n > 0 && i + pn->fuse_n < sel.size();
+        for (int f = 1; whole && f <= pn->fuse_n; ++f) whole = sel[i + f] == pn + f;
+        if (whole) {
           k = fused_kernel(*pn, B);
-          ++i;
+          i += pn->fuse_n;
         } else {
           patch(k, *pn, B);
         }

@@ -297,6 +297,7 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   GemmParams& p = k.gemm;
   p.bias = nullptr;
   p.bias_bf16 = 0;
+  p.act = 0;
   p.A = A.ptr;
   p.B = B.ptr;
   p.C = const_cast<void*>(C.ptr);

@@ -317,9 +317,11 @@ Graph build_transformer(const fluid_model_cfg& c) {
       int o0 = b.add(FLUID_OP_MATMUL, {c2, b.add_const(FLUID_ROLE_WEIGHT, {H, H}, dt)}, {B, S, H});
       int r1 = b.add(FLUID_OP_ADD, {o0, x}, {B, S, H});
       int h1 = rmsnorm(r1);
-      int gg = b.add(FLUID_OP_MATMUL, {h1, b.add_const(FLUID_ROLE_WEIGHT, {H, F}, dt)}, {B, S, F});
-      int uu = b.add(FLUID_OP_MATMUL, {h1, b.add_const(FLUID_ROLE_WEIGHT, {H, F}, dt)}, {B, S, F});
+      const int wg = b.add_const(FLUID_ROLE_WEIGHT, {H, F}, dt);
+      const int wu = b.add_const(FLUID_ROLE_WEIGHT, {H, F}, dt);
+      int gg = b.add(FLUID_OP_MATMUL, {h1, wg}, {B, S, F});
       int sg = b.add(FLUID_OP_SILU, {gg}, {B, S, F});
+      int uu = b.add(FLUID_OP_MATMUL, {h1, wu}, {B, S, F});
       int m = b.add(FLUID_OP_MUL, {sg, uu}, {B, S, F});
       int d = b.add(FLUID_OP_MATMUL, {m, b.add_const(FLUID_ROLE_WEIGHT, {F, H}, dt)}, {B, S, H});
       x = b.add(FLUID_OP_ADD, {d, r1}, {B, S, H});

@@ -100,10 +100,12 @@ struct GemmParams {
   // every n > m may be skipped; bit 1, A[m][k] = 0 for k > m, so the K loop
   // of rows m0 .. m0 + BM - 1 may stop at m0 + BM.
   uint32_t causal;
-  // Bias epilogue: C[m][n] = sum_k A B + bias[n], bias a dense [N] vector of
-  // the graph dtype (bf16 when bias_bf16), or none when bias is null.
+  // Epilogue: C[m][n] = act(sum_k A B + bias[n]), bias a dense [N] vector of
+  // the graph dtype (bf16 when bias_bf16) or none when null; act 0 none,
+  // 1 GELU (erf form), 2 SiLU.
   const void* bias;
   uint32_t bias_bf16;
+  uint32_t act;
 };
 
 }  // namespace fluid
