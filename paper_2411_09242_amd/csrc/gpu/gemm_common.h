@@ -12,7 +12,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 struct TileCoord {
   uint32_t m0, n0;
-  int32_t a_base, b_base, c_base;
+  int32_t a_base, b_base, c_base, r_base;
 };
 
 // Buffer resource over [base, base + bytes).  A buffer load at a byte offset
@@ -34,32 +34,6 @@ __device__ __forceinline__ uint16_t bload2(Rsrc r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
 
-// Bias of output column n.
-__device__ __forceinline__ float gemm_bias(const GemmParams& p, uint32_t n) {
-  return p.bias_bf16 ? bf16_to_f32(((const uint16_t*)p.bias)[n]) : ((const float*)p.bias)[n];
-}
-// The epilogue of one output value of column n (bias, then activation).
-__device__ __forceinline__ float gemm_epi(const GemmParams& p, uint32_t n, float v) {
-  if (p.bias) v += gemm_bias(p, n);
-  if (p.act == 1) v = gelu_erf(v);
-  else if (p.act == 2) v = silu(v);
-  return v;
-}
-// The epilogue of the 16 accumulators of a 32 x 32 MFMA block whose lane
-// holds output column n (the 32x32 layouts: column l % 32 of the block).
-__device__ __forceinline__ void epi16(const GemmParams& p, uint32_t n, f32x16& v) {
-  if ((p.bias || p.act) && n < p.N) {
-    const float b = p.bias ? gemm_bias(p, n) : 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      float x = p.bias ? v[i] + b : v[i];
-      if (p.act == 1) x = gelu_erf(x);
-      else if (p.act == 2) x = silu(x);
-      v[i] = x;
-    }
-  }
-}
-
 // s_waitcnt immediate (gfx9 encoding) waiting until at most n vector-memory
 // operations are outstanding; export and LDS counters left unconstrained.
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
@@ -79,6 +53,7 @@ __device__ __forceinline__ TileCoord tile_coord_at(const GemmParams& p, uint32_t
   t.a_base = (int32_t)g1 * p.a_g1 + (int32_t)g2 * p.a_g2;
   t.b_base = (int32_t)g1 * p.b_g1 + (int32_t)g2 * p.b_g2;
   t.c_base = (int32_t)g1 * p.c_g1 + (int32_t)g2 * p.c_g2;
+  t.r_base = (int32_t)g1 * p.r_g1 + (int32_t)g2 * p.r_g2;
   return t;
 }
 // One workgroup per tile.
@@ -91,6 +66,57 @@ __device__ __forceinline__ int32_t row_off(const GemmParams& p, uint32_t m, int3
   const uint32_t m1 = fdiv(m, p.m2div);
   return (int32_t)m1 * s1 + (int32_t)(m - m1 * p.M2) * s2;
 }
+
+// ---- epilogue: bias, activation, then the elementwise Add / Mul with R
+// Offset of row m of R.  It splits m with R's own copy of the divisor: the
+// compiler cannot share that split with the stores' (which would keep the
+// split of every row of a tile live from the epilogue to the stores).
+__device__ __forceinline__ int32_t r_row_off(const GemmParams& p, uint32_t m) {
+  const uint32_t m1 = fdiv(m, p.r_m2div);
+  return (int32_t)m1 * p.r_m1 + (int32_t)(m - m1 * p.r_m2div.d) * p.r_m2;
+}
+__device__ __forceinline__ float epi_load(const GemmParams& p, const void* base, int32_t off) {
+  return p.epi_bf16 ? bf16_to_f32(((const uint16_t*)base)[off]) : ((const float*)base)[off];
+}
+__device__ __forceinline__ float epi_act(const GemmParams& p, float x) {
+  if (p.act == 1) return gelu_erf(x);
+  if (p.act == 2) return silu(x);
+  return x;
+}
+__device__ __forceinline__ float epi_rop(const GemmParams& p, float x, float r) {
+  return p.rop == 1 ? x + r : x * r;
+}
+// One output value at (m, n) of the batch whose R offset is r_base.  RES:
+// the kernel instance that performs the Add / Mul with R (a separate
+// instance, so that the others keep their register budget).
+template <bool RES>
+__device__ __forceinline__ float gemm_epi(const GemmParams& p, int32_t r_base, uint32_t m, uint32_t n, float v) {
+  if (p.bias) v += epi_load(p, p.bias, (int32_t)n);
+  v = epi_act(p, v);
+  if (RES && m < p.M)
+    v = epi_rop(p, v, epi_load(p, p.R, r_base + r_row_off(p, m) + (int32_t)n * p.r_n));
+  return v;
+}
+// The 16 accumulators of a 32 x 32 MFMA block (the 32x32 output layout:
+// value v of a lane sits at row m_first + 8 (v / 4) + v % 4 of column n).
+// ACT false: an instance without the activation step.
+template <bool RES, bool ACT = true>
+__device__ __forceinline__ void epi16(const GemmParams& p, int32_t r_base, uint32_t m_first, uint32_t n,
+                                      f32x16& v) {
+  if ((p.bias || (ACT && p.act) || RES) && n < p.N) {
+    const float b = p.bias ? epi_load(p, p.bias, (int32_t)n) : 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float x = ACT ? epi_act(p, v[i] + b) : v[i] + b;
+      if (RES) {
+        const uint32_t m = m_first + 8 * (i / 4) + (i % 4);
+        if (m < p.M) x = epi_rop(p, x, epi_load(p, p.R, r_base + r_row_off(p, m) + (int32_t)n * p.r_n));
+      }
+      v[i] = x;
+    }
+  }
+}
+
 
 // Four rows of four bf16 (rows[t] = elements 0..3 at k + t) -> four rows of
 // four k (out[j] = k .. k+3 of element j).

@@ -21,7 +21,7 @@
 namespace fluid {
 
 // ============================================================== fp32
-template <int BM, int BN, int AM, int BMD>
+template <int BM, int BN, int AM, int BMD, bool RES>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
   constexpr int BK = 16;
   constexpr int WM = BM / 2, WN = BN / 2;
@@ -218,7 +218,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) epi16(p, tc.n0 + wn * WN + j * 32 + lr, acc[i][j]);
+    for (int j = 0; j < FN; ++j)
+      epi16<RES>(p, tc.r_base, tc.m0 + wm * WM + i * 32 + 4 * lk, tc.n0 + wn * WN + j * 32 + lr, acc[i][j]);
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 // lane fetches its 8 bf16 MFMA inputs with one 16-byte LDS read.  An
 // M-/N-contiguous HBM operand is transposed on the way in: each thread loads
 // a 4(k) x 4(m|n) block with four 8-byte loads and writes four 8-byte rows.
-template <int BM, int BN, int AM, int BMD>
+template <int BM, int BN, int AM, int BMD, bool RES>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
   constexpr int BK = 32;
   constexpr int WM = BM / 2, WN = BN / 2;
@@ -460,7 +461,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const uint32_t n = tc.n0 + wn * WN + j * 32 + lr;
-      epi16(p, n, acc[i][j]);
+      epi16<RES>(p, tc.r_base, tc.m0 + wm * WM + i * 32 + 4 * (lane >> 5), n, acc[i][j]);
       if (n >= p.N) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -485,7 +486,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
 // Each iteration covers U such steps and the next iteration's loads are
 // issued before the current MFMAs (ping-pong registers with compile-time
 // indices), so 2 x 16U K-values per wavefront are in flight.
-template <typename T, int FM, int FN, int W, int U, bool AVK, bool BVK>
+template <typename T, int FM, int FN, int W, int U, bool AVK, bool BVK, bool RES>
 __global__ __launch_bounds__(64 * W) void gemm_sk_kernel(GemmParams p) {
   constexpr int TM = 32 * FM, TN = 32 * FN, RP = TN + 1;
   constexpr int KI = 16 * U;  // K values per iteration
@@ -649,7 +650,7 @@ __global__ __launch_bounds__(64 * W) void gemm_sk_kernel(GemmParams p) {
     float sum = 0.f;
 #pragma unroll
     for (int q = 0; q < W; ++q) sum += red[q * TM * RP + ml * RP + nl];
-    sum = gemm_epi(p, n, sum);
+    sum = gemm_epi<RES>(p, tc.r_base, m, n, sum);
     Elem<T>::store(p.C, tc.c_base + row_off(p, m, p.c_m1, p.c_m2) + (int32_t)n * p.c_n, sum);
   }
 }
@@ -661,10 +662,16 @@ hipError_t gemm_sk_go(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
   const bool avk = k.amode == GM_K, bvk = k.bmode == GM_K;
-  if (avk && bvk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, true, true>), grid, dim3(64 * W), 0, s, p);
-  else if (avk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, true, false>), grid, dim3(64 * W), 0, s, p);
-  else if (bvk) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, false, true>), grid, dim3(64 * W), 0, s, p);
-  else hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, false, false>), grid, dim3(64 * W), 0, s, p);
+#define FLUID_SK(AV, BV)                                                                              \
+  do {                                                                                      \
+  if (p.rop) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, AV, BV, true>), grid, dim3(64 * W), 0, s, p); \
+  else hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, AV, BV, false>), grid, dim3(64 * W), 0, s, p); \
+} while (0)
+  if (avk && bvk) FLUID_SK(true, true);
+  else if (avk) FLUID_SK(true, false);
+  else if (bvk) FLUID_SK(false, true);
+  else FLUID_SK(false, false);
+#undef FLUID_SK
   return hipGetLastError();
 }
 
@@ -682,8 +689,13 @@ template <int T, int AM, int BMD>
 hipError_t gemm_go(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
-  if (k.dtype == DT_BF16) hipLaunchKernelGGL((gemm_bf16_kernel<T, T, AM, BMD>), grid, dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((gemm_f32_kernel<T, T, AM, BMD>), grid, dim3(256), 0, s, p);
+  if (k.dtype == DT_BF16) {
+    if (p.rop) hipLaunchKernelGGL((gemm_bf16_kernel<T, T, AM, BMD, true>), grid, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((gemm_bf16_kernel<T, T, AM, BMD, false>), grid, dim3(256), 0, s, p);
+  } else {
+    if (p.rop) hipLaunchKernelGGL((gemm_f32_kernel<T, T, AM, BMD, true>), grid, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((gemm_f32_kernel<T, T, AM, BMD, false>), grid, dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 

@@ -77,6 +77,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     c.a_base = (int32_t)g1 * p.a_g1 + (int32_t)g2 * p.a_g2;
     c.b_base = (int32_t)g1 * p.b_g1 + (int32_t)g2 * p.b_g2;
     c.c_base = (int32_t)g1 * p.c_g1 + (int32_t)g2 * p.c_g2;
+    c.r_base = 0;  // no Add / Mul epilogue here
     return c;
   };
 
@@ -206,7 +207,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) epi16(p, cur.n0 + wn * 64 + 32 * j + lr, acc[i][j]);
+      for (int j = 0; j < 2; ++j)
+        epi16<false, false>(p, cur.r_base, cur.m0 + wm * 64 + 32 * i + 4 * lh, cur.n0 + wn * 64 + 32 * j + lr, acc[i][j]);
     if (p.cmode == 1 || p.cmode == 2) {
       // every wavefront is done with the A tile: park the output there
       lds_barrier();
@@ -309,6 +311,8 @@ hipError_t launch_gemm_bf16_qk(const NodeKernel& k, hipStream_t s) {
   const uint64_t ntiles = (uint64_t)(tri ? p.tiles_m * (p.tiles_m + 1) / 2 : p.tiles_m * p.tiles_n) * p.G;
   const dim3 grid((uint32_t)std::min<uint64_t>(ntiles, 2 * (uint64_t)n_cu));
   if (grid.x == 0) return hipSuccess;
+  // an epilogue of bias only (the register budget is spent)
+  if (p.rop || p.act) return hipErrorInvalidValue;
   if (k.bmode == GM_MN) hipLaunchKernelGGL((gemm_bf16_qk_kernel<GM_MN>), grid, dim3(256), 0, s, p);
   else hipLaunchKernelGGL((gemm_bf16_qk_kernel<GM_K>), grid, dim3(256), 0, s, p);
   return hipGetLastError();

@@ -31,7 +31,7 @@ constexpr int SK_DEPTH = 4;          // 16-k groups in flight per wavefront
 
 }  // namespace
 
-template <int W, int SK_FM, int AM, int BMD>
+template <int W, int SK_FM, int AM, int BMD, bool RES>
 __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
   constexpr int SK_TM = 16 * SK_FM;
   __shared__ float red[W * SK_TM * SK_RP];
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
       for (int t = 0; t < 4; ++t) {
         float sum = 0.f;
         for (int w = 0; w < W; ++w) sum += red[(w * SK_TM + r0 + t) * SK_RP + c];
-        o[t] = gemm_epi(p, n, sum);
+        o[t] = gemm_epi<RES>(p, tc.r_base, m0 + t, n, sum);
       }
       // four rows m0..m0+3 lie in one M2 run (M2 % 4 == 0 in this mode)
       if (m0 + 3 < p.M) {
@@ -181,7 +181,7 @@ __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
       for (int t = 0; t < 4; ++t) {
         float sum = 0.f;
         for (int w = 0; w < W; ++w) sum += red[(w * SK_TM + r) * SK_RP + c0 + t];
-        o[t] = n0 + t < p.N ? gemm_epi(p, n0 + t, sum) : sum;
+        o[t] = n0 + t < p.N ? gemm_epi<RES>(p, tc.r_base, m, n0 + t, sum) : sum;
       }
       const int32_t base = tc.c_base + row_off(p, m, p.c_m1, p.c_m2);
       if (p.cmode == 1 && n0 + 3 < p.N && ((uintptr_t)(C + base + (int32_t)n0) & 15u) == 0) {
@@ -197,8 +197,11 @@ __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
 hipError_t launch_gemm_f32_dl(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
-#define FLUID_F32DL(Wv, FMv, AMv, BMv) \
-  hipLaunchKernelGGL((gemm_f32_dl_kernel<Wv, FMv, AMv, BMv>), grid, dim3(64 * Wv), 0, s, p)
+#define FLUID_F32DL(Wv, FMv, AMv, BMv)                                                                  \
+  do {                                                                                      \
+  if (p.rop) hipLaunchKernelGGL((gemm_f32_dl_kernel<Wv, FMv, AMv, BMv, true>), grid, dim3(64 * Wv), 0, s, p); \
+  else hipLaunchKernelGGL((gemm_f32_dl_kernel<Wv, FMv, AMv, BMv, false>), grid, dim3(64 * Wv), 0, s, p); \
+} while (0)
 #define FLUID_F32DL_W(Wv, FMv)                                                          \
   if (k.amode == GM_K && k.bmode == GM_MN) FLUID_F32DL(Wv, FMv, GM_K, GM_MN);           \
   else if (k.amode == GM_K && k.bmode == GM_K) FLUID_F32DL(Wv, FMv, GM_K, GM_K);        \

@@ -38,14 +38,15 @@ struct PreparedNode {
   std::vector<Bind> in;  // one per node input (activations and constants)
   Bind out;
   std::vector<Operand> ops;  // the inputs as prepared (for re-preparing a fused launch)
-  // Epilogue fusion: this MatMul also performs the fuse_n nodes after it (a
-  // bias Add, an activation, or a bias Add then an activation) and writes the
-  // last one's output (fout) directly; those nodes are then not launched by
-  // fluid_run.
+  // Epilogue fusion: this MatMul also performs the fuse_n nodes after it (in
+  // this order, each optional: a bias Add, a GELU / SiLU, an Add or Mul with
+  // another tensor) and writes the last one's output (fout) directly; those
+  // nodes are then not launched by fluid_run.
   int fuse_n = 0;
   NodeKernel kf;
   Bind fout;
   int fbias = -1;           // constant id of the bias, -1 when none
+  Bind fr;                  // the other tensor of the Add / Mul (kf.gemm.rop set)
   bool fused_away = false;  // this node is performed by a MatMul before it
 };
 
@@ -84,14 +85,17 @@ std::pair<int64_t, int64_t> arena_range(const Graph& g, const ArenaPlan& ap, int
 }
 
 // Epilogue fusion.  A MatMul absorbs the node `nx` launched right after the
-// chain it already performs (its own product, or product + bias) when nx is
-// the chain output's only reader (which is no graph output) and is either an
-// Add of a bias constant [N] (only as the first step) or a GELU / SiLU (the
-// last step).  The MatMul is then re-prepared to write nx's output, in nx's
-// output layout, with bias and activation applied in fp32 before the one
-// rounding.  Not when nx's output shares arena bytes with a MatMul operand:
-// that output only becomes live after the MatMul has read its operands, so
-// the arena may have placed it over them.
+// chain it already performs when nx is the chain output's only reader (which
+// is no graph output) and is, in this order of steps: an Add of a bias
+// constant [N] (first step only), a GELU / SiLU, or an Add / Mul of the chain
+// output and another activation tensor R of the same shape (the last step).
+// The MatMul is then re-prepared to write nx's output, in nx's output layout,
+// with every step applied in fp32 before the one rounding.  Not when nx's
+// output shares arena bytes with a MatMul operand: that output only becomes
+// live after the MatMul has read its operands, so the arena may have placed
+// it over them.  R is produced before the MatMul (the chain's intermediates
+// have no other reader, so R is none of them) and is live, and not written,
+// until nx; nx's output never shares bytes with R, both being live at nx.
 // `tail` is the output edge of the chain's last node.
 void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan& ap, PreparedNode& mm, int tail,
                        PreparedNode& nx, const Operand& nx_out) {
@@ -99,18 +103,30 @@ void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan& ap
   const Node& xn = g.nodes[nx.node];
   const Node& mn = g.nodes[mm.node];
   const uint32_t act_now = mm.fuse_n ? mm.kf.gemm.act : 0u;
-  if (mn.ins.size() != 2) return;
+  const uint32_t rop_now = mm.fuse_n ? mm.kf.gemm.rop : 0u;
+  const int caps = gemm_epilogue_caps(lp.variant[mm.node]);
+  if (mn.ins.size() != 2 || rop_now) return;
   if (g.is_output[tail] || g.readers[tail].size() != 1 || g.readers[tail][0] != nx.node) return;
   int bias = mm.fbias;
-  uint32_t act = 0;
-  if (xn.op == FLUID_OP_ADD && mm.fuse_n == 0 && xn.ins.size() == 2) {
+  uint32_t act = act_now, rop = 0;
+  int rslot = -1;
+  if ((xn.op == FLUID_OP_ADD || xn.op == FLUID_OP_MUL) && xn.ins.size() == 2) {
     const int slot = xn.ins[0] == tail ? 0 : 1;
-    if (xn.ins[1 - slot] >= 0) return;
-    const int c = ~xn.ins[1 - slot];
-    const Shape& cs = g.consts[c].shape;
-    if (cs.size() != 1 || cs[0] != mn.out_shape.back() || g.consts[c].dtype != g.dtype) return;
-    bias = c;
-  } else if ((xn.op == FLUID_OP_GELU || xn.op == FLUID_OP_SILU) && act_now == 0) {
+    const int o = xn.ins[1 - slot];
+    if (o == tail) return;
+    if (o < 0) {
+      const int c = ~o;
+      const Shape& cs = g.consts[c].shape;
+      if (xn.op != FLUID_OP_ADD || mm.fuse_n != 0 || cs.size() != 1 || cs[0] != mn.out_shape.back() ||
+          g.consts[c].dtype != g.dtype)
+        return;
+      bias = c;
+    } else {
+      if (g.edge_shape(o) != mn.out_shape || !(caps & EPI_ROP)) return;
+      rop = xn.op == FLUID_OP_ADD ? 1u : 2u;
+      rslot = 1 - slot;
+    }
+  } else if ((xn.op == FLUID_OP_GELU || xn.op == FLUID_OP_SILU) && act_now == 0 && (caps & EPI_ACT)) {
     act = xn.op == FLUID_OP_GELU ? 1u : 2u;
   } else {
     return;
@@ -123,8 +139,22 @@ void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan& ap
   }
   NodeKernel kf = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, nx_out);
   if (!kf.available) return;
-  kf.gemm.bias_bf16 = g.dtype == FLUID_BF16 ? 1u : 0u;
-  kf.gemm.act = act ? act : act_now;
+  if (rop) {
+    // R's strides in the output's batch / row decomposition: prepare the
+    // product as if it wrote R
+    const NodeKernel kr = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, nx.ops[rslot]);
+    if (!kr.available) return;
+    kf.gemm.r_g1 = kr.gemm.c_g1;
+    kf.gemm.r_g2 = kr.gemm.c_g2;
+    kf.gemm.r_m1 = kr.gemm.c_m1;
+    kf.gemm.r_m2 = kr.gemm.c_m2;
+    kf.gemm.r_n = kr.gemm.c_n;
+    kf.gemm.r_m2div = kf.gemm.m2div;
+    mm.fr = nx.in[rslot];
+  }
+  kf.gemm.epi_bf16 = g.dtype == FLUID_BF16 ? 1u : 0u;
+  kf.gemm.act = act;
+  kf.gemm.rop = rop;
   mm.fuse_n += 1;
   mm.kf = kf;
   mm.fout = nx.out;
@@ -234,6 +264,7 @@ NodeKernel fused_kernel(const PreparedNode& pn, const Bases& B) {
   k.gemm.B = resolve(pn.in[1], B);
   k.gemm.C = resolve(pn.fout, B);
   k.gemm.bias = pn.fbias >= 0 ? B.consts[pn.fbias] : nullptr;
+  k.gemm.R = k.gemm.rop ? resolve(pn.fr, B) : nullptr;
   return k;
 }
 

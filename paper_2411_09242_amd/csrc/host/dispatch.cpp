@@ -296,8 +296,11 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   const int rA = (int)A.shape.size(), rB = (int)B.shape.size();
   GemmParams& p = k.gemm;
   p.bias = nullptr;
-  p.bias_bf16 = 0;
+  p.epi_bf16 = 0;
   p.act = 0;
+  p.R = nullptr;
+  p.r_g1 = p.r_g2 = p.r_m1 = p.r_m2 = p.r_n = 0;
+  p.rop = 0;
   p.A = A.ptr;
   p.B = B.ptr;
   p.C = const_cast<void*>(C.ptr);
@@ -424,6 +427,10 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
 }
 
 }  // namespace
+
+// tile 9 (the whole-K-in-LDS kernel for short-K attention products) has no
+// registers to spare: bias only
+int gemm_epilogue_caps(int variant) { return variant == 9 ? EPI_BIAS : EPI_BIAS | EPI_ACT | EPI_ROP; }
 
 NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
   if (variant < 0 || variant >= num_variants(nd.op)) {

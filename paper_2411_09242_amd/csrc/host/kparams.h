@@ -100,12 +100,18 @@ struct GemmParams {
   // every n > m may be skipped; bit 1, A[m][k] = 0 for k > m, so the K loop
   // of rows m0 .. m0 + BM - 1 may stop at m0 + BM.
   uint32_t causal;
-  // Epilogue: C[m][n] = act(sum_k A B + bias[n]), bias a dense [N] vector of
-  // the graph dtype (bf16 when bias_bf16) or none when null; act 0 none,
-  // 1 GELU (erf form), 2 SiLU.
+  // Epilogue: C[m][n] = act(sum_k A B + bias[n]) (rop 0), that plus R[m][n]
+  // (rop 1) or times R[m][n] (rop 2); bias a dense [N] vector or none when
+  // null; act 0 none, 1 GELU (erf form), 2 SiLU; R a tensor of C's shape
+  // with its own strides (batch and row decomposition as C's).  Bias and R
+  // hold bf16 when epi_bf16, else fp32.
   const void* bias;
-  uint32_t bias_bf16;
+  uint32_t epi_bf16;
   uint32_t act;
+  const void* R;
+  int32_t r_g1, r_g2, r_m1, r_m2, r_n;
+  FastDiv r_m2div;            // a copy of m2div
+  uint32_t rop;
 };
 
 }  // namespace fluid
