@@ -222,7 +222,7 @@ def ablation(F, g, table, ex, steps, torch):
                         ("dp_layouts_variant0", F.NO_VARIANTS),
                         ("dp_layouts_best_variant", 0)):
         lp_a = F.LayoutPlan(g, table, flags)
-        ap_a = F.ArenaPlan(g, lp_a)
+        ap_a = F.ArenaPlan(g, lp_a, epilogue=True)
         ex_a = F.Executor(g, lp_a, ap_a, ex.consts, ex.inputs)
         for _ in range(2):
             ex_a.run()
@@ -301,7 +301,11 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     if save_table:
         table.save(save_table)
     lp = F.LayoutPlan(g, table)
-    apl = F.ArenaPlan(g, lp)
+    # operands of a MatMul live until the end of the nodes its epilogue
+    # absorbs, so that every such fusion happens; the paper's lifetimes are
+    # reported beside it
+    apl = F.ArenaPlan(g, lp, epilogue=True)
+    apl_paper = F.ArenaPlan(g, lp)
     lp_naive = F.LayoutPlan(g, table, F.NO_DP)
     ap_naive = F.ArenaPlan(g, lp_naive, no_reuse=True)
     ex = F.Executor(g, lp, apl, consts, [x])
@@ -411,6 +415,8 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         "speedup_vs_naive": round(ms_naive / ms_step, 3),
         "peak_arena_mb": round(apl.peak / 2**20, 3), "naive_arena_mb": round(ap_naive.peak / 2**20, 3),
         "max_live_lower_bound_mb": round(apl.lower_bound / 2**20, 3),
+        "paper_lifetimes_arena_mb": round(apl_paper.peak / 2**20, 3),
+        "paper_lifetimes_launches_per_step": F.fluid_run_launches(g.h, lp.h, apl_paper.h),
         "launches_per_step": n_launch, "naive_launches_per_step": n_launch_naive,
         "plan_table_ns": lp.total_ns, "naive_table_ns": lp_naive.total_ns, "guard_used": lp.guard_used,
         "planned_vs_naive_max_abs_diff": agree, "cost_table_s": round(t_measure, 1),

@@ -135,7 +135,8 @@ fluid_status fluid_build_graph(const fluid_graph_desc* desc, fluid_graph** out);
  * projections (MatMul [+ bias Add], Reshape to heads, [RoPE], Transpose to
  * [B,NH,S,D], keys to [B,NH,D,S]), scores MatMul, Softmax(1/sqrt(D)),
  * context MatMul, Transpose + Reshape back, output projection, residual,
- * norm, FFN, residual[, norm]. */
+ * norm, FFN (up, bias, GELU, down, bias; SwiGLU: gate, SiLU, up, Mul, down),
+ * residual[, norm]. */
 typedef struct {
   int32_t arch;
   int32_t layers, batch, seq, hidden, heads, ffn;
@@ -208,13 +209,18 @@ fluid_status fluid_edge_layout(const fluid_graph* g, const fluid_layout_plan* lp
                                int32_t* perm_out);
 
 #define FLUID_ARENA_NO_REUSE 1u  /* naive plan: every buffer its own slice     */
+#define FLUID_ARENA_EPILOGUE 2u  /* lifetimes that let every epilogue fuse    */
 
 /* Arena plan (Alg. 4, Greedy-by-Size): a Transpose/Reshape that the layouts
  * make a view owns no bytes; every other non-output node result is a buffer
  * of size rounded up to `align` (a power of two >= 16; 256 recommended)
  * with lifetime [producer, last reader]; buffers by size descending take
  * the smallest fitting gap among lifetime-overlapping buffers, else the end.
- * FLUID_ARENA_NO_REUSE places them at prefix sums in edge order instead. */
+ * FLUID_ARENA_NO_REUSE places them at prefix sums in edge order instead.
+ * FLUID_ARENA_EPILOGUE (an addition to the paper's lifetimes): a MatMul
+ * that fluid_run can fuse with the nodes after it (see fluid_run) keeps its
+ * operands live until the last of those nodes, so that no fused output is
+ * placed over them and every such fusion happens; the peak can grow. */
 fluid_status fluid_plan_arena(const fluid_graph* g, const fluid_layout_plan* lp, uint64_t align,
                               uint32_t flags, fluid_arena_plan** out);
 
@@ -228,11 +234,15 @@ fluid_status fluid_arena_plan_get(const fluid_arena_plan* ap, uint64_t* peak_byt
 
 /* Executes the graph (Section 4 "Virtual Machine": the invoke interface):
  * enqueues one kernel per non-view node, in node order, on hip_stream; the
- * caller synchronises.  One exception: a MatMul directly followed (in node
- * order, views aside) by the Add of a bias constant [N] to its output, that
- * output being read by nothing else and not a graph output, runs as one
- * kernel that writes the Add's output with the bias added before rounding
- * (unless the Add's output shares arena bytes with a MatMul operand).  arena: device memory of at least the plan's peak,
+ * caller synchronises.  One exception, epilogue fusion: a MatMul also
+ * performs the nodes launched right after it that form, in this order, an
+ * Add of a bias constant [N], a GELU or SiLU, and an Add or Mul with
+ * another tensor of the product's shape (each step optional; the last one
+ * only for the kernel variants that have it), when each step's input is
+ * read by nothing else and is no graph output; the launch writes the last
+ * step's output, rounding once after all steps (a step is left to its own
+ * kernel when its output shares arena bytes with a MatMul operand).  arena:
+ * device memory of at least the plan's peak,
  * 256-B aligned; consts[i], inputs[i], outputs[i]: device pointers to dense
  * row-major tensors of the graph's dtype (RoPE tables fp32).  No device
  * allocation.  Errors before any launch: FLUID_E_INVALID (NULL pointer,
@@ -248,18 +258,18 @@ fluid_status fluid_run(const fluid_graph* g, const fluid_layout_plan* lp, const 
  * uses for them (profiling aid: the time of chosen kernels back to back,
  * without the rest of the graph).  Same argument rules and errors as
  * fluid_run; nodes: n_nodes node ids, each a non-view node under the plan
- * (else FLUID_E_INVALID); repeat >= 1.  A MatMul whose bias Add fluid_run
- * performs in the same launch does so here too when the Add follows it in
- * the list; listed alone, each runs its own kernel.  Reads and writes the arena like a
- * run would, so it leaves the arena contents of a partial run.  GPU build
- * only. */
+ * (else FLUID_E_INVALID); repeat >= 1.  A MatMul that fluid_run fuses with
+ * the nodes after it does so here too when all those nodes follow it in the
+ * list; otherwise each listed node runs its own kernel.  Reads and writes
+ * the arena like a run would, so it leaves the arena contents of a partial
+ * run.  GPU build only. */
 fluid_status fluid_run_nodes(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
                              void* arena, uint64_t arena_bytes, const void* const* consts,
                              const void* const* inputs, void* const* outputs, const int32_t* nodes,
                              int32_t n_nodes, int32_t repeat, void* hip_stream);
 
 /* Number of kernel launches one fluid_run of these plans enqueues (the
- * non-view nodes, less the bias Adds performed by their MatMul).  Errors:
+ * non-view nodes, less those performed in a MatMul's epilogue).  Errors:
  * FLUID_E_INVALID (NULL argument, plans of another graph).  GPU build only. */
 fluid_status fluid_run_launches(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
                                 int32_t* launches);

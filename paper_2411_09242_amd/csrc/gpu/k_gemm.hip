@@ -662,11 +662,11 @@ hipError_t gemm_sk_go(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
   const bool avk = k.amode == GM_K, bvk = k.bmode == GM_K;
-#define FLUID_SK(AV, BV)                                                                              \
-  do {                                                                                      \
-  if (p.rop) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, AV, BV, true>), grid, dim3(64 * W), 0, s, p); \
-  else hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, AV, BV, false>), grid, dim3(64 * W), 0, s, p); \
-} while (0)
+#define FLUID_SK(AV, BV)                                                                         \
+  do {                                                                                           \
+    if (p.rop) hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, AV, BV, true>), grid, dim3(64 * W), 0, s, p); \
+    else hipLaunchKernelGGL((gemm_sk_kernel<T, FM, FN, W, U, AV, BV, false>), grid, dim3(64 * W), 0, s, p);      \
+  } while (0)
   if (avk && bvk) FLUID_SK(true, true);
   else if (avk) FLUID_SK(true, false);
   else if (bvk) FLUID_SK(false, true);
@@ -689,11 +689,15 @@ template <int T, int AM, int BMD>
 hipError_t gemm_go(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
+  // the 128 x 128 tiles leave an Add / Mul to its own kernel (an instance
+  // with it would lose a workgroup per SIMD)
+  constexpr bool kRes = T != 128;
+  if (p.rop && !kRes) return hipErrorInvalidValue;
   if (k.dtype == DT_BF16) {
-    if (p.rop) hipLaunchKernelGGL((gemm_bf16_kernel<T, T, AM, BMD, true>), grid, dim3(256), 0, s, p);
+    if (p.rop) hipLaunchKernelGGL((gemm_bf16_kernel<T, T, AM, BMD, kRes>), grid, dim3(256), 0, s, p);
     else hipLaunchKernelGGL((gemm_bf16_kernel<T, T, AM, BMD, false>), grid, dim3(256), 0, s, p);
   } else {
-    if (p.rop) hipLaunchKernelGGL((gemm_f32_kernel<T, T, AM, BMD, true>), grid, dim3(256), 0, s, p);
+    if (p.rop) hipLaunchKernelGGL((gemm_f32_kernel<T, T, AM, BMD, kRes>), grid, dim3(256), 0, s, p);
     else hipLaunchKernelGGL((gemm_f32_kernel<T, T, AM, BMD, false>), grid, dim3(256), 0, s, p);
   }
   return hipGetLastError();

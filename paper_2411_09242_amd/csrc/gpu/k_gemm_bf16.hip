@@ -14,7 +14,7 @@
 
 namespace fluid {
 
-template <int BM, int AM, int BMD, bool RES>
+template <int BM, int AM, int BMD>
 __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
   constexpr int BN = 128, BK = 32;
   constexpr int FM = BM / 64, FN = 2;  // per wavefront (BM/2) x 64
@@ -194,7 +194,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_pipe_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const uint32_t n = tc.n0 + wn * 64 + j * 32 + lr;
-      epi16<RES>(p, tc.r_base, tc.m0 + wm * (BM / 2) + i * 32 + 4 * (lane >> 5), n, acc[i][j]);
+      epi16<false>(p, tc.r_base, tc.m0 + wm * (BM / 2) + i * 32 + 4 * (lane >> 5), n, acc[i][j]);
       if (n >= p.N) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -209,12 +209,9 @@ namespace {
 template <int BM>
 hipError_t pipe_go(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
+  if (p.rop) return hipErrorInvalidValue;  // the Add / Mul runs as its own kernel after these tiles
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
-#define FLUID_PIPE(AMv, BMv)                                                                  \
-  do {                                                                                      \
-  if (p.rop) hipLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, AMv, BMv, true>), grid, dim3(256), 0, s, p); \
-  else hipLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, AMv, BMv, false>), grid, dim3(256), 0, s, p); \
-} while (0)
+#define FLUID_PIPE(AMv, BMv) hipLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, AMv, BMv>), grid, dim3(256), 0, s, p)
   if (k.amode == GM_K && k.bmode == GM_MN) FLUID_PIPE(GM_K, GM_MN);
   else if (k.amode == GM_K && k.bmode == GM_K) FLUID_PIPE(GM_K, GM_K);
   else if (k.amode == GM_K) FLUID_PIPE(GM_K, GM_GENERIC);

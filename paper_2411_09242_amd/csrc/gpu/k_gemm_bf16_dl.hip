@@ -62,7 +62,7 @@ __device__ __forceinline__ int a_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; 
 // (VGPRs and AGPRs together), so that two workgroups share a CU and one's
 // loads, barrier waits and epilogue overlap the other's MFMAs: faster where
 // there are many tiles or K is short (Q K^T, the 11008-wide FFN GEMMs).
-template <int BMD, int NS, bool RES>
+template <int BMD, int NS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NS == 3 ? 2 : 1, NS == 3 ? 2 : 1)))
 void gemm_bf16_dl_kernel(GemmParams p) {
   static_assert(NS == 3 || NS == 4, "three or four stages");
@@ -236,7 +236,7 @@ void gemm_bf16_dl_kernel(GemmParams p) {
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) epi16<RES>(p, tc.r_base, wm0 + i * 32 + 4 * lh, tc.n0 + j * 32 + lr, acc[i][j]);
+    for (int j = 0; j < FN; ++j) epi16<false>(p, tc.r_base, wm0 + i * 32 + 4 * lh, tc.n0 + j * 32 + lr, acc[i][j]);
   if (p.cmode == 1 || p.cmode == 2) {
     // the padding tiles' loads land in the ring: drain them, and let every
     // wavefront finish its last tile, before the ring is reused
@@ -325,13 +325,10 @@ void gemm_bf16_dl_kernel(GemmParams p) {
 hipError_t launch_gemm_bf16_dl(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   if (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_MN && k.bmode != GM_K)) return hipErrorInvalidValue;
+  if (p.rop) return hipErrorInvalidValue;  // the Add / Mul runs as its own kernel after these tiles
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
   // tile 8: the three-stage ring, two workgroups per CU
-#define FLUID_DL(BMv, NSv)                                                                   \
-  do {                                                                                      \
-  if (p.rop) hipLaunchKernelGGL((gemm_bf16_dl_kernel<BMv, NSv, true>), grid, dim3(256), 0, s, p); \
-  else hipLaunchKernelGGL((gemm_bf16_dl_kernel<BMv, NSv, false>), grid, dim3(256), 0, s, p); \
-} while (0)
+#define FLUID_DL(BMv, NSv) hipLaunchKernelGGL((gemm_bf16_dl_kernel<BMv, NSv>), grid, dim3(256), 0, s, p)
   if (k.gemm_tile == 8) {
     if (k.bmode == GM_MN) FLUID_DL(GM_MN, 3);
     else FLUID_DL(GM_K, 3);

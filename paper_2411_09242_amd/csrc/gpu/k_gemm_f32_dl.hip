@@ -197,11 +197,11 @@ __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
 hipError_t launch_gemm_f32_dl(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
-#define FLUID_F32DL(Wv, FMv, AMv, BMv)                                                                  \
-  do {                                                                                      \
-  if (p.rop) hipLaunchKernelGGL((gemm_f32_dl_kernel<Wv, FMv, AMv, BMv, true>), grid, dim3(64 * Wv), 0, s, p); \
-  else hipLaunchKernelGGL((gemm_f32_dl_kernel<Wv, FMv, AMv, BMv, false>), grid, dim3(64 * Wv), 0, s, p); \
-} while (0)
+#define FLUID_F32DL(Wv, FMv, AMv, BMv)                                                                     \
+  do {                                                                                                     \
+    if (p.rop) hipLaunchKernelGGL((gemm_f32_dl_kernel<Wv, FMv, AMv, BMv, true>), grid, dim3(64 * Wv), 0, s, p); \
+    else hipLaunchKernelGGL((gemm_f32_dl_kernel<Wv, FMv, AMv, BMv, false>), grid, dim3(64 * Wv), 0, s, p);      \
+  } while (0)
 #define FLUID_F32DL_W(Wv, FMv)                                                          \
   if (k.amode == GM_K && k.bmode == GM_MN) FLUID_F32DL(Wv, FMv, GM_K, GM_MN);           \
   else if (k.amode == GM_K && k.bmode == GM_K) FLUID_F32DL(Wv, FMv, GM_K, GM_K);        \

@@ -10,6 +10,7 @@
 #include "handles.h"
 #include "dispatch.h"
 #include "layouts.h"
+#include "prepare.h"
 
 namespace fluid {
 
@@ -195,12 +196,24 @@ fluid_status fluid_plan_arena(const fluid_graph* g, const fluid_layout_plan* lp,
     require(g && lp && out, "NULL argument");
     require(lp->p.graph_serial == g->serial, "plan belongs to another graph");
     require(align >= 16 && (align & (align - 1)) == 0, "align must be a power of two >= 16");
-    require((flags & ~1u) == 0, "unknown flags");
+    require((flags & ~3u) == 0, "unknown flags");
     auto h = std::make_unique<fluid_arena_plan>();
-    h->a = plan_arena(g->g, lp->p.perm, align, (flags & FLUID_ARENA_NO_REUSE) != 0);
+    std::vector<int> until;
+    if (flags & FLUID_ARENA_EPILOGUE) until = epilogue_reads_until(g->g, lp->p);
+    h->a = plan_arena(g->g, lp->p.perm, align, (flags & FLUID_ARENA_NO_REUSE) != 0, until);
     h->a.graph_serial = g->serial;
     h->serial = next_serial();
     *out = h.release();
+  });
+}
+
+fluid_status fluid_run_launches(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah,
+                                int32_t* launches) {
+  return call_guarded([&] {
+    require(gh && lh && ah && launches, "fluid_run_launches: NULL argument");
+    require(lh->p.graph_serial == gh->serial && ah->a.graph_serial == gh->serial,
+            "fluid_run_launches: plans belong to another graph");
+    *launches = prepared_launches(*prepare(gh->g, lh->p, &ah->a));
   });
 }
 

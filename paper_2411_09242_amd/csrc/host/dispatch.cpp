@@ -428,9 +428,20 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
 
 }  // namespace
 
-// tile 9 (the whole-K-in-LDS kernel for short-K attention products) has no
-// registers to spare: bias only
-int gemm_epilogue_caps(int variant) { return variant == 9 ? EPI_BIAS : EPI_BIAS | EPI_ACT | EPI_ROP; }
+// Tile 9 (the whole-K-in-LDS kernel for short-K attention products) has no
+// registers to spare: bias only.  The Add / Mul with another tensor reads
+// that tensor one element per lane at the end of each tile: measured against
+// the product and a separate elementwise kernel, that is faster on the 64 x
+// 64 tiles, the split-K tiles and the fp32 direct-load tiles, but slower on
+// the 128 x 128 tiles (an instance with the extra reads drops from three to
+// two workgroups per SIMD) and on the large bf16 tiles (the reads come after
+// the last MFMA, with nothing left to hide their latency), so those tiles
+// leave the Add / Mul to its own kernel.
+int gemm_epilogue_caps(int variant, int dtype) {
+  if (variant == 9) return EPI_BIAS;
+  const bool rop = (variant >= 1 && variant <= 5) || (dtype == FLUID_F32 && variant >= 6);
+  return EPI_BIAS | EPI_ACT | (rop ? EPI_ROP : 0);
+}
 
 NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
   if (variant < 0 || variant >= num_variants(nd.op)) {
@@ -461,10 +472,17 @@ std::string NodeKernel::name() const {
     case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
     case KF_GEMM: {
+      // fused epilogue steps: b bias, g GELU, s SiLU, a / m Add / Mul of R
+      auto epi_suffix = [&]() {
+        std::string e = std::string(gemm.bias ? "b" : "") + (gemm.act == 1 ? "g" : gemm.act == 2 ? "s" : "") +
+                        (gemm.rop == 1 ? "a" : gemm.rop == 2 ? "m" : "");
+        return e.empty() ? e : "_e" + e;
+      };
       static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "p256x128", "p128", "p256x128s3", "q128"};
       static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4", "-", "-"};
       return "gemm_" + dt + "_" + (dtype == DT_BF16 ? tiles : tiles_f32)[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
-             (cmode == 1 ? "n" : cmode == 2 ? "m" : "g") + (gemm.causal ? "_causal" + std::to_string(gemm.causal) : "");
+             (cmode == 1 ? "n" : cmode == 2 ? "m" : "g") + (gemm.causal ? "_causal" + std::to_string(gemm.causal) : "") +
+             epi_suffix();
     }
   }
   return "?";

@@ -50,11 +50,11 @@ struct NodeKernel {
 };
 
 int num_variants(int op);
-// Epilogue steps the kernels of MatMul variant `variant` can perform after
-// the product (GemmParams): bit 0 bias, bit 1 activation, bit 2 the Add /
-// Mul with another tensor.
+// Epilogue steps the kernels of MatMul variant `variant` perform after the
+// product for a graph of dtype `dtype` (GemmParams): bit 0 bias, bit 1
+// activation, bit 2 the Add / Mul with another tensor.
 enum : int { EPI_BIAS = 1, EPI_ACT = 2, EPI_ROP = 4 };
-int gemm_epilogue_caps(int variant);
+int gemm_epilogue_caps(int variant, int dtype);
 NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins,
                         const Operand& out);
 

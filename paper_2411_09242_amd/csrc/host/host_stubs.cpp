@@ -25,10 +25,6 @@ fluid_status fluid_run_nodes(const fluid_graph*, const fluid_layout_plan*, const
   return unsupported("fluid_run_nodes");
 }
 
-fluid_status fluid_run_launches(const fluid_graph*, const fluid_layout_plan*, const fluid_arena_plan*, int32_t*) {
-  return unsupported("fluid_run_launches");
-}
-
 fluid_status fluid_measure_costs(const fluid_graph*, uint32_t, void*, uint64_t, void*, fluid_cost_table**) {
   return unsupported("fluid_measure_costs");
 }

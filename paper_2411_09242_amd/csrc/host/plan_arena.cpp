@@ -33,7 +33,7 @@ struct Buffers {
   std::vector<uint64_t> size;
 };
 
-Buffers collect(const Graph& g, const std::vector<Perm>& perm, uint64_t align) {
+Buffers collect(const Graph& g, const std::vector<Perm>& perm, uint64_t align, const std::vector<int>& until) {
   Buffers B;
   const int E = g.n_edges();
   B.root.resize(E);
@@ -59,7 +59,7 @@ Buffers collect(const Graph& g, const std::vector<Perm>& perm, uint64_t align) {
   for (int n = 0; n < g.n_nodes(); ++n)
     for (int e : g.act_in[n]) {
       int r = B.root[e];
-      if (is_buf[r]) B.last[r] = std::max(B.last[r], n);
+      if (is_buf[r]) B.last[r] = std::max(B.last[r], until.empty() ? n : until[n]);
     }
   return B;
 }
@@ -68,8 +68,9 @@ bool overlaps(const Buffers& B, int a, int b) { return B.def[a] <= B.last[b] && 
 
 }  // namespace
 
-ArenaPlan plan_arena(const Graph& g, const std::vector<Perm>& perm, uint64_t align, bool no_reuse) {
-  Buffers B = collect(g, perm, align);
+ArenaPlan plan_arena(const Graph& g, const std::vector<Perm>& perm, uint64_t align, bool no_reuse,
+                     const std::vector<int>& reads_until) {
+  Buffers B = collect(g, perm, align, reads_until);
   ArenaPlan ap;
   const int E = g.n_edges();
   ap.root = B.root;
@@ -126,7 +127,7 @@ ArenaPlan plan_arena(const Graph& g, const std::vector<Perm>& perm, uint64_t ali
   {
     std::vector<Perm> ident;
     for (int e = 0; e < E; ++e) ident.push_back(identity_perm((int)g.edge_shape(e).size()));
-    Buffers N = collect(g, ident, align);
+    Buffers N = collect(g, ident, align, {});
     uint64_t s = 0;
     for (int b : N.list) s += N.size[b];
     ap.naive = s;

@@ -35,6 +35,9 @@ struct ArenaPlan {
 };
 
 bool node_is_view(const Graph& g, int n, const std::vector<Perm>& perm_of_edge);
-ArenaPlan plan_arena(const Graph& g, const std::vector<Perm>& perm_of_edge, uint64_t align, bool no_reuse);
+// reads_until (empty: each node itself): per node, the last node id until
+// which that node's inputs must stay live.
+ArenaPlan plan_arena(const Graph& g, const std::vector<Perm>& perm_of_edge, uint64_t align, bool no_reuse,
+                     const std::vector<int>& reads_until = {});
 
 }  // namespace fluid

@@ -1,0 +1,187 @@
+#include "prepare.h"
+
+#include <algorithm>
+#include <string>
+
+#include "handles.h"
+#include "layouts.h"
+
+namespace fluid {
+
+namespace {
+
+// Bases are validated to be 256-byte (arena) or 16-byte (caller tensors)
+// aligned, so preparing with base address 0 keeps every alignment decision
+// valid for the real addresses.
+const void* fake_ptr(const Bind& b) { return (const void*)(uintptr_t)b.off; }
+
+Bind bind_edge(const Graph& g, const ArenaPlan* ap, int e) {
+  Bind b;
+  const int r = ap ? ap->root[e] : e;
+  if (r < g.n_inputs()) {
+    b.kind = BK_INPUT;
+    b.index = r;
+  } else if (g.is_output[r]) {
+    b.kind = BK_OUTPUT;
+    b.index = (int)(std::find(g.outputs.begin(), g.outputs.end(), r) - g.outputs.begin());
+  } else {
+    b.kind = BK_ARENA;
+    b.off = ap ? ap->offset[e] : 0;
+  }
+  return b;
+}
+
+// Bytes [lo, hi) an arena-bound edge occupies (empty for caller tensors).
+std::pair<int64_t, int64_t> arena_range(const Graph& g, const ArenaPlan* ap, int e, const Bind& b) {
+  if (!ap || b.kind != BK_ARENA) return {0, 0};
+  const int64_t bytes = numel(g.edge_shape(e)) * (g.dtype == FLUID_BF16 ? 2 : 4);
+  return {b.off, b.off + bytes};
+}
+
+// Epilogue fusion.  A MatMul absorbs the node `nx` launched right after the
+// chain it already performs when nx is the chain output's only reader (which
+// is no graph output) and is, in this order of steps: an Add of a bias
+// constant [N] (first step only), a GELU / SiLU, or an Add / Mul of the chain
+// output and another activation tensor R of the same shape (the last step).
+// The MatMul is then re-prepared to write nx's output, in nx's output layout,
+// with every step applied in fp32 before the one rounding.  Not when nx's
+// output shares arena bytes with a MatMul operand: that output only becomes
+// live after the MatMul has read its operands, so the arena may have placed
+// it over them.  R is produced before the MatMul (the chain's intermediates
+// have no other reader, so R is none of them) and is live, and not written,
+// until nx; nx's output never shares bytes with R, both being live at nx.
+// `tail` is the output edge of the chain's last node.
+void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan* ap, PreparedNode& mm, int tail,
+                       PreparedNode& nx, const Operand& nx_out) {
+  if (mm.k.family != KF_GEMM || mm.fused_away) return;
+  const Node& xn = g.nodes[nx.node];
+  const Node& mn = g.nodes[mm.node];
+  const uint32_t act_now = mm.fuse_n ? mm.kf.gemm.act : 0u;
+  const uint32_t rop_now = mm.fuse_n ? mm.kf.gemm.rop : 0u;
+  const int caps = gemm_epilogue_caps(lp.variant[mm.node], g.dtype);
+  if (mn.ins.size() != 2 || rop_now) return;
+  if (g.is_output[tail] || g.readers[tail].size() != 1 || g.readers[tail][0] != nx.node) return;
+  int bias = mm.fbias;
+  uint32_t act = act_now, rop = 0;
+  int rslot = -1;
+  if ((xn.op == FLUID_OP_ADD || xn.op == FLUID_OP_MUL) && xn.ins.size() == 2) {
+    const int slot = xn.ins[0] == tail ? 0 : 1;
+    const int o = xn.ins[1 - slot];
+    if (o == tail) return;
+    if (o < 0) {
+      const int c = ~o;
+      const Shape& cs = g.consts[c].shape;
+      if (xn.op != FLUID_OP_ADD || mm.fuse_n != 0 || cs.size() != 1 || cs[0] != mn.out_shape.back() ||
+          g.consts[c].dtype != g.dtype)
+        return;
+      bias = c;
+    } else {
+      if (g.edge_shape(o) != mn.out_shape || !(caps & EPI_ROP)) return;
+      rop = xn.op == FLUID_OP_ADD ? 1u : 2u;
+      rslot = 1 - slot;
+    }
+  } else if ((xn.op == FLUID_OP_GELU || xn.op == FLUID_OP_SILU) && act_now == 0 && (caps & EPI_ACT)) {
+    act = xn.op == FLUID_OP_GELU ? 1u : 2u;
+  } else {
+    return;
+  }
+  const auto ro = arena_range(g, ap, g.out_edge(nx.node), nx.out);
+  for (int i = 0; i < 2; ++i) {
+    if (mn.ins[i] < 0) continue;
+    const auto ri = arena_range(g, ap, mn.ins[i], mm.in[i]);
+    if (ro.first < ro.second && ri.first < ri.second && ro.first < ri.second && ri.first < ro.second) return;
+  }
+  NodeKernel kf = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, nx_out);
+  if (!kf.available) return;
+  if (rop) {
+    // R's strides in the output's batch / row decomposition: prepare the
+    // product as if it wrote R
+    const NodeKernel kr = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, nx.ops[rslot]);
+    if (!kr.available) return;
+    kf.gemm.r_g1 = kr.gemm.c_g1;
+    kf.gemm.r_g2 = kr.gemm.c_g2;
+    kf.gemm.r_m1 = kr.gemm.c_m1;
+    kf.gemm.r_m2 = kr.gemm.c_m2;
+    kf.gemm.r_n = kr.gemm.c_n;
+    kf.gemm.r_m2div = kf.gemm.m2div;
+    mm.fr = nx.in[rslot];
+  }
+  kf.gemm.epi_bf16 = g.dtype == FLUID_BF16 ? 1u : 0u;
+  kf.gemm.act = act;
+  kf.gemm.rop = rop;
+  mm.fuse_n += 1;
+  mm.kf = kf;
+  mm.fout = nx.out;
+  mm.fbias = bias;
+  nx.fused_away = true;
+}
+
+}  // namespace
+
+std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const ArenaPlan* ap) {
+  auto P = std::make_shared<Prepared>();
+  for (int n = 0; n < g.n_nodes(); ++n) {
+    if (lp.variant[n] < 0) continue;  // view: no kernel
+    const Node& nd = g.nodes[n];
+    PreparedNode pn;
+    pn.node = n;
+    std::vector<Operand> ins;
+    for (int v : nd.ins) {
+      Operand o;
+      Bind b;
+      if (v >= 0) {
+        b = bind_edge(g, ap, v);
+        o.shape = g.edge_shape(v);
+        o.stride = dense_strides(o.shape, lp.perm[v]);
+        o.dtype = g.dtype;
+      } else {
+        b.kind = BK_CONST;
+        b.index = ~v;
+        o.shape = g.consts[~v].shape;
+        o.stride = row_major_strides(o.shape);
+        o.dtype = g.consts[~v].dtype;
+      }
+      o.ptr = fake_ptr(b);
+      ins.push_back(o);
+      pn.in.push_back(b);
+    }
+    const int eo = g.out_edge(n);
+    pn.out = bind_edge(g, ap, eo);
+    Operand out;
+    out.shape = nd.out_shape;
+    out.stride = dense_strides(out.shape, lp.perm[eo]);
+    out.dtype = g.dtype;
+    out.ptr = fake_ptr(pn.out);
+    pn.k = prepare_node(nd, lp.variant[n], g.dtype, ins, out);
+    if (!pn.k.available)
+      fail(FLUID_E_INVALID, "node " + std::to_string(n) + ": variant " + std::to_string(lp.variant[n]) +
+                                " cannot run with these layouts (" + pn.k.why + ")");
+    pn.ops = ins;
+    if (!P->nodes.empty()) {
+      // the MatMul whose fused chain ends at the previous launch, if any
+      size_t j = P->nodes.size() - 1;
+      while (j > 0 && P->nodes[j].fused_away) --j;
+      if (j + P->nodes[j].fuse_n == P->nodes.size() - 1)
+        try_fuse_epilogue(g, lp, ap, P->nodes[j], g.out_edge(P->nodes.back().node), pn, out);
+    }
+    P->nodes.push_back(std::move(pn));
+  }
+  return P;
+}
+
+std::vector<int> epilogue_reads_until(const Graph& g, const LayoutPlan& lp) {
+  std::vector<int> until(g.n_nodes());
+  for (int n = 0; n < g.n_nodes(); ++n) until[n] = n;
+  const auto P = prepare(g, lp, nullptr);
+  for (size_t i = 0; i < P->nodes.size(); ++i)
+    if (P->nodes[i].fuse_n > 0) until[P->nodes[i].node] = P->nodes[i + P->nodes[i].fuse_n].node;
+  return until;
+}
+
+int prepared_launches(const Prepared& P) {
+  int n = 0;
+  for (const PreparedNode& pn : P.nodes) n += pn.fused_away ? 0 : 1;
+  return n;
+}
+
+}  // namespace fluid

@@ -28,7 +28,7 @@ OPS = {"matmul": 0, "add": 1, "mul": 2, "transpose": 3, "reshape": 4, "softmax":
 ROLES = {"other": 0, "weight": 1, "bias": 2, "gamma": 3, "beta": 4, "rope_cos": 5, "rope_sin": 6}
 ARCH = {"post_ln": 0, "pre_ln": 1, "llama": 2}
 NO_DP, NO_VARIANTS, NO_GUARD = 1, 2, 4
-ARENA_NO_REUSE = 1
+ARENA_NO_REUSE, ARENA_EPILOGUE = 1, 2
 STATUS = {0: "OK", -1: "INVALID", -2: "UNSUPPORTED", -3: "INFEASIBLE", -4: "ARENA_TOO_SMALL",
           -5: "HIP", -6: "NOMEM"}
 
@@ -376,9 +376,10 @@ class LayoutPlan:
 
 
 class ArenaPlan:
-    def __init__(self, graph, lplan, align=256, no_reuse=False):
+    def __init__(self, graph, lplan, align=256, no_reuse=False, epilogue=False):
         self.graph = graph
-        self.h = fluid_plan_arena(graph.h, lplan.h, align, ARENA_NO_REUSE if no_reuse else 0)
+        flags = (ARENA_NO_REUSE if no_reuse else 0) | (ARENA_EPILOGUE if epilogue else 0)
+        self.h = fluid_plan_arena(graph.h, lplan.h, align, flags)
         self.peak, self.naive, self.lower_bound, self.offset, self.root = fluid_arena_plan_get(
             self.h, graph.n_edges)
 
@@ -416,8 +417,8 @@ class Executor:
         return self.outputs
 
     def launches(self):
-        """Kernel launches one run enqueues (bias Adds fused into their
-        MatMul are not counted)."""
+        """Kernel launches one run enqueues (nodes performed in a MatMul's
+        epilogue are not counted)."""
         return fluid_run_launches(self.graph.h, self.lplan.h, self.aplan.h)
 
     def run_nodes(self, nodes, repeat=1, stream=None):

@@ -1,0 +1,90 @@
+"""Epilogue fusion decisions on the CPU (host-only library): how many
+launches a run of a plan enqueues, and the arena option that keeps a fused
+MatMul's operands live until the end of the nodes it absorbs."""
+import os
+
+import pytest
+
+import synth_inputs
+from gpu_util import forced_table
+from oracle import graph as OG, plan_arena as PA
+from paper_2411_09242_amd import fluid as F
+from tables import synthetic_table, write_table
+from test_gpu_ops import EPILOGUES, epilogue_graph, fusable_steps
+
+
+@pytest.fixture(scope="module", autouse=True)
+def host_lib():
+    return F.load(host_only=True)
+
+
+def _plan(og, table_obj, tmp_path, flags=0):
+    g = F.Graph.from_desc(og.export())
+    path = os.path.join(tmp_path, "t.json")
+    write_table(table_obj, path)
+    t = F.CostTable.load(path, g)
+    return g, F.LayoutPlan(g, t, flags)
+
+
+def _launches(g, lp, **kw):
+    ap = F.ArenaPlan(g, lp, **kw)
+    return F.fluid_run_launches(g.h, lp.h, ap.h), ap
+
+
+@pytest.mark.parametrize("chain", sorted(EPILOGUES))
+@pytest.mark.parametrize("v", [0, 2, 7, 9])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_epilogue_arena_lets_every_chain_fuse(chain, v, dtype, tmp_path):
+    """Without keep-alive readers, the default arena may put the chain's
+    output over the MatMul's input (its lifetime ends at the MatMul), which
+    refuses the fusion; with FLUID_ARENA_EPILOGUE the chain always fuses, as
+    far as the variant's epilogue reaches."""
+    if dtype == "f32" and v >= 8:
+        pytest.skip("variants 8 and 9 are bf16 only")
+    og, a, r, edges = epilogue_graph(2, 24, 32, 32, dtype, keep_a=False, chain=chain)
+    mm = [i for i, nd in enumerate(og.nodes) if nd.op == "matmul"][0]
+    g, lp = _plan(og, forced_table(og, {}, {mm: v}), tmp_path)
+    nonview = sum(1 for n in range(g.n_nodes) if lp.kernel(n) != "view")
+    n_def, _ = _launches(g, lp)
+    n_epi, ap = _launches(g, lp, epilogue=True)
+    n_nr, _ = _launches(g, lp, no_reuse=True)
+    assert n_epi == n_nr == nonview - fusable_steps(chain, v, dtype)
+    assert n_def >= n_epi
+
+
+CFGS = [synth_inputs.config(1, arch="post_ln", layers=2, seq=17, hidden=40, heads=5, ffn=72),
+        synth_inputs.config(1, arch="pre_ln", layers=2, seq=19, hidden=36, heads=3, ffn=52),
+        synth_inputs.config(1, arch="llama", layers=2, seq=21, hidden=48, heads=4, ffn=40, dtype="bf16")]
+
+
+@pytest.mark.parametrize("cfg", CFGS, ids=lambda c: c["arch"])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_epilogue_arena_on_transformers(cfg, seed, tmp_path):
+    """Transformer stacks planned on random tables: with the option every
+    fusion that a no-reuse arena allows happens, and the plan is still a
+    valid arena under the paper's lifetimes (no two buffers live at the same
+    node share a byte), no smaller than their max-live bound."""
+    og = OG.build_transformer(cfg)
+    tab = synthetic_table(og, seed=seed, mode="random", lo=1, hi=1000)
+    # MatMul variants 0-2 run with any layouts; other operators keep
+    # variant 0, which does too
+    for sig in tab["sigs"]:
+        for ent in sig["entries"]:
+            ent[2] = [c if v == 0 or sig["op"] == "matmul" else -1 for v, c in enumerate(ent[2])]
+            if max(ent[2]) < 0:
+                ent[2][0] = 1
+    g, lp = _plan(og, tab, tmp_path)
+    n_def, ap_def = _launches(g, lp)
+    n_epi, ap = _launches(g, lp, epilogue=True)
+    n_nr, _ = _launches(g, lp, no_reuse=True)
+    assert n_epi == n_nr <= n_def
+    lay = {e: lp.perm(e) for e in range(og.n_edges)}
+    ref = PA.plan_arena(og, lay)
+    for b in ref.buffers:
+        assert ap.offset[b] >= 0 and ap.offset[b] + ref.size[b] <= ap.peak
+    for i, x in enumerate(ref.buffers):
+        for y in ref.buffers[i + 1:]:
+            if ref.defn[x] <= ref.last[y] and ref.defn[y] <= ref.last[x]:
+                assert (ap.offset[x] + ref.size[x] <= ap.offset[y] or
+                        ap.offset[y] + ref.size[y] <= ap.offset[x]), (x, y)
+    assert ap.peak >= ap_def.lower_bound
