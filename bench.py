@@ -37,28 +37,32 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 # (workload, kernel, output shape, input shapes) and only while the kernel
 # sources hash to TRAFFIC_SRC -- a changed kernel makes the figure stale, and
 # then null.
-TRAFFIC_SRC = "03d3722195f168b9"
+TRAFFIC_SRC = "467c2f8b0fbaec3f"
 TRAFFIC = {
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6004029,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14269889,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155491201,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 229547587,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 225652680,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 594951228,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16651399,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28424446,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16628910,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 913797883,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185039712,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 893977536,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14289331,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_amn_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14277026,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 768), ((1, 128, 3072), ('c', 3072, 768))): 22512906,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_amn_bmn_cn', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6020398,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16628845,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16648284,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28446950,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28424477,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6061363,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6042926,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14302641,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14315915,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_sk32w8_ak_bmn_cn', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6108467,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14299569,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_amn_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14322064,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14338495,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_sk32w4_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6170895,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155481798,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238702975,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238525372,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237674557,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155464454,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237695977,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 595177228,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cn', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 596031723,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16674934,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16697459,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28472546,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28490976,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cm', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185186688,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894938442,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 914175678,
 }
 
 

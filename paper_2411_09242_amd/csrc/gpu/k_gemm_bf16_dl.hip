@@ -236,7 +236,7 @@ void gemm_bf16_dl_kernel(GemmParams p) {
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) epi16<false>(p, tc.r_base, wm0 + i * 32 + 4 * lh, tc.n0 + j * 32 + lr, acc[i][j]);
+    for (int j = 0; j < FN; ++j) epi16<false, false>(p, tc.r_base, wm0 + i * 32 + 4 * lh, tc.n0 + j * 32 + lr, acc[i][j]);
   if (p.cmode == 1 || p.cmode == 2) {
     // the padding tiles' loads land in the ring: drain them, and let every
     // wavefront finish its last tile, before the ring is reused
@@ -325,7 +325,9 @@ void gemm_bf16_dl_kernel(GemmParams p) {
 hipError_t launch_gemm_bf16_dl(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   if (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_MN && k.bmode != GM_K)) return hipErrorInvalidValue;
-  if (p.rop) return hipErrorInvalidValue;  // the Add / Mul runs as its own kernel after these tiles
+  // a bias epilogue only: activations and the Add / Mul run as their own
+  // kernels after these tiles
+  if (p.rop || p.act) return hipErrorInvalidValue;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
   // tile 8: the three-stage ring, two workgroups per CU
 #define FLUID_DL(BMv, NSv) hipLaunchKernelGGL((gemm_bf16_dl_kernel<BMv, NSv>), grid, dim3(256), 0, s, p)

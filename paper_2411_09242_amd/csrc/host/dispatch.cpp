@@ -428,18 +428,20 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
 
 }  // namespace
 
-// Tile 9 (the whole-K-in-LDS kernel for short-K attention products) has no
-// registers to spare: bias only.  The Add / Mul with another tensor reads
-// that tensor one element per lane at the end of each tile: measured against
-// the product and a separate elementwise kernel, that is faster on the 64 x
-// 64 tiles, the split-K tiles and the fp32 direct-load tiles, but slower on
-// the 128 x 128 tiles (an instance with the extra reads drops from three to
-// two workgroups per SIMD) and on the large bf16 tiles (the reads come after
-// the last MFMA, with nothing left to hide their latency), so those tiles
-// leave the Add / Mul to its own kernel.
+// Which steps pay off inside the product's launch was measured per tile
+// against the product followed by separate elementwise kernels.  Tile 9 (the
+// whole-K-in-LDS kernel for short-K attention products) has no registers to
+// spare: bias only.  On the large bf16 tiles (6, 8) the epilogue runs after
+// the last MFMA with nothing left to overlap it: a GELU or SiLU there costs
+// 13-41 us on a 2048 x 11008 output, more than its own kernel (17-21 us),
+// and the per-element reads of an Add / Mul tensor 15-75 us: bias only.  The
+// Add / Mul also stays out of the 128 x 128 tiles (an instance with its
+// reads drops from three to two workgroups per SIMD); on the 64 x 64, the
+// split-K and the fp32 direct-load tiles every step is faster fused.
 int gemm_epilogue_caps(int variant, int dtype) {
-  if (variant == 9) return EPI_BIAS;
-  const bool rop = (variant >= 1 && variant <= 5) || (dtype == FLUID_F32 && variant >= 6);
+  const bool bf16 = dtype == FLUID_BF16;
+  if (variant == 9 || (bf16 && (variant == 6 || variant == 8))) return EPI_BIAS;
+  const bool rop = (variant >= 1 && variant <= 5) || (!bf16 && variant >= 6);
   return EPI_BIAS | EPI_ACT | (rop ? EPI_ROP : 0);
 }
 

@@ -120,13 +120,14 @@ def epilogue_graph(B, S, K, N, dtype, keep_a, chain="bias_gelu"):
 
 def fusable_steps(chain, v, dtype):
     """How many of the chain's steps a MatMul of variant v absorbs when
-    nothing else stops it: variant 9 (short-K attention products) takes a
-    bias only; the Add / Mul with another tensor is taken by variants 1-5,
-    and by the fp32 variants 6-7."""
+    nothing else stops it: variant 9 (short-K attention products) and the
+    bf16 variants 6 and 8 take a bias only; the Add / Mul with another tensor
+    is taken by variants 1-5, and by the fp32 variants 6-7."""
+    bias_only = v == 9 or (dtype == "bf16" and v in (6, 8))
     rop = 1 <= v <= 5 or (dtype == "f32" and v in (6, 7))
     n = 0
     for step in EPILOGUES[chain]:
-        if step == "bias" or (step in ("gelu", "silu") and v != 9) or (step.endswith("_r") and rop):
+        if step == "bias" or (step in ("gelu", "silu") and not bias_only) or (step.endswith("_r") and rop):
             n += 1
         else:
             break
