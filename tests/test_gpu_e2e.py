@@ -11,13 +11,13 @@ from oracle import execute, graph as OG, layouts
 pytestmark = pytest.mark.gpu
 
 
-def _device_run(cfg, x, consts, table=None, flags=0, no_reuse=False, graph=None):
+def _device_run(cfg, x, consts, table=None, flags=0, no_reuse=False, graph=None, epilogue=False):
     import torch
     from paper_2411_09242_amd import fluid as F
     g = graph if graph is not None else F.Graph.transformer(cfg)
     t = table(g) if callable(table) else (table or F.CostTable.measure(g, reps=3))
     lp = F.LayoutPlan(g, t, flags)
-    ap = F.ArenaPlan(g, lp, no_reuse=no_reuse)
+    ap = F.ArenaPlan(g, lp, no_reuse=no_reuse, epilogue=epilogue)
     assert ap.lower_bound <= ap.peak <= (ap.naive if not no_reuse else ap.peak)
     ex = F.Executor(g, lp, ap, consts, [x])
     ex.arena.fill_(0xFF)
@@ -42,15 +42,20 @@ def test_config_planned_and_naive_match_oracle(idx):
     from paper_2411_09242_amd import fluid as F
     out2, *_ = _device_run(cfg, x, consts, table=t, graph=g, flags=F.NO_DP, no_reuse=True)
     assert_close(out2, ref, cfg["dtype"], f"cfg{idx} naive")
+    # the arena that lets every epilogue fuse (what the benchmark runs)
+    out3, _, lp3, ap3, _ = _device_run(cfg, x, consts, table=t, graph=g, epilogue=True)
+    assert F.fluid_run_launches(g.h, lp3.h, ap3.h) <= F.fluid_run_launches(g.h, lp.h, ap.h)
+    assert_close(out3, ref, cfg["dtype"], f"cfg{idx} planned, fusion lifetimes")
 
 
 @pytest.mark.parametrize("arch,dtype", [("post_ln", "f32"), ("pre_ln", "f32"), ("llama", "f32"), ("llama", "bf16")])
-def test_ragged_small_stacks(arch, dtype):
+@pytest.mark.parametrize("epilogue", [False, True])
+def test_ragged_small_stacks(arch, dtype, epilogue):
     cfg = synth_inputs.config(1, arch=arch, dtype=dtype, layers=2, batch=2, seq=37, hidden=72, heads=3, ffn=100)
     og = OG.build_transformer(cfg)
     x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), 11)
     (ref,) = execute.run_canonical(og, [x], consts)
-    out, *_ = _device_run(cfg, x, consts)
+    out, *_ = _device_run(cfg, x, consts, epilogue=epilogue)
     assert_close(out, ref, dtype, f"{arch} {dtype}")
 
 

@@ -32,7 +32,7 @@ def test_large_config_matches_oracle_samples(idx):
     say(f"cfg{idx}: measuring the cost table")
     t = F.CostTable.measure(g, reps=2)
     lp = F.LayoutPlan(g, t)
-    ap = F.ArenaPlan(g, lp)
+    ap = F.ArenaPlan(g, lp, epilogue=True)   # the benchmark's configuration
     say(f"cfg{idx}: plan {lp.total_ns} ns (guard {lp.guard_used}); arena {ap.peak / 2**20:.1f} MiB "
         f"(naive {ap.naive / 2**20:.1f}, lower bound {ap.lower_bound / 2**20:.1f})")
     assert ap.lower_bound <= ap.peak < ap.naive
