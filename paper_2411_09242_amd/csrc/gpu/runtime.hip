@@ -4,9 +4,10 @@
 // fluid_run is the paper's VM invoke path (Section 4): every non-view node
 // becomes one kernel launch, in node order, on the caller's stream, with
 // all activations inside the caller's single arena at their planned
-// offsets.  The per-node launch parameters depend only on the graph and the
+// offsets -- except the nodes a MatMul performs in its epilogue
+// (prepare.cpp).  The launch parameters depend only on the graph and the
 // two plans, so they are prepared once per (layout plan, arena plan) pair
-// and cached; each call only patches the five base addresses.
+// and cached; each call only patches the base addresses.
 #include <algorithm>
 #include <cmath>
 #include <cstring>

@@ -6,8 +6,11 @@
 //   MATMUL                      0: 128x128 tile, 1: 64x64 tile (LDS-staged);
 //                               2, 3, 5: 32x32 tile with K split over 4, 8,
 //                               16 wavefronts; 4: 64x32 tile, K over 4;
-//                               6: 256x128, 7: 128x128 tile, loads two
-//                               K-tiles ahead, LDS double-buffered (bf16)
+//                               bf16 6: 256x128, 7: 128x128 tile, loads K
+//                               tiles ahead; 8: 256x128, two workgroups per
+//                               CU; 9: 128x128, whole K (<= 128) in LDS;
+//                               fp32 6: 16x32, 7: 32x32 tiles, operands
+//                               straight into registers
 //   ADD MUL                     0: streaming elementwise in output order
 //   GELU SILU TRANSPOSE RESHAPE 0: streaming; 1: LDS-tiled (input and output
 //                               unit-stride dims differ)
