@@ -37,32 +37,38 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 # (workload, kernel, output shape, input shapes) and only while the kernel
 # sources hash to TRAFFIC_SRC -- a changed kernel makes the figure stale, and
 # then null.
-TRAFFIC_SRC = "467c2f8b0fbaec3f"
+TRAFFIC_SRC = "8f63784f1266ee27"
 TRAFFIC = {
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6061363,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6042926,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14302641,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14315915,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_sk32w8_ak_bmn_cn', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6108467,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14299569,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_amn_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14322064,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14338495,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_sk32w4_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6170895,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155481798,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238702975,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238525372,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237674557,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155464454,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237695977,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 595177228,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cn', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 596031723,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16674934,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16697459,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28472546,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28490976,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cm', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185186688,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894938442,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 914175678,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14336453,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_amn_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14322058,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14317999,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 241113229,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155271967,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 596332922,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238541904,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237697728,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155464653,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 240243941,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 572282244,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28470615,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16697509,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_amn_bmn_cn', (1, 512, 768), ((1, 512, 3072), ('c', 3072, 768))): 63495038,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28472673,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_t64_amn_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28395788,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28493066,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16677010,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16661609,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16695404,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28491008,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cm', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185075788,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894171351,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 913747485,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cm', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894170370,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6042939,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14315963,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14302689,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16674970,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185076973,
 }
 
 
