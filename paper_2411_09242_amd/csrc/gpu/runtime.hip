@@ -401,10 +401,13 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
           for (int v = 0; v < num_variants(nd.op); ++v) {
             NodeKernel k = prepare_node(nd, v, g.dtype, ins, ou);
             if (!k.available) { en.costs.push_back(-1); continue; }
-            // a warm-up launch, timed on its own: clearly losing
-            // combinations get no more launches
-            hip_check(hipEventRecord(ev[0], s), "hipEventRecord");
+            // an untimed warm-up launch (the first launch of a kernel
+            // instance also loads its code, which can take milliseconds),
+            // then one launch timed on its own: clearly losing combinations
+            // get no more launches
             hip_check(launch_node_kernel(k, s), "warm-up launch");
+            hip_check(hipEventRecord(ev[0], s), "hipEventRecord");
+            hip_check(launch_node_kernel(k, s), "first timed launch");
             hip_check(hipEventRecord(ev[1], s), "hipEventRecord");
             hip_check(hipEventSynchronize(ev[1]), "hipEventSynchronize");
             float first = 0.f;
