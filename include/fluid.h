@@ -241,7 +241,10 @@ fluid_status fluid_arena_plan_get(const fluid_arena_plan* ap, uint64_t* peak_byt
  * only for the kernel variants that have it), when each step's input is
  * read by nothing else and is no graph output; the launch writes the last
  * step's output, rounding once after all steps (a step is left to its own
- * kernel when its output shares arena bytes with a MatMul operand).  arena:
+ * kernel when its output shares arena bytes with a MatMul operand).  And
+ * consecutive fp32 MatMul launches of the same direct-load kernel (the Q, K
+ * and V projections) go out as one grouped launch when none reads or
+ * overwrites what another writes.  arena:
  * device memory of at least the plan's peak,
  * 256-B aligned; consts[i], inputs[i], outputs[i]: device pointers to dense
  * row-major tensors of the graph's dtype (RoPE tables fp32).  No device
@@ -260,16 +263,18 @@ fluid_status fluid_run(const fluid_graph* g, const fluid_layout_plan* lp, const 
  * fluid_run; nodes: n_nodes node ids, each a non-view node under the plan
  * (else FLUID_E_INVALID); repeat >= 1.  A MatMul that fluid_run fuses with
  * the nodes after it does so here too when all those nodes follow it in the
- * list; otherwise each listed node runs its own kernel.  Reads and writes
- * the arena like a run would, so it leaves the arena contents of a partial
- * run.  GPU build only. */
+ * list; otherwise each listed node runs its own kernel.  Products that
+ * fluid_run groups into one launch run one launch each here (the same tile
+ * code, so the same results).  Reads and writes the arena like a run would,
+ * so it leaves the arena contents of a partial run.  GPU build only. */
 fluid_status fluid_run_nodes(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
                              void* arena, uint64_t arena_bytes, const void* const* consts,
                              const void* const* inputs, void* const* outputs, const int32_t* nodes,
                              int32_t n_nodes, int32_t repeat, void* hip_stream);
 
 /* Number of kernel launches one fluid_run of these plans enqueues (the
- * non-view nodes, less those performed in a MatMul's epilogue).  Errors:
+ * non-view nodes, less those performed in a MatMul's epilogue, less the
+ * products launched with an earlier one).  Errors:
  * FLUID_E_INVALID (NULL argument, plans of another graph).  GPU build only. */
 fluid_status fluid_run_launches(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
                                 int32_t* launches);

@@ -31,11 +31,12 @@ constexpr int SK_DEPTH = 4;          // 16-k groups in flight per wavefront
 
 }  // namespace
 
+// One workgroup's tile: tile `bid` of the product p; red is the workgroup's
+// W * 16 SK_FM * SK_RP floats of LDS.
 template <int W, int SK_FM, int AM, int BMD, bool RES>
-__global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
+__device__ __forceinline__ void gemm_f32_dl_tile(const GemmParams& p, uint32_t bid, float* red) {
   constexpr int SK_TM = 16 * SK_FM;
-  __shared__ float red[W * SK_TM * SK_RP];
-  const TileCoord tc = tile_coord(p, SK_TM, SK_TN);
+  const TileCoord tc = tile_coord_at(p, bid, SK_TM, SK_TN);
   // causal attention: a tile entirely above the diagonal is never read; a
   // row block's A is zero past its last row, so K stops there
   if ((p.causal & 1u) && tc.n0 > tc.m0 + SK_TM - 1) return;
@@ -194,6 +195,23 @@ __global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
   }
 }
 
+template <int W, int SK_FM, int AM, int BMD, bool RES>
+__global__ __launch_bounds__(64 * W) void gemm_f32_dl_kernel(GemmParams p) {
+  __shared__ float red[W * 16 * SK_FM * SK_RP];
+  gemm_f32_dl_tile<W, SK_FM, AM, BMD, RES>(p, blockIdx.x, red);
+}
+
+// The members of a group share tile shape, operand modes and epilogue
+// instance; each workgroup runs one tile of its member.
+template <int W, int SK_FM, int AM, int BMD, bool RES>
+__global__ __launch_bounds__(64 * W) void gemm_f32_dl_group_kernel(GemmGroup G) {
+  __shared__ float red[W * 16 * SK_FM * SK_RP];
+  uint32_t i = 0;
+  while (i + 1 < G.n && blockIdx.x >= G.tiles[i + 1]) ++i;
+  gemm_f32_dl_tile<W, SK_FM, AM, BMD, RES>(G.p[i], blockIdx.x - G.tiles[i], red);
+}
+
+
 hipError_t launch_gemm_f32_dl(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
@@ -216,6 +234,32 @@ hipError_t launch_gemm_f32_dl(const NodeKernel& k, hipStream_t s) {
   }
 #undef FLUID_F32DL_W
 #undef FLUID_F32DL
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_f32_dl_group(const NodeKernel& k, const GemmGroup& G, hipStream_t s) {
+  if (k.dtype != DT_F32 || (k.gemm_tile != 6 && k.gemm_tile != 7) || G.n < 1 || G.n > (uint32_t)kMaxGroup)
+    return hipErrorInvalidValue;
+  const bool res = k.gemm.rop != 0;
+  const dim3 grid(G.tiles[G.n]);
+#define FLUID_F32DLG(Wv, FMv, AMv, BMv)                                                                          \
+  do {                                                                                                           \
+    if (res) hipLaunchKernelGGL((gemm_f32_dl_group_kernel<Wv, FMv, AMv, BMv, true>), grid, dim3(64 * Wv), 0, s, G); \
+    else hipLaunchKernelGGL((gemm_f32_dl_group_kernel<Wv, FMv, AMv, BMv, false>), grid, dim3(64 * Wv), 0, s, G);    \
+  } while (0)
+#define FLUID_F32DLG_W(Wv, FMv)                                                          \
+  if (k.amode == GM_K && k.bmode == GM_MN) FLUID_F32DLG(Wv, FMv, GM_K, GM_MN);           \
+  else if (k.amode == GM_K && k.bmode == GM_K) FLUID_F32DLG(Wv, FMv, GM_K, GM_K);        \
+  else if (k.amode == GM_MN && k.bmode == GM_MN) FLUID_F32DLG(Wv, FMv, GM_MN, GM_MN);    \
+  else if (k.amode == GM_MN && k.bmode == GM_K) FLUID_F32DLG(Wv, FMv, GM_MN, GM_K);      \
+  else return hipErrorInvalidValue;
+  if (k.gemm_tile == 6) {
+    FLUID_F32DLG_W(8, 1)
+  } else {
+    FLUID_F32DLG_W(4, 2)
+  }
+#undef FLUID_F32DLG_W
+#undef FLUID_F32DLG
   return hipGetLastError();
 }
 

@@ -210,18 +210,37 @@ fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const
     std::unique_lock<std::mutex> tl(g_trace_mu);
     const bool tracing = g_trace.on && g_trace.graph_serial == gh->serial;
     if (!tracing) tl.unlock();
-    for (const PreparedNode& pn : prep->nodes) {
-      if (pn.fused_away) continue;  // performed by a MatMul before it
+    auto kernel_of = [&](const PreparedNode& pn) {
+      if (pn.fuse_n) return fused_kernel(pn, B);
       NodeKernel k = pn.k;
-      if (pn.fuse_n) k = fused_kernel(pn, B);
-      else patch(k, pn, B);
+      patch(k, pn, B);
+      return k;
+    };
+    for (const PreparedNode& pn : prep->nodes) {
+      if (pn.fused_away || pn.grouped) continue;  // launched with an earlier node
+      const NodeKernel k = kernel_of(pn);
       int rec = -1;
       if (tracing && g_trace.mask[pn.node] && (int)g_trace.node_of.size() < g_trace.max_records) {
         rec = (int)g_trace.node_of.size();
         g_trace.node_of.push_back(pn.node);
         hip_check(hipEventRecord(g_trace.ev[2 * rec], s), "hipEventRecord");
       }
-      hipError_t e = launch_node_kernel(k, s);
+      hipError_t e;
+      if (!pn.group.empty()) {
+        GemmGroup G{};
+        G.n = 1 + (uint32_t)pn.group.size();
+        G.p[0] = k.gemm;
+        G.tiles[0] = 0;
+        G.tiles[1] = k.gemm.tiles_m * k.gemm.tiles_n * k.gemm.G;
+        for (size_t t = 0; t < pn.group.size(); ++t) {
+          const GemmParams q = kernel_of(prep->nodes[pn.group[t]]).gemm;
+          G.p[t + 1] = q;
+          G.tiles[t + 2] = G.tiles[t + 1] + q.tiles_m * q.tiles_n * q.G;
+        }
+        e = launch_gemm_f32_dl_group(k, G, s);
+      } else {
+        e = launch_node_kernel(k, s);
+      }
       if (e != hipSuccess)
         fail(FLUID_E_HIP, "node " + std::to_string(pn.node) + " (" + k.name() + "): " + hipGetErrorString(e));
       if (rec >= 0) hip_check(hipEventRecord(g_trace.ev[2 * rec + 1], s), "hipEventRecord");

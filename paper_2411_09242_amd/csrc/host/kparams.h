@@ -114,4 +114,14 @@ struct GemmParams {
   uint32_t rop;
 };
 
+// Up to kMaxGroup independent products of one kernel shape in one launch
+// (the Q, K and V projections of a layer): workgroups [tiles[i],
+// tiles[i+1]) run member i.
+constexpr int kMaxGroup = 4;
+struct GemmGroup {
+  GemmParams p[kMaxGroup];
+  uint32_t n;
+  uint32_t tiles[kMaxGroup + 1];
+};
+
 }  // namespace fluid

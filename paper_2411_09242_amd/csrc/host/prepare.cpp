@@ -105,6 +105,7 @@ void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan* ap
     kf.gemm.r_n = kr.gemm.c_n;
     kf.gemm.r_m2div = kf.gemm.m2div;
     mm.fr = nx.in[rslot];
+    mm.fr_edge = xn.ins[rslot];
   }
   kf.gemm.epi_bf16 = g.dtype == FLUID_BF16 ? 1u : 0u;
   kf.gemm.act = act;
@@ -114,6 +115,81 @@ void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan* ap
   mm.fout = nx.out;
   mm.fbias = bias;
   nx.fused_away = true;
+}
+
+// The output edge and binding a prepared launch writes.
+int written_edge(const Graph& g, const Prepared& P, size_t i) {
+  return g.out_edge(P.nodes[i + P.nodes[i].fuse_n].node);
+}
+const Bind& written_bind(const Prepared& P, size_t i) {
+  return P.nodes[i].fuse_n ? P.nodes[i].fout : P.nodes[i].out;
+}
+
+// Whether two bindings may share bytes: arena ranges that intersect, or the
+// same caller tensor.
+bool may_alias(const Graph& g, const ArenaPlan* ap, int e1, const Bind& b1, int e2, const Bind& b2) {
+  if (b1.kind == BK_ARENA && b2.kind == BK_ARENA) {
+    const auto r1 = arena_range(g, ap, e1, b1), r2 = arena_range(g, ap, e2, b2);
+    return r1.first < r2.second && r2.first < r1.second;
+  }
+  return b1.kind == b2.kind && b1.kind != BK_CONST && b1.index == b2.index;
+}
+
+// Activation operands (edge, binding) a prepared launch reads.
+std::vector<std::pair<int, Bind>> read_operands(const Graph& g, const Prepared& P, size_t i) {
+  const PreparedNode& pn = P.nodes[i];
+  std::vector<std::pair<int, Bind>> r;
+  const Node& nd = g.nodes[pn.node];
+  for (size_t s = 0; s < nd.ins.size(); ++s)
+    if (nd.ins[s] >= 0) r.push_back({nd.ins[s], pn.in[s]});
+  if (pn.fr_edge >= 0) r.push_back({pn.fr_edge, pn.fr});
+  return r;
+}
+
+// Grouped launches.  Consecutive launches of fp32 products with the same
+// direct-load tile (6 or 7), operand modes and epilogue instance -- the Q,
+// K and V projections of a layer once their bias Adds are fused and their
+// head reshapes are views -- go out as one launch when none reads or
+// overwrites what another writes (they run concurrently).
+void group_launches(const Graph& g, const ArenaPlan* ap, Prepared& P) {
+  auto kern = [&](size_t i) -> const NodeKernel& { return P.nodes[i].fuse_n ? P.nodes[i].kf : P.nodes[i].k; };
+  auto eligible = [&](size_t i) {
+    const NodeKernel& k = kern(i);
+    return !P.nodes[i].fused_away && k.family == KF_GEMM && k.dtype == DT_F32 &&
+           (k.gemm_tile == 6 || k.gemm_tile == 7);
+  };
+  auto next_launch = [&](size_t i) {
+    size_t j = i + 1;
+    while (j < P.nodes.size() && P.nodes[j].fused_away) ++j;
+    return j;
+  };
+  for (size_t i = 0; i < P.nodes.size(); i = next_launch(i)) {
+    if (!eligible(i)) continue;
+    std::vector<size_t> mem = {i};
+    for (size_t j = next_launch(i); j < P.nodes.size() && mem.size() < (size_t)kMaxGroup; j = next_launch(j)) {
+      const NodeKernel &a = kern(i), &b = kern(j);
+      if (!eligible(j) || b.gemm_tile != a.gemm_tile || b.amode != a.amode || b.bmode != a.bmode ||
+          (b.gemm.rop != 0) != (a.gemm.rop != 0))
+        break;
+      bool indep = true;
+      for (size_t m : mem) {
+        const int we = written_edge(g, P, j), wm = written_edge(g, P, m);
+        if (may_alias(g, ap, we, written_bind(P, j), wm, written_bind(P, m))) indep = false;
+        for (const auto& [e, bd] : read_operands(g, P, j))
+          if (may_alias(g, ap, e, bd, wm, written_bind(P, m))) indep = false;
+        for (const auto& [e, bd] : read_operands(g, P, m))
+          if (may_alias(g, ap, e, bd, we, written_bind(P, j))) indep = false;
+      }
+      if (!indep) break;
+      mem.push_back(j);
+    }
+    if (mem.size() < 2) continue;
+    for (size_t t = 1; t < mem.size(); ++t) {
+      P.nodes[i].group.push_back((int)mem[t]);
+      P.nodes[mem[t]].grouped = true;
+    }
+    i = mem.back();
+  }
 }
 
 }  // namespace
@@ -166,6 +242,7 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
     }
     P->nodes.push_back(std::move(pn));
   }
+  if (ap) group_launches(g, ap, *P);
   return P;
 }
 
@@ -180,7 +257,7 @@ std::vector<int> epilogue_reads_until(const Graph& g, const LayoutPlan& lp) {
 
 int prepared_launches(const Prepared& P) {
   int n = 0;
-  for (const PreparedNode& pn : P.nodes) n += pn.fused_away ? 0 : 1;
+  for (const PreparedNode& pn : P.nodes) n += (pn.fused_away || pn.grouped) ? 0 : 1;
   return n;
 }
 

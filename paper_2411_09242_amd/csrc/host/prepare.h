@@ -38,6 +38,12 @@ struct PreparedNode {
   Bind fout;
   int fbias = -1;           // constant id of the bias, -1 when none
   Bind fr;                  // the other tensor of the Add / Mul (kf.gemm.rop set)
+  int fr_edge = -1;         // its edge
+  // Grouped launch: this product also launches the products of these nodes
+  // (indices into Prepared::nodes, launched right after it), which are then
+  // not launched on their own (grouped set).
+  std::vector<int> group;
+  bool grouped = false;
   bool fused_away = false;  // this node is performed by a MatMul before it
 };
 

@@ -418,7 +418,8 @@ class Executor:
 
     def launches(self):
         """Kernel launches one run enqueues (nodes performed in a MatMul's
-        epilogue are not counted)."""
+        epilogue, and products launched together with an earlier one, are
+        not counted)."""
         return fluid_run_launches(self.graph.h, self.lplan.h, self.aplan.h)
 
     def run_nodes(self, nodes, repeat=1, stream=None):

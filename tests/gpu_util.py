@@ -110,7 +110,7 @@ def random_inputs(og, seed, scale=1.0):
     return xs, cs
 
 
-def run_device(og, table_obj, xs, cs, tmp_path, flags=0, no_reuse=False, poison=True):
+def run_device(og, table_obj, xs, cs, tmp_path, flags=0, no_reuse=False, poison=True, epilogue=False):
     """Build the graph in the C library, load the table, plan, run on the GPU
     and return (outputs as float64 numpy, layout plan, arena plan)."""
     import torch
@@ -121,7 +121,7 @@ def run_device(og, table_obj, xs, cs, tmp_path, flags=0, no_reuse=False, poison=
         json.dump(table_obj, f)
     t = F.CostTable.load(str(path), g)
     lp = F.LayoutPlan(g, t, flags)
-    ap = F.ArenaPlan(g, lp, no_reuse=no_reuse)
+    ap = F.ArenaPlan(g, lp, no_reuse=no_reuse, epilogue=epilogue)
     ex = F.Executor(g, lp, ap, cs, xs)
     if poison:
         ex.arena.fill_(0xFF)     # NaN bytes: reads of unwritten bytes show up

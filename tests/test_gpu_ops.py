@@ -196,6 +196,60 @@ def test_matmul_epilogue(dtype, shape, keep_a, chain, tmp_path):
         assert total > 0
 
 
+def siblings_graph(B, S, K, N, dtype, chained=False):
+    """gelu -> three MatMuls of the same input, each + bias (the Q, K, V
+    projections), combined as (q * k) + v.  With chained the second product
+    reads the first's output instead, so the two may not share a launch.
+    Returns the graph, the product edges and the bias-Add edges."""
+    g = Graph(dtype=dtype)
+    x = g.add_input((B, S, K))
+    a = g.add_node("gelu", [x], (B, S, K))
+    prods, outs = [], []
+    for i in range(3):
+        src = outs[0] if (chained and i == 1) else a
+        c = g.add_node("matmul", [src, g.add_const("weight", (K if src == a else N, N))], (B, S, N))
+        prods.append(c)
+        outs.append(g.add_node("add", [c, g.add_const("bias", (N,))], (B, S, N)))
+    y = g.add_node("mul", [outs[0], outs[1]], (B, S, N))
+    y = g.add_node("add", [y, outs[2]], (B, S, N))
+    g.outputs = [y]
+    return g, prods, outs
+
+
+@pytest.mark.parametrize("shape", [(1, 37, 64, 64), (2, 130, 96, 96)], ids=str)
+@pytest.mark.parametrize("variant", [6, 7])
+@pytest.mark.parametrize("chained", [False, True])
+def test_grouped_products(shape, variant, chained, tmp_path):
+    """Sibling fp32 products launched as one grouped launch (each with its
+    fused bias and its own output layout): same result as the oracle with
+    the fused intermediates unrounded, and one launch for the group unless a
+    member reads another's output."""
+    from paper_2411_09242_amd import fluid as F
+    og, prods, outs = siblings_graph(*shape, "f32", chained)
+    L = layouts.layout_list(og.edge_shape(outs[0]))
+    mms = [i for i, nd in enumerate(og.nodes) if nd.op == "matmul"]
+    for lays in ((0, 0, 0), (1, 0, 1), (0, 1, 1)):
+        want = {e: L[l] for e, l in zip(outs, lays)}
+        say(f"grouped {shape} v{variant} chained={chained} {want}")
+        xs, cs = random_inputs(og, sum(lays))
+        try:
+            out, lp, ap = run_device(og, forced_table(og, want, {m: variant for m in mms}), xs, cs, tmp_path,
+                                     epilogue=True)
+        except Exception as ex:  # noqa: BLE001
+            # chained: the second product reads the first's output, which in
+            # an M-contiguous layout with M % 4 != 0 no direct-load tile takes
+            if chained and "cannot run with these layouts" in str(ex):
+                continue
+            raise
+        nonview = sum(1 for x in lp.variant if x >= 0)
+        n = F.fluid_run_launches(lp.graph.h, lp.h, ap.h)
+        # three bias Adds fused; the products grouped into one launch (two
+        # when the second reads the first: it then waits for it)
+        assert n == nonview - 3 - (1 if chained else 2)
+        ref = reference_rounding_except(og, xs, cs, set(prods))
+        assert_close(out[0], ref[0], "f32", f"want={want} v{variant}")
+
+
 def attn_graph(B, NH, S, D, dtype, pv=False):
     g = Graph(dtype=dtype)
     if not pv:

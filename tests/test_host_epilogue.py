@@ -52,6 +52,22 @@ def test_epilogue_arena_lets_every_chain_fuse(chain, v, dtype, tmp_path):
     assert n_def >= n_epi
 
 
+@pytest.mark.parametrize("chained", [False, True])
+@pytest.mark.parametrize("variant,dtype,grouped", [(6, "f32", True), (7, "f32", True), (2, "f32", False),
+                                                   (6, "bf16", False)])
+def test_grouped_launch_count(chained, variant, dtype, grouped, tmp_path):
+    """Sibling products of the fp32 direct-load tiles share one launch
+    unless one reads another's output; other tiles launch one by one."""
+    from test_gpu_ops import siblings_graph
+    og, prods, outs = siblings_graph(1, 37, 64, 64, dtype, chained)
+    mms = [i for i, nd in enumerate(og.nodes) if nd.op == "matmul"]
+    g, lp = _plan(og, forced_table(og, {}, {m: variant for m in mms}), tmp_path)
+    nonview = sum(1 for n in range(g.n_nodes) if lp.kernel(n) != "view")
+    n, _ = _launches(g, lp, epilogue=True)
+    saved = (1 if chained else 2) if grouped else 0
+    assert n == nonview - 3 - saved
+
+
 CFGS = [synth_inputs.config(1, arch="post_ln", layers=2, seq=17, hidden=40, heads=5, ffn=72),
         synth_inputs.config(1, arch="pre_ln", layers=2, seq=19, hidden=36, heads=3, ffn=52),
         synth_inputs.config(1, arch="llama", layers=2, seq=21, hidden=48, heads=4, ffn=40, dtype="bf16")]
