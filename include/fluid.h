@@ -244,7 +244,10 @@ fluid_status fluid_arena_plan_get(const fluid_arena_plan* ap, uint64_t* peak_byt
  * kernel when its output shares arena bytes with a MatMul operand).  And
  * consecutive fp32 MatMul launches of the same direct-load kernel (the Q, K
  * and V projections) go out as one grouped launch when none reads or
- * overwrites what another writes.  arena:
+ * overwrites what another writes; and an fp32 attention S = Q K^T, P =
+ * Softmax(S), O = P V whose S and P have no other reader, with at most 128
+ * keys and a head dim of at most 128, runs as one launch that writes only O
+ * (not when O shares arena bytes with Q, K^T or V).  arena:
  * device memory of at least the plan's peak,
  * 256-B aligned; consts[i], inputs[i], outputs[i]: device pointers to dense
  * row-major tensors of the graph's dtype (RoPE tables fp32).  No device

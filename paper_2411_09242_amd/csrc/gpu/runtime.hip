@@ -69,9 +69,16 @@ void patch(NodeKernel& k, const PreparedNode& pn, const Bases& B) {
   }
 }
 
-// The fused MatMul + epilogue launch of pn (fuse_n > 0).
+// The fused launch of pn (fuse_n > 0): MatMul + epilogue, or attention.
 NodeKernel fused_kernel(const PreparedNode& pn, const Bases& B) {
   NodeKernel k = pn.kf;
+  if (k.family == KF_ATTN) {
+    k.attn.Q = (const float*)resolve(pn.in[0], B);
+    k.attn.Kt = (const float*)resolve(pn.in[1], B);
+    k.attn.V = (const float*)resolve(pn.fr, B);
+    k.attn.O = (float*)resolve(pn.fout, B);
+    return k;
+  }
   k.gemm.A = resolve(pn.in[0], B);
   k.gemm.B = resolve(pn.in[1], B);
   k.gemm.C = resolve(pn.fout, B);

@@ -68,6 +68,20 @@ def test_grouped_launch_count(chained, variant, dtype, grouped, tmp_path):
     assert n == nonview - 3 - saved
 
 
+@pytest.mark.parametrize("T,D,extra,fused", [(128, 64, False, True), (129, 64, False, False),
+                                             (128, 132, False, False), (64, 64, True, False)])
+def test_attention_launch_count(T, D, extra, fused, tmp_path):
+    """Q K^T, softmax and P V run as one launch only for at most 128 keys and
+    a head dim of at most 128, and only when nothing else reads the scores."""
+    from test_gpu_ops import chain_attn_graph
+    og, *_ = chain_attn_graph(1, 2, 40, T, D, False, extra)
+    g, lp = _plan(og, forced_table(og, {}), tmp_path)
+    nonview = sum(1 for n in range(g.n_nodes) if lp.kernel(n) != "view")
+    n, _ = _launches(g, lp, epilogue=True)
+    # unfused, the GELU after P V goes into that MatMul's epilogue instead
+    assert n == nonview - (2 if fused else 1)
+
+
 CFGS = [synth_inputs.config(1, arch="post_ln", layers=2, seq=17, hidden=40, heads=5, ffn=72),
         synth_inputs.config(1, arch="pre_ln", layers=2, seq=19, hidden=36, heads=3, ffn=52),
         synth_inputs.config(1, arch="llama", layers=2, seq=21, hidden=48, heads=4, ffn=40, dtype="bf16")]
