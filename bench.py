@@ -483,8 +483,8 @@ def main():
                     help="launch only each workload's dominant kernel (for counter runs); prints what ran")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(see DESIGN.md for how the graph would shard).", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the executor has no multi-GPU path "
+              "(one GPU's share of a sharded graph runs the same kernels).", file=sys.stderr)
         sys.exit(2)
 
     import torch

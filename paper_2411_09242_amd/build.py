@@ -27,7 +27,8 @@ HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
 CXXFLAGS = ["-std=c++17", "-O2", "-fPIC", "-Wall", "-Wno-unused-function", f"-I{INCLUDE}"]
-# Packed fp32 VALU ops are disabled for all device code.
+# Packed fp32 VALU instructions are disabled for all device code: the
+# compiler would otherwise form them from plain fp32 code.
 HIPFLAGS = ["-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", f"-I{INCLUDE}",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
             "-Wno-unused-result"]
