@@ -37,37 +37,34 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 # (workload, kernel, output shape, input shapes) and only while the kernel
 # sources hash to TRAFFIC_SRC -- a changed kernel makes the figure stale, and
 # then null.
-TRAFFIC_SRC = "d6caa8c7368895b2"
+TRAFFIC_SRC = "5890e0af5d8eb817"
 TRAFFIC = {
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14311868,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14302629,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14308736,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6046008,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6048045,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 241691868,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155272165,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 596271542,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238541710,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237691306,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155464058,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28463353,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16691287,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16670816,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16695375,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28466350,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16667766,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894413767,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 913774593,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185076893,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6103347,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14359978,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6098204,
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14354870,
     ('bert-base-12l-b1-s128-h768', 'gemm_f32_sk32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6108453,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6052146,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237687827,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 570642804,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cg', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 205340487,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 768), ((1, 512, 3072), ('c', 3072, 768))): 62044915,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28490965,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16718967,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16713855,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28509395,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_amn_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16730251,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28474615,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28482827,
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28494143,
     ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_t64_amn_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28391682,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238686516,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155464256,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237667233,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 570642804,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238606915,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237719346,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cg', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 205340487,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155490764,
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 596381872,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185076732,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 913793811,
     ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cm', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894194637,
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894587397,
 }
 
 

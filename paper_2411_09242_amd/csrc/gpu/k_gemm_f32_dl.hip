@@ -11,12 +11,17 @@
 //    MFMAs consume, straight from HBM into registers, four 16-k steps ahead.
 //    A K-contiguous operand gives a lane four consecutive k in one 16-byte
 //    load (one k per MFMA step); an M-/N-contiguous operand is read 4 bytes
-//    per lane, sixteen lanes covering 64 contiguous bytes.
+//    per lane, sixteen lanes covering 64 contiguous bytes.  A slice of at
+//    most six 16-k groups is loaded whole before its first MFMA: a load
+//    past the slice (which the rotating four-group loop issues, reading
+//    zeros) costs as much issue time as a real one.
 //
 // MFMA 16x16x4 f32 operand layout: lane l holds A[l % 16][k = l / 16] and
 // B[k = l / 16][l % 16]; the result lane l holds D[4 (l / 16) + v][l % 16].
 // Step s of a 16-k group uses, in the k slot l / 16, the real k
 // 4 (l / 16) + s, the same for A and B.
+#include <type_traits>
+
 #include "gemm_common.h"
 #include "launch.h"
 
@@ -41,7 +46,7 @@ __device__ __forceinline__ void gemm_f32_dl_tile(const GemmParams& p, uint32_t b
   // row block's A is zero past its last row, so K stops there
   if ((p.causal & 1u) && tc.n0 > tc.m0 + SK_TM - 1) return;
   const uint32_t Kc = (p.causal & 2u) ? min(p.K, tc.m0 + SK_TM) : p.K;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lq = lane >> 4;
   const Rsrc ra = make_rsrc(p.A, p.a_bytes);
   const Rsrc rb = make_rsrc(p.B, p.b_bytes);
@@ -122,21 +127,43 @@ __device__ __forceinline__ void gemm_f32_dl_tile(const GemmParams& p, uint32_t b
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(G.a[i][s], G.b[j][s], acc[i][j], 0, 0, 0);
   };
 
-  // group g travels in register set g % 4, loaded three groups before use;
-  // groups past the slice read zeros and their MFMAs are skipped
-  Grp G0, G1, G2, G3;
-  load(G0, 0);
-  load(G1, 1);
-  load(G2, 2);
-  for (uint32_t g = 0; g < ngroups; g += SK_DEPTH) {
-    load(G3, g + 3);
-    compute(G0);
-    load(G0, g + 4);
-    if (g + 1 < ngroups) compute(G1);
-    load(G1, g + 5);
-    if (g + 2 < ngroups) compute(G2);
-    load(G2, g + 6);
-    if (g + 3 < ngroups) compute(G3);
+  if (ngroups <= 6) {
+    // a short slice: all its groups are loaded before the first MFMA, with
+    // no load past its end
+    auto straight = [&](auto nc) {
+      constexpr int n = decltype(nc)::value;
+      Grp S[n];
+#pragma unroll
+      for (int i = 0; i < n; ++i) load(S[i], i);
+#pragma unroll
+      for (int i = 0; i < n; ++i) compute(S[i]);
+    };
+    switch (ngroups) {
+      case 1: straight(std::integral_constant<int, 1>{}); break;
+      case 2: straight(std::integral_constant<int, 2>{}); break;
+      case 3: straight(std::integral_constant<int, 3>{}); break;
+      case 4: straight(std::integral_constant<int, 4>{}); break;
+      case 5: straight(std::integral_constant<int, 5>{}); break;
+      case 6: straight(std::integral_constant<int, 6>{}); break;
+      default: break;  // an empty slice
+    }
+  } else {
+    // group g travels in register set g % 4, loaded three groups before
+    // use; groups past the slice read zeros and their MFMAs are skipped
+    Grp G0, G1, G2, G3;
+    load(G0, 0);
+    load(G1, 1);
+    load(G2, 2);
+    for (uint32_t g = 0; g < ngroups; g += SK_DEPTH) {
+      load(G3, g + 3);
+      compute(G0);
+      load(G0, g + 4);
+      if (g + 1 < ngroups) compute(G1);
+      load(G1, g + 5);
+      if (g + 2 < ngroups) compute(G2);
+      load(G2, g + 6);
+      if (g + 3 < ngroups) compute(G3);
+    }
   }
 
   // partial tiles -> LDS, then every thread sums W partials of some outputs
