@@ -76,3 +76,46 @@ def write_table(obj, path):
     with open(path, "w") as f:
         json.dump(obj, f)
     return str(path)
+
+
+def rank2_table(g, costs):
+    """A hand-written table for a graph of [2,3] tensors.  costs[n] is a dict
+    {(slot layout idx ..., out idx): cost}; the layouts of a [2,3] tensor are
+    (0,1) row-major = 0 and (1,0) = 1; graph inputs and outputs keep only
+    row-major.  A combination absent from costs[n] has no entry (+inf)."""
+    P = [[0, 1], [1, 0]]
+    L = []
+    for e in range(g.n_edges):
+        pinned = e < g.n_inputs or e in g.outputs
+        L.append([P[0]] if pinned else P)
+    sigs = []
+    for n in range(len(g.nodes)):
+        ents = [[[P[i] for i in key[:-1]], P[key[-1]], [c]] for key, c in costs[n].items()]
+        sigs.append({"op": g.nodes[n].op, "in_shapes": [], "out_shape": [2, 3], "entries": ents})
+    return {"format": "fluid-cost-table/1", "edges": L, "sigs": sigs,
+            "node_sig": list(range(len(g.nodes)))}
+
+
+def fanout_costs(infeasible_after_vote=False):
+    """Costs for tinygraphs.fanout_graph where the majority vote hurts.
+    Node order: a, b, b2, c, d, s, y.  Path [a b b2 s y] pays 100 more on b
+    when a is column-major; paths [c] and [d] each save 1 with a
+    column-major.  With infeasible_after_vote, b has no entry at all for a
+    column-major a, so the path that owns a cannot follow the vote."""
+    same = {(0, 0): 10, (1, 1): 10, (0, 1): 50, (1, 0): 50}
+    if infeasible_after_vote:
+        b = {(0, 0): 10, (0, 1): 110}
+    else:
+        b = {(0, 0): 10, (1, 0): 110, (0, 1): 110, (1, 1): 110}
+    reader = {(0, 0): 10, (1, 0): 9, (0, 1): 50, (1, 1): 50}
+    import itertools
+    add3 = {k: (10 if k == (0, 0, 0) else 100) for k in itertools.product((0, 1), repeat=3)}
+    return [
+        {(0, 0): 10, (0, 1): 10},                                # a (x pinned)
+        b,                                                       # b
+        dict(same),                                              # b2
+        dict(reader),                                            # c
+        dict(reader),                                            # d
+        add3,                                                    # s
+        {k: v for k, v in add3.items() if k[2] == 0},            # y (pinned)
+    ]

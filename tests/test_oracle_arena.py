@@ -18,6 +18,34 @@ def test_hand_worked_best_fit_example():
     off, peak = pa.greedy_by_size(list(size), size, defn, last)
     assert off == {1: 0, 4: 600, 2: 1000, 3: 1300, 0: 1000}
     assert peak == 1500
+    # max-live bound by hand: at nodes 2 and 3 buffers 1, 2, 3, 4 are live
+    # (600 + 300 + 200 + 400); at 4..6 only 0, 3, 4 (700); at 0..1 only 1
+    assert pa.lower_bound(list(size), size, defn, last, 7) == 1500
+
+
+def test_lower_bound_below_optimum_hand_worked():
+    """Seven buffers (in units of 256 B) whose max-live bound is 5 units while
+    no placement fits in 5.  Live sets: node 1 {4:2, 2:3}, node 2 {2:3, 1:1,
+    5:1}, node 3 {1:1, 3:2, 5:1}, node 4 {0:2, 3:2, 5:1}, node 5 {0:2, 6:3}:
+    at most 5 units.  In 5 units, node 1 forces buffer 2 to one end (the two
+    units of buffer 4 must be contiguous), say the bottom [0,3) (the other
+    case is its mirror image); node 2 then puts buffers 1 and 5 in units 3
+    and 4; node 3 leaves buffer 3 inside [0,3); node 5 forces buffer 0 to an
+    end; at node 4 buffer 0 cannot take [0,2) (buffer 3 overlaps it) nor
+    [3,5) (buffer 5 sits in unit 3 or 4).  So the optimum is 6 units, which
+    Greedy-by-Size reaches.  With half-open lifetimes the bound would be only
+    3 units (buffers ending at a node would not count there)."""
+    u = 256
+    items = {0: (2, 4, 5), 1: (1, 2, 3), 2: (3, 1, 2), 3: (2, 3, 4), 4: (2, 0, 1), 5: (1, 2, 4), 6: (3, 5, 6)}
+    bs = sorted(items)
+    size = {b: items[b][0] * u for b in bs}
+    defn = {b: items[b][1] for b in bs}
+    last = {b: items[b][2] for b in bs}
+    assert pa.lower_bound(bs, size, defn, last, 7) == 5 * u
+    assert brute.best_arena_peak(bs, size, defn, last) == 6 * u
+    off, peak = pa.greedy_by_size(bs, size, defn, last)
+    assert peak == 6 * u
+    assert pa.check_disjoint(pa.ArenaPlan(None, bs, size, defn, last, off, peak))
 
 
 def test_no_reuse_when_all_lifetimes_overlap():

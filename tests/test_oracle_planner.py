@@ -7,8 +7,8 @@ import pytest
 import synth_inputs
 from oracle import brute, costtable, graph, plan_layout as PL
 from oracle.graph import Graph
-from tables import synthetic_table
-from tinygraphs import chain_graph, diamond_graph, t1_graph, t2_graph
+from tables import fanout_costs, rank2_table, synthetic_table
+from tinygraphs import chain_graph, diamond_graph, fanout_graph, t1_graph, t2_graph
 
 
 def _all_paths_len(g, S):
@@ -102,19 +102,7 @@ def test_branched_plan_between_optimum_and_identity(builder, seed):
 
 
 def _rank2_table(g, costs):
-    """costs[n] : dict {(slot layout idx..., out idx): cost}; layouts of a
-    [2,3] tensor are (0,1) row-major = 0 and (1,0) = 1."""
-    P = [[0, 1], [1, 0]]
-    L = []
-    for e in range(g.n_edges):
-        pinned = e < g.n_inputs or e in g.outputs
-        L.append([P[0]] if pinned else P)
-    sigs = []
-    for n in range(len(g.nodes)):
-        ents = [[[P[i] for i in key[:-1]], P[key[-1]], [c]] for key, c in costs[n].items()]
-        sigs.append({"op": g.nodes[n].op, "in_shapes": [], "out_shape": [2, 3], "entries": ents})
-    return {"format": "fluid-cost-table/1", "edges": L, "sigs": sigs,
-            "node_sig": list(range(len(g.nodes)))}
+    return rank2_table(g, costs)
 
 
 def _hand_diamond():
@@ -165,13 +153,44 @@ def test_hand_worked_vote_with_cost_tie_breaks():
 
 
 def test_guard_returns_identity_when_vote_hurts():
-    g, costs = _hand_diamond()
-    costs[2] = {(0, 0): 11, (1, 1): 1, (0, 1): 50, (1, 0): 50}   # row-major c cheaper now
-    costs[5] = {(0, 0): 10, (1, 0): 200}
-    ct = costtable.load(_rank2_table(g, costs), g)
+    """Worked by hand on the fan-out graph (paths [a b b2 s y], [c], [d]).
+    Alone, the first path costs 50 all row-major (a column-major would add
+    100 on b); [c] and [d] each cost 9 with a column-major a (10 row-major).
+    Ballots on a: row (owner), column, column -> column wins 2:1.  Edges c
+    and d get their owners' row-major states.  Re-optimised with a column:
+    150 + 9 + 9 = 168 > 70, the all-row-major cost (seven nodes at 10), so
+    the guard returns the row-major plan."""
+    g = fanout_graph()
+    ct = costtable.load(rank2_table(g, fanout_costs()), g)
+    paths = PL.split(g)
+    assert paths == [[0, 1, 2, 5, 6], [3], [4]]
+    infos = [PL.PathInfo(g, p) for p in paths]
+    firsts = [PL.dp_path(g, ct, False, i, {}) for i in infos]
+    assert [f[0] for f in firsts] == [50, 9, 9]
+    assert firsts[0][1][0] == 0 and firsts[1][2][0] == {1: 1} and firsts[2][2][0] == {1: 1}
+    assert PL.plan_cost(g, ct, False, [0] * g.n_edges) == 70
+    voted = PL.plan_layouts(g, ct, PL.NO_GUARD)
+    assert voted.layout_idx == [0, 1, 0, 0, 0, 0, 0, 0]
+    assert voted.total == 168 and voted.guard_used == 0
+    assert PL.plan_cost(g, ct, False, voted.layout_idx) == 168
     plan = PL.plan_layouts(g, ct)
-    ident = PL.plan_cost(g, ct, False, [0] * 7)
-    assert plan.total <= ident
+    assert plan.layout_idx == [0] * g.n_edges
+    assert plan.total == 70 and plan.guard_used == 1
+    assert plan.variant == [0] * len(g.nodes)
+
+
+def test_guard_catches_a_path_infeasible_after_the_vote():
+    """Same ballots, but b has no entry for a column-major a: after the vote
+    fixes a column-major, the first path has no feasible layout.  With the
+    guard the row-major plan is returned (guard_used 1); without it the
+    planner reports the path as infeasible."""
+    g = fanout_graph()
+    ct = costtable.load(rank2_table(g, fanout_costs(infeasible_after_vote=True)), g)
+    plan = PL.plan_layouts(g, ct)
+    assert plan.layout_idx == [0] * g.n_edges
+    assert plan.total == 70 and plan.guard_used == 1
+    with pytest.raises(PL.Infeasible, match="after the vote"):
+        PL.plan_layouts(g, ct, PL.NO_GUARD)
 
 
 def test_missing_identity_entry_is_infeasible():

@@ -95,3 +95,21 @@ def ffn_block(B=1, S=4, H=8, F=16):
     y = g.add_node("layernorm", [r, gm, bt], (B, S, H), fattr=1e-5)
     g.outputs = [y]
     return g
+
+
+def fanout_graph():
+    """x -> a=gelu(x) -> b=silu(a) -> b2=silu(b); c=gelu(a); d=gelu(a);
+    s=add(b2, c); y=add(s, d).  Paths: [a b b2 s y], [c], [d]; edge a is
+    produced on the first path and read in boundary slots by the other two,
+    so three ballots decide it."""
+    g = Graph(dtype="f32")
+    x = g.add_input((2, 3))
+    a = g.add_node("gelu", [x], (2, 3))
+    b = g.add_node("silu", [a], (2, 3))
+    b2 = g.add_node("silu", [b], (2, 3))
+    c = g.add_node("gelu", [a], (2, 3))
+    d = g.add_node("gelu", [a], (2, 3))
+    s = g.add_node("add", [b2, c], (2, 3))
+    y = g.add_node("add", [s, d], (2, 3))
+    g.outputs = [y]
+    return g
