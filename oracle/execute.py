@@ -39,8 +39,8 @@ def op_matmul(a, b):
     return np.matmul(a, b)
 
 
-def op_softmax(x, scale, causal):
-    z = np.float64(scale) * x
+def op_softmax(x, scale, causal, dt=np.float64):
+    z = dt(scale) * x
     if causal:
         q, k = x.shape[-2], x.shape[-1]
         mask = np.arange(k)[None, :] > np.arange(q)[:, None]
@@ -50,15 +50,15 @@ def op_softmax(x, scale, causal):
     return e / e.sum(axis=-1, keepdims=True)
 
 
-def op_layernorm(x, gamma, beta, eps):
+def op_layernorm(x, gamma, beta, eps, dt=np.float64):
     mu = x.mean(axis=-1, keepdims=True)
     var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
-    return (x - mu) / np.sqrt(var + np.float64(eps)) * gamma + beta
+    return (x - mu) / np.sqrt(var + dt(eps)) * gamma + beta
 
 
-def op_rmsnorm(x, gamma, eps):
+def op_rmsnorm(x, gamma, eps, dt=np.float64):
     ms = (x * x).mean(axis=-1, keepdims=True)
-    return x / np.sqrt(ms + np.float64(eps)) * gamma
+    return x / np.sqrt(ms + dt(eps)) * gamma
 
 
 def op_gelu(x):
@@ -77,8 +77,9 @@ def op_rope(x, cos, sin):
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
-def eval_node(nd, args):
-    """float64 result of one operator on float64 arguments (not yet rounded)."""
+def eval_node(nd, args, dt=np.float64):
+    """Result of one operator on arguments of the arithmetic type dt (float64
+    unless a caller asks for float32 arithmetic), not yet rounded."""
     op = nd.op
     if op == "matmul":
         return op_matmul(args[0], args[1])
@@ -91,11 +92,11 @@ def eval_node(nd, args):
     if op == "reshape":
         return args[0].reshape(nd.out_shape)
     if op == "softmax":
-        return op_softmax(args[0], nd.fattr, nd.iattr)
+        return op_softmax(args[0], nd.fattr, nd.iattr, dt)
     if op == "layernorm":
-        return op_layernorm(args[0], args[1], args[2], nd.fattr)
+        return op_layernorm(args[0], args[1], args[2], nd.fattr, dt)
     if op == "rmsnorm":
-        return op_rmsnorm(args[0], args[1], nd.fattr)
+        return op_rmsnorm(args[0], args[1], nd.fattr, dt)
     if op == "gelu":
         return op_gelu(args[0])
     if op == "silu":
@@ -113,16 +114,24 @@ def _const_values(g, consts):
     return out
 
 
-def run_canonical(g, inputs, consts, keep=False):
+def run_canonical(g, inputs, consts, keep=False, arith=np.float64):
     """Row-major reference execution.  Returns the graph outputs (float64
-    arrays of dtype-representable values); with ``keep`` also every edge."""
+    arrays of dtype-representable values); with ``keep`` also every edge.
+
+    ``arith`` is the type every operator computes in before its result is
+    rounded to the edge dtype: float64 is the definition; float32 gives a
+    second, equally valid pipeline for bfloat16 graphs (the rounding points
+    are the same, only the arithmetic between them differs), used to measure
+    how far two valid bfloat16 executions drift apart."""
     cv = _const_values(g, consts)
     vals = {}
     for e, a in enumerate(inputs):
         vals[e] = numerics.round_to(np.asarray(a, np.float64).reshape(g.input_shapes[e]), g.dtype)
     for n, nd in enumerate(g.nodes):
         args = [vals[v] if v >= 0 else cv[~v] for v in nd.ins]
-        y = eval_node(nd, args)
+        if arith is not np.float64:
+            args = [a.astype(arith) for a in args]
+        y = eval_node(nd, args, arith)
         assert tuple(y.shape) == tuple(nd.out_shape), (n, nd.op, y.shape, nd.out_shape)
         vals[g.out_edge(n)] = numerics.round_to(y, g.dtype)
     outs = [vals[e] for e in g.outputs]

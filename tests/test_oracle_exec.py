@@ -131,3 +131,26 @@ def test_bf16_edges_hold_bf16_values():
     for e, v in vals.items():
         f = v.astype(np.float32)
         assert np.array_equal(numerics.bf16_bits_to_f32(numerics.f32_to_bf16_bits(f)), f)
+
+
+def test_float32_arithmetic_pipeline():
+    """The float32-arithmetic option (used only to measure how far two valid
+    bfloat16 executions drift apart) computes every operator in float32 --
+    no operand or constant upcasts it -- and rounds at the same edges: on a
+    small bf16 Llama stack every edge lands within one bfloat16 ulp of the
+    definition (relative to the edge's largest value) and most edges differ
+    from it somewhere."""
+    cfg = synth_inputs.config(1, arch="llama", layers=2, seq=64, hidden=256, heads=4, ffn=512, dtype="bf16")
+    g = graph.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, g.const_specs(), 4)
+    _, vals = execute.run_canonical(g, [x], consts, keep=True)
+    cv = [numerics.round_to(np.asarray(a, np.float64).reshape(s), dt) for (_, s, dt), a in zip(g.consts, consts)]
+    for nd in g.nodes:
+        args = [(vals[v] if v >= 0 else cv[~v]).astype(np.float32) for v in nd.ins]
+        assert execute.eval_node(nd, args, np.float32).dtype == np.float32, nd.op
+    (y64,), v64 = execute.run_canonical(g, [x], consts, keep=True)
+    (y32,), v32 = execute.run_canonical(g, [x], consts, keep=True, arith=np.float32)
+    assert np.array_equal(numerics.round_bf16(y32), y32)
+    assert sum(not np.array_equal(v32[e], v64[e]) for e in v64) > len(v64) // 2
+    for e in v64:
+        assert np.abs(v32[e] - v64[e]).max() <= 2.0 ** -8 * max(np.abs(v64[e]).max(), 1e-3), e
