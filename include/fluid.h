@@ -232,6 +232,17 @@ fluid_status fluid_arena_plan_get(const fluid_arena_plan* ap, uint64_t* peak_byt
                                   uint64_t* lower_bound_bytes, int64_t* offset_per_edge,
                                   int32_t* root_per_edge);
 
+/* The lifetimes the arena plan placed its buffers by (Alg. 4's input): per
+ * edge, size_per_edge the buffer bytes after rounding to the alignment, and
+ * def_per_edge / last_per_edge the producing node and the last node that
+ * reads any edge rooted at the buffer (with FLUID_ARENA_EPILOGUE, the
+ * extended end), for edges that are arena buffers; 0 / -1 / -1 for the
+ * others (graph inputs and outputs, views).  Arrays of n_edges entries,
+ * each may be NULL.  Errors: FLUID_E_INVALID (NULL plan, n_edges not the
+ * plan's edge count). */
+fluid_status fluid_arena_plan_lifetimes(const fluid_arena_plan* ap, int32_t n_edges, uint64_t* size_per_edge,
+                                        int32_t* def_per_edge, int32_t* last_per_edge);
+
 /* Executes the graph (Section 4 "Virtual Machine": the invoke interface):
  * enqueues one kernel per non-view node, in node order, on hip_stream; the
  * caller synchronises.  One exception, epilogue fusion: a MatMul also
@@ -244,10 +255,8 @@ fluid_status fluid_arena_plan_get(const fluid_arena_plan* ap, uint64_t* peak_byt
  * kernel when its output shares arena bytes with a MatMul operand).  And
  * consecutive fp32 MatMul launches of the same direct-load kernel (the Q, K
  * and V projections) go out as one grouped launch when none reads or
- * overwrites what another writes; and an fp32 attention S = Q K^T, P =
- * Softmax(S), O = P V whose S and P have no other reader, with at most 128
- * keys and a head dim of at most 128, runs as one launch that writes only O
- * (not when O shares arena bytes with Q, K^T or V).  arena:
+ * overwrites what another writes (fluid_run_schedule lists the launches).
+ * arena:
  * device memory of at least the plan's peak,
  * 256-B aligned; consts[i], inputs[i], outputs[i]: device pointers to dense
  * row-major tensors of the graph's dtype (RoPE tables fp32).  No device
@@ -267,9 +276,11 @@ fluid_status fluid_run(const fluid_graph* g, const fluid_layout_plan* lp, const 
  * (else FLUID_E_INVALID); repeat >= 1.  A MatMul that fluid_run fuses with
  * the nodes after it does so here too when all those nodes follow it in the
  * list; otherwise each listed node runs its own kernel.  Products that
- * fluid_run groups into one launch run one launch each here (the same tile
- * code, so the same results).  Reads and writes the arena like a run would,
- * so it leaves the arena contents of a partial run.  GPU build only. */
+ * fluid_run groups into one launch run as that launch when the list holds
+ * all its nodes (the products and the nodes they absorb) consecutively in
+ * node order, else one launch each (the same tile code, so the same
+ * results).  Reads and writes the arena like a run would, so it leaves the
+ * arena contents of a partial run.  GPU build only. */
 fluid_status fluid_run_nodes(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
                              void* arena, uint64_t arena_bytes, const void* const* consts,
                              const void* const* inputs, void* const* outputs, const int32_t* nodes,
@@ -278,9 +289,25 @@ fluid_status fluid_run_nodes(const fluid_graph* g, const fluid_layout_plan* lp, 
 /* Number of kernel launches one fluid_run of these plans enqueues (the
  * non-view nodes, less those performed in a MatMul's epilogue, less the
  * products launched with an earlier one).  Errors:
- * FLUID_E_INVALID (NULL argument, plans of another graph).  GPU build only. */
+ * FLUID_E_INVALID (NULL argument, plans of another graph).  Both builds. */
 fluid_status fluid_run_launches(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
                                 int32_t* launches);
+
+/* The launches one fluid_run of these plans enqueues, in order (Section 4
+ * "Virtual Machine" runs the planned operators in sequence; here with the
+ * epilogue fusion and grouped launches described at fluid_run).  Per node:
+ * launch_of_node the index of the launch that performs it (-1 for a view),
+ * output_written 1 if that launch stores the node's output (0 for a view
+ * and for a node whose output a fused launch keeps on chip).  names: the
+ * kernel name of every launch, '\n'-separated, NUL-terminated (a grouped
+ * launch of k products ends in "_x<k>"); names_len receives the bytes
+ * needed including the NUL.  n_launches receives the launch count.  Any
+ * output pointer may be NULL; arrays have n_nodes entries.  Errors:
+ * FLUID_E_INVALID (NULL graph or plan, plans of another graph, names_cap
+ * below the bytes needed).  Both builds. */
+fluid_status fluid_run_schedule(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
+                                int32_t* launch_of_node, uint8_t* output_written, char* names, uint64_t names_cap,
+                                uint64_t* names_len, int32_t* n_launches);
 
 /* Per-node timing of later fluid_run calls (profiling aid).  While enabled,
  * fluid_run records a HIP event pair around every launch of a node whose

@@ -69,22 +69,40 @@ void patch(NodeKernel& k, const PreparedNode& pn, const Bases& B) {
   }
 }
 
-// The fused launch of pn (fuse_n > 0): MatMul + epilogue, or attention.
+// The fused launch of pn (fuse_n > 0): the MatMul and its epilogue.
 NodeKernel fused_kernel(const PreparedNode& pn, const Bases& B) {
   NodeKernel k = pn.kf;
-  if (k.family == KF_ATTN) {
-    k.attn.Q = (const float*)resolve(pn.in[0], B);
-    k.attn.Kt = (const float*)resolve(pn.in[1], B);
-    k.attn.V = (const float*)resolve(pn.fr, B);
-    k.attn.O = (float*)resolve(pn.fout, B);
-    return k;
-  }
   k.gemm.A = resolve(pn.in[0], B);
   k.gemm.B = resolve(pn.in[1], B);
   k.gemm.C = resolve(pn.fout, B);
   k.gemm.bias = pn.fbias >= 0 ? B.consts[pn.fbias] : nullptr;
   k.gemm.R = k.gemm.rop ? resolve(pn.fr, B) : nullptr;
   return k;
+}
+
+// The prepared launch of pn (the launch of its whole chain when it has
+// absorbed the nodes after it).
+NodeKernel launch_kernel(const PreparedNode& pn, const Bases& B) {
+  if (pn.fuse_n) return fused_kernel(pn, B);
+  NodeKernel k = pn.k;
+  patch(k, pn, B);
+  return k;
+}
+
+// One launch of pn's product (kernel k) and the products grouped with it.
+hipError_t launch_group(const Prepared& P, const PreparedNode& pn, const NodeKernel& k, const Bases& B,
+                        hipStream_t s) {
+  GemmGroup G{};
+  G.n = 1 + (uint32_t)pn.group.size();
+  G.p[0] = k.gemm;
+  G.tiles[0] = 0;
+  G.tiles[1] = k.gemm.tiles_m * k.gemm.tiles_n * k.gemm.G;
+  for (size_t t = 0; t < pn.group.size(); ++t) {
+    const GemmParams q = launch_kernel(P.nodes[pn.group[t]], B).gemm;
+    G.p[t + 1] = q;
+    G.tiles[t + 2] = G.tiles[t + 1] + q.tiles_m * q.tiles_n * q.G;
+  }
+  return launch_gemm_f32_dl_group(k, G, s);
 }
 
 // ------------------------------------------------------------ tracing
@@ -217,37 +235,16 @@ fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const
     std::unique_lock<std::mutex> tl(g_trace_mu);
     const bool tracing = g_trace.on && g_trace.graph_serial == gh->serial;
     if (!tracing) tl.unlock();
-    auto kernel_of = [&](const PreparedNode& pn) {
-      if (pn.fuse_n) return fused_kernel(pn, B);
-      NodeKernel k = pn.k;
-      patch(k, pn, B);
-      return k;
-    };
     for (const PreparedNode& pn : prep->nodes) {
       if (pn.fused_away || pn.grouped) continue;  // launched with an earlier node
-      const NodeKernel k = kernel_of(pn);
+      const NodeKernel k = launch_kernel(pn, B);
       int rec = -1;
       if (tracing && g_trace.mask[pn.node] && (int)g_trace.node_of.size() < g_trace.max_records) {
         rec = (int)g_trace.node_of.size();
         g_trace.node_of.push_back(pn.node);
         hip_check(hipEventRecord(g_trace.ev[2 * rec], s), "hipEventRecord");
       }
-      hipError_t e;
-      if (!pn.group.empty()) {
-        GemmGroup G{};
-        G.n = 1 + (uint32_t)pn.group.size();
-        G.p[0] = k.gemm;
-        G.tiles[0] = 0;
-        G.tiles[1] = k.gemm.tiles_m * k.gemm.tiles_n * k.gemm.G;
-        for (size_t t = 0; t < pn.group.size(); ++t) {
-          const GemmParams q = kernel_of(prep->nodes[pn.group[t]]).gemm;
-          G.p[t + 1] = q;
-          G.tiles[t + 2] = G.tiles[t + 1] + q.tiles_m * q.tiles_n * q.G;
-        }
-        e = launch_gemm_f32_dl_group(k, G, s);
-      } else {
-        e = launch_node_kernel(k, s);
-      }
+      const hipError_t e = pn.group.empty() ? launch_node_kernel(k, s) : launch_group(*prep, pn, k, B, s);
       if (e != hipSuccess)
         fail(FLUID_E_HIP, "node " + std::to_string(pn.node) + " (" + k.name() + "): " + hipGetErrorString(e));
       if (rec >= 0) hip_check(hipEventRecord(g_trace.ev[2 * rec + 1], s), "hipEventRecord");
@@ -276,10 +273,27 @@ fluid_status fluid_run_nodes(const fluid_graph* gh, const fluid_layout_plan* lh,
     Bases B{(char*)arena, inputs, outputs, consts};
     hipStream_t s = (hipStream_t)hip_stream;
     // a fused MatMul followed in the list by every node it absorbs runs as in
-    // fluid_run; otherwise each node runs its own kernel
+    // fluid_run, and so does a grouped launch whose nodes (the products and
+    // the nodes they absorb) all follow in fluid_run's order; otherwise each
+    // node runs its own kernel
+    const PreparedNode* first = prep->nodes.data();
     for (int32_t r = 0; r < repeat; ++r)
       for (size_t i = 0; i < sel.size(); ++i) {
         const PreparedNode* pn = sel[i];
+        if (!pn->group.empty()) {
+          const size_t last = (size_t)pn->group.back();
+          const size_t span = last + prep->nodes[last].fuse_n - (size_t)(pn - first) + 1;
+          bool whole = i + span <= sel.size();
+          for (size_t t = 0; whole && t < span; ++t) whole = sel[i + t] == pn + t;
+          if (whole) {
+            const NodeKernel k = launch_kernel(*pn, B);
+            const hipError_t e = launch_group(*prep, *pn, k, B, s);
+            if (e != hipSuccess)
+              fail(FLUID_E_HIP, "node " + std::to_string(pn->node) + " (" + k.name() + "): " + hipGetErrorString(e));
+            i += span - 1;
+            continue;
+          }
+        }
         NodeKernel k = pn->k;
         bool whole = pn->fuse_n > 0 && i + pn->fuse_n < sel.size();
         for (int f = 1; whole && f <= pn->fuse_n; ++f) whole = sel[i + f] == pn + f;

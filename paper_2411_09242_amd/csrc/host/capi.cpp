@@ -229,6 +229,67 @@ fluid_status fluid_arena_plan_get(const fluid_arena_plan* ap, uint64_t* peak, ui
   });
 }
 
+fluid_status fluid_run_schedule(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah,
+                                int32_t* launch_of_node, uint8_t* output_written, char* names, uint64_t names_cap,
+                                uint64_t* names_len, int32_t* n_launches) {
+  return call_guarded([&] {
+    require(gh && lh && ah, "fluid_run_schedule: NULL argument");
+    require(lh->p.graph_serial == gh->serial && ah->a.graph_serial == gh->serial,
+            "fluid_run_schedule: plans belong to another graph");
+    const Graph& g = gh->g;
+    const auto P = prepare(g, lh->p, &ah->a);
+    std::vector<int32_t> launch(g.n_nodes(), -1);
+    std::vector<uint8_t> written(g.n_nodes(), 0);
+    std::string all;
+    int32_t L = 0;
+    // a prepared launch performs its node and the fuse_n nodes after it, and
+    // writes the output of the last of them
+    auto claim = [&](size_t i, int32_t l) {
+      const PreparedNode& pn = P->nodes[i];
+      for (int f = 0; f <= pn.fuse_n; ++f) {
+        launch[P->nodes[i + f].node] = l;
+        written[P->nodes[i + f].node] = f == pn.fuse_n ? 1 : 0;
+      }
+    };
+    for (size_t i = 0; i < P->nodes.size(); ++i) {
+      const PreparedNode& pn = P->nodes[i];
+      if (pn.fused_away || pn.grouped) continue;
+      claim(i, L);
+      for (int m : pn.group) claim((size_t)m, L);
+      std::string nm = (pn.fuse_n ? pn.kf : pn.k).name();
+      if (!pn.group.empty()) nm += "_x" + std::to_string(1 + pn.group.size());
+      all += (L ? "\n" : "") + nm;
+      ++L;
+    }
+    if (names_len) *names_len = all.size() + 1;
+    if (names) {
+      require(names_cap >= all.size() + 1, "fluid_run_schedule: names buffer too small");
+      std::memcpy(names, all.c_str(), all.size() + 1);
+    }
+    for (int n = 0; n < g.n_nodes(); ++n) {
+      if (launch_of_node) launch_of_node[n] = launch[n];
+      if (output_written) output_written[n] = written[n];
+    }
+    if (n_launches) *n_launches = L;
+  });
+}
+
+fluid_status fluid_arena_plan_lifetimes(const fluid_arena_plan* ap, int32_t n_edges, uint64_t* size,
+                                        int32_t* def, int32_t* last) {
+  return call_guarded([&] {
+    require(ap, "NULL plan");
+    const auto& a = ap->a;
+    require(n_edges == (int32_t)a.root.size(), "n_edges is not the plan's edge count");
+    std::vector<char> is_buf(a.root.size(), 0);
+    for (int b : a.buffers) is_buf[b] = 1;
+    for (int32_t e = 0; e < n_edges; ++e) {
+      if (size) size[e] = is_buf[e] ? a.size[e] : 0;
+      if (def) def[e] = is_buf[e] ? a.def[e] : -1;
+      if (last) last[e] = is_buf[e] ? a.last[e] : -1;
+    }
+  });
+}
+
 fluid_status fluid_node_kernel(const fluid_graph* gh, const fluid_layout_plan* lh, int32_t node, char* buf, uint64_t cap) {
   return call_guarded([&] {
     require(gh && lh && buf && cap > 0, "fluid_node_kernel: bad argument");

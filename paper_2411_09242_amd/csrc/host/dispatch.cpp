@@ -473,7 +473,6 @@ std::string NodeKernel::name() const {
     case KF_ROPE: return "rope_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
-    case KF_ATTN: return "attn_small_" + dt;
     case KF_GEMM: {
       // fused epilogue steps: b bias, g GELU, s SiLU, a / m Add / Mul of R
       auto epi_suffix = [&]() {

@@ -114,25 +114,6 @@ struct GemmParams {
   uint32_t rop;
 };
 
-// Attention of short sequences in one launch: O = softmax(scale Q K^T, with
-// keys after the query masked when causal) V over G = G1 * G2 heads; Q
-// [G, S, D], K^T [G, D, T], V [G, T, D], O [G, S, D], each with its own
-// strides (batch index g = g1 * G2 + g2).  T, D <= 128.
-struct AttnParams {
-  const float* Q;
-  const float* Kt;
-  const float* V;
-  float* O;
-  uint32_t G, G2, S, T, D;
-  FastDiv g2div;
-  int32_t q_g1, q_g2, q_s, q_d;
-  int32_t k_g1, k_g2, k_d, k_t;
-  int32_t v_g1, v_g2, v_t, v_d;
-  int32_t o_g1, o_g2, o_s, o_d;
-  float scale;
-  uint32_t causal;
-};
-
 // Up to kMaxGroup independent products of one kernel shape in one launch
 // (the Q, K and V projections of a layer): workgroups [tiles[i],
 // tiles[i+1]) run member i.

@@ -117,63 +117,6 @@ void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan* ap
   nx.fused_away = true;
 }
 
-// Attention of short sequences.  When the last three launches are a batched
-// fp32 MatMul S = Q K^T, a Softmax of S (its only reader) and a MatMul O =
-// P V of the Softmax output P (its only reader), with T keys and head dim D
-// both at most 128 (and D the same for Q and V), the first runs all three
-// (attn_small): S and P stay on chip, the launch writes O.  Not when O shares
-// arena bytes with Q, K^T or V (they are read while O is written).
-void try_fuse_attention(const Graph& g, const ArenaPlan* ap, Prepared& P) {
-  const size_t n = P.nodes.size();
-  if (n < 3) return;
-  PreparedNode &qk = P.nodes[n - 3], &sm = P.nodes[n - 2], &pv = P.nodes[n - 1];
-  if (qk.fused_away || qk.fuse_n || sm.fused_away || pv.fused_away) return;
-  const Node &qn = g.nodes[qk.node], &sn = g.nodes[sm.node], &pn_ = g.nodes[pv.node];
-  if (qn.op != FLUID_OP_MATMUL || sn.op != FLUID_OP_SOFTMAX || pn_.op != FLUID_OP_MATMUL) return;
-  if (g.dtype != FLUID_F32 || qk.k.family != KF_GEMM || pv.k.family != KF_GEMM) return;
-  if (qn.out_shape.size() != 4 || qn.ins.size() != 2 || pn_.ins.size() != 2 || qn.ins[1] < 0 || pn_.ins[1] < 0 ||
-      qn.ins[0] < 0)
-    return;
-  const int es = g.out_edge(qk.node), ep = g.out_edge(sm.node);
-  if (sn.ins[0] != es || pn_.ins[0] != ep) return;
-  if (g.is_output[es] || g.is_output[ep] || g.readers[es].size() != 1 || g.readers[ep].size() != 1) return;
-  const GemmParams &a = qk.k.gemm, &b = pv.k.gemm;
-  if (a.N > 128 || a.K > 128 || b.N != a.K || b.K != a.N || b.M != a.M || b.G != a.G || b.G2 != a.G2 ||
-      a.M2 != a.M || b.M2 != b.M)
-    return;
-  const int ev = pn_.ins[1];
-  const auto ro = arena_range(g, ap, g.out_edge(pv.node), pv.out);
-  const std::pair<int, const Bind*> reads[3] = {{qn.ins[0], &qk.in[0]}, {qn.ins[1], &qk.in[1]}, {ev, &pv.in[1]}};
-  for (const auto& [e, bd] : reads) {
-    const auto ri = arena_range(g, ap, e, *bd);
-    if (ro.first < ro.second && ri.first < ri.second && ro.first < ri.second && ri.first < ro.second) return;
-  }
-  NodeKernel k;
-  k.family = KF_ATTN;
-  k.available = true;
-  k.dtype = DT_F32;
-  AttnParams& t = k.attn;
-  t.G = a.G;
-  t.G2 = a.G2;
-  t.g2div = a.g2div;
-  t.S = a.M;
-  t.T = a.N;
-  t.D = a.K;
-  t.q_g1 = a.a_g1; t.q_g2 = a.a_g2; t.q_s = a.a_m2; t.q_d = a.a_k;
-  t.k_g1 = a.b_g1; t.k_g2 = a.b_g2; t.k_d = a.b_k; t.k_t = a.b_n;
-  t.v_g1 = b.b_g1; t.v_g2 = b.b_g2; t.v_t = b.b_k; t.v_d = b.b_n;
-  t.o_g1 = b.c_g1; t.o_g2 = b.c_g2; t.o_s = b.c_m2; t.o_d = b.c_n;
-  t.scale = sn.fattr;
-  t.causal = sn.iattr ? 1u : 0u;
-  qk.kf = k;
-  qk.fuse_n = 2;
-  qk.fout = pv.out;
-  qk.fr = pv.in[1];
-  qk.fr_edge = ev;
-  sm.fused_away = true;
-  pv.fused_away = true;
-}
-
 // The output edge and binding a prepared launch writes.
 int written_edge(const Graph& g, const Prepared& P, size_t i) {
   return g.out_edge(P.nodes[i + P.nodes[i].fuse_n].node);
@@ -298,7 +241,6 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
         try_fuse_epilogue(g, lp, ap, P->nodes[j], g.out_edge(P->nodes.back().node), pn, out);
     }
     P->nodes.push_back(std::move(pn));
-    try_fuse_attention(g, ap, *P);
   }
   if (ap) group_launches(g, ap, *P);
   return P;

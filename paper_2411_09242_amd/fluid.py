@@ -17,7 +17,9 @@ import json
 import os
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIBDIR = os.path.join(_PKG, "lib")
+# FLUID_LIBDIR: load the libraries from another directory (e.g. a
+# sanitizer build of the host library)
+LIBDIR = os.environ.get("FLUID_LIBDIR") or os.path.join(_PKG, "lib")
 
 MAX_RANK = 6
 MAX_IN = 4
@@ -80,11 +82,15 @@ _PROTOS = {
     "fluid_plan_arena": (C.c_int, [_VP, _VP, C.c_uint64, C.c_uint32, C.POINTER(_VP)]),
     "fluid_arena_plan_get": (C.c_int, [_VP, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                                        C.POINTER(C.c_uint64), C.POINTER(C.c_int64), C.POINTER(C.c_int32)]),
+    "fluid_arena_plan_lifetimes": (C.c_int, [_VP, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_int32),
+                                             C.POINTER(C.c_int32)]),
     "fluid_run": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
                             C.POINTER(_VP), _VP]),
     "fluid_run_nodes": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
                                   C.POINTER(_VP), C.POINTER(C.c_int32), C.c_int32, C.c_int32, _VP]),
     "fluid_run_launches": (C.c_int, [_VP, _VP, _VP, C.POINTER(C.c_int32)]),
+    "fluid_run_schedule": (C.c_int, [_VP, _VP, _VP, C.POINTER(C.c_int32), C.POINTER(C.c_uint8), C.c_char_p,
+                                     C.c_uint64, C.POINTER(C.c_uint64), C.POINTER(C.c_int32)]),
     "fluid_trace_enable": (C.c_int, [_VP, C.POINTER(C.c_uint8), C.c_int32]),
     "fluid_trace_collect": (C.c_int, [_VP, C.POINTER(C.c_double), C.POINTER(C.c_int32)]),
     "fluid_node_kernel": (C.c_int, [_VP, _VP, C.c_int32, C.c_char_p, C.c_uint64]),
@@ -253,6 +259,14 @@ def fluid_arena_plan_get(ap, n_edges):
     return peak.value, naive.value, lb.value, list(off), list(root)
 
 
+def fluid_arena_plan_lifetimes(ap, n_edges):
+    size = (C.c_uint64 * n_edges)()
+    d = (C.c_int32 * n_edges)()
+    last = (C.c_int32 * n_edges)()
+    _check(_L().fluid_arena_plan_lifetimes(ap, n_edges, size, d, last))
+    return list(size), list(d), list(last)
+
+
 def _ptr_array(ptrs):
     arr = (_VP * max(len(ptrs), 1))()
     for i, p in enumerate(ptrs):
@@ -277,6 +291,20 @@ def fluid_run_launches(g, lp, ap):
     n = C.c_int32(0)
     _check(_L().fluid_run_launches(g, lp, ap, C.byref(n)))
     return n.value
+
+
+def fluid_run_schedule(g, lp, ap, n_nodes):
+    """(launch index per node, output-written flag per node, kernel name per
+    launch)."""
+    need = C.c_uint64(0)
+    _check(_L().fluid_run_schedule(g, lp, ap, None, None, None, 0, C.byref(need), None))
+    launch = (C.c_int32 * n_nodes)()
+    written = (C.c_uint8 * n_nodes)()
+    buf = C.create_string_buffer(need.value)
+    n = C.c_int32(0)
+    _check(_L().fluid_run_schedule(g, lp, ap, launch, written, buf, need.value, None, C.byref(n)))
+    names = buf.value.decode().split("\n") if n.value else []
+    return list(launch), [bool(w) for w in written], names
 
 
 def fluid_trace_enable(g, mask, max_records):
@@ -383,6 +411,11 @@ class ArenaPlan:
         self.peak, self.naive, self.lower_bound, self.offset, self.root = fluid_arena_plan_get(
             self.h, graph.n_edges)
 
+    def lifetimes(self):
+        """{buffer edge: (bytes, producer node, last reader node)}."""
+        size, d, last = fluid_arena_plan_lifetimes(self.h, self.graph.n_edges)
+        return {e: (size[e], d[e], last[e]) for e in range(self.graph.n_edges) if d[e] >= 0}
+
     def __del__(self):
         if getattr(self, "h", None) and _lib is not None:
             _lib.fluid_arena_plan_free(self.h)
@@ -421,6 +454,11 @@ class Executor:
         epilogue, and products launched together with an earlier one, are
         not counted)."""
         return fluid_run_launches(self.graph.h, self.lplan.h, self.aplan.h)
+
+    def schedule(self):
+        """(launch index per node, output-written flag per node, kernel name
+        per launch) of one run."""
+        return fluid_run_schedule(self.graph.h, self.lplan.h, self.aplan.h, self.graph.n_nodes)
 
     def run_nodes(self, nodes, repeat=1, stream=None):
         """Launch only the kernels of ``nodes`` (in list order), ``repeat``

@@ -6,6 +6,7 @@ import pytest
 
 import synth_inputs
 from gpu_util import assert_close, forced_table, say
+from plan_check import assert_plans_match_oracle, load_json
 from oracle import execute, graph as OG, layouts
 
 pytestmark = pytest.mark.gpu
@@ -28,7 +29,7 @@ def _device_run(cfg, x, consts, table=None, flags=0, no_reuse=False, graph=None,
 
 
 @pytest.mark.parametrize("idx", [1, 2, 3])
-def test_config_planned_and_naive_match_oracle(idx):
+def test_config_planned_and_naive_match_oracle(idx, tmp_path):
     cfg = synth_inputs.config(idx)
     og = OG.build_transformer(cfg)
     x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), idx)
@@ -39,6 +40,10 @@ def test_config_planned_and_naive_match_oracle(idx):
     say(f"cfg{idx}: planned total {lp.total_ns} ns guard {lp.guard_used} peak {ap.peak} naive {ap.naive}")
     err = assert_close(out, ref, cfg["dtype"], f"cfg{idx} planned")
     say(f"cfg{idx}: planned max abs err {err:.3g}")
+    # the plans on the GPU-measured table equal the oracle planners' on it
+    t.save(str(tmp_path / "measured.json"))
+    summary = assert_plans_match_oracle(og, g, load_json(tmp_path / "measured.json"), lp)
+    say(f"cfg{idx}: plans equal the oracle's on the measured table: {summary}")
     from paper_2411_09242_amd import fluid as F
     out2, *_ = _device_run(cfg, x, consts, table=t, graph=g, flags=F.NO_DP, no_reuse=True)
     assert_close(out2, ref, cfg["dtype"], f"cfg{idx} naive")
@@ -137,3 +142,54 @@ def test_run_nodes_replays_the_run_bit_for_bit():
             ex.run_nodes([views[0]])
     with pytest.raises(F.FluidError):
         ex.run_nodes([])
+
+
+def test_run_rejects_bad_arguments_before_any_launch():
+    """fluid_run validates everything before it enqueues: an arena below the
+    plan's peak (ARENA_TOO_SMALL), a misaligned or NULL arena, a NULL or
+    misaligned constant, input or output, and plans of another graph
+    (INVALID) -- and the caller's output is untouched; a correct call then
+    still gives the planned result."""
+    import torch
+    from paper_2411_09242_amd import fluid as F
+    cfg = synth_inputs.config(1)
+    og = OG.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), 1)
+    (ref,) = execute.run_canonical(og, [x], consts)
+    g = F.Graph.transformer(cfg)
+    t = F.CostTable.measure(g, reps=2)
+    lp = F.LayoutPlan(g, t)
+    ap = F.ArenaPlan(g, lp)
+    ex = F.Executor(g, lp, ap, consts, [x])
+    s = torch.cuda.current_stream().cuda_stream
+    ex.outputs[0].fill_(float("nan"))
+    torch.cuda.synchronize()
+    args = dict(arena=ex.arena_ptr, nbytes=ap.peak, consts=list(ex._cp), inputs=list(ex._ip),
+                outputs=list(ex._op), lp=lp, ap=ap)
+
+    def run(**kw):
+        a = dict(args, **kw)
+        F.fluid_run(g.h, a["lp"].h, a["ap"].h, a["arena"], a["nbytes"], a["consts"], a["inputs"],
+                    a["outputs"], s)
+
+    other = F.Graph.transformer(synth_inputs.config(1, seq=16))
+    lp_other = F.LayoutPlan(other, F.CostTable.measure(other, reps=1))
+    bad = [
+        (dict(nbytes=ap.peak - 1), -4, "plan needs"),
+        (dict(arena=ex.arena_ptr + 16), -1, "aligned"),
+        (dict(arena=None), -1, "NULL arena"),
+        (dict(consts=[None] + args["consts"][1:]), -1, "const 0"),
+        (dict(consts=[args["consts"][0] + 4] + args["consts"][1:]), -1, "const 0"),
+        (dict(inputs=[None]), -1, "input 0"),
+        (dict(outputs=[args["outputs"][0] + 8]), -1, "output 0"),
+        (dict(lp=lp_other), -1, "another graph"),
+    ]
+    for kw, status, msg in bad:
+        with pytest.raises(F.FluidError, match=msg) as ei:
+            run(**kw)
+        assert ei.value.status == status, (kw, ei.value)
+    torch.cuda.synchronize()
+    assert torch.isnan(ex.outputs[0]).all()
+    run()
+    torch.cuda.synchronize()
+    assert_close(ex.outputs[0].float().cpu().numpy(), ref, "f32", "after rejected calls")

@@ -15,13 +15,14 @@ import pytest
 
 import synth_inputs
 from gpu_util import assert_close, say
+from plan_check import assert_plans_match_oracle, load_json
 
 pytestmark = pytest.mark.gpu
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 @pytest.mark.parametrize("idx", [4, 5])
-def test_large_config_matches_oracle_samples(idx):
+def test_large_config_matches_oracle_samples(idx, tmp_path):
     import torch
     from paper_2411_09242_amd import fluid as F
     gold = np.load(os.path.join(HERE, "golden", f"oracle_rows_cfg{idx}.npz"), allow_pickle=False)
@@ -36,8 +37,15 @@ def test_large_config_matches_oracle_samples(idx):
     say(f"cfg{idx}: plan {lp.total_ns} ns (guard {lp.guard_used}); arena {ap.peak / 2**20:.1f} MiB "
         f"(naive {ap.naive / 2**20:.1f}, lower bound {ap.lower_bound / 2**20:.1f})")
     assert ap.lower_bound <= ap.peak < ap.naive
+    # the plans on the GPU-measured table (at workload 4 with the trimmed
+    # candidate lists the measurement writes) equal the oracle planners' on it
+    from oracle import graph as OG
+    t.save(str(tmp_path / "measured.json"))
+    summary = assert_plans_match_oracle(OG.build_transformer(cfg), g, load_json(tmp_path / "measured.json"), lp)
+    say(f"cfg{idx}: plans equal the oracle's on the measured table: {summary}")
     ex = F.Executor(g, lp, ap, consts, [x])
-    del consts
+    if idx != 4:
+        del consts
     ex.arena.fill_(0xFF)
     ex.outputs[0].fill_(float("nan"))
     y = ex.run()[0]
@@ -51,18 +59,107 @@ def test_large_config_matches_oracle_samples(idx):
     if cfg["dtype"] == "f32":
         err = assert_close(got, ref, "f32", f"cfg{idx} sampled rows")
         say(f"cfg{idx}: {len(rows)} sampled rows within tolerance, max abs err {err:.3g}")
+        # the encoder's sequences are independent (attention stays inside a
+        # sequence, every other operator is per token), so the oracle of one
+        # sequence at full width gives that sequence's exact output: the
+        # first and the last sequence, every element
+        from oracle import execute, graph as OG
+        og1 = OG.build_transformer(synth_inputs.config(idx, batch=1))
+        for b in (0, cfg["batch"] - 1):
+            say(f"cfg{idx}: oracle of sequence {b}")
+            (ref_b,) = execute.run_canonical(og1, [x[b:b + 1]], consts)
+            err = assert_close(y[b:b + 1], ref_b, "f32", f"cfg{idx} sequence {b}")
+            say(f"cfg{idx}: sequence {b} ({ref_b.size} elements) within tolerance, max abs err {err:.3g}")
+        del consts
     else:
-        # bf16 through 8 layers: rounding flips compound, and two valid bf16
-        # pipelines (fp64 vs fp32 arithmetic before each rounding) already
-        # differ by rel-L2 0.017 and max |diff| 0.11 on this output, so the
-        # rel 2e-2 bound is applied norm-wise, with a gross-error cap per element
+        # bf16 through 8 layers: rounding flips compound, so no valid bf16
+        # execution meets the per-element bound everywhere.  The spread of two
+        # valid executions (the oracle with float32 instead of float64
+        # arithmetic before the same roundings) was measured on these rows
+        # by golden/make_bf16_spread.py; the device run must stay within
+        # rel-L2 2e-2 and within 1.5x that spread in max |diff|, 99th
+        # percentile |diff| and share of elements outside the per-element
+        # bound.  The single-layer test below checks every edge per element.
+        import json
+        with open(os.path.join(HERE, "golden", "bf16_spread_cfg5.json")) as f:
+            spread = json.load(f)["sampled_rows"]
+        d = np.abs(got - ref)
         rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
-        mx = float(np.abs(got - ref).max())
-        say(f"cfg{idx}: sampled rows rel-L2 {rel:.4g}, max abs err {mx:.3g}")
+        mx, p99 = float(d.max()), float(np.quantile(d, 0.99))
+        frac = float((d > 1e-2 + 2e-2 * np.abs(ref)).mean())
+        say(f"cfg{idx}: sampled rows rel-L2 {rel:.4g} (spread {spread['rel_l2']:.4g}), max abs err {mx:.3g} "
+            f"({spread['max_abs']:.3g}), p99 {p99:.3g} ({spread['p99_abs']:.3g}), outside the per-element "
+            f"bound {frac:.3f} ({spread['frac_outside_per_element_bound']:.3f})")
         assert rel <= 2e-2, rel
-        assert mx <= 0.25, mx
+        assert mx <= 1.5 * spread["max_abs"], mx
+        assert p99 <= 1.5 * spread["p99_abs"], p99
+        assert frac <= 1.5 * spread["frac_outside_per_element_bound"], frac
     # whole-output statistics (every element enters these sums)
     rtol = 1e-5 if cfg["dtype"] == "f32" else 1e-2
     assert abs(np.abs(y).mean() - float(gold["mean_abs"])) <= rtol * float(gold["mean_abs"])
     assert abs((y * y).sum() - float(gold["sumsq"])) <= rtol * float(gold["sumsq"])
     assert abs(y.mean() - float(gold["mean"])) <= 1e-3
+
+
+def test_llama_layer_full_width_every_stored_edge(tmp_path):
+    """One Llama layer at the full width of the 8-layer workload (seq 2048,
+    hidden 4096, 32 heads of 128, SwiGLU 11008, bf16), planned on a
+    GPU-measured table.  It runs once in the benchmark's arena (fusion
+    lifetimes, Greedy-by-Size) and once in a no-reuse arena, where every
+    buffer keeps its bytes to the end; both enqueue the same launches
+    (kernels, fusions), so their outputs agree bit for bit.  Every edge a
+    launch stores is then read back from the no-reuse arena through its
+    offset and permutation and compared per element with the oracle's edge
+    (atol 1e-2 + rtol 2e-2); the edges a fused launch keeps on chip have no
+    bytes to read."""
+    import torch
+    from oracle import execute, graph as OG
+    from paper_2411_09242_amd import fluid as F
+    cfg = synth_inputs.config(5, layers=1)
+    og = OG.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), 5)
+    say("llama layer full width: oracle (every edge)")
+    (ref_out,), vals = execute.run_canonical(og, [x], consts, keep=True)
+    g = F.Graph.transformer(cfg)
+    say("llama layer full width: measuring the cost table")
+    t = F.CostTable.measure(g, reps=2)
+    lp = F.LayoutPlan(g, t)
+    t.save(str(tmp_path / "measured.json"))
+    assert_plans_match_oracle(og, g, load_json(tmp_path / "measured.json"), lp)
+    ap_b = F.ArenaPlan(g, lp, epilogue=True)
+    ap_n = F.ArenaPlan(g, lp, no_reuse=True)
+    ex_b = F.Executor(g, lp, ap_b, consts, [x])
+    ex_n = F.Executor(g, lp, ap_n, consts, [x])
+    del consts
+    sched = ex_n.schedule()
+    assert sched[0] == ex_b.schedule()[0] and sched[2] == ex_b.schedule()[2]
+    launch, written, names = sched
+    say(f"llama layer full width: {len(names)} launches; arena {ap_b.peak / 2**20:.0f} MiB "
+        f"(no reuse {ap_n.peak / 2**20:.0f})")
+    for ex in (ex_b, ex_n):
+        ex.arena.fill_(0xFF)
+        ex.outputs[0].fill_(float("nan"))
+        ex.run()
+    torch.cuda.synchronize()
+    assert torch.equal(ex_b.outputs[0], ex_n.outputs[0])
+    base = ex_n.arena_ptr - ex_n.arena.data_ptr()
+    checked = 0
+    for n, nd in enumerate(og.nodes):
+        if not written[n]:
+            continue
+        e = og.out_edge(n)
+        shape = og.edge_shape(e)
+        if e in og.outputs:
+            got = ex_n.outputs[og.outputs.index(e)]
+        else:
+            perm = lp.perm(e)
+            cnt = int(np.prod(shape))
+            off = base + ap_n.offset[e]
+            raw = ex_n.arena[off: off + 2 * cnt].view(torch.bfloat16)
+            got = raw.reshape([shape[d] for d in perm]).permute(*np.argsort(perm).tolist())
+        got = got.float().cpu().numpy().astype(np.float64)
+        err = assert_close(got, vals[e], "bf16", f"node {n} {nd.op} edge {e} kernel {names[launch[n]]}")
+        say(f"  node {n:2d} {nd.op:9s} {str(shape):22s} {names[launch[n]]:40s} max abs err {err:.3g}")
+        checked += 1
+    assert checked >= 15
+    assert_close(ex_n.outputs[0].float().cpu().numpy(), ref_out, "bf16", "layer output")

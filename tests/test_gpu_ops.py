@@ -253,7 +253,7 @@ def test_grouped_products(shape, variant, chained, tmp_path):
 def chain_attn_graph(B, NH, S, T, D, causal, extra_reader=False):
     """q = gelu, k = silu, v = gelu of three inputs; O = softmax(Q K^T / 8,
     causal) V, then gelu.  With extra_reader the scores are also an output
-    (read by a second node), so the three cannot run as one launch."""
+    (read by a second node)."""
     g = Graph(dtype="f32")
     xq = g.add_input((B, NH, S, D))
     xk = g.add_input((B, NH, D, T))
@@ -269,30 +269,6 @@ def chain_attn_graph(B, NH, S, T, D, causal, extra_reader=False):
     if extra_reader:
         g.outputs.append(g.add_node("silu", [s], (B, NH, S, T)))
     return g, q, k, v, s, p, o
-
-
-@pytest.mark.parametrize("shape", [(1, 2, 37, 37, 16), (2, 3, 64, 64, 24), (1, 2, 128, 128, 64),
-                                   (1, 1, 70, 100, 128)], ids=str)
-@pytest.mark.parametrize("causal", [False, True])
-def test_small_attention_one_launch(shape, causal, tmp_path):
-    """Q K^T, softmax and P V of short fp32 sequences as one launch (with the
-    fusion lifetimes), for several layouts of Q, K^T, V and O: same result
-    as the oracle, two launches fewer."""
-    from paper_2411_09242_amd import fluid as F
-    B, NH, S, T, D = shape
-    if causal and S != T:
-        pytest.skip("causal attention is square here")
-    og, q, k, v, s, p, o = chain_attn_graph(B, NH, S, T, D, causal)
-    L4 = {e: layouts.layout_list(og.edge_shape(e)) for e in (q, k, v, o)}
-    for pick in (0, 1, 2):
-        want = {e: L[min(len(L) - 1, (pick + i) % len(L))] for i, (e, L) in enumerate(L4.items())}
-        say(f"small attention {shape} causal={causal} {want}")
-        xs, cs = random_inputs(og, pick)
-        out, lp, ap = run_device(og, forced_table(og, want), xs, cs, tmp_path, epilogue=True)
-        nonview = sum(1 for x in lp.variant if x >= 0)
-        assert F.fluid_run_launches(lp.graph.h, lp.h, ap.h) == nonview - 2
-        ref = reference_rounding_except(og, xs, cs, {s, p})
-        assert_close(out[0], ref[0], "f32", f"want={want}")
 
 
 def attn_graph(B, NH, S, D, dtype, pv=False):

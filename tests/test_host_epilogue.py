@@ -68,18 +68,23 @@ def test_grouped_launch_count(chained, variant, dtype, grouped, tmp_path):
     assert n == nonview - 3 - saved
 
 
-@pytest.mark.parametrize("T,D,extra,fused", [(128, 64, False, True), (129, 64, False, False),
-                                             (128, 132, False, False), (64, 64, True, False)])
-def test_attention_launch_count(T, D, extra, fused, tmp_path):
-    """Q K^T, softmax and P V run as one launch only for at most 128 keys and
-    a head dim of at most 128, and only when nothing else reads the scores."""
+@pytest.mark.parametrize("T,D,extra", [(128, 64, False), (40, 32, True)])
+def test_attention_runs_as_its_three_operators(T, D, extra, tmp_path):
+    """Q K^T, Softmax and P V each run their own launch (the scores and
+    probabilities are arena tensors, as in the paper's operator chain); only
+    the GELU after P V goes into that product's epilogue."""
     from test_gpu_ops import chain_attn_graph
-    og, *_ = chain_attn_graph(1, 2, 40, T, D, False, extra)
+    og, q, k, v, s, p, o = chain_attn_graph(1, 2, 40, T, D, False, extra)
     g, lp = _plan(og, forced_table(og, {}), tmp_path)
     nonview = sum(1 for n in range(g.n_nodes) if lp.kernel(n) != "view")
-    n, _ = _launches(g, lp, epilogue=True)
-    # unfused, the GELU after P V goes into that MatMul's epilogue instead
-    assert n == nonview - (2 if fused else 1)
+    n, ap = _launches(g, lp, epilogue=True)
+    assert n == nonview - 1
+    launch, written, names = F.fluid_run_schedule(g.h, lp.h, ap.h, g.n_nodes)
+    sn, pn, on = og.producer(s), og.producer(p), og.producer(o)
+    assert len({launch[sn], launch[pn], launch[on]}) == 3
+    assert written[sn] and written[pn] and not written[on]
+    assert launch[on + 1] == launch[on] and written[on + 1]
+    assert names[launch[on]].endswith("_eg") and names[launch[pn]].startswith("softmax")
 
 
 CFGS = [synth_inputs.config(1, arch="post_ln", layers=2, seq=17, hidden=40, heads=5, ffn=72),
@@ -118,3 +123,16 @@ def test_epilogue_arena_on_transformers(cfg, seed, tmp_path):
                 assert (ap.offset[x] + ref.size[x] <= ap.offset[y] or
                         ap.offset[y] + ref.size[y] <= ap.offset[x]), (x, y)
     assert ap.peak >= ap_def.lower_bound
+    # the launch schedule: every non-view node is performed by one launch;
+    # a node whose output no launch stores is read only inside its own launch
+    launch, written, names = F.fluid_run_schedule(g.h, lp.h, ap.h, g.n_nodes)
+    assert len(names) == n_epi == max(launch) + 1
+    for n, nd in enumerate(og.nodes):
+        is_view = lp.kernel(n) == "view"
+        assert (launch[n] < 0) == is_view and not (is_view and written[n])
+        e = og.out_edge(n)
+        if e in og.outputs:
+            assert written[n]
+        if launch[n] >= 0 and not written[n]:
+            readers = [m for m, md in enumerate(og.nodes) if e in md.ins]
+            assert readers and all(launch[m] == launch[n] for m in readers), (n, readers)

@@ -11,8 +11,9 @@ import pytest
 import synth_inputs
 from oracle import costtable, graph as OG, layouts, plan_arena as PA, plan_layout as PL
 from paper_2411_09242_amd import fluid as F
-from tables import synthetic_table, write_table
-from tinygraphs import chain_graph, diamond_graph, ffn_block, mlp_graph, t1_graph, t2_graph
+from plan_check import assert_plans_match_oracle
+from tables import fanout_costs, rank2_table, synthetic_table, write_table
+from tinygraphs import chain_graph, diamond_graph, fanout_graph, ffn_block, mlp_graph, t1_graph, t2_graph
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -32,7 +33,7 @@ def test_library_exports_every_declared_symbol(name):
     import ctypes
     lib = ctypes.CDLL(os.path.join(F.LIBDIR, name))
     syms = _header_symbols()
-    assert len(syms) == 24
+    assert len(syms) == 26
     for s in syms:
         assert hasattr(lib, s), s
     assert set(syms) == set(F.SYMBOLS)
@@ -132,6 +133,32 @@ def test_planner_parity_flags(flags, tmp_path):
 def test_planner_parity_config_graphs(idx, mode, tmp_path):
     og = OG.build_transformer(synth_inputs.config(idx))
     _compare_plans(og, synthetic_table(og, seed=idx, mode=mode), tmp_path)
+    # the arena the benchmark runs (fusion lifetimes, same Greedy-by-Size);
+    # preparing the fusions needs kernels that run on the chosen layouts, so
+    # this table offers variant 0 only (it exists for every layout)
+    obj = synthetic_table(og, seed=idx + 10, mode=mode, n_variants=1)
+    lp = _compare_plans(og, obj, tmp_path)
+    summary = assert_plans_match_oracle(og, lp.graph, obj, lp)
+    if idx in (2, 3, 4):
+        assert summary["extended_lifetimes"] > 0
+
+
+@pytest.mark.parametrize("infeasible", [False, True])
+@pytest.mark.parametrize("flags", [0, PL.NO_GUARD])
+def test_planner_parity_guard_branches(infeasible, flags, tmp_path):
+    """The hand-worked table on which the majority vote costs more than the
+    row-major plan (or leaves a path infeasible): both planners return the
+    row-major plan with guard_used 1, or, without the guard, the voted plan
+    (168 ns) or the same infeasibility error."""
+    og = fanout_graph()
+    lp = _compare_plans(og, rank2_table(og, fanout_costs(infeasible)), tmp_path, flags)
+    if infeasible and flags:
+        assert lp is None
+    elif flags:
+        assert (lp.guard_used, lp.total_ns, lp.layout_idx[1]) == (0, 168, 1)
+    else:
+        assert (lp.guard_used, lp.total_ns) == (1, 70)
+        assert lp.layout_idx == [0] * og.n_edges
 
 
 def test_ragged_config_parity(tmp_path):
