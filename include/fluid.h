@@ -21,9 +21,11 @@
  *    is owned by the caller; the library never allocates or frees device
  *    memory.  Arguments are validated before any HIP call.
  *  - Tensor shapes are int64 element counts, at most FLUID_MAX_RANK dims.
- *    Constants, graph inputs and graph outputs are always dense row-major.
+ *    Graph inputs and outputs are always dense row-major; constants are
+ *    dense, row-major unless the layout plan packs a weight
+ *    (fluid_constant_layout, fluid_pack_constant).
  *  - The host-only build of this library (no GPU code) exports the same
- *    symbols; there fluid_run and fluid_measure_costs return
+ *    symbols; there the entry points that touch the GPU return
  *    FLUID_E_UNSUPPORTED.
  */
 #ifndef FLUID_H
@@ -200,6 +202,26 @@ fluid_status fluid_measure_costs(const fluid_graph* g, uint32_t reps, void* scra
 fluid_status fluid_plan_layouts(const fluid_graph* g, const fluid_cost_table* t, uint32_t flags,
                                 fluid_layout_plan** out);
 
+/* Constant layouts (the weight layout is planned with the MatMul that reads
+ * it, Section 2's ahead-of-time constants with Section 3's loop reordering):
+ * MatMul variants 0..9 read their weight [K, N] row-major as supplied,
+ * variants 10..19 run the same tiles on the weight stored K-contiguous
+ * (physically [N, K]) -- offered only for a 2-D weight that no other node
+ * reads.  fluid_constant_layout writes the permutation constant c must be
+ * stored in for runs of this plan (rank entries: the identity, or {1, 0}
+ * for a packed weight).  Errors: FLUID_E_INVALID (NULL argument, plan of
+ * another graph, c out of range).  Both builds. */
+fluid_status fluid_constant_layout(const fluid_graph* g, const fluid_layout_plan* lp, int32_t c,
+                                   int32_t* perm_out);
+/* Writes constant c, given row-major at device address src, into device
+ * memory dst (caller-allocated, same byte size, 16-byte aligned, not
+ * overlapping src) in the layout fluid_constant_layout gives, enqueued on
+ * hip_stream -- once, before the runs that use this plan; fluid_run then
+ * takes dst as constant c.  No device allocation.  Errors: FLUID_E_INVALID,
+ * FLUID_E_HIP.  GPU build only. */
+fluid_status fluid_pack_constant(const fluid_graph* g, const fluid_layout_plan* lp, int32_t c, const void* src,
+                                 void* dst, void* hip_stream);
+
 /* Plan contents: layout index into L(e) per edge (n_edges), kernel variant per
  * node (n_nodes; -1 = view, no kernel), summed table cost, guard flag. */
 fluid_status fluid_layout_plan_get(const fluid_layout_plan* lp, int32_t* layout_idx_per_edge,
@@ -259,7 +281,8 @@ fluid_status fluid_arena_plan_lifetimes(const fluid_arena_plan* ap, int32_t n_ed
  * arena:
  * device memory of at least the plan's peak,
  * 256-B aligned; consts[i], inputs[i], outputs[i]: device pointers to dense
- * row-major tensors of the graph's dtype (RoPE tables fp32).  No device
+ * tensors of the graph's dtype (RoPE tables fp32), row-major except a
+ * constant the plan packs (stored as fluid_constant_layout says).  No device
  * allocation.  Errors before any launch: FLUID_E_INVALID (NULL pointer,
  * misaligned arena, plans of another graph), FLUID_E_ARENA_TOO_SMALL;
  * FLUID_E_HIP if a launch fails.  Concurrent calls on different streams

@@ -1,5 +1,5 @@
 """Build the host-only library with AddressSanitizer and UndefinedBehavior-
-Sanitizer (g++, CPU code only) into lib/san/libfluid_host.so.
+Sanitizer (g++, CPU code only) into _build/san/lib/libfluid_host.so.
 
 The CPU tests can then run against it (FLUID_LIBDIR=<that directory>, with
 the ASan runtime preloaded into the interpreter): every planner, table
@@ -21,7 +21,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build", "san")
-LIBDIR = os.path.join(PKG, "lib", "san")
+LIBDIR = os.path.join(PKG, "_build", "san", "lib")
 SANFLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer"]
 CXXFLAGS = ["-std=c++17", "-O1", "-g", "-fPIC", "-Wall", "-Wno-unused-function", f"-I{INCLUDE}"] + SANFLAGS
 

@@ -220,6 +220,27 @@ std::shared_ptr<Prepared> cached_prepared(const fluid_graph* gh, const fluid_lay
   return prep;
 }
 
+// Enqueues the launches of a prepared run.
+void run_prepared(const fluid_graph* gh, const Prepared& prep, const Bases& B, hipStream_t s) {
+  std::unique_lock<std::mutex> tl(g_trace_mu);
+  const bool tracing = g_trace.on && g_trace.graph_serial == gh->serial;
+  if (!tracing) tl.unlock();
+  for (const PreparedNode& pn : prep.nodes) {
+    if (pn.fused_away || pn.grouped) continue;  // launched with an earlier node
+    const NodeKernel k = launch_kernel(pn, B);
+    int rec = -1;
+    if (tracing && g_trace.mask[pn.node] && (int)g_trace.node_of.size() < g_trace.max_records) {
+      rec = (int)g_trace.node_of.size();
+      g_trace.node_of.push_back(pn.node);
+      hip_check(hipEventRecord(g_trace.ev[2 * rec], s), "hipEventRecord");
+    }
+    const hipError_t e = pn.group.empty() ? launch_node_kernel(k, s) : launch_group(prep, pn, k, B, s);
+    if (e != hipSuccess)
+      fail(FLUID_E_HIP, "node " + std::to_string(pn.node) + " (" + k.name() + "): " + hipGetErrorString(e));
+    if (rec >= 0) hip_check(hipEventRecord(g_trace.ev[2 * rec + 1], s), "hipEventRecord");
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -230,25 +251,44 @@ fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const
   return call_guarded([&] {
     std::shared_ptr<Prepared> prep =
         checked_prepared(gh, lh, ah, arena, arena_bytes, consts, inputs, outputs, "fluid_run");
-    Bases B{(char*)arena, inputs, outputs, consts};
+    run_prepared(gh, *prep, Bases{(char*)arena, inputs, outputs, consts}, (hipStream_t)hip_stream);
+  });
+}
+
+fluid_status fluid_pack_constant(const fluid_graph* gh, const fluid_layout_plan* lh, int32_t c, const void* src,
+                                 void* dst, void* hip_stream) {
+  return call_guarded([&] {
+    require(gh && lh && src && dst, "fluid_pack_constant: NULL argument");
+    require(lh->p.graph_serial == gh->serial, "fluid_pack_constant: plan belongs to another graph");
+    const Graph& g = gh->g;
+    require(c >= 0 && c < (int32_t)g.consts.size(), "fluid_pack_constant: constant id out of range");
+    require(aligned(src, 16) && aligned(dst, 16), "fluid_pack_constant: src and dst must be 16-byte aligned");
+    const Const& k = g.consts[c];
+    const uint64_t bytes = (uint64_t)numel(k.shape) * dtype_bytes(k.dtype);
+    const uintptr_t s0 = (uintptr_t)src, d0 = (uintptr_t)dst;
+    require(s0 + bytes <= d0 || d0 + bytes <= s0, "fluid_pack_constant: src and dst overlap");
     hipStream_t s = (hipStream_t)hip_stream;
-    std::unique_lock<std::mutex> tl(g_trace_mu);
-    const bool tracing = g_trace.on && g_trace.graph_serial == gh->serial;
-    if (!tracing) tl.unlock();
-    for (const PreparedNode& pn : prep->nodes) {
-      if (pn.fused_away || pn.grouped) continue;  // launched with an earlier node
-      const NodeKernel k = launch_kernel(pn, B);
-      int rec = -1;
-      if (tracing && g_trace.mask[pn.node] && (int)g_trace.node_of.size() < g_trace.max_records) {
-        rec = (int)g_trace.node_of.size();
-        g_trace.node_of.push_back(pn.node);
-        hip_check(hipEventRecord(g_trace.ev[2 * rec], s), "hipEventRecord");
-      }
-      const hipError_t e = pn.group.empty() ? launch_node_kernel(k, s) : launch_group(*prep, pn, k, B, s);
-      if (e != hipSuccess)
-        fail(FLUID_E_HIP, "node " + std::to_string(pn.node) + " (" + k.name() + "): " + hipGetErrorString(e));
-      if (rec >= 0) hip_check(hipEventRecord(g_trace.ev[2 * rec + 1], s), "hipEventRecord");
+    const Perm p = constant_layout(g, lh->p, c);
+    if (p == identity_perm((int)k.shape.size())) {
+      hip_check(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s), "hipMemcpyAsync");
+      return;
     }
+    // a relayout copy of the [K, N] row-major weight into K-contiguous order
+    Node nd;
+    nd.op = FLUID_OP_RESHAPE;
+    nd.out_shape = k.shape;
+    Operand in, out;
+    in.shape = out.shape = k.shape;
+    in.dtype = out.dtype = k.dtype;
+    in.stride = row_major_strides(k.shape);
+    out.stride = dense_strides(k.shape, p);
+    in.ptr = src;
+    out.ptr = dst;
+    NodeKernel kk = prepare_node(nd, 1, k.dtype, {in}, out);
+    if (!kk.available) kk = prepare_node(nd, 0, k.dtype, {in}, out);
+    require(kk.available, "fluid_pack_constant: no copy kernel for this constant (" + kk.why + ")");
+    const hipError_t e = launch_node_kernel(kk, s);
+    if (e != hipSuccess) fail(FLUID_E_HIP, std::string("fluid_pack_constant: ") + hipGetErrorString(e));
   });
 }
 
@@ -385,6 +425,15 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
       const int eo = g.out_edge(n);
       if (t.L[eo].size() > out_lists[si].size()) out_lists[si] = t.L[eo];
     }
+    // packed-weight MatMul variants: only where every node of the
+    // signature reads a weight that no other node reads
+    std::vector<char> packable(rep_node.size(), 1);
+    for (int n = 0; n < g.n_nodes(); ++n) {
+      const Node& nd = g.nodes[n];
+      if (nd.op != FLUID_OP_MATMUL || nd.ins.size() != 2 || nd.ins[1] >= 0 ||
+          g.const_readers[~nd.ins[1]].size() != 1)
+        packable[t.node_sig[n]] = 0;
+    }
     hipEvent_t ev[2 * 64];
     const uint32_t R = std::min<uint32_t>(reps, 64);
     for (auto& e : ev) hip_check(hipEventCreate(&e), "hipEventCreate");
@@ -439,7 +488,11 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
           ou.dtype = g.dtype;
           ou.ptr = base + off;
           for (int v = 0; v < num_variants(nd.op); ++v) {
-            NodeKernel k = prepare_node(nd, v, g.dtype, ins, ou);
+            if (packs_weight(nd.op, v) && !packable[si]) { en.costs.push_back(-1); continue; }
+            std::vector<Operand> vins = ins;
+            for (size_t s2 = 0; s2 < nd.ins.size(); ++s2)
+              if (nd.ins[s2] < 0) vins[s2].stride = const_strides(nd, (int)s2, v, vins[s2].shape);
+            NodeKernel k = prepare_node(nd, v, g.dtype, vins, ou);
             if (!k.available) { en.costs.push_back(-1); continue; }
             // an untimed warm-up launch (the first launch of a kernel
             // instance also loads its code, which can take milliseconds),

@@ -274,6 +274,16 @@ fluid_status fluid_run_schedule(const fluid_graph* gh, const fluid_layout_plan* 
   });
 }
 
+fluid_status fluid_constant_layout(const fluid_graph* gh, const fluid_layout_plan* lh, int32_t c, int32_t* perm_out) {
+  return call_guarded([&] {
+    require(gh && lh && perm_out, "fluid_constant_layout: NULL argument");
+    require(lh->p.graph_serial == gh->serial, "plan belongs to another graph");
+    require(c >= 0 && c < (int32_t)gh->g.consts.size(), "constant id out of range");
+    const Perm p = constant_layout(gh->g, lh->p, c);
+    for (size_t i = 0; i < p.size(); ++i) perm_out[i] = p[i];
+  });
+}
+
 fluid_status fluid_arena_plan_lifetimes(const fluid_arena_plan* ap, int32_t n_edges, uint64_t* size,
                                         int32_t* def, int32_t* last) {
   return call_guarded([&] {
@@ -300,10 +310,12 @@ fluid_status fluid_node_kernel(const fluid_graph* gh, const fluid_layout_plan* l
     if (lh->p.variant[node] >= 0) {
       const Node& nd = g.nodes[node];
       std::vector<Operand> ins;
-      for (int v : nd.ins) {
+      for (size_t slot = 0; slot < nd.ins.size(); ++slot) {
+        const int v = nd.ins[slot];
         Operand o;
         o.shape = v >= 0 ? g.edge_shape(v) : g.consts[~v].shape;
-        o.stride = v >= 0 ? dense_strides(o.shape, lh->p.perm[v]) : row_major_strides(o.shape);
+        o.stride = v >= 0 ? dense_strides(o.shape, lh->p.perm[v])
+                          : const_strides(nd, (int)slot, lh->p.variant[node], o.shape);
         o.dtype = v >= 0 ? g.dtype : g.consts[~v].dtype;
         ins.push_back(o);
       }

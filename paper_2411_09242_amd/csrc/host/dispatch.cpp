@@ -22,7 +22,7 @@ std::vector<int64_t> row_major_strides(const Shape& s) {
 
 int num_variants(int op) {
   switch (op) {
-    case FLUID_OP_MATMUL: return 10;
+    case FLUID_OP_MATMUL: return 2 * kGemmTiles;
     case FLUID_OP_GELU:
     case FLUID_OP_SILU:
     case FLUID_OP_TRANSPOSE:
@@ -32,6 +32,11 @@ int num_variants(int op) {
     case FLUID_OP_RMSNORM: return 2;
     default: return 1;
   }
+}
+
+std::vector<int64_t> const_strides(const Node& nd, int slot, int variant, const Shape& shape) {
+  if (packs_weight(nd.op, variant) && slot == 1 && shape.size() == 2) return {1, shape[0]};
+  return row_major_strides(shape);
 }
 
 namespace {
@@ -285,6 +290,11 @@ NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector
 
 NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
   NodeKernel k;
+  if (packs_weight(nd.op, variant) && (nd.ins.size() != 2 || nd.ins[1] >= 0 || ins[1].shape.size() != 2)) {
+    k.why = "a packed-weight variant needs a 2-D constant B operand";
+    return k;
+  }
+  const int tile = gemm_tile_of(variant);
   k.family = KF_GEMM;
   k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
   const Operand& A = ins[0];
@@ -385,7 +395,7 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   const int64_t sa = span_bytes(A), sb = span_bytes(B);
   p.a_bytes = (uint32_t)std::min<int64_t>(sa, 0x7fffffff);
   p.b_bytes = (uint32_t)std::min<int64_t>(sb, 0x7fffffff);
-  k.gemm_tile = variant;
+  k.gemm_tile = tile;
   // tile sizes: 0: 128x128, 1: 64x64 (LDS-staged); 2, 3: 32x32 and 4: 64x32
   // with the K range split over the workgroup's wavefronts
   // bf16 6: 256x128 and 7: 128x128, loads two or more K-tiles ahead, 8:
@@ -395,19 +405,19 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   // loaded straight into MFMA registers
   static const uint32_t TM[] = {128, 64, 32, 32, 64, 32, 256, 128, 256, 128};
   static const uint32_t TN[] = {128, 64, 32, 32, 32, 32, 128, 128, 128, 128};
-  uint32_t tm = TM[variant], tn = TN[variant];
-  if (variant >= 8 && (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_K && k.bmode != GM_MN))) {
+  uint32_t tm = TM[tile], tn = TN[tile];
+  if (tile >= 8 && (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_K && k.bmode != GM_MN))) {
     k.available = false;
     k.why = "tiles 8 and 9 are bf16 with a K-contiguous A and a K- or N-contiguous B";
     return k;
   }
-  if (variant == 9 && p.K > 128) {
+  if (tile == 9 && p.K > 128) {
     k.available = false;
     k.why = "tile 9 holds the whole K (at most 128) in LDS";
     return k;
   }
-  if (variant >= 6 && k.dtype != DT_BF16) {
-    tm = variant == 6 ? 16 : 32;
+  if (tile >= 6 && k.dtype != DT_BF16) {
+    tm = tile == 6 ? 16 : 32;
     tn = 32;
     if ((k.amode != GM_K && k.amode != GM_MN) || (k.bmode != GM_K && k.bmode != GM_MN)) {
       k.available = false;
@@ -415,7 +425,7 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
       return k;
     }
   }
-  if (variant >= 6 && (sa >= 0x7fffffff || sb >= 0x7fffffff)) {
+  if (tile >= 6 && (sa >= 0x7fffffff || sb >= 0x7fffffff)) {
     k.available = false;
     k.why = "buffer-load tiles address at most 2 GiB per operand";
     return k;
@@ -439,6 +449,7 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
 // reads drops from three to two workgroups per SIMD); on the 64 x 64, the
 // split-K and the fp32 direct-load tiles every step is faster fused.
 int gemm_epilogue_caps(int variant, int dtype) {
+  variant = gemm_tile_of(variant);
   const bool bf16 = dtype == FLUID_BF16;
   if (variant == 9 || (bf16 && (variant == 6 || variant == 8))) return EPI_BIAS;
   const bool rop = (variant >= 1 && variant <= 5) || (!bf16 && variant >= 6);

@@ -53,6 +53,18 @@ struct NodeKernel {
 };
 
 int num_variants(int op);
+// MatMul variants come in two halves: tile t (0 .. kGemmTiles-1) with the
+// weight (a constant B operand [K, N]) stored row-major, and variant
+// kGemmTiles + t, the same tile with the weight stored K-contiguous
+// (physically [N, K]).  A weight is read by one MatMul, so its layout is a
+// choice local to that node, made with the node's kernel: the cost table's
+// minimum over variants picks the weight layout too.
+constexpr int kGemmTiles = 10;
+inline int gemm_tile_of(int variant) { return variant % kGemmTiles; }
+inline bool packs_weight(int op, int variant) { return op == FLUID_OP_MATMUL && variant >= kGemmTiles; }
+// Element strides of constant operand `slot` (shape `shape`) of node nd
+// under `variant`: row-major, or K-contiguous for a packed weight.
+std::vector<int64_t> const_strides(const Node& nd, int slot, int variant, const Shape& shape);
 // Epilogue steps the kernels of MatMul variant `variant` perform after the
 // product for a graph of dtype `dtype` (GemmParams): bit 0 bias, bit 1
 // activation, bit 2 the Add / Mul with another tensor.

@@ -195,6 +195,10 @@ void Graph::finalize() {
   for (size_t n = 0; n < nodes.size(); ++n)
     for (int e : act_in[n])
       if (readers[e].empty() || readers[e].back() != (int)n) readers[e].push_back((int)n);
+  const_readers.assign(consts.size(), {});
+  for (size_t n = 0; n < nodes.size(); ++n)
+    for (int v : nodes[n].ins)
+      if (v < 0 && (const_readers[~v].empty() || const_readers[~v].back() != (int)n)) const_readers[~v].push_back((int)n);
   cand.assign(E, {});
   for (int e = 0; e < E; ++e)
     cand[e] = pinned(e) ? std::vector<Perm>{identity_perm((int)edge_shape(e).size())} : layout_list(edge_shape(e));

@@ -44,6 +44,7 @@ struct Graph {
   // derived (filled by finalize)
   std::vector<std::vector<int>> act_in;   // per node: activation input edges, slot order
   std::vector<std::vector<int>> readers;  // per edge: nodes reading it (ascending, unique)
+  std::vector<std::vector<int>> const_readers;  // per constant: nodes reading it (ascending, unique)
   std::vector<char> is_output;            // per edge
   std::vector<std::vector<Perm>> cand;    // per edge: candidate layouts L(e)
 

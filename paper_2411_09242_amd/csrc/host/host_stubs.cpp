@@ -19,6 +19,10 @@ fluid_status fluid_run(const fluid_graph*, const fluid_layout_plan*, const fluid
   return unsupported("fluid_run");
 }
 
+fluid_status fluid_pack_constant(const fluid_graph*, const fluid_layout_plan*, int32_t, const void*, void*, void*) {
+  return unsupported("fluid_pack_constant");
+}
+
 fluid_status fluid_run_nodes(const fluid_graph*, const fluid_layout_plan*, const fluid_arena_plan*, void*, uint64_t,
                              const void* const*, const void* const*, void* const*, const int32_t*, int32_t, int32_t,
                              void*) {

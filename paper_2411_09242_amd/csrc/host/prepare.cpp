@@ -202,7 +202,12 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
     PreparedNode pn;
     pn.node = n;
     std::vector<Operand> ins;
-    for (int v : nd.ins) {
+    if (packs_weight(nd.op, lp.variant[n]) && nd.ins.size() == 2 && nd.ins[1] < 0 &&
+        g.const_readers[~nd.ins[1]].size() != 1)
+      fail(FLUID_E_INVALID, "node " + std::to_string(n) + ": a packed-weight variant needs a weight read by this "
+                                                          "node only");
+    for (size_t slot = 0; slot < nd.ins.size(); ++slot) {
+      const int v = nd.ins[slot];
       Operand o;
       Bind b;
       if (v >= 0) {
@@ -214,7 +219,7 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
         b.kind = BK_CONST;
         b.index = ~v;
         o.shape = g.consts[~v].shape;
-        o.stride = row_major_strides(o.shape);
+        o.stride = const_strides(nd, (int)slot, lp.variant[n], o.shape);
         o.dtype = g.consts[~v].dtype;
       }
       o.ptr = fake_ptr(b);
@@ -253,6 +258,15 @@ std::vector<int> epilogue_reads_until(const Graph& g, const LayoutPlan& lp) {
   for (size_t i = 0; i < P->nodes.size(); ++i)
     if (P->nodes[i].fuse_n > 0) until[P->nodes[i].node] = P->nodes[i + P->nodes[i].fuse_n].node;
   return until;
+}
+
+Perm constant_layout(const Graph& g, const LayoutPlan& lp, int c) {
+  const auto& rd = g.const_readers[c];
+  if (rd.size() == 1) {
+    const Node& nd = g.nodes[rd[0]];
+    if (packs_weight(nd.op, lp.variant[rd[0]]) && nd.ins.size() == 2 && nd.ins[1] == ~c) return {1, 0};
+  }
+  return identity_perm((int)g.consts[c].shape.size());
 }
 
 int prepared_launches(const Prepared& P) {

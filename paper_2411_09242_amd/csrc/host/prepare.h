@@ -64,6 +64,11 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
 // done with its operands once it has written that node's output.
 std::vector<int> epilogue_reads_until(const Graph& g, const LayoutPlan& lp);
 
+// The layout constant c must be stored in for a run of this plan: the
+// identity (row-major as supplied), or (1, 0) -- K-contiguous -- for a
+// weight whose one reader runs a packed-weight MatMul variant.
+Perm constant_layout(const Graph& g, const LayoutPlan& lp, int c);
+
 // Kernel launches of a prepared run.
 int prepared_launches(const Prepared& P);
 

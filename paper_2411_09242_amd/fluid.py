@@ -86,6 +86,8 @@ _PROTOS = {
                                              C.POINTER(C.c_int32)]),
     "fluid_run": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
                             C.POINTER(_VP), _VP]),
+    "fluid_constant_layout": (C.c_int, [_VP, _VP, C.c_int32, C.POINTER(C.c_int32)]),
+    "fluid_pack_constant": (C.c_int, [_VP, _VP, C.c_int32, _VP, _VP, _VP]),
     "fluid_run_nodes": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
                                   C.POINTER(_VP), C.POINTER(C.c_int32), C.c_int32, C.c_int32, _VP]),
     "fluid_run_launches": (C.c_int, [_VP, _VP, _VP, C.POINTER(C.c_int32)]),
@@ -279,6 +281,16 @@ def fluid_run(g, lp, ap, arena_ptr, arena_bytes, const_ptrs, input_ptrs, output_
                           _ptr_array(input_ptrs), _ptr_array(output_ptrs), stream))
 
 
+def fluid_constant_layout(g, lp, c, rank):
+    p = (C.c_int32 * max(rank, 1))()
+    _check(_L().fluid_constant_layout(g, lp, c, p))
+    return tuple(p[:rank])
+
+
+def fluid_pack_constant(g, lp, c, src_ptr, dst_ptr, stream):
+    _check(_L().fluid_pack_constant(g, lp, c, src_ptr, dst_ptr, stream))
+
+
 def fluid_run_nodes(g, lp, ap, arena_ptr, arena_bytes, const_ptrs, input_ptrs, output_ptrs, nodes, repeat,
                     stream):
     arr = (C.c_int32 * len(nodes))(*nodes)
@@ -397,6 +409,10 @@ class LayoutPlan:
     def kernel(self, n):
         return fluid_node_kernel(self.graph.h, self.h, n)
 
+    def constant_layout(self, c):
+        """The permutation constant c is stored in for runs of this plan."""
+        return fluid_constant_layout(self.graph.h, self.h, c, len(self.graph.desc["consts"][c]["shape"]))
+
     def __del__(self):
         if getattr(self, "h", None) and _lib is not None:
             _lib.fluid_layout_plan_free(self.h)
@@ -434,6 +450,16 @@ class Executor:
         for c, a in zip(graph.desc["consts"], consts):
             cdt = torch.bfloat16 if c["dtype"] == "bf16" else torch.float32
             self.consts.append(torch.as_tensor(a).to(device=device, dtype=cdt).contiguous())
+        # weights the plan packs (fluid_constant_layout) are rewritten once,
+        # by the library, into buffers of their own
+        s = torch.cuda.current_stream().cuda_stream
+        for c, t in enumerate(self.consts):
+            perm = lplan.constant_layout(c)
+            if perm != tuple(range(len(perm))):
+                packed = torch.empty_like(t)
+                fluid_pack_constant(graph.h, lplan.h, c, t.data_ptr(), packed.data_ptr(), s)
+                self.consts[c] = packed
+        torch.cuda.synchronize()
         self.inputs = [torch.as_tensor(a).to(device=device, dtype=dt).contiguous() for a in inputs]
         self.outputs = [torch.empty(graph.edge_shape(e), dtype=dt, device=device)
                         for e in graph.desc["outputs"]]

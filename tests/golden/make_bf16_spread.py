@@ -9,7 +9,12 @@ the layers.  The statistics are taken on the rows that
 oracle_rows_cfg5.npz samples (the rows the GPU test compares) and on the
 whole output, and written to bf16_spread_cfg5.json.
 
-Usage: python tests/golden/make_bf16_spread.py
+With --one-layer, the same comparison on every edge of one layer at the
+workload's full width (bf16_spread_cfg5_layer.json): the spread the GPU test
+of that layer allows when it compares each stored edge with the oracle's
+own edge (rather than with the oracle applied to the device's inputs).
+
+Usage: python tests/golden/make_bf16_spread.py [--one-layer]
 """
 import json
 import os
@@ -65,5 +70,32 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def one_layer():
+    idx = 5
+    cfg = synth_inputs.config(idx, layers=1)
+    og = graph.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), idx)
+    _, v64 = execute.run_canonical(og, [x], consts, keep=True)
+    _, v32 = execute.run_canonical(og, [x], consts, keep=True, arith=np.float32)
+    edges = {}
+    for n, nd in enumerate(og.nodes):
+        e = og.out_edge(n)
+        if nd.op in ("transpose", "reshape"):
+            continue
+        edges[str(e)] = dict(stats(v32[e], v64[e]), node=n, op=nd.op)
+    out = {"workload": cfg["name"], "layers": 1,
+           "what": "per edge: oracle with float32 arithmetic before each bfloat16 rounding vs the float64 "
+                   "oracle, each on its own inputs",
+           "edges": edges}
+    path = os.path.join(HERE, f"bf16_spread_cfg{idx}_layer.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out), flush=True)
+
+
 if __name__ == "__main__":
-    main()
+    if "--one-layer" in sys.argv[1:]:
+        one_layer()
+    else:
+        main()

@@ -19,15 +19,16 @@ pytestmark = pytest.mark.gpu
 
 
 def _check_gemm(og, want, variants, tmp_path, seed, dtype):
-    """_check for a forced GEMM variant; the fp32 direct-load variants (6, 7)
-    need unit-stride K or M/N operands, and variants 8 and 9 (bf16 only) a
+    """_check for a forced GEMM variant (tile = variant % 10; variants 10-19
+    read the weight packed K-contiguous); the fp32 direct-load tiles (6, 7)
+    need unit-stride K or M/N operands, and tiles 8 and 9 (bf16 only) a
     K-contiguous A and a K- or N-contiguous B (9 also K <= 128): they are
     skipped where they cannot run."""
     try:
         return _check(og, want, variants, tmp_path, seed=seed)
     except Exception as ex:  # noqa: BLE001
-        v = max(variants.values())
-        if (v >= 8 or (dtype == "f32" and v >= 6)) and "cannot run with these layouts" in str(ex):
+        t = max(variants.values()) % 10
+        if (t >= 8 or (dtype == "f32" and t >= 6)) and "cannot run with these layouts" in str(ex):
             return None
         raise
 
@@ -60,8 +61,10 @@ PROJ_SHAPES = [(1, 37, 29, 53), (1, 130, 64, 70), (2, 65, 96, 40), (1, 256, 128,
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("shape", PROJ_SHAPES, ids=str)
-@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5, 6, 7, 8, 9])
+@pytest.mark.parametrize("variant", list(range(20)))
 def test_projection_gemm_all_layouts(dtype, shape, variant, tmp_path):
+    """Every tile, with the weight row-major (variants 0-9) and packed
+    K-contiguous by fluid_pack_constant (10-19), for every layout of A and C."""
     B, S, K, N = shape
     og, a, c = proj_graph(B, S, K, N, dtype)
     mm = 1
@@ -69,7 +72,23 @@ def test_projection_gemm_all_layouts(dtype, shape, variant, tmp_path):
     Lc = layouts.layout_list((B, S, N))
     for pa, pc in itertools.product(La, Lc):
         say(f"gemm proj {dtype} {shape} v{variant} A{pa} C{pc}")
-        _check_gemm(og, {a: pa, c: pc}, {mm: variant}, tmp_path, B * S + K, dtype)
+        lp = _check_gemm(og, {a: pa, c: pc}, {mm: variant}, tmp_path, B * S + K, dtype)
+        if lp is not None:
+            assert lp.constant_layout(0) == ((1, 0) if variant >= 10 else (0, 1))
+
+
+@pytest.mark.parametrize("shape", [(1, 37, 1000, 70), (2, 65, 3100, 40)], ids=str)
+@pytest.mark.parametrize("variant", [6, 7, 16, 17])
+def test_projection_gemm_long_k(shape, variant, tmp_path):
+    """The fp32 direct-load tiles on K slices of more than six 16-k groups
+    (the rotating K loop), group counts not divisible by 4 and K not
+    divisible by 16, with A in every layout and the weight row-major (6, 7)
+    or K-contiguous (16, 17)."""
+    B, S, K, N = shape
+    og, a, c = proj_graph(B, S, K, N, "f32")
+    for pa, pc in itertools.product(layouts.layout_list((B, S, K)), layouts.layout_list((B, S, N))[:2]):
+        say(f"gemm long K {shape} v{variant} A{pa} C{pc}")
+        _check_gemm(og, {a: pa, c: pc}, {1: variant}, tmp_path, B * S + K, "f32")
 
 
 # epilogue chains after the MatMul: Add of a bias [N], GELU, SiLU, and the
