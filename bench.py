@@ -1,18 +1,22 @@
 """Benchmark: planned graph latency on one MI355X.
 
 One step = one fluid_run of the whole layout-planned, arena-planned
-transformer graph (every operator of the chain, one kernel per non-view
-node) over one batch of synthetic input already resident in HBM.
+transformer graph (every operator of the chain: one launch per non-view
+node, except the nodes a MatMul performs in its epilogue and the products
+launched together) over one batch of synthetic input already resident in
+HBM.
 
-Default workload: the 12-layer BERT-base-shaped post-LN encoder, fp32,
-batch 1, seq 128, hidden 768, 12 heads, FFN 3072 (seed 2).  The cost table
-is measured on the GPU first (untimed), then the layout plan and the
-Greedy-by-Size arena are computed, then W warm-up and K timed steps run.
-The same K steps are timed for the naive plan (row-major layouts, every
-transpose materialised, one arena slice per tensor) for comparison.
+Default workload: the 24-layer BERT-large-shaped post-LN encoder, fp32,
+batch 8, seq 512, hidden 1024, 16 heads, FFN 4096 (seed 4) -- the largest
+fp32 workload.  The cost table is measured on the GPU first (untimed), then
+the layout plan and the Greedy-by-Size arena are computed, then W warm-up
+and K timed steps run.  The same K steps are timed for the naive plan
+(row-major layouts, every transpose materialised, one arena slice per
+tensor) for comparison.  The other workloads (BERT-base, GPT-2-small
+prefill, Llama prefill in bf16) are reported under extra_workloads.
 
 Prints one JSON line.  Usage:
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4] [--extra 2,3,5]
 """
 from __future__ import annotations
 
@@ -30,42 +34,15 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 
-# HBM bytes per launch of each workload's dominant kernel: two rocprofv3
-# --pmc passes (FETCH_SIZE, then WRITE_SIZE) over that kernel, each scaled by
-# what the same counter read for the 256 MiB calibration copy (FETCH_SIZE
-# 0.5001x, WRITE_SIZE 1.0000x).  Reported as `traffic` only for the same
-# (workload, kernel, output shape, input shapes) and only while the kernel
-# sources hash to TRAFFIC_SRC -- a changed kernel makes the figure stale, and
-# then null.
-TRAFFIC_SRC = "5890e0af5d8eb817"
-TRAFFIC = {
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6103347,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14359978,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6098204,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 128, 3072), ((1, 128, 768), ('c', 768, 3072))): 14354870,
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_sk32w8_ak_bmn_cm', (1, 128, 768), ((1, 128, 768), ('c', 768, 768))): 6108453,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_ak_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16718967,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16713855,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_ak_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28509395,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl16x32w8_amn_bmn_cm', (1, 512, 768), ((1, 512, 768), ('c', 768, 768))): 16730251,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28474615,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28482827,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_amn_bmn_cn', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28494143,
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_t64_amn_bmn_cm', (1, 512, 3072), ((1, 512, 768), ('c', 768, 3072))): 28391682,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238686516,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155464256,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_ak_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237667233,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 570642804,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 238606915,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cn', (8, 512, 4096), ((8, 512, 1024), ('c', 1024, 4096))): 237719346,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cg', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 205340487,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_ak_bmn_cn', (8, 512, 1024), ((8, 512, 1024), ('c', 1024, 1024))): 155490764,
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t64_amn_bmn_cm', (8, 512, 1024), ((8, 512, 4096), ('c', 4096, 1024))): 596381872,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 4096), ((1, 2048, 4096), ('c', 4096, 4096))): 185076732,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 913793811,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cm', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894194637,
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn', (1, 2048, 11008), ((1, 2048, 4096), ('c', 4096, 11008))): 894587397,
-}
+# HBM bytes per launch of each workload's dominant launch: two rocprofv3
+# --pmc passes (FETCH_SIZE, then WRITE_SIZE) over `bench.py --kernel-only`
+# (that launch alone, planned from the saved cost tables), each scaled by
+# what the same counter read for the 256 MiB calibration copy.  Keyed by
+# (workload, launch name, node signatures); reported as `traffic` only while
+# the kernel sources hash to TRAFFIC_SRC -- a changed kernel makes the figure
+# stale, and then null.
+TRAFFIC_SRC = ""
+TRAFFIC = {}
 
 
 def kernel_source_hash():
@@ -136,6 +113,40 @@ def node_work(g, n):
     return "bytes", float(b)
 
 
+def node_sig(g, n):
+    """(op, output shape, input shapes) of node n; constants as ('c', ...)."""
+    nd = g.desc["nodes"][n]
+    return (nd["op"], tuple(nd["out_shape"]),
+            tuple(tuple(g.edge_shape(v)) if v >= 0 else ("c",) + tuple(g.desc["consts"][~v]["shape"])
+                  for v in nd["ins"]))
+
+
+def launch_units(g, ex):
+    """The launches one fluid_run enqueues, in order: per launch its kernel
+    name (with the fused epilogue steps and the group size), the nodes it
+    performs (node order) and its algorithmic work -- the flops of its
+    products for a GEMM launch (grouped products summed; a fused bias or
+    activation adds no flops), else the bytes of its one node."""
+    launch, _, names = ex.schedule()
+    units = [{"name": nm, "nodes": []} for nm in names]
+    for n, l in enumerate(launch):
+        if l >= 0:
+            units[l]["nodes"].append(n)
+    for i, u in enumerate(units):
+        mm = [n for n in u["nodes"] if g.desc["nodes"][n]["op"] == "matmul"]
+        if mm:
+            u["op"], u["kind"] = "matmul", "flop"
+            u["work"] = sum(node_work(g, n)[1] for n in mm)
+        else:
+            assert len(u["nodes"]) == 1, u
+            n = u["nodes"][0]
+            u["op"] = g.desc["nodes"][n]["op"]
+            u["kind"], u["work"] = node_work(g, n)
+        u["index"] = i
+        u["sig"] = (u["name"],) + tuple(node_sig(g, n) for n in u["nodes"])
+    return units
+
+
 def time_steps(ex, steps, stream, torch):
     """K eager steps, an event after each: (mean ms, [per-step ms])."""
     torch.cuda.synchronize()
@@ -149,11 +160,14 @@ def time_steps(ex, steps, stream, torch):
     return ev[0].elapsed_time(ev[-1]) / steps, per
 
 
-def time_nodes(ex, nodes, repeat, torch, marker=None):
-    """ms per pass of the given nodes' kernels launched back to back:
-    `repeat` passes captured in one HIP graph (so that host launch cost does
-    not pace small kernels), one warm-up replay, then one replay between two
-    events on the replay stream."""
+def time_units(ex, units, repeat, torch, marker=None):
+    """ms per pass of the given launches issued back to back exactly as
+    fluid_run issues them (fluid_run_nodes over their nodes, so that fused
+    epilogues and grouped products run as one launch): `repeat` passes
+    captured in one HIP graph (so that host launch cost does not pace small
+    kernels), one warm-up replay, then one replay between two events on the
+    replay stream."""
+    nodes = [n for u in units for n in u["nodes"]]
     g = torch.cuda.CUDAGraph()
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
@@ -178,25 +192,25 @@ def time_nodes(ex, nodes, repeat, torch, marker=None):
     return e0.elapsed_time(e1) / repeat
 
 
-def op_class_rates(F, g, lp, ex, steps, torch):
-    """Per operator class: ms per step of its launches back to back (one
-    HIP graph), and the rate against the class's bound."""
+def op_class_rates(g, units, ex, steps, torch):
+    """Per operator class (the operator of a launch's first node; a GEMM
+    launch with a fused epilogue counts as matmul): ms per step of its
+    launches back to back (one HIP graph) and the rate against the class's
+    bound.  Nodes performed inside another launch are not counted again."""
     by_op = {}
-    for n in range(g.n_nodes):
-        if lp.variant[n] >= 0:
-            by_op.setdefault(g.desc["nodes"][n]["op"], []).append(n)
+    for u in units:
+        by_op.setdefault(u["op"], []).append(u)
     out = {}
-    for op, nodes in by_op.items():
-        ms_c = time_nodes(ex, nodes, max(3, min(steps, 20)), torch)
-        kind = node_work(g, nodes[0])[0]
-        work = sum(node_work(g, n)[1] for n in nodes)
-        if kind == "flop":
+    for op, us in by_op.items():
+        ms_c = time_units(ex, us, max(3, min(steps, 20)), torch)
+        work = sum(u["work"] for u in us)
+        if us[0]["kind"] == "flop":
             rate = work / (ms_c * 1e-3) / 1e12
             peak, unit = PEAK_TFLOPS[g.dtype], "TFLOP/s"
         else:
             rate = work / (ms_c * 1e-3) / 1e9
             peak, unit = PEAK_HBM_GBS, "GB/s"
-        out[op] = {"ms_per_step": round(ms_c, 4), "launches_per_step": len(nodes),
+        out[op] = {"ms_per_step": round(ms_c, 4), "launches_per_step": len(us),
                    "achieved": round(rate, 2), "unit": unit, "frac": round(rate / peak, 4)}
     return dict(sorted(out.items(), key=lambda kv: -kv[1]["ms_per_step"]))
 
@@ -238,7 +252,8 @@ def ablation(F, g, table, ex, steps, torch):
         out[name] = {"ms_per_step": round(graph_ms(ex_a, steps, torch), 4), "table_ns": lp_a.total_ns,
                      "launches_per_step": ex_a.launches(),
                      "peak_arena_mb": round(ap_a.peak / 2**20, 3),
-                     "op_ms": {op: c["ms_per_step"] for op, c in op_class_rates(F, g, lp_a, ex_a, steps, torch).items()}}
+                     "op_ms": {op: c["ms_per_step"]
+                               for op, c in op_class_rates(g, launch_units(g, ex_a), ex_a, steps, torch).items()}}
         del ex_a
         torch.cuda.empty_cache()
     return out
@@ -259,8 +274,12 @@ def calibration_copy(torch, mib=256):
     torch.cuda.empty_cache()
 
 
-def cpu_baseline(cfg, budget_s=20.0):
-    """Oracle (plain NumPy, float64) on the same workload, on the host."""
+def cpu_baseline(cfg, budget_s=20.0, seed=4):
+    """The oracle (plain NumPy, float64, as it stands) on the host, on a
+    bounded sample of the workload: for the large workloads the graph of the
+    first two layers at full batch and sequence (the layers are identical, so
+    a step costs layers / 2 times as much), else the whole graph; median of
+    the runs that fit in the budget (at least one), scaled to one step."""
     import synth_inputs
     from oracle import execute, graph as OG
     try:
@@ -268,8 +287,10 @@ def cpu_baseline(cfg, budget_s=20.0):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # noqa: BLE001
         threads = len(os.sched_getaffinity(0))
-    og = OG.build_transformer(cfg)
-    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), 2)
+    big = cfg["batch"] * cfg["seq"] * cfg["hidden"] >= 2 ** 21
+    k = 2 if big and cfg["layers"] > 2 else cfg["layers"]
+    og = OG.build_transformer(dict(cfg, layers=k))
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), seed)
     times = []
     t_start = time.time()
     while True:
@@ -278,9 +299,31 @@ def cpu_baseline(cfg, budget_s=20.0):
         times.append(time.time() - t)
         if time.time() - t_start > budget_s or len(times) >= 5:
             break
-    return {"value": round(1000.0 * float(np.median(times)), 3), "unit": "ms", "cores": int(threads),
+    scale = cfg["layers"] / k
+    what = (f"first {k} of {cfg['layers']} layers at full batch and sequence, x{scale:g}" if k < cfg["layers"]
+            else f"whole {cfg['layers']}-layer graph")
+    return {"value": round(1000.0 * float(np.median(times)) * scale, 3), "unit": "ms", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"whole {cfg['layers']}-layer graph, {len(times)} run(s), median; float64 NumPy"}
+            "sample": f"{what}; {len(times)} run(s), median {1000.0 * float(np.median(times)):.1f} ms per run; "
+                      f"float64 NumPy"}
+
+
+def row_major_weights(F, g, table):
+    """The same cost table without the packed-weight MatMul variants
+    (10-19): the naive plan keeps every weight row-major as supplied."""
+    import tempfile
+    with tempfile.TemporaryDirectory() as d:
+        p = os.path.join(d, "t.json")
+        table.save(p)
+        with open(p) as f:
+            obj = json.load(f)
+        for sig in obj["sigs"]:
+            if sig["op"] == "matmul":
+                for ent in sig["entries"]:
+                    ent[2] = [c if v < 10 else -1 for v, c in enumerate(ent[2])]
+        with open(p, "w") as f:
+            json.dump(obj, f)
+        return F.CostTable.load(p, g)
 
 
 def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=None, tables=None,
@@ -314,7 +357,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     # reported beside it
     apl = F.ArenaPlan(g, lp, epilogue=True)
     apl_paper = F.ArenaPlan(g, lp)
-    lp_naive = F.LayoutPlan(g, table, F.NO_DP)
+    lp_naive = F.LayoutPlan(g, row_major_weights(F, g, table), F.NO_DP)
     ap_naive = F.ArenaPlan(g, lp_naive, no_reuse=True)
     ex = F.Executor(g, lp, apl, consts, [x])
     ex_naive = F.Executor(g, lp_naive, ap_naive, consts, [x])
@@ -329,29 +372,26 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         ex.run(stream)
         ex_naive.run(stream)
     torch.cuda.synchronize()
-    launched = [n for n in range(g.n_nodes) if lp.variant[n] >= 0]    # fluid_run's launch order
+    units = launch_units(g, ex)
     by_sig = {}
-    for n in launched:
-        nd = g.desc["nodes"][n]
-        key = (lp.kernel(n), nd["op"], tuple(nd["out_shape"]),
-               tuple(tuple(g.edge_shape(v)) if v >= 0 else ("c",) + tuple(g.desc["consts"][~v]["shape"])
-                     for v in nd["ins"]))
-        by_sig.setdefault(key, []).append(n)
-    # dominant kernel: the signature with the largest summed algorithmic
-    # time at its bound's peak (flops / MFMA peak or bytes / HBM peak) --
-    # fixed by the graph and the plan, not by timing noise or by the
-    # per-dispatch overhead a tracer adds
-    def ideal_ms(nodes):
-        kind, work = node_work(g, nodes[0])
-        return len(nodes) * work / ((PEAK_TFLOPS[g.dtype] * 1e12) if kind == "flop" else (PEAK_HBM_GBS * 1e9))
-    dom_key = max(by_sig, key=lambda k: (ideal_ms(by_sig[k]), -by_sig[k][0]))
-    dom_nodes = by_sig[dom_key]
+    for u in units:
+        by_sig.setdefault(u["sig"], []).append(u)
+    # dominant kernel: the launch signature (kernel instance with its fused
+    # epilogue and group, and the shapes of the nodes it performs) with the
+    # largest summed algorithmic time at its bound's peak (flops / MFMA peak
+    # or bytes / HBM peak) -- fixed by the graph and the plan, not by timing
+    # noise or by the per-dispatch overhead a tracer adds
+    def ideal_ms(us):
+        peak = (PEAK_TFLOPS[g.dtype] * 1e12) if us[0]["kind"] == "flop" else (PEAK_HBM_GBS * 1e9)
+        return sum(u["work"] for u in us) / peak
+    dom_key = max(by_sig, key=lambda k: (ideal_ms(by_sig[k]), -by_sig[k][0]["index"]))
+    dom = by_sig[dom_key]
     if kernel_only:
-        ex.run_nodes(dom_nodes, steps, stream)
+        ex.run_nodes([n for u in dom for n in u["nodes"]], steps, stream)
         torch.cuda.synchronize()
-        return {"kernel": dom_key[0], "node_op": dom_key[1], "out_shape": list(dom_key[2]),
-                "in_shapes": [list(s) for s in dom_key[3]], "launches": steps * len(dom_nodes)}
-    op_classes = op_class_rates(F, g, lp, ex, steps, torch)
+        return {"kernel": dom[0]["name"], "node_sigs": [list(map(str, x)) for x in dom_key[1:]],
+                "launches": steps * len(dom)}
+    op_classes = op_class_rates(g, units, ex, steps, torch)
 
     # timed region 1: K eager steps (whole graph, no per-launch events)
     MARK.push(f"{wl}/eager_timed")
@@ -361,8 +401,8 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     # back to back, K times over, with the bindings of a run (the arena holds
     # the data of the last step), replayed as one HIP graph between two
     # events on the replay stream
-    launches = steps * len(dom_nodes)
-    avg_ms = time_nodes(ex, dom_nodes, steps, torch, marker=f"{wl}/kernel_timed") / len(dom_nodes)
+    launches = steps * len(dom)
+    avg_ms = time_units(ex, dom, steps, torch, marker=f"{wl}/kernel_timed") / len(dom)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     # timed region 2 (the reported latency): the same K steps captured into
     # one HIP graph; one warm-up replay, then one timed replay
@@ -390,23 +430,21 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     del hg_naive
     ms_naive_eager, _ = time_steps(ex_naive, steps, stream, torch)
 
-    kind, work = node_work(g, dom_nodes[0])
+    kind, work = dom[0]["kind"], dom[0]["work"]
+    tkey = (wl, dom[0]["name"], str(dom_key[1:]))
+    traffic = TRAFFIC.get(tkey) if kernel_source_hash() == TRAFFIC_SRC else None
     if kind == "flop":
         achieved = work / (avg_ms * 1e-3) / 1e12
         peak = PEAK_TFLOPS[g.dtype]
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None}
-        if kernel_source_hash() == TRAFFIC_SRC:
-            roof["traffic"] = TRAFFIC.get((wl, dom_key[0], tuple(dom_key[2]), dom_key[3]))
+                "frac": round(achieved / peak, 4), "traffic": traffic}
     else:
         achieved = work / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
-        if kernel_source_hash() == TRAFFIC_SRC:
-            roof["traffic"] = TRAFFIC.get((wl, dom_key[0], tuple(dom_key[2]), dom_key[3]))
-    roof.update({"kernel": dom_key[0], "node_op": dom_key[1], "out_shape": list(dom_key[2]),
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic}
+    roof.update({"kernel": dom[0]["name"], "node_sigs": [list(map(str, x)) for x in dom_key[1:]],
                  "avg_launch_us": round(avg_ms * 1e3, 3), "launches": launches,
-                 "positions_in_step": [launched.index(n) for n in dom_nodes],
+                 "positions_in_step": [u["index"] for u in dom],
                  "work_per_launch": work, "work_unit": "flop" if kind == "flop" else "byte"})
 
     abl = ablation(F, g, table, ex, steps, torch)
@@ -467,10 +505,10 @@ def device_inputs(torch, F, cfg, seed):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2)
-    ap.add_argument("--extra", default="3,4,5", help="extra workloads to report ('' for none)")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--extra", default="2,3,5", help="extra workloads to report ('' for none)")
     ap.add_argument("--reps", type=int, default=7, help="timed launches per cost-table entry")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--save-table", default=None)
@@ -522,8 +560,8 @@ def main():
         c = synth_inputs.config(idx)
         log(f"extra workload {c['name']}")
         xe, ce = device_inputs(torch, F, c, idx)
-        st = max(5, a.steps // 5) if idx in (4, 5) else a.steps
-        e = measure_workload(F, torch, c, xe, ce, st, max(2, a.warmup // 5), max(2, a.reps // 2), None, tables)
+        st = max(5, a.steps // 2) if idx in (4, 5) else a.steps
+        e = measure_workload(F, torch, c, xe, ce, st, max(2, a.warmup // 2), max(2, a.reps // 2), None, tables)
         e.update({"workload": c["name"], "dtype": c["dtype"], "steps": st,
                   "data": "synthetic, drawn on the GPU"})
         extras[f"cfg{idx}"] = e
@@ -533,7 +571,7 @@ def main():
         res["extra_workloads"] = extras
     if not a.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        res["cpu_baseline"] = cpu_baseline(cfg)
+        res["cpu_baseline"] = cpu_baseline(cfg, seed=a.config)
     print(json.dumps(res), flush=True)
 
 
