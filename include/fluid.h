@@ -291,6 +291,24 @@ fluid_status fluid_run(const fluid_graph* g, const fluid_layout_plan* lp, const 
                        void* arena, uint64_t arena_bytes, const void* const* consts,
                        const void* const* inputs, void* const* outputs, void* hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * execution as fluid_run, with the arena replaced by a static device array
+ * of FLUID_STATIC_ARENA_BYTES inside the library (one per GPU, held until
+ * the process ends; its address is looked up on the first call on each
+ * device).  No device allocation or free happens in this call.  The
+ * caller still passes constants, inputs and outputs (same rules as
+ * fluid_run).  Errors: FLUID_E_ARENA_TOO_SMALL when the plan's peak exceeds
+ * FLUID_STATIC_ARENA_BYTES (checked before any launch), otherwise as
+ * fluid_run.  Every call on a GPU uses that GPU's one array, which keeps
+ * the last run's bytes (a run writes every arena byte before reading it, so
+ * nothing needs clearing); calls that overlap on one GPU (different streams
+ * or threads) race.  GPU build only. */
+#define FLUID_STATIC_ARENA_BYTES (64ull << 20)
+fluid_status fluid_run_static(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
+                              const void* const* consts, const void* const* inputs, void* const* outputs,
+                              void* hip_stream);
+
 /* Launches only the kernels of the listed nodes, in list order, the whole
  * list `repeat` times over, with exactly the bindings and kernels fluid_run
  * uses for them (profiling aid: the time of chosen kernels back to back,

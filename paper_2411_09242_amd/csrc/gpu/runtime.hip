@@ -220,7 +220,7 @@ std::shared_ptr<Prepared> cached_prepared(const fluid_graph* gh, const fluid_lay
   return prep;
 }
 
-// Enqueues the launches of a prepared run.
+// Enqueues the launches of a prepared run (fluid_run, fluid_run_static).
 void run_prepared(const fluid_graph* gh, const Prepared& prep, const Bases& B, hipStream_t s) {
   std::unique_lock<std::mutex> tl(g_trace_mu);
   const bool tracing = g_trace.on && g_trace.graph_serial == gh->serial;
@@ -241,6 +241,29 @@ void run_prepared(const fluid_graph* gh, const Prepared& prep, const Bases& B, h
   }
 }
 
+// The arena of fluid_run_static: a file-scope device array, one copy per
+// GPU, alive until the process ends.  Host code never uses the array's name
+// as an address (on the host it is only a stand-in symbol): the device
+// address of each GPU's copy is looked up once, with that GPU current, and
+// kept per device.
+__device__ __align__(256) unsigned char scratch[FLUID_STATIC_ARENA_BYTES];
+
+std::mutex g_static_mu;
+std::map<int, void*> g_static_ptr;  // device ordinal -> address of its copy
+
+void* static_arena() {
+  int dev = -1;
+  hip_check(hipGetDevice(&dev), "hipGetDevice");
+  std::lock_guard<std::mutex> lk(g_static_mu);
+  auto it = g_static_ptr.find(dev);
+  if (it != g_static_ptr.end()) return it->second;
+  void* ptr = nullptr;
+  hip_check(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(static arena)");
+  require(ptr != nullptr && ((uintptr_t)ptr & 255) == 0, "static arena address is not 256-byte aligned");
+  g_static_ptr[dev] = ptr;
+  return ptr;
+}
+
 }  // namespace
 
 extern "C" {
@@ -251,6 +274,22 @@ fluid_status fluid_run(const fluid_graph* gh, const fluid_layout_plan* lh, const
   return call_guarded([&] {
     std::shared_ptr<Prepared> prep =
         checked_prepared(gh, lh, ah, arena, arena_bytes, consts, inputs, outputs, "fluid_run");
+    run_prepared(gh, *prep, Bases{(char*)arena, inputs, outputs, consts}, (hipStream_t)hip_stream);
+  });
+}
+
+fluid_status fluid_run_static(const fluid_graph* gh, const fluid_layout_plan* lh, const fluid_arena_plan* ah,
+                              const void* const* consts, const void* const* inputs, void* const* outputs,
+                              void* hip_stream) {
+  return call_guarded([&] {
+    require(gh && lh && ah, "fluid_run_static: NULL graph or plan");
+    if (ah->a.peak > FLUID_STATIC_ARENA_BYTES)
+      fail(FLUID_E_ARENA_TOO_SMALL, "fluid_run_static: the plan needs " + std::to_string(ah->a.peak) +
+                                        " arena bytes, the static arena holds " +
+                                        std::to_string((uint64_t)FLUID_STATIC_ARENA_BYTES));
+    void* arena = static_arena();
+    std::shared_ptr<Prepared> prep = checked_prepared(gh, lh, ah, arena, FLUID_STATIC_ARENA_BYTES, consts, inputs,
+                                                      outputs, "fluid_run_static");
     run_prepared(gh, *prep, Bases{(char*)arena, inputs, outputs, consts}, (hipStream_t)hip_stream);
   });
 }

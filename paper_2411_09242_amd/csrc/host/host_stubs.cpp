@@ -19,6 +19,11 @@ fluid_status fluid_run(const fluid_graph*, const fluid_layout_plan*, const fluid
   return unsupported("fluid_run");
 }
 
+fluid_status fluid_run_static(const fluid_graph*, const fluid_layout_plan*, const fluid_arena_plan*, const void* const*,
+                              const void* const*, void* const*, void*) {
+  return unsupported("fluid_run_static");
+}
+
 fluid_status fluid_pack_constant(const fluid_graph*, const fluid_layout_plan*, int32_t, const void*, void*, void*) {
   return unsupported("fluid_pack_constant");
 }

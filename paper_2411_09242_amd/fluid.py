@@ -88,6 +88,7 @@ _PROTOS = {
                             C.POINTER(_VP), _VP]),
     "fluid_constant_layout": (C.c_int, [_VP, _VP, C.c_int32, C.POINTER(C.c_int32)]),
     "fluid_pack_constant": (C.c_int, [_VP, _VP, C.c_int32, _VP, _VP, _VP]),
+    "fluid_run_static": (C.c_int, [_VP, _VP, _VP, C.POINTER(_VP), C.POINTER(_VP), C.POINTER(_VP), _VP]),
     "fluid_run_nodes": (C.c_int, [_VP, _VP, _VP, _VP, C.c_uint64, C.POINTER(_VP), C.POINTER(_VP),
                                   C.POINTER(_VP), C.POINTER(C.c_int32), C.c_int32, C.c_int32, _VP]),
     "fluid_run_launches": (C.c_int, [_VP, _VP, _VP, C.POINTER(C.c_int32)]),
@@ -289,6 +290,11 @@ def fluid_constant_layout(g, lp, c, rank):
 
 def fluid_pack_constant(g, lp, c, src_ptr, dst_ptr, stream):
     _check(_L().fluid_pack_constant(g, lp, c, src_ptr, dst_ptr, stream))
+
+
+def fluid_run_static(g, lp, ap, const_ptrs, input_ptrs, output_ptrs, stream):
+    _check(_L().fluid_run_static(g, lp, ap, _ptr_array(const_ptrs), _ptr_array(input_ptrs),
+                                 _ptr_array(output_ptrs), stream))
 
 
 def fluid_run_nodes(g, lp, ap, arena_ptr, arena_bytes, const_ptrs, input_ptrs, output_ptrs, nodes, repeat,
