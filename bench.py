@@ -37,22 +37,36 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 # HBM bytes per launch of each workload's dominant launch: two rocprofv3
 # --pmc passes (FETCH_SIZE, then WRITE_SIZE) over `bench.py --kernel-only`
 # (that launch alone, planned from the saved cost tables), each scaled by
-# what the same counter read for the 256 MiB calibration copy.  Keyed by
-# (workload, launch name, node signatures); reported as `traffic` only while
-# the kernel sources hash to TRAFFIC_SRC -- a changed kernel makes the figure
-# stale, and then null.
-TRAFFIC_SRC = ""
-TRAFFIC = {}
+# what the same counter read for the 256 MiB calibration copy (FETCH_SIZE
+# counts half the bytes read, WRITE_SIZE all the bytes written).  Keyed by
+# (workload, launch name, node signatures); each figure carries the hash of
+# its kernel family's device sources when it was taken and is reported as
+# `traffic` only while they are unchanged (else null).
+TRAFFIC = {
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm_eg',
+     "[['matmul', '(8, 512, 4096)', \"((8, 512, 1024), ('c', 1024, 4096))\"], ['add', '(8, 512, 4096)', "
+     "\"((8, 512, 4096), ('c', 4096))\"], ['gelu', '(8, 512, 4096)', '((8, 512, 4096),)']]"): (235893161, "5d68c6d18b39ba47"),
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn',
+     "[['matmul', '(1, 2048, 11008)', \"((1, 2048, 4096), ('c', 4096, 11008))\"]]"): (894260458, "5d68c6d18b39ba47"),
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm_eg',
+     "[['matmul', '(1, 512, 3072)', \"((1, 512, 768), ('c', 768, 3072))\"], ['add', '(1, 512, 3072)', "
+     "\"((1, 512, 3072), ('c', 3072))\"], ['gelu', '(1, 512, 3072)', '((1, 512, 3072),)']]"): (28487123, "5d68c6d18b39ba47"),
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm_eg',
+     "[['matmul', '(1, 128, 3072)', \"((1, 128, 768), ('c', 768, 3072))\"], ['add', '(1, 128, 3072)', "
+     "\"((1, 128, 3072), ('c', 3072))\"], ['gelu', '(1, 128, 3072)', '((1, 128, 3072),)']]"): (14374435, "5d68c6d18b39ba47"),
+}
+
+# the device sources of each kernel family (by launch-name prefix)
+FAMILY_SOURCES = {"gemm": ["k_gemm*.hip", "gemm_common.h", "dev.h"], "conv": ["k_conv.hip", "dev.h"],
+                  "": ["k_elementwise.hip", "k_reduce.hip", "dev.h"]}
 
 
-def kernel_source_hash():
+def kernel_source_hash(launch_name):
     import glob
     import hashlib
-    d = os.path.join(ROOT, "paper_2411_09242_amd", "csrc")
-    # the kernels (k_*.hip and their headers) and the host code that fills
-    # their parameters; not the executor or the cost measurement
-    files = sorted(glob.glob(os.path.join(d, "gpu", "k_*.hip")) + glob.glob(os.path.join(d, "gpu", "*.h")) +
-                   [os.path.join(d, "host", "dispatch.cpp"), os.path.join(d, "host", "kparams.h")])
+    d = os.path.join(ROOT, "paper_2411_09242_amd", "csrc", "gpu")
+    fam = next(f for f in ("gemm", "conv", "") if launch_name.startswith(f))
+    files = sorted(f for pat in FAMILY_SOURCES[fam] for f in glob.glob(os.path.join(d, pat)))
     h = hashlib.sha256()
     for f in files:
         h.update(os.path.basename(f).encode())
@@ -431,8 +445,9 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     ms_naive_eager, _ = time_steps(ex_naive, steps, stream, torch)
 
     kind, work = dom[0]["kind"], dom[0]["work"]
-    tkey = (wl, dom[0]["name"], str(dom_key[1:]))
-    traffic = TRAFFIC.get(tkey) if kernel_source_hash() == TRAFFIC_SRC else None
+    tkey = (wl, dom[0]["name"], str([list(map(str, x)) for x in dom_key[1:]]))
+    entry = TRAFFIC.get(tkey)
+    traffic = entry[0] if entry and entry[1] == kernel_source_hash(dom[0]["name"]) else None
     if kind == "flop":
         achieved = work / (avg_ms * 1e-3) / 1e12
         peak = PEAK_TFLOPS[g.dtype]
