@@ -119,6 +119,9 @@ def node_work(g, n):
         N = nd["out_shape"][-1]
         M = int(np.prod(nd["out_shape"][:-1]))
         return "flop", 2.0 * M * N * K
+    if nd["op"] == "conv":      # 2 * output elements * (C * KH * KW)
+        w = g.desc["consts"][~nd["ins"][1]]["shape"]
+        return "flop", 2.0 * float(np.prod(nd["out_shape"])) * float(np.prod(w[1:]))
     b = 0
     for v in nd["ins"]:
         if v >= 0:
@@ -147,9 +150,9 @@ def launch_units(g, ex):
         if l >= 0:
             units[l]["nodes"].append(n)
     for i, u in enumerate(units):
-        mm = [n for n in u["nodes"] if g.desc["nodes"][n]["op"] == "matmul"]
+        mm = [n for n in u["nodes"] if g.desc["nodes"][n]["op"] in ("matmul", "conv")]
         if mm:
-            u["op"], u["kind"] = "matmul", "flop"
+            u["op"], u["kind"] = g.desc["nodes"][mm[0]]["op"], "flop"
             u["work"] = sum(node_work(g, n)[1] for n in mm)
         else:
             assert len(u["nodes"]) == 1, u
@@ -301,8 +304,8 @@ def cpu_baseline(cfg, budget_s=20.0, seed=4):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # noqa: BLE001
         threads = len(os.sched_getaffinity(0))
-    big = cfg["batch"] * cfg["seq"] * cfg["hidden"] >= 2 ** 21
-    k = 2 if big and cfg["layers"] > 2 else cfg["layers"]
+    big = cfg["arch"] != "vgg" and cfg["batch"] * cfg["seq"] * cfg["hidden"] >= 2 ** 21
+    k = 2 if big and cfg["layers"] > 2 else cfg.get("layers", 1)
     og = OG.build_transformer(dict(cfg, layers=k))
     x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), seed)
     times = []
@@ -493,19 +496,25 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
 def device_inputs(torch, F, cfg, seed):
     """Synthetic inputs drawn on the GPU (same distributions as the seeded
     host recipe: x ~ N(0,1), weights 0.02 N(0,1), biases/beta 0, gamma 1,
-    RoPE tables from positions); used for the extra workloads to keep the
+    RoPE tables from positions; for the convolutional workload an image batch
+    and sqrt(2 / fan_in) N(0,1) weights); used for the extra workloads to keep the
     benchmark short.  Timing does not depend on the values."""
     import synth_inputs
     g = F.Graph.transformer(cfg)
     dt = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
     gen = torch.Generator(device="cuda").manual_seed(seed)
-    x = torch.randn((cfg["batch"], cfg["seq"], cfg["hidden"]), generator=gen, device="cuda").to(dt)
+    conv = cfg["arch"] == "vgg"
+    xs = ((cfg["batch"], cfg["channels"], cfg["image"], cfg["image"]) if conv
+          else (cfg["batch"], cfg["seq"], cfg["hidden"]))
+    x = torch.randn(xs, generator=gen, device="cuda").to(dt)
     consts = []
     for c in g.desc["consts"]:
         shape, role = tuple(c["shape"]), c["role"]
         cdt = torch.bfloat16 if c["dtype"] == "bf16" else torch.float32
         if role == "weight":
-            a = (0.02 * torch.randn(shape, generator=gen, device="cuda")).to(cdt)
+            fan_in = (int(np.prod(shape[1:])) if len(shape) == 4 else shape[0]) if conv else 0
+            std = float(np.sqrt(2.0 / fan_in)) if conv else 0.02
+            a = (std * torch.randn(shape, generator=gen, device="cuda")).to(cdt)
         elif role == "gamma":
             a = torch.ones(shape, device="cuda", dtype=cdt)
         elif role in ("rope_cos", "rope_sin"):
@@ -523,7 +532,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4)
-    ap.add_argument("--extra", default="2,3,5", help="extra workloads to report ('' for none)")
+    ap.add_argument("--extra", default="2,3,5,6", help="extra workloads to report ('' for none)")
     ap.add_argument("--reps", type=int, default=7, help="timed launches per cost-table entry")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--save-table", default=None)
@@ -560,9 +569,10 @@ def main():
         "value": r["ms_per_step"], "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": r["ms_per_step"], "higher_is_better": False, "scaling": "weak",
         "vs_baseline": None, "dtype": cfg["dtype"], "data": "synthetic",
-        "config": {"workload": cfg["name"], "arch": cfg["arch"], "layers": cfg["layers"],
-                   "batch": cfg["batch"], "seq": cfg["seq"], "hidden": cfg["hidden"],
-                   "heads": cfg["heads"], "ffn": cfg["ffn"], "parallelism": "none (1 GPU)"},
+        "config": dict({"workload": cfg["name"]},
+                       **{k: cfg[k] for k in ("arch", "layers", "batch", "seq", "hidden", "heads", "ffn", "channels",
+                                              "image", "stages", "fc", "classes") if k in cfg},
+                       parallelism="none (1 GPU)"),
         "timing": "value: K steps captured in one HIP graph, one timed replay; roofline: the "
                   "dominant kernel's launches (all nodes of its signature) back to back K times over, "
                   "replayed as one HIP graph between two HIP events, per-launch mean",

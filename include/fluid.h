@@ -72,12 +72,22 @@ typedef enum { FLUID_F32 = 0, FLUID_BF16 = 1 } fluid_dtype;
  *  GELU      0.5 x (1 + erf(x / sqrt 2));  SILU  x / (1 + exp(-x)).
  *  ROPE      in[0] [B, S, NH, D] (D even); in[1] cos, in[2] sin: fp32
  *            constants [S, D/2]; rotate-half: for i < D/2,
- *            y_i = x_i c - x_{i+D/2} s,  y_{i+D/2} = x_{i+D/2} c + x_i s.   */
+ *            y_i = x_i c - x_{i+D/2} s,  y_{i+D/2} = x_{i+D/2} c + x_i s.
+ *  PAD       in[0] [N, C, H, W]; zero padding of i_attr[0] >= 0 on both
+ *            sides of H and W: out [N, C, H + 2p, W + 2p].
+ *  CONV      in[0] x [N, C, H, W]; in[1] weight constant [Co, C, KH, KW]
+ *            (row-major); optional in[2] bias constant [Co]; ONNX Conv with
+ *            no padding, stride 1, one group: out [N, Co, H-KH+1, W-KW+1],
+ *            y[n,o,i,j] = sum_{c,u,v} x[n,c,i+u,j+v] w[o,c,u,v] + b[o].
+ *  RELU      max(x, 0).
+ *  MAXPOOL   in[0] [N, C, H, W], window k = i_attr[0] dividing H and W,
+ *            stride k: out [N, C, H/k, W/k], the maximum of each window.  */
 typedef enum {
   FLUID_OP_MATMUL = 0, FLUID_OP_ADD = 1, FLUID_OP_MUL = 2,
   FLUID_OP_TRANSPOSE = 3, FLUID_OP_RESHAPE = 4, FLUID_OP_SOFTMAX = 5,
   FLUID_OP_LAYERNORM = 6, FLUID_OP_RMSNORM = 7, FLUID_OP_GELU = 8,
-  FLUID_OP_SILU = 9, FLUID_OP_ROPE = 10
+  FLUID_OP_SILU = 9, FLUID_OP_ROPE = 10, FLUID_OP_PAD = 11,
+  FLUID_OP_CONV = 12, FLUID_OP_RELU = 13, FLUID_OP_MAXPOOL = 14
 } fluid_op;
 
 /* Informational tag of a constant (how the synthetic workloads fill it). */
@@ -98,7 +108,8 @@ typedef struct {
   int64_t out_shape[FLUID_MAX_RANK];
   int32_t perm[FLUID_MAX_RANK];        /* TRANSPOSE only                        */
   float f_attr[2];                     /* SOFTMAX scale; LAYERNORM/RMSNORM eps  */
-  int32_t i_attr[2];                   /* SOFTMAX causal flag                   */
+  int32_t i_attr[2];                   /* SOFTMAX causal flag; PAD width;
+                                          MAXPOOL window                        */
 } fluid_node_desc;
 
 /* Shapes of inputs / constants: arrays of n * FLUID_MAX_RANK int64, row i
@@ -138,13 +149,23 @@ fluid_status fluid_build_graph(const fluid_graph_desc* desc, fluid_graph** out);
  * [B,NH,S,D], keys to [B,NH,D,S]), scores MatMul, Softmax(1/sqrt(D)),
  * context MatMul, Transpose + Reshape back, output projection, residual,
  * norm, FFN (up, bias, GELU, down, bias; SwiGLU: gate, SiLU, up, Mul, down),
- * residual[, norm]. */
+ * residual[, norm].
+ * arch 3: VGG-shaped convolutional network (fp32; the paper's VGG and
+ * ConvBERT models, Section 5): input [batch, channels, image, image]; per
+ * stage s, stage_convs[s] times Pad(1), 3x3 Conv with bias to
+ * stage_width[s] channels, ReLU, then MaxPool(2); flatten by two Reshapes
+ * (merge H, W; merge C, H*W); MatMul, bias Add, ReLU to fc twice; MatMul and
+ * bias Add to classes; Softmax (scale 1).  Uses batch, dtype and the fields
+ * after rope_base (layers, seq, hidden, heads, ffn are ignored). */
+#define FLUID_MAX_STAGES 8
 typedef struct {
   int32_t arch;
   int32_t layers, batch, seq, hidden, heads, ffn;
   int32_t dtype;                       /* fluid_dtype                           */
   float eps;                           /* norm epsilon (1e-5)                   */
   float rope_base;                     /* 10000                                 */
+  int32_t channels, image, fc, classes, n_stages;            /* arch 3 only */
+  int32_t stage_width[FLUID_MAX_STAGES], stage_convs[FLUID_MAX_STAGES];
 } fluid_model_cfg;
 fluid_status fluid_build_transformer(const fluid_model_cfg* cfg, fluid_graph** out);
 

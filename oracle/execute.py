@@ -25,6 +25,10 @@ Operator semantics follow ONNX, the paper's front-end format:
   GELU        0.5 x (1 + erf(x / sqrt 2));  SiLU: x / (1 + exp(-x))
   RoPE        rotate-half on the last axis of [B, S, NH, D] with tables
               cos/sin [S, D/2] indexed by the position (axis 1)
+  Pad         zero padding of width p on both sides of H and W ([N,C,H,W])
+  Conv        y[n,o,i,j] = sum_{c,u,v} x[n,c,i+u,j+v] w[o,c,u,v] + b[o]
+              (ONNX Conv with no padding, stride 1, one group)
+  ReLU        max(x, 0);  MaxPool: maximum over k x k windows, stride k
 """
 from __future__ import annotations
 
@@ -77,6 +81,33 @@ def op_rope(x, cos, sin):
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
+def op_pad(x, p):
+    return np.pad(x, ((0, 0), (0, 0), (p, p), (p, p)))
+
+
+def op_conv(x, w, b=None):
+    """The convolution sum written as one matrix product over the unfolded
+    input windows (im2col): rows (n, i, j), columns (c, u, v)."""
+    N, C, H, W = x.shape
+    Co, Ci, KH, KW = w.shape
+    OH, OW = H - KH + 1, W - KW + 1
+    win = np.lib.stride_tricks.sliding_window_view(x, (KH, KW), axis=(2, 3))   # [N, C, OH, OW, KH, KW]
+    cols = np.ascontiguousarray(win.transpose(0, 2, 3, 1, 4, 5)).reshape(N * OH * OW, C * KH * KW)
+    y = (cols @ w.reshape(Co, Ci * KH * KW).T).reshape(N, OH, OW, Co).transpose(0, 3, 1, 2)
+    if b is not None:
+        y = y + b[None, :, None, None]
+    return y
+
+
+def op_relu(x):
+    return np.maximum(x, 0)
+
+
+def op_maxpool(x, k):
+    N, C, H, W = x.shape
+    return x.reshape(N, C, H // k, k, W // k, k).max(axis=(3, 5))
+
+
 def eval_node(nd, args, dt=np.float64):
     """Result of one operator on arguments of the arithmetic type dt (float64
     unless a caller asks for float32 arithmetic), not yet rounded."""
@@ -103,6 +134,14 @@ def eval_node(nd, args, dt=np.float64):
         return op_silu(args[0])
     if op == "rope":
         return op_rope(args[0], args[1], args[2])
+    if op == "pad":
+        return op_pad(args[0], nd.iattr)
+    if op == "conv":
+        return op_conv(args[0], args[1], args[2] if len(args) > 2 else None)
+    if op == "relu":
+        return op_relu(args[0])
+    if op == "maxpool":
+        return op_maxpool(args[0], nd.iattr)
     raise ValueError(op)
 
 

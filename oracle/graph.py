@@ -19,7 +19,8 @@ from dataclasses import dataclass, field
 import numpy as np
 
 OPS = ("matmul", "add", "mul", "transpose", "reshape", "softmax",
-       "layernorm", "rmsnorm", "gelu", "silu", "rope")
+       "layernorm", "rmsnorm", "gelu", "silu", "rope",
+       "pad", "conv", "relu", "maxpool")
 
 
 @dataclass
@@ -29,7 +30,7 @@ class Node:
     out_shape: tuple
     perm: tuple = ()
     fattr: float = 0.0     # Softmax scale / norm eps (a float32 value)
-    iattr: int = 0         # Softmax causal flag
+    iattr: int = 0         # Softmax causal flag; Pad width; MaxPool window
 
 
 @dataclass
@@ -138,14 +139,52 @@ def _attention_block(g, h, B, S, H, NH, causal, biases, rope, cos_c, sin_c):
     return c2
 
 
+def build_vgg(cfg: dict) -> Graph:
+    """VGG-shaped convolutional network (the paper's VGG and ConvBERT models
+    in Section 5 carry Conv and Pad operators).  Per stage (width, n): n
+    times zero Pad of 1 on H and W, 3x3 Conv with bias (no padding of its
+    own, stride 1), ReLU; then a 2x2 MaxPool.  Then the feature map
+    [B, C, h, w] is flattened by two Reshapes (merge h, w; merge C, h*w)
+    and classified: MatMul, bias Add, ReLU twice (width fc), MatMul and bias
+    Add to `classes`, Softmax (scale 1)."""
+    B, C, S = cfg["batch"], cfg["channels"], cfg["image"]
+    g = Graph(dtype=cfg["dtype"])
+    e = g.add_input((B, C, S, S))
+    for width, n in cfg["stages"]:
+        for _ in range(n):
+            p = g.add_node("pad", [e], (B, C, S + 2, S + 2), iattr=1)
+            w = g.add_const("weight", (width, C, 3, 3)); b = g.add_const("bias", (width,))
+            c = g.add_node("conv", [p, w, b], (B, width, S, S))
+            e = g.add_node("relu", [c], (B, width, S, S))
+            C = width
+        e = g.add_node("maxpool", [e], (B, C, S // 2, S // 2), iattr=2)
+        S //= 2
+    e = g.add_node("reshape", [e], (B, C, S * S))
+    e = g.add_node("reshape", [e], (B, C * S * S))
+    K = C * S * S
+    for i, N in enumerate((cfg["fc"], cfg["fc"], cfg["classes"])):
+        w = g.add_const("weight", (K, N)); b = g.add_const("bias", (N,))
+        e = g.add_node("matmul", [e, w], (B, N))
+        e = g.add_node("add", [e, b], (B, N))
+        if i < 2:
+            e = g.add_node("relu", [e], (B, N))
+        K = N
+    e = g.add_node("softmax", [e], (B, cfg["classes"]), fattr=1.0, iattr=0)
+    g.outputs = [e]
+    return g
+
+
 def build_transformer(cfg: dict) -> Graph:
     """Build one of the three layer stacks (post-LN encoder, pre-LN decoder,
-    Llama-style decoder) as an explicit operator graph.
+    Llama-style decoder) as an explicit operator graph (or, for
+    arch "vgg", the convolutional network of build_vgg).
 
     The chain operand always comes first in a binary node (e.g. the residual
     add is Add(o1, x)), which fixes the chain slot used by the planner.
     """
     arch = cfg["arch"]
+    if arch == "vgg":
+        return build_vgg(cfg)
     B, S, H, NH, F = (cfg["batch"], cfg["seq"], cfg["hidden"], cfg["heads"],
                       cfg["ffn"])
     L = cfg["layers"]

@@ -17,6 +17,7 @@ __device__ __forceinline__ float ew_apply(float a, float b) {
   else if constexpr (OP == EW_MUL) return a * b;
   else if constexpr (OP == EW_GELU) return gelu_erf(a);
   else if constexpr (OP == EW_SILU) return silu(a);
+  else if constexpr (OP == EW_RELU) return a < 0.f ? 0.f : a;   // a NaN stays NaN
   else return a;
 }
 
@@ -245,7 +246,45 @@ hipError_t ew_dispatch(const NodeKernel& k, hipStream_t s) {
     case EW_MUL: return ew_dispatch_op<T, EW_MUL>(k, s);
     case EW_GELU: return ew_dispatch_op<T, EW_GELU>(k, s);
     case EW_SILU: return ew_dispatch_op<T, EW_SILU>(k, s);
+    case EW_RELU: return ew_dispatch_op<T, EW_RELU>(k, s);
     default: return ew_dispatch_op<T, EW_COPY>(k, s);
+  }
+}
+
+// Zero Pad and MaxPool: each thread produces output elements in the
+// output's physical order (coalesced stores) and reads the input through its
+// strides; out-of-range padding positions are zero; the pool maximum keeps a
+// NaN (as a maximum over the window must).
+template <typename T>
+__global__ __launch_bounds__(256) void window_kernel(WinParams p) {
+  const uint32_t step = gridDim.x * 256u;
+  for (uint32_t idx = blockIdx.x * 256u + threadIdx.x; idx < p.total; idx += step) {
+    uint32_t rem = idx;
+    int32_t yo = 0, xo = 0, h = 0, w = 0;
+#pragma unroll
+    for (int d = 3; d >= 0; --d) {
+      const uint32_t q = fdiv(rem, p.div[d]);
+      const int32_t c = (int32_t)(rem - q * p.ext[d]);
+      rem = q;
+      yo += c * p.os[d];
+      if (p.role[d] == 0) xo += c * p.is[d];
+      else if (p.role[d] == 1) h = c;
+      else w = c;
+    }
+    float v;
+    if (p.op == 0) {
+      const int32_t hi = h - p.k, wi = w - p.k;
+      v = (hi >= 0 && hi < p.in_h && wi >= 0 && wi < p.in_w) ? Elem<T>::load(p.x, xo + hi * p.is_h + wi * p.is_w)
+                                                             : 0.f;
+    } else {
+      v = -INFINITY;
+      for (int32_t u = 0; u < p.k; ++u)
+        for (int32_t t = 0; t < p.k; ++t) {
+          const float a = Elem<T>::load(p.x, xo + (h * p.k + u) * p.is_h + (w * p.k + t) * p.is_w);
+          v = (a > v || a != a) ? a : v;
+        }
+    }
+    Elem<T>::store(p.y, yo, v);
   }
 }
 
@@ -253,6 +292,13 @@ hipError_t ew_dispatch(const NodeKernel& k, hipStream_t s) {
 
 hipError_t launch_elementwise(const NodeKernel& k, hipStream_t s) {
   return k.dtype == DT_BF16 ? ew_dispatch<uint16_t>(k, s) : ew_dispatch<float>(k, s);
+}
+
+hipError_t launch_window(const NodeKernel& k, hipStream_t s) {
+  const uint32_t g = grid_for(k.win.total);
+  if (k.dtype == DT_BF16) hipLaunchKernelGGL(window_kernel<uint16_t>, dim3(g), dim3(256), 0, s, k.win);
+  else hipLaunchKernelGGL(window_kernel<float>, dim3(g), dim3(256), 0, s, k.win);
+  return hipGetLastError();
 }
 
 hipError_t launch_rope(const NodeKernel& k, hipStream_t s) {

@@ -19,6 +19,8 @@ hipError_t launch_gemm_f32_dl(const NodeKernel& k, hipStream_t s);
 // epilogue instance (fp32 tiles 6 and 7).
 hipError_t launch_gemm_f32_dl_group(const NodeKernel& k, const GemmGroup& G, hipStream_t s);
 hipError_t launch_fill(void* p, uint64_t bytes, uint32_t seed, hipStream_t s);
+hipError_t launch_window(const NodeKernel& k, hipStream_t s);
+hipError_t launch_conv(const NodeKernel& k, hipStream_t s);
 
 inline hipError_t launch_node_kernel(const NodeKernel& k, hipStream_t s) {
   switch (k.family) {
@@ -28,6 +30,8 @@ inline hipError_t launch_node_kernel(const NodeKernel& k, hipStream_t s) {
     case KF_RED_ROW:
     case KF_RED_COL: return launch_reduce(k, s);
     case KF_GEMM: return launch_gemm(k, s);
+    case KF_WIN: return launch_window(k, s);
+    case KF_CONV: return launch_conv(k, s);
     default: return hipSuccess;
   }
 }

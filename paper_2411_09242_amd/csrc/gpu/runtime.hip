@@ -64,6 +64,13 @@ void patch(NodeKernel& k, const PreparedNode& pn, const Bases& B) {
     case KF_GEMM:
       k.gemm.A = in0; k.gemm.B = in1; k.gemm.C = out;
       break;
+    case KF_WIN:
+      k.win.x = in0; k.win.y = out;
+      break;
+    case KF_CONV:
+      k.conv.x = (const float*)in0; k.conv.w = (const float*)in1; k.conv.bias = (const float*)in2;
+      k.conv.y = (float*)out;
+      break;
     default:
       break;
   }

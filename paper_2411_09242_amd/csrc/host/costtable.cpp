@@ -11,7 +11,7 @@ namespace fluid {
 namespace {
 
 int op_from_name(const std::string& s) {
-  for (int op = 0; op <= FLUID_OP_ROPE; ++op)
+  for (int op = 0; op <= FLUID_OP_MAXPOOL; ++op)
     if (s == op_name(op)) return op;
   fail(FLUID_E_INVALID, "cost table: unknown op '" + s + "'");
 }

@@ -25,8 +25,10 @@ int num_variants(int op) {
     case FLUID_OP_MATMUL: return 2 * kGemmTiles;
     case FLUID_OP_GELU:
     case FLUID_OP_SILU:
+    case FLUID_OP_RELU:
     case FLUID_OP_TRANSPOSE:
     case FLUID_OP_RESHAPE: return 2;
+    case FLUID_OP_CONV: return 2;
     case FLUID_OP_SOFTMAX:
     case FLUID_OP_LAYERNORM:
     case FLUID_OP_RMSNORM: return 2;
@@ -80,6 +82,7 @@ int ew_op_of(int op) {
     case FLUID_OP_MUL: return EW_MUL;
     case FLUID_OP_GELU: return EW_GELU;
     case FLUID_OP_SILU: return EW_SILU;
+    case FLUID_OP_RELU: return EW_RELU;
     default: return EW_COPY;
   }
 }
@@ -436,6 +439,84 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   return k;
 }
 
+// Pad / MaxPool: the output's four dims ordered by output stride (outermost
+// first) so that consecutive threads write consecutive addresses.
+NodeKernel prepare_window(const Node& nd, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+  NodeKernel k;
+  k.family = KF_WIN;
+  k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
+  const Operand& x = ins[0];
+  check_small(out, "window");
+  check_small(x, "window");
+  WinParams& p = k.win;
+  int order[4] = {0, 1, 2, 3};
+  std::stable_sort(order, order + 4, [&](int a, int b) { return out.stride[a] > out.stride[b]; });
+  for (int d = 0; d < 4; ++d) {
+    const int l = order[d];
+    p.ext[d] = (uint32_t)out.shape[l];
+    p.div[d] = make_fastdiv(p.ext[d]);
+    p.os[d] = (int32_t)out.stride[l];
+    p.is[d] = l < 2 ? (int32_t)x.stride[l] : 0;
+    p.role[d] = l < 2 ? 0 : (l == 2 ? 1 : 2);
+  }
+  p.in_h = (int32_t)x.shape[2];
+  p.in_w = (int32_t)x.shape[3];
+  p.is_h = (int32_t)x.stride[2];
+  p.is_w = (int32_t)x.stride[3];
+  p.total = (uint32_t)numel(out.shape);
+  p.op = nd.op == FLUID_OP_PAD ? 0 : 1;
+  p.k = nd.iattr;
+  p.x = x.ptr;
+  p.y = const_cast<void*>(out.ptr);
+  k.available = true;
+  return k;
+}
+
+// Conv: variant 0 reduces over (c, u, v) with wavefronts along pixels, 1
+// over (u, v, c) with wavefronts along channels (k_conv.hip).
+NodeKernel prepare_conv(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+  NodeKernel k;
+  k.family = KF_CONV;
+  k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
+  if (k.dtype != DT_F32) { k.why = "the convolution kernel is fp32"; return k; }
+  const Operand& x = ins[0];
+  const Operand& w = ins[1];
+  check_small(x, "conv");
+  check_small(out, "conv");
+  check_small(w, "conv");
+  const bool row_major_w = w.stride == row_major_strides(w.shape);
+  if (!row_major_w || (ins.size() > 2 && ins[2].stride[0] != 1)) { k.why = "weights must be row-major"; return k; }
+  ConvParams& p = k.conv;
+  const uint32_t C = (uint32_t)x.shape[1], KH = (uint32_t)w.shape[2], KW = (uint32_t)w.shape[3];
+  const uint32_t OH = (uint32_t)out.shape[2], OW = (uint32_t)out.shape[3];
+  p.x = (const float*)x.ptr;
+  p.w = (const float*)w.ptr;
+  p.bias = ins.size() > 2 ? (const float*)ins[2].ptr : nullptr;
+  p.y = (float*)out.ptr;
+  p.M = (uint32_t)out.shape[0] * OH * OW;
+  p.Co = (uint32_t)out.shape[1];
+  p.C = C;
+  p.K = C * KH * KW;
+  p.OHW = OH * OW;
+  p.OW = OW;
+  p.KHW = KH * KW;
+  p.KW = KW;
+  p.KWC = KW * C;
+  p.ohw_div = make_fastdiv(p.OHW);
+  p.ow_div = make_fastdiv(OW);
+  p.khw_div = make_fastdiv(p.KHW);
+  p.kw_div = make_fastdiv(KW);
+  p.kwc_div = make_fastdiv(p.KWC);
+  p.c_div = make_fastdiv(C);
+  p.x_n = (int32_t)x.stride[0]; p.x_c = (int32_t)x.stride[1]; p.x_h = (int32_t)x.stride[2]; p.x_w = (int32_t)x.stride[3];
+  p.y_n = (int32_t)out.stride[0]; p.y_c = (int32_t)out.stride[1]; p.y_h = (int32_t)out.stride[2];
+  p.y_w = (int32_t)out.stride[3];
+  p.tiles_n = (p.Co + 63) / 64;
+  k.conv_kord = variant;
+  k.available = true;
+  return k;
+}
+
 }  // namespace
 
 // Which steps pay off inside the product's launch was measured per tile
@@ -468,12 +549,15 @@ NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vecto
     case FLUID_OP_LAYERNORM:
     case FLUID_OP_RMSNORM: return prepare_red(nd, variant, dtype, ins, out);
     case FLUID_OP_ROPE: return prepare_rope(nd, dtype, ins, out);
+    case FLUID_OP_PAD:
+    case FLUID_OP_MAXPOOL: return prepare_window(nd, dtype, ins, out);
+    case FLUID_OP_CONV: return prepare_conv(nd, variant, dtype, ins, out);
     default: return prepare_ew(nd, variant, dtype, ins, out);
   }
 }
 
 std::string NodeKernel::name() const {
-  static const char* ew_names[] = {"copy", "add", "mul", "gelu", "silu"};
+  static const char* ew_names[] = {"copy", "add", "mul", "gelu", "silu", "relu"};
   static const char* red_names[] = {"softmax", "layernorm", "rmsnorm"};
   static const char* gm[] = {"g", "k", "mn"};
   const std::string dt = dtype == DT_BF16 ? "bf16" : "f32";
@@ -484,6 +568,8 @@ std::string NodeKernel::name() const {
     case KF_ROPE: return "rope_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
+    case KF_WIN: return std::string(win.op == 0 ? "pad_" : "maxpool_") + dt;
+    case KF_CONV: return "conv_" + dt + (conv_kord == 0 ? "_t64_kcuv" : "_t64_kuvc");
     case KF_GEMM: {
       // fused epilogue steps: b bias, g GELU, s SiLU, a / m Add / Mul of R
       auto epi_suffix = [&]() {

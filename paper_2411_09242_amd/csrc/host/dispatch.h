@@ -33,7 +33,7 @@ struct Operand {
   int dtype = FLUID_F32;
 };
 
-enum KernelFamily : int { KF_VIEW, KF_EW, KF_EW_TILED, KF_ROPE, KF_RED_ROW, KF_RED_COL, KF_GEMM };
+enum KernelFamily : int { KF_VIEW, KF_EW, KF_EW_TILED, KF_ROPE, KF_RED_ROW, KF_RED_COL, KF_GEMM, KF_WIN, KF_CONV };
 
 enum GemmMode : int { GM_GENERIC = 0, GM_K = 1, GM_MN = 2 };  // A: K-/M-contig; B: K-/N-contig
 
@@ -48,6 +48,9 @@ struct NodeKernel {
   RopeParams rope{};
   RedParams red{};
   GemmParams gemm{};
+  WinParams win{};
+  ConvParams conv{};
+  int conv_kord = 0;
   int gemm_tile = 0, amode = 0, bmode = 0, cmode = 0;  // cmode 0 generic, 1 N-contig, 2 M-contig
   std::string name() const;
 };

@@ -17,9 +17,10 @@ std::string shape_str(const Shape& s) {
 }
 
 const char* op_name(int op) {
-  static const char* names[] = {"matmul", "add",     "mul",     "transpose", "reshape", "softmax",
-                                "layernorm", "rmsnorm", "gelu", "silu",      "rope"};
-  return (op >= 0 && op <= FLUID_OP_ROPE) ? names[op] : "?";
+  static const char* names[] = {"matmul", "add",     "mul",     "transpose", "reshape", "softmax", "layernorm",
+                                "rmsnorm", "gelu",    "silu",    "rope",      "pad",     "conv",    "relu",
+                                "maxpool"};
+  return (op >= 0 && op <= FLUID_OP_MAXPOOL) ? names[op] : "?";
 }
 
 ReshapeKind reshape_kind(const Shape& xs, const Shape& ys, int* axis) {
@@ -69,7 +70,7 @@ void Graph::finalize() {
   for (size_t n = 0; n < nodes.size(); ++n) {
     const Node& nd = nodes[n];
     std::string where = "node " + std::to_string(n) + " (" + op_name(nd.op) + ")";
-    require(nd.op >= 0 && nd.op <= FLUID_OP_ROPE, where + ": unknown op");
+    require(nd.op >= 0 && nd.op <= FLUID_OP_MAXPOOL, where + ": unknown op");
     check_shape(nd.out_shape, where + " output");
     const int self = out_edge((int)n);
     std::vector<const Shape*> in_shapes;
@@ -167,9 +168,44 @@ void Graph::finalize() {
       }
       case FLUID_OP_GELU:
       case FLUID_OP_SILU:
+      case FLUID_OP_RELU:
         arity(1); act(0);
         require(y == *in_shapes[0], where + ": output shape");
         break;
+      case FLUID_OP_PAD: {
+        arity(1); act(0);
+        const Shape& a = *in_shapes[0];
+        require(a.size() == 4, where + ": input must be [N, C, H, W]");
+        require(nd.iattr >= 0, where + ": pad width must be >= 0");
+        const int64_t p = nd.iattr;
+        require(y == Shape({a[0], a[1], a[2] + 2 * p, a[3] + 2 * p}), where + ": output shape");
+        break;
+      }
+      case FLUID_OP_CONV: {
+        require(nd.ins.size() == 2 || nd.ins.size() == 3, where + ": expects 2 or 3 inputs");
+        act(0); cst(1);
+        const Shape& a = *in_shapes[0];
+        const Shape& w = *in_shapes[1];
+        require(a.size() == 4 && w.size() == 4, where + ": input [N, C, H, W] and weight [Co, C, KH, KW]");
+        require(w[1] == a[1] && w[2] <= a[2] && w[3] <= a[3], where + ": weight does not fit the input");
+        require(consts[~nd.ins[1]].dtype == dtype, where + ": weight dtype must be the graph's");
+        if (nd.ins.size() == 3) {
+          cst(2);
+          require(*in_shapes[2] == Shape({w[0]}), where + ": bias must be [Co]");
+          require(consts[~nd.ins[2]].dtype == dtype, where + ": bias dtype must be the graph's");
+        }
+        require(y == Shape({a[0], w[0], a[2] - w[2] + 1, a[3] - w[3] + 1}), where + ": output shape");
+        break;
+      }
+      case FLUID_OP_MAXPOOL: {
+        arity(1); act(0);
+        const Shape& a = *in_shapes[0];
+        const int64_t k = nd.iattr;
+        require(a.size() == 4 && k >= 1 && a[2] % k == 0 && a[3] % k == 0,
+                where + ": input [N, C, H, W] with H and W multiples of the window");
+        require(y == Shape({a[0], a[1], a[2] / k, a[3] / k}), where + ": output shape");
+        break;
+      }
       case FLUID_OP_ROPE: {
         arity(3); act(0); cst(1); cst(2);
         const Shape& a = *in_shapes[0];
@@ -240,8 +276,60 @@ struct Builder {
 
 }  // namespace
 
+namespace {
+
+// VGG-shaped convolutional network (arch 3): Pad, 3x3 Conv with bias, ReLU
+// per convolution; MaxPool(2) per stage; flatten; three classifier layers.
+Graph build_vgg(const fluid_model_cfg& c) {
+  require(c.batch >= 1 && c.channels >= 1 && c.image >= 1 && c.fc >= 1 && c.classes >= 1,
+          "model sizes must be positive");
+  require(c.n_stages >= 1 && c.n_stages <= FLUID_MAX_STAGES, "n_stages must be 1..FLUID_MAX_STAGES");
+  require(c.dtype == FLUID_F32, "the convolutional network is fp32");
+  Graph g;
+  g.dtype = c.dtype;
+  Builder b{g};
+  const int dt = c.dtype;
+  const int64_t B = c.batch;
+  int64_t C = c.channels, S = c.image;
+  g.inputs.push_back({B, C, S, S});
+  int e = 0;
+  for (int s = 0; s < c.n_stages; ++s) {
+    const int64_t Wd = c.stage_width[s];
+    require(Wd >= 1 && c.stage_convs[s] >= 1, "stage widths and counts must be positive");
+    for (int k = 0; k < c.stage_convs[s]; ++k) {
+      int p = b.add(FLUID_OP_PAD, {e}, {B, C, S + 2, S + 2}, {}, 0.f, 1);
+      int w = b.add_const(FLUID_ROLE_WEIGHT, {Wd, C, 3, 3}, dt);
+      int bi = b.add_const(FLUID_ROLE_BIAS, {Wd}, dt);
+      int cv = b.add(FLUID_OP_CONV, {p, w, bi}, {B, Wd, S, S});
+      e = b.add(FLUID_OP_RELU, {cv}, {B, Wd, S, S});
+      C = Wd;
+    }
+    require(S % 2 == 0, "every stage's image size must be even");
+    e = b.add(FLUID_OP_MAXPOOL, {e}, {B, C, S / 2, S / 2}, {}, 0.f, 2);
+    S /= 2;
+  }
+  e = b.add(FLUID_OP_RESHAPE, {e}, {B, C, S * S});
+  e = b.add(FLUID_OP_RESHAPE, {e}, {B, C * S * S});
+  int64_t K = C * S * S;
+  const int64_t widths[3] = {c.fc, c.fc, c.classes};
+  for (int i = 0; i < 3; ++i) {
+    const int64_t N = widths[i];
+    e = b.add(FLUID_OP_MATMUL, {e, b.add_const(FLUID_ROLE_WEIGHT, {K, N}, dt)}, {B, N});
+    e = b.add(FLUID_OP_ADD, {e, b.add_const(FLUID_ROLE_BIAS, {N}, dt)}, {B, N});
+    if (i < 2) e = b.add(FLUID_OP_RELU, {e}, {B, N});
+    K = N;
+  }
+  e = b.add(FLUID_OP_SOFTMAX, {e}, {B, (int64_t)c.classes}, {}, 1.0f, 0);
+  g.outputs = {e};
+  g.finalize();
+  return g;
+}
+
+}  // namespace
+
 Graph build_transformer(const fluid_model_cfg& c) {
-  require(c.arch >= 0 && c.arch <= 2, "arch must be 0 (post-LN), 1 (pre-LN) or 2 (Llama)");
+  if (c.arch == 3) return build_vgg(c);
+  require(c.arch >= 0 && c.arch <= 2, "arch must be 0 (post-LN), 1 (pre-LN), 2 (Llama) or 3 (VGG-shaped)");
   require(c.layers >= 1 && c.batch >= 1 && c.seq >= 1 && c.hidden >= 1 && c.heads >= 1 && c.ffn >= 1,
           "model sizes must be positive");
   require(c.hidden % c.heads == 0, "hidden must be a multiple of heads");

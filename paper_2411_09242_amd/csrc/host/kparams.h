@@ -17,7 +17,7 @@ FastDiv make_fastdiv(uint32_t d);
 
 constexpr int kMaxDims = 6;
 
-enum EwOp : int { EW_COPY = 0, EW_ADD = 1, EW_MUL = 2, EW_GELU = 3, EW_SILU = 4 };
+enum EwOp : int { EW_COPY = 0, EW_ADD = 1, EW_MUL = 2, EW_GELU = 3, EW_SILU = 4, EW_RELU = 5 };
 enum DType : int { DT_F32 = 0, DT_BF16 = 1 };
 
 // Elementwise / relayout over a canonical iteration space: dims ordered
@@ -78,6 +78,42 @@ struct RedParams {
   float attr;                 // softmax scale or norm eps
   int causal;
   int op;
+};
+
+// Zero Pad and MaxPool over [N, C, H, W]: one thread per output element; the
+// four output dims are walked outer -> inner in the output's physical order
+// (dims sorted by output stride), each with its input stride (N and C) or
+// its role (H, W), whose input coordinate the op derives.
+struct WinParams {
+  uint32_t ext[4];
+  FastDiv div[4];
+  int32_t os[4], is[4];       // output strides; input strides of N / C dims
+  int32_t role[4];            // 0 batch or channel, 1 H, 2 W
+  int32_t in_h, in_w;         // input extents of H and W
+  int32_t is_h, is_w;         // input strides of H and W
+  uint32_t total;
+  int32_t op;                 // 0 pad, 1 maxpool
+  int32_t k;                  // pad width / pool window
+  const void* x;
+  void* y;
+};
+
+// Convolution (no padding, stride 1) as an implicit GEMM: row m = (n, i, j)
+// an output pixel, column o an output channel, reduction index k over
+// (c, u, v) -- in the weight's row-major order (KORD 0) or as (u, v, c)
+// (KORD 1, channel fastest) -- so that x[n, c, i+u, j+v] sits at
+// row_offset(m) + col_offset(k) for any layout of x.
+struct ConvParams {
+  const float* x;
+  const float* w;             // [Co, C, KH, KW] row-major
+  const float* bias;          // [Co] or null
+  float* y;
+  uint32_t M, Co, K, C;       // M = N*OH*OW, K = C*KH*KW
+  uint32_t OHW, OW, KHW, KW, KWC;
+  FastDiv ohw_div, ow_div, khw_div, kw_div, kwc_div, c_div;
+  int32_t x_n, x_c, x_h, x_w;
+  int32_t y_n, y_c, y_h, y_w;
+  uint32_t tiles_n;
 };
 
 // C[g, m, n] = sum_k A[g, m, k] * B[g, k, n]; g = g1 * G2 + g2 and

@@ -26,9 +26,11 @@ MAX_IN = 4
 
 F32, BF16 = 0, 1
 OPS = {"matmul": 0, "add": 1, "mul": 2, "transpose": 3, "reshape": 4, "softmax": 5,
-       "layernorm": 6, "rmsnorm": 7, "gelu": 8, "silu": 9, "rope": 10}
+       "layernorm": 6, "rmsnorm": 7, "gelu": 8, "silu": 9, "rope": 10,
+       "pad": 11, "conv": 12, "relu": 13, "maxpool": 14}
 ROLES = {"other": 0, "weight": 1, "bias": 2, "gamma": 3, "beta": 4, "rope_cos": 5, "rope_sin": 6}
-ARCH = {"post_ln": 0, "pre_ln": 1, "llama": 2}
+ARCH = {"post_ln": 0, "pre_ln": 1, "llama": 2, "vgg": 3}
+MAX_STAGES = 8
 NO_DP, NO_VARIANTS, NO_GUARD = 1, 2, 4
 ARENA_NO_REUSE, ARENA_EPILOGUE = 1, 2
 STATUS = {0: "OK", -1: "INVALID", -2: "UNSUPPORTED", -3: "INFEASIBLE", -4: "ARENA_TOO_SMALL",
@@ -61,7 +63,10 @@ class GraphDesc(C.Structure):
 class ModelCfg(C.Structure):
     _fields_ = [("arch", C.c_int32), ("layers", C.c_int32), ("batch", C.c_int32), ("seq", C.c_int32),
                 ("hidden", C.c_int32), ("heads", C.c_int32), ("ffn", C.c_int32), ("dtype", C.c_int32),
-                ("eps", C.c_float), ("rope_base", C.c_float)]
+                ("eps", C.c_float), ("rope_base", C.c_float),
+                ("channels", C.c_int32), ("image", C.c_int32), ("fc", C.c_int32), ("classes", C.c_int32),
+                ("n_stages", C.c_int32), ("stage_width", C.c_int32 * MAX_STAGES),
+                ("stage_convs", C.c_int32 * MAX_STAGES)]
 
 
 _VP = C.c_void_p
@@ -146,9 +151,20 @@ def _check(st):
 
 # ----------------------------------------------------------------- raw calls
 def fluid_build_transformer(cfg: dict):
-    c = ModelCfg(ARCH[cfg["arch"]], cfg["layers"], cfg["batch"], cfg["seq"], cfg["hidden"],
-                 cfg["heads"], cfg["ffn"], BF16 if cfg["dtype"] == "bf16" else F32,
-                 cfg.get("eps", 1e-5), cfg.get("rope_base", 10000.0))
+    c = ModelCfg()
+    c.arch = ARCH[cfg["arch"]]
+    c.batch = cfg["batch"]
+    c.dtype = BF16 if cfg["dtype"] == "bf16" else F32
+    c.eps = cfg.get("eps", 1e-5)
+    c.rope_base = cfg.get("rope_base", 10000.0)
+    if cfg["arch"] == "vgg":
+        c.channels, c.image, c.fc, c.classes = cfg["channels"], cfg["image"], cfg["fc"], cfg["classes"]
+        c.n_stages = len(cfg["stages"])
+        for i, (w, n) in enumerate(cfg["stages"]):
+            c.stage_width[i], c.stage_convs[i] = w, n
+    else:
+        c.layers, c.seq, c.hidden, c.heads, c.ffn = (cfg["layers"], cfg["seq"], cfg["hidden"], cfg["heads"],
+                                                     cfg["ffn"])
     h = _VP()
     _check(_L().fluid_build_transformer(C.byref(c), C.byref(h)))
     return h

@@ -18,6 +18,12 @@ Recipe (same for every workload):
     cast); they are returned as float32 arrays holding bf16-exact values.
   * Rotary tables [S, D/2]: cos / sin of ``p * base**(-2i/D)`` evaluated in
     float64 and rounded to float32, p the sequence position, i < D/2.
+  * Convolutional workload (VGG-shaped): the input is an image batch
+    ``x = rng.standard_normal((B, C, H, W))``; every weight -- convolution
+    kernels [Co, Ci, KH, KW] and classifier matrices [K, N] -- is
+    ``sqrt(2 / fan_in) * rng.standard_normal(shape)`` with fan_in = Ci*KH*KW
+    or K (scaled so that activations keep their size through the ReLU
+    layers); biases are 0.
 """
 from __future__ import annotations
 
@@ -38,6 +44,13 @@ CONFIGS = {
     5: dict(name="llama-8l-b1-s2048-h4096-prefill", arch="llama", layers=8,
             batch=1, seq=2048, hidden=4096, heads=32, ffn=11008,
             dtype="bf16"),
+    # VGG-16-shaped convolutional network: five stages of 3x3 convolutions
+    # (zero Pad then Conv with bias then ReLU), a 2x2 MaxPool after each
+    # stage, then the classifier (two 4096-wide layers with ReLU, 1000
+    # classes, Softmax)
+    6: dict(name="vgg16-b1-224", arch="vgg", batch=1, channels=3, image=224,
+            stages=((64, 2), (128, 2), (256, 3), (512, 3), (512, 3)), fc=4096,
+            classes=1000, dtype="f32"),
 }
 EPS = 1e-5
 ROPE_BASE = 10000.0
@@ -76,12 +89,18 @@ def make_inputs(cfg: dict, const_specs, seed: int, rope_head_dim=None):
     ``x`` float32 [B, S, H]; ``consts`` a list of float32 arrays.
     """
     rng = np.random.default_rng(seed)
-    B, S, H = cfg["batch"], cfg["seq"], cfg["hidden"]
-    x = rng.standard_normal((B, S, H)).astype(np.float32)
+    conv = cfg["arch"] == "vgg"
+    if conv:
+        x = rng.standard_normal((cfg["batch"], cfg["channels"], cfg["image"], cfg["image"])).astype(np.float32)
+    else:
+        x = rng.standard_normal((cfg["batch"], cfg["seq"], cfg["hidden"])).astype(np.float32)
     consts = []
     for role, shape in const_specs:
         shape = tuple(int(s) for s in shape)
-        if role == "weight":
+        if role == "weight" and conv:
+            fan_in = int(np.prod(shape[1:])) if len(shape) == 4 else shape[0]
+            a = (np.sqrt(2.0 / fan_in) * rng.standard_normal(shape)).astype(np.float32)
+        elif role == "weight":
             a = (WEIGHT_STD * rng.standard_normal(shape)).astype(np.float32)
         elif role in ("bias", "beta"):
             a = np.zeros(shape, np.float32)

@@ -47,10 +47,14 @@ CFGS = [synth_inputs.config(i) for i in range(1, 6)] + [
     synth_inputs.config(1, arch="pre_ln", layers=2, seq=19, hidden=36, heads=3, ffn=52),
     synth_inputs.config(1, arch="llama", layers=2, seq=21, hidden=48, heads=4, ffn=40, dtype="bf16"),
     synth_inputs.config(1, arch="post_ln", layers=2, batch=3, seq=17, hidden=40, heads=5, ffn=72),
+    synth_inputs.config(6),
+    dict(synth_inputs.config(6), name="vgg-ragged", batch=2, channels=5, image=12, stages=((7, 1), (9, 2)), fc=13,
+         classes=11),
 ]
 
 
-@pytest.mark.parametrize("cfg", CFGS, ids=lambda c: f"{c['arch']}-{c['layers']}-{c['seq']}-{c['hidden']}")
+@pytest.mark.parametrize("cfg", CFGS, ids=lambda c: c["name"] if c["arch"] == "vgg" else
+                         f"{c['arch']}-{c['layers']}-{c['seq']}-{c['hidden']}")
 def test_cpp_builder_matches_oracle_builder(cfg):
     og = OG.build_transformer(cfg)
     g = F.Graph.transformer(cfg)
@@ -128,7 +132,7 @@ def test_planner_parity_flags(flags, tmp_path):
     _compare_plans(og, synthetic_table(og, seed=5, mode="random", lo=1, hi=30), tmp_path, flags)
 
 
-@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5, 6])
 @pytest.mark.parametrize("mode", ["random", "ties"])
 def test_planner_parity_config_graphs(idx, mode, tmp_path):
     og = OG.build_transformer(synth_inputs.config(idx))
