@@ -78,3 +78,45 @@ def best_layouts(g, ct, use_v0=False):
         if best is None or tot < best[0]:
             best = (tot, list(lay))
     return best
+
+
+def best_layouts_fused(g, ct, use_v0=False):
+    """The minimum total cost over every layout assignment of the
+    non-pinned edges and every set of non-overlapping fusion chains with
+    measured costs (ct.fused): a chain (m, t) costs its fused entry at the
+    layouts of its slots and of node m+t's output, every other node its own
+    entry.  Returns the minimum total."""
+    chains = sorted(ct.fused)
+    choices = []
+    for k in range(len(chains) + 1):
+        for sel in itertools.combinations(chains, k):
+            spans = [set(range(m, m + t + 1)) for m, t in sel]
+            if all(not (a & b) for i, a in enumerate(spans) for b in spans[i + 1:]):
+                choices.append(sel)
+    free = [e for e in range(g.n_edges) if len(ct.L[e]) > 1]
+    best = None
+    lay = [0] * g.n_edges
+    for assign in itertools.product(*[range(len(ct.L[e])) for e in free]):
+        for e, l in zip(free, assign):
+            lay[e] = l
+        for sel in choices:
+            covered = {n for m, t in sel for n in range(m, m + t + 1)}
+            tot = 0
+            for m, t in sel:
+                C = ct.fused[(m, t)].v0 if use_v0 else ct.fused[(m, t)].best
+                slots = list(g.act_inputs(m))
+                last = g.nodes[m + t]
+                if last.op in ("add", "mul"):
+                    other = [v for v in last.ins if v >= 0 and v != g.out_edge(m + t - 1)]
+                    slots += other[:1]
+                key = tuple(lay[e] for e in slots) + (lay[g.out_edge(m + t)],)
+                tot = min(tot + int(C[key]), INF)
+            for n in range(len(g.nodes)):
+                if n in covered:
+                    continue
+                C = ct.nodes[n].v0 if use_v0 else ct.nodes[n].best
+                key = tuple(lay[e] for e in g.act_inputs(n)) + (lay[g.out_edge(n)],)
+                tot = min(tot + int(C[key]), INF)
+            if best is None or tot < best:
+                best = tot
+    return best

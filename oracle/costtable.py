@@ -11,6 +11,12 @@ numbers.  Format ("fluid-cost-table/1"):
               [[slot_perms...], out_perm, [cost_ns per kernel variant]]
               (a cost of -1 means that variant is unavailable)
   node_sig  : the signature index of every node
+  fused_sigs, fused (optional): measured costs of fusion chains (see
+              oracle/fusion.py) -- fused_sigs holds signatures like sigs,
+              whose entries list the layouts of the chain's slots (the
+              MatMul's activation inputs, then R of an Add / Mul step) and of
+              the last node's output; fused lists [m, t, signature index]
+              for the chain of the MatMul node m and length t
 
 A node's activation slots (constants excluded) are listed in slot order.
 Missing combinations cost +infinity.  Layout-only (view) combinations carry
@@ -21,6 +27,8 @@ from __future__ import annotations
 import json
 
 import numpy as np
+
+from . import fusion
 
 INF = 1 << 62
 
@@ -35,9 +43,10 @@ class NodeCosts:
 
 
 class CostTable:
-    def __init__(self, L, nodes):
+    def __init__(self, L, nodes, fused=None):
         self.L = L            # list of lists of perms
         self.nodes = nodes    # list of NodeCosts
+        self.fused = fused or {}   # (m, t) -> NodeCosts over the chain's slots + output
 
 
 def load(path_or_obj, g):
@@ -56,19 +65,16 @@ def load(path_or_obj, g):
             raise ValueError(f"L({e}) must start with the identity layout")
     if len(obj["node_sig"]) != len(g.nodes):
         raise ValueError("node count mismatch")
-    nodes = []
-    for n, sig in enumerate(obj["node_sig"]):
-        slots = g.act_inputs(n)
-        eo = g.out_edge(n)
+    def dense(slots, eo, entries, what):
         dims = [len(L[e]) for e in slots] + [len(L[eo])]
         best = np.full(dims, INF, dtype=np.int64)
         var = np.full(dims, -1, dtype=np.int32)
         v0 = np.full(dims, INF, dtype=np.int64)
         index = [{p: i for i, p in enumerate(L[e])} for e in slots + [eo]]
-        for ent in obj["sigs"][sig]["entries"]:
+        for ent in entries:
             perms = [tuple(p) for p in ent[0]] + [tuple(ent[1])]
             if len(perms) != len(dims):
-                raise ValueError(f"node {n}: entry arity mismatch")
+                raise ValueError(f"{what}: entry arity mismatch")
             try:
                 key = tuple(index[i][p] for i, p in enumerate(perms))
             except KeyError:
@@ -81,5 +87,15 @@ def load(path_or_obj, g):
                 var[key] = v
             if costs and costs[0] >= 0:
                 v0[key] = costs[0]
-        nodes.append(NodeCosts(best, var, v0))
-    return CostTable(L, nodes)
+        return NodeCosts(best, var, v0)
+
+    nodes = [dense(g.act_inputs(n), g.out_edge(n), obj["sigs"][sig]["entries"], f"node {n}")
+             for n, sig in enumerate(obj["node_sig"])]
+    fused = {}
+    chains = fusion.all_chains(g)
+    for m, t, si in obj.get("fused", []):
+        if (m, t) not in chains:
+            raise ValueError(f"fused entry ({m}, {t}) is not a fusion chain of this graph")
+        fused[(m, t)] = dense(fusion.chain_slots(g, m, t), g.out_edge(m + t), obj["fused_sigs"][si]["entries"],
+                              f"chain ({m}, {t})")
+    return CostTable(L, nodes, fused)

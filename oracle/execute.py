@@ -178,12 +178,15 @@ def run_canonical(g, inputs, consts, keep=False, arith=np.float64):
 
 
 def run_in_arena(g, layout_of_edge, root_of_edge, offset_of_root, peak,
-                 inputs, consts, poison=True):
+                 inputs, consts, poison=True, fuse=None):
     """Execute with each edge stored permuted inside one uint8 arena.
 
     ``layout_of_edge[e]`` is a permutation; ``root_of_edge[e]`` the buffer
     edge e lives in; ``offset_of_root[r]`` the byte offset of arena buffer r.
     Graph inputs and outputs live in separate caller buffers (row-major).
+    ``fuse[m] = t`` marks a fused chain: the results of nodes m .. m+t-1
+    never reach memory (they are held outside the arena, as a fused launch
+    holds them on chip).
     """
     isz = numerics.itemsize(g.dtype)
     arena = np.full(max(int(peak), 1), 0xFF if poison else 0, dtype=np.uint8)
@@ -194,6 +197,11 @@ def run_in_arena(g, layout_of_edge, root_of_edge, offset_of_root, peak,
     for e in g.outputs:
         ext[e] = np.full(int(np.prod(g.edge_shape(e))) * isz, 0xFF, np.uint8)
 
+    on_chip = {}
+    for m, t in enumerate(fuse or []):
+        for i in range(t):
+            on_chip[g.out_edge(m + i)] = None
+
     def buf(e):
         r = root_of_edge[e]
         if r in ext:
@@ -201,6 +209,8 @@ def run_in_arena(g, layout_of_edge, root_of_edge, offset_of_root, peak,
         return arena, int(offset_of_root[r])
 
     def load(e):
+        if e in on_chip:
+            return on_chip[e]
         shape = g.edge_shape(e)
         perm = tuple(layout_of_edge[e])
         cnt = int(np.prod(shape))
@@ -210,6 +220,9 @@ def run_in_arena(g, layout_of_edge, root_of_edge, offset_of_root, peak,
         return phys.transpose(np.argsort(perm))
 
     def store(e, val):
+        if e in on_chip:
+            on_chip[e] = val
+            return
         perm = tuple(layout_of_edge[e])
         phys = np.ascontiguousarray(val.transpose(perm))
         raw = numerics.to_bytes(phys, g.dtype)

@@ -22,6 +22,10 @@ byte offset to every tensor ahead of time from tensor lifetimes.
   * Naive plan: one slice per buffer of the row-major plan, offsets the
     prefix sums of the sizes in edge-id order, no reuse.
   * Lower bound: the largest total size of buffers live at one node.
+  * Fused chains of the layout plan (fuse[m] = t: the MatMul m performs
+    nodes m+1 .. m+t in its launch): the intermediate results never reach
+    memory and get no buffer; the launch reads the MatMul's operands while
+    it writes node m+t's output, so their lifetimes run at least to m+t.
 """
 from __future__ import annotations
 
@@ -46,8 +50,9 @@ class ArenaPlan:
         self.peak = peak
 
 
-def buffers_and_lifetimes(g, layout_of_edge, align=256):
-    """Roots, arena buffers, sizes and lifetimes under the given layouts."""
+def buffers_and_lifetimes(g, layout_of_edge, align=256, fuse=None):
+    """Roots, arena buffers, sizes and lifetimes under the given layouts
+    (and the plan's fused chains, if any)."""
     isz = numerics.itemsize(g.dtype)
     root = list(range(g.n_edges))
     view = [False] * len(g.nodes)
@@ -56,8 +61,13 @@ def buffers_and_lifetimes(g, layout_of_edge, align=256):
             view[n] = True
             root[g.out_edge(n)] = root[g.act_inputs(n)[0]]
     outs = set(g.outputs)
+    on_chip, until = set(), {}
+    for m, t in enumerate(fuse or []):
+        if t:
+            on_chip.update(g.out_edge(m + i) for i in range(t))
+            until[m] = m + t
     buffers = [g.out_edge(n) for n in range(len(g.nodes))
-               if not view[n] and g.out_edge(n) not in outs]
+               if not view[n] and g.out_edge(n) not in outs and g.out_edge(n) not in on_chip]
     size = {b: align_up(int(np.prod(g.edge_shape(b))) * isz, align) for b in buffers}
     defn = {b: g.producer(b) for b in buffers}
     last = dict(defn)
@@ -66,7 +76,7 @@ def buffers_and_lifetimes(g, layout_of_edge, align=256):
             if v >= 0:
                 r = root[v]
                 if r in last:
-                    last[r] = max(last[r], n)
+                    last[r] = max(last[r], until.get(n, n))
     return root, buffers, size, defn, last
 
 
@@ -95,8 +105,8 @@ def greedy_by_size(buffers, size, defn, last):
     return offset, peak
 
 
-def plan_arena(g, layout_of_edge, align=256):
-    root, buffers, size, defn, last = buffers_and_lifetimes(g, layout_of_edge, align)
+def plan_arena(g, layout_of_edge, align=256, fuse=None):
+    root, buffers, size, defn, last = buffers_and_lifetimes(g, layout_of_edge, align, fuse)
     offset, peak = greedy_by_size(buffers, size, defn, last)
     return ArenaPlan(root, buffers, size, defn, last, offset, peak)
 

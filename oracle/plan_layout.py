@@ -39,12 +39,14 @@ import itertools
 
 import numpy as np
 
+from . import fusion
 from .costtable import INF
 from .layouts import node_is_view
 
 NO_DP = 1
 NO_VARIANTS = 2
 NO_GUARD = 4
+NO_FUSION = 8
 
 
 class Infeasible(Exception):
@@ -149,18 +151,11 @@ def _allowed(L, FIX, e):
     return [FIX[e]] if e in FIX else list(range(len(L[e])))
 
 
-def _node_gain(g, ct, use_v0, info, j, FIX):
-    """G[a, b] = min over boundary layouts beta of C[n][...], and the argmin
-    beta (lexicographically smallest on ties).  a ranges over the chain
-    edge's full candidate list (size 1 axis when j == 0)."""
-    n = info.path[j]
-    slots = g.act_inputs(n)
-    L = ct.L
-    C = ct.nodes[n].v0 if use_v0 else ct.nodes[n].best
-    cs = info.chain_slot[j]
-    chain_edge = slots[cs] if cs is not None else None
-    be = info.bnd_edges[j]
-    eo = g.out_edge(n)
+def _gain(L, C, slots, chain_edge, be, eo, FIX):
+    """G[a, b] = min over boundary layouts beta of C[slot layouts..., b] with
+    the chain edge in layout a, and the argmin beta (lexicographically
+    smallest on ties).  a ranges over the chain edge's full candidate list
+    (a size-1 axis when there is no chain edge)."""
     A = len(L[chain_edge]) if chain_edge is not None else 1
     Bn = len(L[eo])
     allowed_b = [_allowed(L, FIX, e) for e in be]
@@ -171,7 +166,7 @@ def _node_gain(g, ct, use_v0, info, j, FIX):
         lay = {e: beta[i] for i, e in enumerate(be)}
         # index into C: one axis per slot, then the out axis
         idx = []
-        for s, e in enumerate(slots):
+        for e in slots:
             if chain_edge is not None and e == chain_edge:
                 idx.append(slice(None))
             else:
@@ -191,81 +186,169 @@ def _node_gain(g, ct, use_v0, info, j, FIX):
     return G, arg, betas, be
 
 
-def dp_path(g, ct, use_v0, info, FIX):
-    """Viterbi over one path.  Returns (total, states, betas) where states[j]
-    is the chosen layout index of the output of step j and betas[j] maps each
-    boundary edge of step j to its chosen layout index."""
+def _node_gain(g, ct, use_v0, info, j, FIX):
+    """The gain of step j run as its own node."""
+    n = info.path[j]
+    slots = g.act_inputs(n)
+    C = ct.nodes[n].v0 if use_v0 else ct.nodes[n].best
+    cs = info.chain_slot[j]
+    chain_edge = slots[cs] if cs is not None else None
+    return _gain(ct.L, C, slots, chain_edge, info.bnd_edges[j], g.out_edge(n), FIX)
+
+
+def fused_options(g, ct, info, j):
+    """Chain lengths t for which steps j .. j+t of the path form a fusion
+    chain with measured costs (the MatMul at step j, nodes m+1 .. m+t)."""
+    m = info.path[j]
+    out = []
+    for t in (1, 2, 3):
+        if (m, t) in ct.fused and j + t < len(info.path) and \
+                all(info.path[j + i] == m + i for i in range(1, t + 1)):
+            out.append(t)
+    return out
+
+
+def _fused_gain(g, ct, use_v0, info, j, t, FIX):
+    """The gain of steps j .. j+t run as one fused launch: a virtual node
+    whose slots are the chain's (the MatMul's activation inputs, then R) and
+    whose output is the last node's."""
+    m = info.path[j]
+    slots = fusion.chain_slots(g, m, t)
+    cs = info.chain_slot[j]
+    chain_edge = g.act_inputs(m)[cs] if cs is not None else None
+    be = []
+    for e in slots:
+        if e != chain_edge and e not in be:
+            be.append(e)
+    NC = ct.fused[(m, t)]
+    return _gain(ct.L, NC.v0 if use_v0 else NC.best, slots, chain_edge, be, g.out_edge(m + t), FIX)
+
+
+def dp_path(g, ct, use_v0, info, FIX, fuse=True):
+    """Viterbi over one path.  Returns (total, states, betas, fused) where
+    states[j] is the chosen layout index of the output of step j (0 for a
+    result a fused launch keeps on chip), betas[j] maps each boundary edge
+    of step j to its chosen layout index, and fused[j] is the length t of
+    the fused chain starting at step j (0 when step j runs on its own).
+
+    A step's output layout b is reached either by the step's own node from
+    the previous step's layout a, or -- when fusion chains are priced -- by
+    the fused launch of the chain ending there, from the layout a of the
+    step before the chain.  Ties: the lower cost, then the shorter
+    transition (a node on its own first), then the smaller a."""
     L = ct.L
     m = len(info.path)
-    Vs, backs, gains = [], [], []
-    V = None
+    opts = [fused_options(g, ct, info, j) if fuse else [] for j in range(m)]
+    Vs, backs, choices = [], [], []
     for j in range(m):
         n = info.path[j]
         eo = g.out_edge(n)
-        G, arg, betas, be = _node_gain(g, ct, use_v0, info, j, FIX)
         allowed_out = _allowed(L, FIX, eo)
         mask_b = np.full(len(L[eo]), True)
         mask_b[allowed_out] = False
-        G = np.where(mask_b[None, :], INF, G)
-        if j == 0:
-            Vn = G[0].copy()
-            back = np.full(len(L[eo]), -1, dtype=np.int64)
-        else:
-            tot = sat_add(V[:, None], G)                # [a, b]
-            back = np.argmin(tot, axis=0)               # first = smallest a
-            Vn = tot[back, np.arange(tot.shape[1])]
+        cands = []   # (t, start, G, arg, betas, be)
+        G, arg, betas, be = _node_gain(g, ct, use_v0, info, j, FIX)
+        cands.append((0, j, G, arg, betas, be))
+        for s in range(j - 1, max(0, j - 3) - 1, -1):    # t = 1, 2, 3
+            t = j - s
+            if t in opts[s]:
+                Gf, argf, betasf, bef = _fused_gain(g, ct, use_v0, info, s, t, FIX)
+                cands.append((t, s, Gf, argf, betasf, bef))
+        Vn = np.full(len(L[eo]), INF, dtype=np.int64)
+        back = [(0, -1)] * len(L[eo])
+        for t, s, G, arg, betas, be in cands:
+            G = np.where(mask_b[None, :], INF, G)
+            if s == 0:
+                tot = G[0]
+                aa = np.zeros(len(L[eo]), dtype=np.int64)
+            else:
+                full = sat_add(Vs[s - 1][:, None], G)     # [a, b]
+                aa = np.argmin(full, axis=0)               # first = smallest a
+                tot = full[aa, np.arange(full.shape[1])]
+            for b in range(len(L[eo])):
+                if tot[b] < Vn[b]:
+                    Vn[b] = tot[b]
+                    back[b] = (t, int(aa[b]))
         Vs.append(Vn)
         backs.append(back)
-        gains.append((arg, betas, be))
-        V = Vn
-    total = int(V.min())
-    b = int(np.argmin(V))
+        choices.append({t: (s, arg, betas, be) for t, s, G, arg, betas, be in cands})
+    total = int(Vs[-1].min())
+    b = int(np.argmin(Vs[-1]))
     states = [0] * m
-    chosen_a = [0] * m
-    for j in range(m - 1, -1, -1):
+    fused = [0] * m
+    bsel = [dict() for _ in range(m)]
+    j = m - 1
+    while j >= 0:
+        t, a = backs[j][b]
+        s, arg, betas, be = choices[j][t]
         states[j] = b
-        a = int(backs[j][b]) if j > 0 else 0
-        chosen_a[j] = a
-        b = a
-    bsel = []
-    for j in range(m):
-        arg, betas, be = gains[j]
-        bi = int(arg[chosen_a[j] if j > 0 else 0, states[j]])
+        bi = int(arg[a if s > 0 else 0, b])
         beta = betas[bi] if bi >= 0 else tuple(0 for _ in be)
-        bsel.append({e: beta[i] for i, e in enumerate(be)})
-    return total, states, bsel
+        chosen = {e: beta[i] for i, e in enumerate(be)}
+        # a boundary edge's layout is recorded at every step of the launch
+        # that reads it as a boundary edge
+        for k in range(s, j + 1):
+            bsel[k] = {e: chosen[e] for e in info.bnd_edges[k] if e in chosen}
+        fused[s] = t
+        j = s - 1
+        b = a
+    return total, states, bsel, fused
 
 
 # ---------------------------------------------------------------- full plan
 class LayoutPlan:
-    def __init__(self, layout_idx, variant, total, guard_used, paths):
+    def __init__(self, layout_idx, variant, total, guard_used, paths, fuse=None):
         self.layout_idx = layout_idx    # per edge
-        self.variant = variant          # per node
+        self.variant = variant          # per node (-1 view, -2 performed in a MatMul's fused launch)
         self.total = total
         self.guard_used = guard_used
         self.paths = paths
+        self.fuse = fuse or [0] * len(variant)   # per node: chain length of a fused MatMul, else 0
 
 
 def _node_key(g, n, lay):
     return tuple(lay[e] for e in g.act_inputs(n)) + (lay[g.out_edge(n)],)
 
 
-def plan_cost(g, ct, use_v0, lay):
+def _chain_key(g, m, t, lay):
+    return tuple(lay[e] for e in fusion.chain_slots(g, m, t)) + (lay[g.out_edge(m + t)],)
+
+
+def plan_cost(g, ct, use_v0, lay, fuse=None):
+    """Summed table cost of a plan: every node on its own, except the fused
+    chains (fuse[m] = t), which cost their fused entry."""
+    fuse = fuse or [0] * len(g.nodes)
     total = 0
-    for n in range(len(g.nodes)):
+    n = 0
+    while n < len(g.nodes):
+        if fuse[n]:
+            NC = ct.fused[(n, fuse[n])]
+            C = NC.v0 if use_v0 else NC.best
+            total = int(sat_add(total, C[_chain_key(g, n, fuse[n], lay)]))
+            n += fuse[n] + 1
+            continue
         C = ct.nodes[n].v0 if use_v0 else ct.nodes[n].best
         total = int(sat_add(total, C[_node_key(g, n, lay)]))
+        n += 1
     return total
 
 
-def _variants(g, ct, use_v0, lay):
+def _variants(g, ct, use_v0, lay, fuse=None):
+    fuse = fuse or [0] * len(g.nodes)
     perm_of = {e: ct.L[e][lay[e]] for e in range(g.n_edges)}
     out = []
+    absorbed = set()
+    for m, t in enumerate(fuse):
+        absorbed.update(range(m + 1, m + t + 1))
     for n in range(len(g.nodes)):
-        if node_is_view(g, n, perm_of):
+        if n in absorbed:
+            out.append(-2)
+        elif node_is_view(g, n, perm_of):
             out.append(-1)
         elif use_v0:
             out.append(0)
+        elif fuse[n]:
+            out.append(int(ct.fused[(n, fuse[n])].var[_chain_key(g, n, fuse[n], lay)]))
         else:
             out.append(int(ct.nodes[n].var[_node_key(g, n, lay)]))
     return out
@@ -273,6 +356,7 @@ def _variants(g, ct, use_v0, lay):
 
 def plan_layouts(g, ct, flags=0):
     use_v0 = bool(flags & NO_VARIANTS)
+    fz = not (flags & NO_FUSION)
     paths = split(g)
     ident = [0] * g.n_edges
     ident_cost = plan_cost(g, ct, use_v0, ident)
@@ -295,8 +379,8 @@ def plan_layouts(g, ct, flags=0):
     pinned = set(range(g.n_inputs)) | set(g.outputs)
 
     FIX = {}
-    first = [dp_path(g, ct, use_v0, info, FIX) for info in infos]
-    for pi, (tot, _, _) in enumerate(first):
+    first = [dp_path(g, ct, use_v0, info, FIX, fz) for info in infos]
+    for pi, (tot, _, _, _) in enumerate(first):
         if tot >= INF:
             raise Infeasible(f"path {pi} has no feasible layout")
 
@@ -329,21 +413,23 @@ def plan_layouts(g, ct, flags=0):
                 F2[e] = l
                 c = 0
                 for pi in touch:
-                    c = int(sat_add(c, dp_path(g, ct, use_v0, infos[pi], F2)[0]))
+                    c = int(sat_add(c, dp_path(g, ct, use_v0, infos[pi], F2, fz)[0]))
                 if best is None or c < best:
                     best, win = c, l
         FIX[e] = win
 
     lay = list(ident)
+    fuse = [0] * len(g.nodes)
     for pi, info in enumerate(infos):
-        tot, states, _ = dp_path(g, ct, use_v0, info, FIX)
+        tot, states, _, fz_path = dp_path(g, ct, use_v0, info, FIX, fz)
         if tot >= INF:
             if flags & NO_GUARD:
                 raise Infeasible(f"path {pi} infeasible after the vote")
             return LayoutPlan(ident, _variants(g, ct, use_v0, ident), ident_cost, 1, paths)
         for j, n in enumerate(info.path):
             lay[g.out_edge(n)] = states[j]
-    total = plan_cost(g, ct, use_v0, lay)
+            fuse[n] = fz_path[j]
+    total = plan_cost(g, ct, use_v0, lay, fuse)
     if not (flags & NO_GUARD) and total > ident_cost:
         return LayoutPlan(ident, _variants(g, ct, use_v0, ident), ident_cost, 1, paths)
-    return LayoutPlan(lay, _variants(g, ct, use_v0, lay), total, 0, paths)
+    return LayoutPlan(lay, _variants(g, ct, use_v0, lay, fuse), total, 0, paths, fuse)

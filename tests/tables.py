@@ -119,3 +119,24 @@ def fanout_costs(infeasible_after_vote=False):
         add3,                                                    # s
         {k: v for k, v in add3.items() if k[2] == 0},            # y (pinned)
     ]
+
+
+def add_fused(obj, g, seed, n_variants=3, lo=1, hi=1000, scale=1.0):
+    """Adds random fused entries for every fusion chain of g (oracle's
+    chain rules) to a synthetic table: costs over the chain's slots and the
+    last node's output, drawn like the node entries (times `scale`)."""
+    from oracle import fusion
+    rng = np.random.default_rng(seed + 12345)
+    L = layouts.edge_layouts(g)
+    obj["fused_sigs"], obj["fused"] = [], []
+    for (m, t), nodes in sorted(fusion.all_chains(g).items()):
+        slots = fusion.chain_slots(g, m, t)
+        eo = g.out_edge(m + t)
+        entries = []
+        for combo in __import__("itertools").product(*[L[e] for e in slots], L[eo]):
+            costs = [int(scale * rng.integers(lo, hi + 1)) for _ in range(n_variants)]
+            entries.append([[list(p) for p in combo[:-1]], list(combo[-1]), costs])
+        obj["fused"].append([m, t, len(obj["fused_sigs"])])
+        obj["fused_sigs"].append({"op": "matmul", "steps": t, "in_shapes": [list(g.edge_shape(e)) for e in slots],
+                                  "out_shape": list(g.edge_shape(eo)), "entries": entries})
+    return obj

@@ -142,8 +142,8 @@ def test_hand_worked_vote_with_cost_tie_breaks():
     paths = PL.split(g)
     assert paths == [[0, 1, 3, 4, 5], [2]]
     infos = [PL.PathInfo(g, p) for p in paths]
-    t0, s0, b0 = PL.dp_path(g, ct, False, infos[0], {})
-    t1, s1, b1 = PL.dp_path(g, ct, False, infos[1], {})
+    t0, s0, b0, _ = PL.dp_path(g, ct, False, infos[0], {})
+    t1, s1, b1, _ = PL.dp_path(g, ct, False, infos[1], {})
     assert (t0, s0) == (50, [0, 0, 0, 0, 0]) and b0[3] == {3: 0}
     assert (t1, s1) == (1, [1]) and b1[0] == {1: 1}
     plan = PL.plan_layouts(g, ct)
@@ -218,3 +218,76 @@ def test_identity_favouring_table_gives_identity_plan():
     ct = _ct(g, seed=4, mode="identity")
     p = PL.plan_layouts(g, ct)
     assert p.total <= PL.plan_cost(g, ct, False, [0] * g.n_edges)
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("layers", [1, 2])
+def test_fused_dp_on_pure_chain_equals_brute_force(seed, layers):
+    """With fusion chains priced (MatMul + bias Add + GELU per layer), the
+    per-path DP has skip transitions; on a pure chain it is still exact: its
+    total equals the minimum over every layout assignment and every set of
+    non-overlapping chains, searched exhaustively."""
+    from tables import add_fused
+    g = __import__("tinygraphs").mlp_graph(layers)
+    obj = add_fused(synthetic_table(g, seed=seed, mode="random", lo=1, hi=30), g, seed, lo=1, hi=60)
+    ct = costtable.load(obj, g)
+    plan = PL.plan_layouts(g, ct, PL.NO_GUARD)
+    assert plan.total == brute.best_layouts_fused(g, ct)
+    assert plan.total == PL.plan_cost(g, ct, False, plan.layout_idx, plan.fuse)
+    # the plan's variants: the fused entry's on the MatMul, -2 on the absorbed nodes
+    for m, t in enumerate(plan.fuse):
+        if t:
+            assert all(plan.variant[m + i] == -2 for i in range(1, t + 1))
+            assert plan.variant[m] >= 0
+
+
+def test_fusion_priced_against_running_alone():
+    """Fused entries far more expensive than the separate nodes: no chain is
+    fused and the plan is the plain DP's; far cheaper: every MatMul fuses
+    its whole chain.  NO_FUSION ignores the fused entries."""
+    from tables import add_fused
+    g = __import__("tinygraphs").mlp_graph(2)
+    base = synthetic_table(g, seed=3, mode="random", lo=1, hi=30)
+    plain = PL.plan_layouts(g, costtable.load(base, g))
+    dear = costtable.load(add_fused(json_copy(base), g, 3, lo=10 ** 6, hi=10 ** 6 + 10), g)
+    p1 = PL.plan_layouts(g, dear)
+    assert p1.fuse == [0] * len(g.nodes) and p1.total == plain.total and p1.layout_idx == plain.layout_idx
+    cheap = costtable.load(add_fused(json_copy(base), g, 3, lo=1, hi=1), g)
+    p2 = PL.plan_layouts(g, cheap)
+    assert p2.fuse == [2, 0, 0, 2, 0, 0] and p2.total == 2
+    p3 = PL.plan_layouts(g, cheap, PL.NO_FUSION)
+    assert p3.fuse == [0] * len(g.nodes) and p3.total == plain.total
+
+
+def json_copy(o):
+    import json
+    return json.loads(json.dumps(o))
+
+
+def test_fused_plan_arena_and_permuted_execution():
+    """A fused plan's arena holds no buffer for the results kept on chip,
+    keeps each fused MatMul's operands live to the chain's end, places no two
+    live buffers over each other, and the permuted execution in the poisoned
+    arena equals the row-major result."""
+    from oracle import execute, plan_arena
+    from tables import add_fused
+    import synth_inputs
+    cfg = synth_inputs.config(1, arch="post_ln", layers=1, batch=2, seq=5, hidden=6, heads=2, ffn=8)
+    g = graph.build_transformer(cfg)
+    obj = add_fused(synthetic_table(g, seed=5, mode="random", lo=1, hi=40), g, 5, lo=1, hi=40)
+    ct = costtable.load(obj, g)
+    plan = PL.plan_layouts(g, ct)
+    assert any(plan.fuse)
+    lay = {e: ct.L[e][plan.layout_idx[e]] for e in range(g.n_edges)}
+    ap = plan_arena.plan_arena(g, lay, fuse=plan.fuse)
+    assert plan_arena.check_disjoint(ap)
+    for m, t in enumerate(plan.fuse):
+        for i in range(t):
+            assert g.out_edge(m + i) not in ap.buffers
+        for v in g.act_inputs(m):
+            if v in ap.last:
+                assert ap.last[v] >= m + t
+    x, cs = synth_inputs.make_inputs(cfg, g.const_specs(), 9)
+    ref = execute.run_canonical(g, [x], cs)
+    out = execute.run_in_arena(g, lay, ap.root, ap.offset, ap.peak, [x], cs, fuse=plan.fuse)
+    assert np.array_equal(out[0], ref[0])
