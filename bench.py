@@ -252,13 +252,16 @@ def graph_ms(ex, steps, torch, marker=None):
 
 
 def ablation(F, g, table, ex, steps, torch):
-    """Layout DP and kernel variants switched on one at a time (same cost
-    table, same Greedy-by-Size arena planner): graph latency, planned table
-    total and per-operator-class times of each plan."""
+    """Layout DP, kernel variants and priced fusion chains switched on one
+    at a time (same cost table, same Greedy-by-Size arena planner): graph
+    latency, planned table total and per-operator-class times of each plan.
+    Without pricing (and without the DP) a MatMul performs the nodes after
+    it whenever its tile can (fusion by adjacency, after planning)."""
     out = {}
     for name, flags in (("identity_layouts_variant0", F.NO_DP | F.NO_VARIANTS),
                         ("identity_layouts_best_variant", F.NO_DP),
                         ("dp_layouts_variant0", F.NO_VARIANTS),
+                        ("dp_layouts_best_variant_adjacent_fusion", F.NO_FUSION),
                         ("dp_layouts_best_variant", 0)):
         lp_a = F.LayoutPlan(g, table, flags)
         ap_a = F.ArenaPlan(g, lp_a, epilogue=True)
@@ -267,7 +270,7 @@ def ablation(F, g, table, ex, steps, torch):
             ex_a.run()
         torch.cuda.synchronize()
         out[name] = {"ms_per_step": round(graph_ms(ex_a, steps, torch), 4), "table_ns": lp_a.total_ns,
-                     "launches_per_step": ex_a.launches(),
+                     "launches_per_step": ex_a.launches(), "priced_chains": sum(1 for t in lp_a.fuse if t),
                      "peak_arena_mb": round(ap_a.peak / 2**20, 3),
                      "op_ms": {op: c["ms_per_step"]
                                for op, c in op_class_rates(g, launch_units(g, ex_a), ex_a, steps, torch).items()}}
@@ -334,7 +337,7 @@ def row_major_weights(F, g, table):
         table.save(p)
         with open(p) as f:
             obj = json.load(f)
-        for sig in obj["sigs"]:
+        for sig in obj["sigs"] + obj.get("fused_sigs", []):
             if sig["op"] == "matmul":
                 for ent in sig["entries"]:
                     ent[2] = [c if v < 10 else -1 for v, c in enumerate(ent[2])]
@@ -483,6 +486,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         "paper_lifetimes_launches_per_step": F.fluid_run_launches(g.h, lp.h, apl_paper.h),
         "launches_per_step": n_launch, "naive_launches_per_step": n_launch_naive,
         "plan_table_ns": lp.total_ns, "naive_table_ns": lp_naive.total_ns, "guard_used": lp.guard_used,
+        "fusion_priced": lp.fusion_priced, "priced_chains": sum(1 for t in lp.fuse if t),
         "planned_vs_naive_max_abs_diff": agree, "cost_table_s": round(t_measure, 1),
         "roofline": roof,
         "op_classes": op_classes,

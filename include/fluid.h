@@ -212,14 +212,21 @@ fluid_status fluid_measure_costs(const fluid_graph* g, uint32_t reps, void* scra
 #define FLUID_NO_DP 1u        /* return the all-row-major plan                */
 #define FLUID_NO_VARIANTS 2u  /* plan on the variant-0 column only (ablation) */
 #define FLUID_NO_GUARD 4u     /* keep the voted plan even if it costs more    */
+#define FLUID_NO_FUSION 8u    /* ignore the table's fused entries            */
 
 /* Layout plan (Section 3, Alg. 1-3, Eq. 1 and the vote): longest-path
  * decomposition; per-path dynamic program over output layouts; majority vote
  * on edges shared between paths (ties: lowest re-optimised cost of the
  * touching paths, then lowest index); one re-optimisation with shared edges
  * fixed; then, unless FLUID_NO_GUARD, the all-row-major plan if it is
- * cheaper.  Errors: FLUID_E_INFEASIBLE (no identity entry, or no finite
- * plan), FLUID_E_INVALID. */
+ * cheaper.  Fusion (Section 4: the compiler fuses operators before it plans
+ * layouts): when the table carries fused entries, a MatMul and the bias
+ * Add / GELU or SiLU / Add or Mul with an earlier tensor right after it on
+ * its path (consecutive node ids, single readers) may run as one launch;
+ * the path DP weighs that launch's measured cost against the nodes' own
+ * (ties go to the nodes on their own), and runs then perform exactly the
+ * plan's fusions (fluid_layout_plan_fusion).  Errors: FLUID_E_INFEASIBLE
+ * (no identity entry, or no finite plan), FLUID_E_INVALID. */
 fluid_status fluid_plan_layouts(const fluid_graph* g, const fluid_cost_table* t, uint32_t flags,
                                 fluid_layout_plan** out);
 
@@ -247,6 +254,15 @@ fluid_status fluid_pack_constant(const fluid_graph* g, const fluid_layout_plan* 
  * node (n_nodes; -1 = view, no kernel), summed table cost, guard flag. */
 fluid_status fluid_layout_plan_get(const fluid_layout_plan* lp, int32_t* layout_idx_per_edge,
                                    int32_t* variant_per_node, int64_t* total_ns, int32_t* guard_used);
+/* The plan's fusions: fuse_per_node[n] (n_nodes entries) is the number t
+ * of nodes after MatMul n that its launch performs (nodes n+1 .. n+t have
+ * variant -2 and results n .. n+t-1 never reach memory), 0 otherwise;
+ * *priced is 1 when the plan priced fusion chains (fluid_run then performs
+ * exactly these fusions), 0 when it did not (FLUID_NO_FUSION, FLUID_NO_DP, or
+ * a table without fused entries: fluid_run fuses by its own rule, see
+ * fluid_run).  Either pointer may be NULL.  Both builds. */
+fluid_status fluid_layout_plan_fusion(const fluid_layout_plan* lp, int32_t* fuse_per_node, int32_t* priced);
+
 /* The permutation chosen for one edge (rank entries written to perm_out). */
 fluid_status fluid_edge_layout(const fluid_graph* g, const fluid_layout_plan* lp, int32_t edge,
                                int32_t* perm_out);
@@ -381,8 +397,10 @@ fluid_status fluid_run_schedule(const fluid_graph* g, const fluid_layout_plan* l
 fluid_status fluid_trace_enable(const fluid_graph* g, const uint8_t* node_mask, int32_t max_records);
 fluid_status fluid_trace_collect(const fluid_graph* g, double* ms_per_node, int32_t* launches_per_node);
 
-/* Name of the kernel a node runs under a plan ("view" for views), e.g.
- * "gemm_f32_m128n128_ak_bn_cn". */
+/* Name of the kernel a node runs under a plan, e.g.
+ * "gemm_f32_m128n128_ak_bn_cn": "view" for views, "fused" for a node the
+ * plan performs inside the launch of the MatMul before it (variant -2);
+ * the MatMul's own name is that of its unfused product. */
 fluid_status fluid_node_kernel(const fluid_graph* g, const fluid_layout_plan* lp, int32_t node,
                                char* buf, uint64_t cap);
 

@@ -31,6 +31,16 @@ two implementations agree bit for bit):
   * Re-optimisation: one more DP of every path with all shared edges fixed.
   * Guard (an addition): if the result costs more than the all-row-major
     plan on the same table, the row-major plan is returned.
+  * Fusion chains (an addition, see fusion.py), when the table prices them:
+    the path DP may also step over a chain, the chain's fused entry standing
+    in for its nodes' own.  After the vote, the chains are chosen anew for
+    the final layouts, exactly: chains are runs of consecutive node ids, so
+    the cheapest set of disjoint chains is an interval DP over node ids
+    (ties: a node on its own, then the shorter chain).  Two voted layout
+    assignments compete -- the one from the fusion-aware DP and the one
+    from the plain DP (the paper's) -- each with its best chains; the
+    cheaper total wins, the fusion-aware one on ties.  The guard compares
+    with the row-major plan with its best chains.
 Costs are integers (nanoseconds); +infinity is 2**62 with saturating sums.
 """
 from __future__ import annotations
@@ -255,7 +265,7 @@ def dp_path(g, ct, use_v0, info, FIX, fuse=True):
                 Gf, argf, betasf, bef = _fused_gain(g, ct, use_v0, info, s, t, FIX)
                 cands.append((t, s, Gf, argf, betasf, bef))
         Vn = np.full(len(L[eo]), INF, dtype=np.int64)
-        back = [(0, -1)] * len(L[eo])
+        back = [(0, 0)] * len(L[eo])
         for t, s, G, arg, betas, be in cands:
             G = np.where(mask_b[None, :], INF, G)
             if s == 0:
@@ -266,7 +276,9 @@ def dp_path(g, ct, use_v0, info, FIX, fuse=True):
                 aa = np.argmin(full, axis=0)               # first = smallest a
                 tot = full[aa, np.arange(full.shape[1])]
             for b in range(len(L[eo])):
-                if tot[b] < Vn[b]:
+                # the node on its own always sets the state (also at +inf);
+                # a fused launch replaces it only when strictly cheaper
+                if t == 0 or tot[b] < Vn[b]:
                     Vn[b] = tot[b]
                     back[b] = (t, int(aa[b]))
         Vs.append(Vn)
@@ -285,6 +297,8 @@ def dp_path(g, ct, use_v0, info, FIX, fuse=True):
         bi = int(arg[a if s > 0 else 0, b])
         beta = betas[bi] if bi >= 0 else tuple(0 for _ in be)
         chosen = {e: beta[i] for i, e in enumerate(be)}
+        if s > 0:   # a boundary read of the launch's chain edge sees layout a
+            chosen.setdefault(g.act_inputs(info.path[s])[info.chain_slot[s]], a)
         # a boundary edge's layout is recorded at every step of the launch
         # that reads it as a boundary edge
         for k in range(s, j + 1):
@@ -365,7 +379,62 @@ def plan_layouts(g, ct, flags=0):
     if flags & NO_DP:
         return LayoutPlan(ident, _variants(g, ct, use_v0, ident), ident_cost, 0, paths)
 
+    priced = fz and bool(ct.fused)
+    if priced:
+        ident_fuse = best_chains(g, ct, use_v0, ident)
+        ident_cost = plan_cost(g, ct, use_v0, ident, ident_fuse)
+    else:
+        ident_fuse = None
     infos = [PathInfo(g, p) for p in paths]
+    cands = []
+    for fz_dp in ((True, False) if priced else (False,)):
+        lay = _voted_layouts(g, ct, use_v0, paths, infos, fz_dp)
+        if lay is None:
+            continue
+        fuse = best_chains(g, ct, use_v0, lay) if priced else None
+        cands.append((plan_cost(g, ct, use_v0, lay, fuse), lay, fuse))
+    if not cands:
+        if flags & NO_GUARD:
+            raise Infeasible("every path plan is infeasible after the vote")
+        return LayoutPlan(ident, _variants(g, ct, use_v0, ident, ident_fuse), ident_cost, 1, paths, ident_fuse)
+    total, lay, fuse = min(cands, key=lambda c: c[0])   # the first on ties
+    if not (flags & NO_GUARD) and total > ident_cost:
+        return LayoutPlan(ident, _variants(g, ct, use_v0, ident, ident_fuse), ident_cost, 1, paths, ident_fuse)
+    return LayoutPlan(lay, _variants(g, ct, use_v0, lay, fuse), total, 0, paths, fuse)
+
+
+def best_chains(g, ct, use_v0, lay):
+    """The cheapest set of disjoint fusion chains for fixed layouts: per
+    node, fuse[m] = t for a chain (m, t) run as one launch, else 0.  Chains
+    cover consecutive node ids, so this is an interval DP from the last node
+    back: f(n) = min(cost of n on its own + f(n+1), min over chains (n, t) of
+    their fused entry + f(n+t+1)); ties keep the node on its own, then the
+    shorter chain."""
+    N = len(g.nodes)
+    f = [0] * (N + 1)
+    pick = [0] * N
+    for n in range(N - 1, -1, -1):
+        C = ct.nodes[n].v0 if use_v0 else ct.nodes[n].best
+        f[n] = int(sat_add(C[_node_key(g, n, lay)], f[n + 1]))
+        t = 1
+        while (n, t) in ct.fused:
+            NC = ct.fused[(n, t)]
+            c = int(sat_add((NC.v0 if use_v0 else NC.best)[_chain_key(g, n, t, lay)], f[n + t + 1]))
+            if c < f[n]:
+                f[n], pick[n] = c, t
+            t += 1
+    fuse = [0] * N
+    n = 0
+    while n < N:
+        fuse[n] = pick[n]
+        n += pick[n] + 1
+    return fuse
+
+
+def _voted_layouts(g, ct, use_v0, paths, infos, fz):
+    """The first DP of every path, the vote on shared edges and the
+    re-optimisation with the voted layouts fixed: the layout index per edge,
+    or None when a path has no feasible plan after the vote."""
     owner = {}
     for pi, p in enumerate(paths):
         for n in p:
@@ -418,18 +487,11 @@ def plan_layouts(g, ct, flags=0):
                     best, win = c, l
         FIX[e] = win
 
-    lay = list(ident)
-    fuse = [0] * len(g.nodes)
-    for pi, info in enumerate(infos):
-        tot, states, _, fz_path = dp_path(g, ct, use_v0, info, FIX, fz)
+    lay = [0] * g.n_edges
+    for info in infos:
+        tot, states, _, _ = dp_path(g, ct, use_v0, info, FIX, fz)
         if tot >= INF:
-            if flags & NO_GUARD:
-                raise Infeasible(f"path {pi} infeasible after the vote")
-            return LayoutPlan(ident, _variants(g, ct, use_v0, ident), ident_cost, 1, paths)
+            return None
         for j, n in enumerate(info.path):
             lay[g.out_edge(n)] = states[j]
-            fuse[n] = fz_path[j]
-    total = plan_cost(g, ct, use_v0, lay, fuse)
-    if not (flags & NO_GUARD) and total > ident_cost:
-        return LayoutPlan(ident, _variants(g, ct, use_v0, ident), ident_cost, 1, paths)
-    return LayoutPlan(lay, _variants(g, ct, use_v0, lay, fuse), total, 0, paths, fuse)
+    return lay

@@ -17,6 +17,7 @@
 #include <tuple>
 #include <vector>
 
+#include "../host/fusion.h"
 #include "../host/handles.h"
 #include "../host/layouts.h"
 #include "../host/prepare.h"
@@ -356,40 +357,58 @@ fluid_status fluid_run_nodes(const fluid_graph* gh, const fluid_layout_plan* lh,
       require(found != nullptr, "fluid_run_nodes: node " + std::to_string(n) + " is a view under this plan");
       sel.push_back(found);
     }
-    Bases B{(char*)arena, inputs, outputs, consts};
-    hipStream_t s = (hipStream_t)hip_stream;
+    // what the list launches, decided and checked before the first launch:
     // a fused MatMul followed in the list by every node it absorbs runs as in
     // fluid_run, and so does a grouped launch whose nodes (the products and
     // the nodes they absorb) all follow in fluid_run's order; otherwise each
-    // node runs its own kernel
+    // node runs its own kernel -- which a node the plan performs only inside
+    // a fused launch (a priced fusion chain) does not have, and which would
+    // touch a tensor the plan keeps on chip when it is such a chain's MatMul
+    enum { OWN, CHAIN, GROUP };
+    std::vector<std::pair<const PreparedNode*, int>> todo;
     const PreparedNode* first = prep->nodes.data();
-    for (int32_t r = 0; r < repeat; ++r)
-      for (size_t i = 0; i < sel.size(); ++i) {
-        const PreparedNode* pn = sel[i];
-        if (!pn->group.empty()) {
-          const size_t last = (size_t)pn->group.back();
-          const size_t span = last + prep->nodes[last].fuse_n - (size_t)(pn - first) + 1;
-          bool whole = i + span <= sel.size();
-          for (size_t t = 0; whole && t < span; ++t) whole = sel[i + t] == pn + t;
-          if (whole) {
-            const NodeKernel k = launch_kernel(*pn, B);
-            const hipError_t e = launch_group(*prep, *pn, k, B, s);
-            if (e != hipSuccess)
-              fail(FLUID_E_HIP, "node " + std::to_string(pn->node) + " (" + k.name() + "): " + hipGetErrorString(e));
-            i += span - 1;
-            continue;
-          }
-        }
-        NodeKernel k = pn->k;
-        bool whole = pn->fuse_n > 0 && i + pn->fuse_n < sel.size();
-        for (int f = 1; whole && f <= pn->fuse_n; ++f) whole = sel[i + f] == pn + f;
+    auto stored = [](const Bind& b) { return b.kind != BK_ARENA || b.off >= 0; };
+    for (size_t i = 0; i < sel.size(); ++i) {
+      const PreparedNode* pn = sel[i];
+      if (!pn->group.empty()) {
+        const size_t last = (size_t)pn->group.back();
+        const size_t span = last + prep->nodes[last].fuse_n - (size_t)(pn - first) + 1;
+        bool whole = i + span <= sel.size();
+        for (size_t t = 0; whole && t < span; ++t) whole = sel[i + t] == pn + t;
         if (whole) {
-          k = fused_kernel(*pn, B);
-          i += pn->fuse_n;
-        } else {
-          patch(k, *pn, B);
+          todo.push_back({pn, GROUP});
+          i += span - 1;
+          continue;
         }
-        hipError_t e = launch_node_kernel(k, s);
+      }
+      bool whole = pn->fuse_n > 0 && i + pn->fuse_n < sel.size();
+      for (int f = 1; whole && f <= pn->fuse_n; ++f) whole = sel[i + f] == pn + f;
+      if (whole) {
+        todo.push_back({pn, CHAIN});
+        i += pn->fuse_n;
+        continue;
+      }
+      bool ok = pn->k.available && stored(pn->out);
+      for (const Bind& b : pn->in) ok = ok && stored(b);
+      require(ok, "fluid_run_nodes: node " + std::to_string(pn->node) +
+                      " belongs to a fusion chain whose intermediate results the plan keeps on chip; list the "
+                      "chain's nodes together, in node order");
+      todo.push_back({pn, OWN});
+    }
+    Bases B{(char*)arena, inputs, outputs, consts};
+    hipStream_t s = (hipStream_t)hip_stream;
+    for (int32_t r = 0; r < repeat; ++r)
+      for (const auto& [pn, mode] : todo) {
+        NodeKernel k = pn->k;
+        hipError_t e;
+        if (mode == GROUP) {
+          k = launch_kernel(*pn, B);
+          e = launch_group(*prep, *pn, k, B, s);
+        } else {
+          if (mode == CHAIN) k = fused_kernel(*pn, B);
+          else patch(k, *pn, B);
+          e = launch_node_kernel(k, s);
+        }
         if (e != hipSuccess)
           fail(FLUID_E_HIP, "node " + std::to_string(pn->node) + " (" + k.name() + "): " + hipGetErrorString(e));
       }
@@ -487,6 +506,42 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
       hipEvent_t* ev;
       ~EvGuard() { for (int i = 0; i < 128; ++i) (void)hipEventDestroy(ev[i]); }
     } evg{ev};
+    // one candidate: an untimed warm-up launch (the first launch of a kernel
+    // instance also loads its code, which can take milliseconds), then one
+    // launch timed on its own -- clearly losing candidates (over 8x the
+    // signature's best so far) get no more launches -- then three batches
+    // of R back-to-back launches between two events (the per-launch time
+    // includes the kernel's start-up and the gap to the next launch, as in
+    // a run); the median, in integer ns
+    auto time_kernel = [&](const NodeKernel& k, int64_t& best_so_far) -> int64_t {
+      hip_check(launch_node_kernel(k, s), "warm-up launch");
+      hip_check(hipEventRecord(ev[0], s), "hipEventRecord");
+      hip_check(launch_node_kernel(k, s), "first timed launch");
+      hip_check(hipEventRecord(ev[1], s), "hipEventRecord");
+      hip_check(hipEventSynchronize(ev[1]), "hipEventSynchronize");
+      float first = 0.f;
+      hip_check(hipEventElapsedTime(&first, ev[0], ev[1]), "hipEventElapsedTime");
+      std::vector<float> times = {first};
+      const int64_t first_ns = (int64_t)std::llround((double)first * 1e6);
+      if (!(best_so_far >= 0 && first_ns > 8 * best_so_far)) {
+        times.clear();
+        for (int b = 0; b < 3; ++b) {
+          hip_check(hipEventRecord(ev[2 + 2 * b], s), "hipEventRecord");
+          for (uint32_t r = 0; r < R; ++r) hip_check(launch_node_kernel(k, s), "timed launch");
+          hip_check(hipEventRecord(ev[3 + 2 * b], s), "hipEventRecord");
+        }
+        hip_check(hipEventSynchronize(ev[7]), "hipEventSynchronize");
+        for (int b = 0; b < 3; ++b) {
+          float ms = 0.f;
+          hip_check(hipEventElapsedTime(&ms, ev[2 + 2 * b], ev[3 + 2 * b]), "hipEventElapsedTime");
+          times.push_back(ms / (float)R);
+        }
+      }
+      std::sort(times.begin(), times.end());
+      const int64_t ns_ = std::max<int64_t>(1, (int64_t)std::llround((double)times[times.size() / 2] * 1e6));
+      if (best_so_far < 0 || ns_ < best_so_far) best_so_far = ns_;
+      return ns_;
+    };
     char* base = (char*)scratch;
     for (size_t si = 0; si < rep_node.size(); ++si) {
       const int n = rep_node[si];
@@ -540,40 +595,7 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
               if (nd.ins[s2] < 0) vins[s2].stride = const_strides(nd, (int)s2, v, vins[s2].shape);
             NodeKernel k = prepare_node(nd, v, g.dtype, vins, ou);
             if (!k.available) { en.costs.push_back(-1); continue; }
-            // an untimed warm-up launch (the first launch of a kernel
-            // instance also loads its code, which can take milliseconds),
-            // then one launch timed on its own: clearly losing combinations
-            // get no more launches
-            hip_check(launch_node_kernel(k, s), "warm-up launch");
-            hip_check(hipEventRecord(ev[0], s), "hipEventRecord");
-            hip_check(launch_node_kernel(k, s), "first timed launch");
-            hip_check(hipEventRecord(ev[1], s), "hipEventRecord");
-            hip_check(hipEventSynchronize(ev[1]), "hipEventSynchronize");
-            float first = 0.f;
-            hip_check(hipEventElapsedTime(&first, ev[0], ev[1]), "hipEventElapsedTime");
-            std::vector<float> times = {first};
-            const int64_t first_ns = (int64_t)std::llround((double)first * 1e6);
-            if (!(best_so_far >= 0 && first_ns > 8 * best_so_far)) {
-              // three batches of R back-to-back launches between two events:
-              // the per-launch time includes the kernel's start-up and the
-              // gap to the next launch, as in a run, and no event overhead
-              times.clear();
-              for (int b = 0; b < 3; ++b) {
-                hip_check(hipEventRecord(ev[2 + 2 * b], s), "hipEventRecord");
-                for (uint32_t r = 0; r < R; ++r) hip_check(launch_node_kernel(k, s), "timed launch");
-                hip_check(hipEventRecord(ev[3 + 2 * b], s), "hipEventRecord");
-              }
-              hip_check(hipEventSynchronize(ev[7]), "hipEventSynchronize");
-              for (int b = 0; b < 3; ++b) {
-                float ms = 0.f;
-                hip_check(hipEventElapsedTime(&ms, ev[2 + 2 * b], ev[3 + 2 * b]), "hipEventElapsedTime");
-                times.push_back(ms / (float)R);
-              }
-            }
-            std::sort(times.begin(), times.end());
-            const int64_t ns_ = std::max<int64_t>(1, (int64_t)std::llround((double)times[times.size() / 2] * 1e6));
-            en.costs.push_back(ns_);
-            if (best_so_far < 0 || ns_ < best_so_far) best_so_far = ns_;
+            en.costs.push_back(time_kernel(k, best_so_far));
           }
         }
         sig.entries.push_back(std::move(en));
@@ -586,6 +608,134 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
         if (i < 0) break;
       }
       t.sigs.push_back(std::move(sig));
+    }
+    // fusion chains (fusion.h): one fused signature per (MatMul signature,
+    // epilogue steps); the MatMul's slots and R laid out as for the node,
+    // R in the output's layout only (a fused launch reading R in another
+    // layout than it writes is never the cheap way to run the chain)
+    {
+      struct FusedKey {
+        SigKey k;
+        uint32_t act, rop, bias;
+        bool operator<(const FusedKey& o) const {
+          return std::tie(k, act, rop, bias) < std::tie(o.k, o.act, o.rop, o.bias);
+        }
+      };
+      std::map<FusedKey, int> fsig_of;
+      std::vector<std::pair<int, int>> rep_chain;  // (m, t) per fused signature
+      std::vector<std::vector<std::vector<Perm>>> fslot_lists;
+      std::vector<std::vector<Perm>> fout_lists;
+      for (int m = 0; m < g.n_nodes(); ++m) {
+        const std::vector<ChainStep> steps = chain_steps(g, m);
+        FusedKey fk{sig_key(g, m), 0u, 0u, 0u};
+        for (int tl = 1; tl <= (int)steps.size(); ++tl) {
+          const ChainStep& st = steps[tl - 1];
+          if (st.kind == CH_BIAS) fk.bias = 1u;
+          else if (st.kind == CH_ACT) fk.act = g.nodes[st.node].op == FLUID_OP_GELU ? 1u : 2u;
+          else fk.rop = st.kind == CH_ADD_R ? 1u : 2u;
+          auto it = fsig_of.find(fk);
+          if (it == fsig_of.end()) {
+            it = fsig_of.emplace(fk, (int)rep_chain.size()).first;
+            rep_chain.push_back({m, tl});
+            fslot_lists.emplace_back();
+            fout_lists.emplace_back();
+          }
+          const int fi = it->second;
+          t.fused_refs.push_back({m, tl, fi});
+          const std::vector<int> slots = chain_slots(g, m, tl);
+          auto& sl = fslot_lists[fi];
+          if (sl.empty()) sl.resize(slots.size());
+          for (size_t s2 = 0; s2 < slots.size(); ++s2)
+            if (t.L[slots[s2]].size() > sl[s2].size()) sl[s2] = t.L[slots[s2]];
+          const int eo = g.out_edge(m + tl);
+          if (t.L[eo].size() > fout_lists[fi].size()) fout_lists[fi] = t.L[eo];
+        }
+      }
+      for (size_t fi = 0; fi < rep_chain.size(); ++fi) {
+        const int m = rep_chain[fi].first, tl = rep_chain[fi].second;
+        const Node& mn = g.nodes[m];
+        const std::vector<ChainStep> steps = chain_steps(g, m);
+        uint32_t act = 0, rop = 0;
+        int bias = -1;
+        for (int i = 0; i < tl; ++i) {
+          if (steps[i].kind == CH_BIAS) bias = steps[i].bias;
+          else if (steps[i].kind == CH_ACT) act = g.nodes[steps[i].node].op == FLUID_OP_GELU ? 1u : 2u;
+          else rop = steps[i].kind == CH_ADD_R ? 1u : 2u;
+        }
+        Sig sig;
+        sig.op = mn.op;
+        for (int e : chain_slots(g, m, tl)) sig.in_shapes.push_back(g.edge_shape(e));
+        sig.out_shape = g.nodes[m + tl].out_shape;
+        const auto& lists = fslot_lists[fi];
+        const auto& olist = fout_lists[fi];
+        const int nmm = (int)g.act_in[m].size();  // the MatMul's own slots; R follows
+        const int ns = (int)lists.size();
+        std::vector<size_t> idx(ns + 1, 0);
+        int64_t best_so_far = -1;
+        for (;;) {
+          SigEntry en;
+          for (int i = 0; i < ns; ++i) en.in.push_back(lists[i][idx[i]]);
+          en.out = olist[idx[ns]];
+          if (!rop || en.in[nmm] == en.out) {
+            std::vector<Operand> ins;
+            uint64_t off = 0;
+            int slot = 0;
+            for (int v : mn.ins) {
+              Operand o;
+              if (v >= 0) {
+                o.shape = g.edge_shape(v);
+                o.stride = dense_strides(o.shape, en.in[slot++]);
+                o.dtype = g.dtype;
+              } else {
+                o.shape = g.consts[~v].shape;
+                o.stride = row_major_strides(o.shape);
+                o.dtype = g.consts[~v].dtype;
+              }
+              o.ptr = base + off;
+              off = align256(off + (uint64_t)numel(o.shape) * dtype_bytes(o.dtype));
+              ins.push_back(o);
+            }
+            void* bias_ptr = nullptr;
+            if (bias >= 0) {
+              bias_ptr = base + off;
+              off = align256(off + (uint64_t)numel(g.consts[bias].shape) * dtype_bytes(g.dtype));
+            }
+            Operand r;
+            if (rop) {
+              r.shape = sig.out_shape;
+              r.stride = dense_strides(r.shape, en.in[nmm]);
+              r.dtype = g.dtype;
+              r.ptr = base + off;
+              off = align256(off + (uint64_t)numel(r.shape) * dtype_bytes(g.dtype));
+            }
+            Operand ou;
+            ou.shape = sig.out_shape;
+            ou.stride = dense_strides(ou.shape, en.out);
+            ou.dtype = g.dtype;
+            ou.ptr = base + off;
+            for (int v = 0; v < num_variants(mn.op); ++v) {
+              if (packs_weight(mn.op, v) && !packable[t.node_sig[m]]) { en.costs.push_back(-1); continue; }
+              std::vector<Operand> vins = ins;
+              for (size_t s2 = 0; s2 < mn.ins.size(); ++s2)
+                if (mn.ins[s2] < 0) vins[s2].stride = const_strides(mn, (int)s2, v, vins[s2].shape);
+              NodeKernel k = fused_gemm_kernel(mn, v, g.dtype, vins, ou, act, rop, rop ? &r : nullptr);
+              if (!k.available) { en.costs.push_back(-1); continue; }
+              k.gemm.bias = bias_ptr;
+              k.gemm.R = rop ? r.ptr : nullptr;
+              en.costs.push_back(time_kernel(k, best_so_far));
+            }
+            sig.entries.push_back(std::move(en));
+          }
+          int i = ns;
+          for (; i >= 0; --i) {
+            const size_t lim = i == ns ? olist.size() : lists[i].size();
+            if (++idx[i] < lim) break;
+            idx[i] = 0;
+          }
+          if (i < 0) break;
+        }
+        t.fused_sigs.push_back(std::move(sig));
+      }
     }
     hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
     t.bind(g);

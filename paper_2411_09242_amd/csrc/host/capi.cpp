@@ -33,6 +33,9 @@ uint64_t measure_scratch_bytes(const Graph& g) {
       s += (uint64_t)numel(sh) * b + 256;
     }
     s += (uint64_t)numel(g.nodes[n].out_shape) * isz + 256;
+    // a fused launch also reads R (the output's shape) and a bias [N]
+    if (g.nodes[n].op == FLUID_OP_MATMUL)
+      s += (uint64_t)numel(g.nodes[n].out_shape) * isz + 256 + (uint64_t)g.nodes[n].out_shape.back() * isz + 256;
     best = std::max(best, s);
   }
   return best;
@@ -161,7 +164,7 @@ fluid_status fluid_plan_layouts(const fluid_graph* g, const fluid_cost_table* t,
   return call_guarded([&] {
     require(g && t && out, "NULL argument");
     require(t->serial == g->serial, "cost table was loaded for another graph");
-    require((flags & ~7u) == 0, "unknown flags");
+    require((flags & ~15u) == 0, "unknown flags");
     auto h = std::make_unique<fluid_layout_plan>();
     h->p = plan_layouts(g->g, t->t, flags);
     h->p.graph_serial = g->serial;
@@ -177,6 +180,15 @@ fluid_status fluid_layout_plan_get(const fluid_layout_plan* lp, int32_t* lay, in
     if (var) for (size_t n = 0; n < lp->p.variant.size(); ++n) var[n] = lp->p.variant[n];
     if (total) *total = lp->p.total;
     if (guard) *guard = lp->p.guard_used;
+  });
+}
+
+fluid_status fluid_layout_plan_fusion(const fluid_layout_plan* lp, int32_t* fuse, int32_t* priced) {
+  return call_guarded([&] {
+    require(lp, "NULL plan");
+    if (fuse)
+      for (size_t n = 0; n < lp->p.fuse.size(); ++n) fuse[n] = lp->p.fuse[n];
+    if (priced) *priced = lp->p.fusion_priced ? 1 : 0;
   });
 }
 
@@ -198,9 +210,13 @@ fluid_status fluid_plan_arena(const fluid_graph* g, const fluid_layout_plan* lp,
     require(align >= 16 && (align & (align - 1)) == 0, "align must be a power of two >= 16");
     require((flags & ~3u) == 0, "unknown flags");
     auto h = std::make_unique<fluid_arena_plan>();
+    // a plan that priced fusion chains fixes the fusions and their
+    // lifetimes; otherwise FLUID_ARENA_EPILOGUE extends the lifetimes for
+    // the executor's own fusion rule
     std::vector<int> until;
-    if (flags & FLUID_ARENA_EPILOGUE) until = epilogue_reads_until(g->g, lp->p);
-    h->a = plan_arena(g->g, lp->p.perm, align, (flags & FLUID_ARENA_NO_REUSE) != 0, until);
+    if (!lp->p.fusion_priced && (flags & FLUID_ARENA_EPILOGUE)) until = epilogue_reads_until(g->g, lp->p);
+    h->a = plan_arena(g->g, lp->p.perm, align, (flags & FLUID_ARENA_NO_REUSE) != 0, until,
+                      lp->p.fusion_priced ? lp->p.fuse : std::vector<int>{});
     h->a.graph_serial = g->serial;
     h->serial = next_serial();
     *out = h.release();
@@ -306,7 +322,7 @@ fluid_status fluid_node_kernel(const fluid_graph* gh, const fluid_layout_plan* l
     require(lh->p.graph_serial == gh->serial, "plan belongs to another graph");
     const Graph& g = gh->g;
     require(node >= 0 && node < g.n_nodes(), "node out of range");
-    std::string name = "view";
+    std::string name = lh->p.variant[node] == -2 ? "fused" : "view";
     if (lh->p.variant[node] >= 0) {
       const Node& nd = g.nodes[node];
       std::vector<Operand> ins;

@@ -1,4 +1,5 @@
 #include "costtable.h"
+#include "fusion.h"
 
 #include <algorithm>
 #include <map>
@@ -49,7 +50,7 @@ CostTable cost_table_from_json(const Json& j) {
     for (const Json& p : lst.arr()) ls.push_back(perm_of(p));
     t.L.push_back(std::move(ls));
   }
-  for (const Json& sj : j.at("sigs").arr()) {
+  auto parse_sig = [&](const Json& sj) {
     Sig s;
     s.op = op_from_name(sj.at("op").s);
     if (sj.has("in_shapes"))
@@ -64,8 +65,17 @@ CostTable cost_table_from_json(const Json& j) {
       for (const Json& c : a[2].arr()) e.costs.push_back(c.as_int());
       s.entries.push_back(std::move(e));
     }
-    t.sigs.push_back(std::move(s));
-  }
+    return s;
+  };
+  for (const Json& sj : j.at("sigs").arr()) t.sigs.push_back(parse_sig(sj));
+  if (j.has("fused_sigs"))
+    for (const Json& sj : j.at("fused_sigs").arr()) t.fused_sigs.push_back(parse_sig(sj));
+  if (j.has("fused"))
+    for (const Json& f : j.at("fused").arr()) {
+      const auto& a = f.arr();
+      require(a.size() == 3, "cost table: a fused reference is [m, t, signature]");
+      t.fused_refs.push_back({(int)a[0].as_int(), (int)a[1].as_int(), (int)a[2].as_int()});
+    }
   for (const Json& v : j.at("node_sig").arr()) t.node_sig.push_back((int)v.as_int());
   return t;
 }
@@ -84,34 +94,15 @@ void CostTable::bind(const Graph& g) {
     if (g.pinned(e)) require(L[e].size() == 1, "cost table: graph input/output edges must be row-major only");
   }
   require((int)node_sig.size() == g.n_nodes(), "cost table: node count mismatch");
-  nodes.assign(g.n_nodes(), {});
-  for (int n = 0; n < g.n_nodes(); ++n) {
-    const int si = node_sig[n];
-    require(si >= 0 && si < (int)sigs.size(), "cost table: bad signature index");
-    const Sig& s = sigs[si];
-    const Node& nd = g.nodes[n];
-    const auto& slots = g.act_in[n];
-    const int eo = g.out_edge(n);
-    require(s.op == nd.op, "cost table: node " + std::to_string(n) + " op mismatch");
-    if (!s.in_shapes.empty()) {
-      require(s.in_shapes.size() == slots.size(), "cost table: node " + std::to_string(n) + " slot count");
-      for (size_t i = 0; i < slots.size(); ++i)
-        require(s.in_shapes[i] == g.edge_shape(slots[i]), "cost table: node " + std::to_string(n) + " input shape");
-    }
-    if (!s.out_shape.empty()) require(s.out_shape == nd.out_shape, "cost table: node " + std::to_string(n) + " output shape");
-    NodeCost& nc = nodes[n];
-    nc.dims.clear();
+  // dense costs over (slot layout index..., out layout index)
+  auto dense = [&](const std::vector<int>& slots, int eo, const Sig& s, const std::string& what, const Node* nd) {
+    NodeCost nc;
     std::vector<std::map<Perm, int>> index;
-    for (int e : slots) {
+    for (size_t i = 0; i <= slots.size(); ++i) {
+      const int e = i < slots.size() ? slots[i] : eo;
       nc.dims.push_back((int)L[e].size());
       std::map<Perm, int> m;
-      for (size_t i = 0; i < L[e].size(); ++i) m[L[e][i]] = (int)i;
-      index.push_back(std::move(m));
-    }
-    {
-      nc.dims.push_back((int)L[eo].size());
-      std::map<Perm, int> m;
-      for (size_t i = 0; i < L[eo].size(); ++i) m[L[eo][i]] = (int)i;
+      for (size_t k = 0; k < L[e].size(); ++k) m[L[e][k]] = (int)k;
       index.push_back(std::move(m));
     }
     size_t total = 1;
@@ -120,7 +111,7 @@ void CostTable::bind(const Graph& g) {
     nc.var.assign(total, -1);
     nc.v0.assign(total, kInf);
     for (const SigEntry& en : s.entries) {
-      require(en.in.size() == slots.size(), "cost table: node " + std::to_string(n) + " entry arity");
+      require(en.in.size() == slots.size(), "cost table: " + what + " entry arity");
       size_t flat = 0;
       bool ok = true;
       for (size_t i = 0; i <= slots.size() && ok; ++i) {
@@ -130,10 +121,9 @@ void CostTable::bind(const Graph& g) {
         flat = flat * nc.dims[i] + it->second;
       }
       if (!ok) continue;  // a layout outside this node's candidates
-      if (nd.op == FLUID_OP_TRANSPOSE || nd.op == FLUID_OP_RESHAPE) {
-        if (is_view(nd.op, nd.perm, g.edge_shape(slots[0]), nd.out_shape, en.in[0], en.out))
-          for (int64_t c : en.costs)
-            require(c <= 0, "cost table: node " + std::to_string(n) + ": a view combination must cost 0");
+      if (nd && (nd->op == FLUID_OP_TRANSPOSE || nd->op == FLUID_OP_RESHAPE)) {
+        if (is_view(nd->op, nd->perm, g.edge_shape(slots[0]), nd->out_shape, en.in[0], en.out))
+          for (int64_t c : en.costs) require(c <= 0, "cost table: " + what + ": a view combination must cost 0");
       }
       int64_t best = kInf;
       int var = -1;
@@ -145,6 +135,32 @@ void CostTable::bind(const Graph& g) {
       nc.var[flat] = var;
       nc.v0[flat] = (!en.costs.empty() && en.costs[0] >= 0) ? std::min(en.costs[0], kInf) : kInf;
     }
+    return nc;
+  };
+  nodes.assign(g.n_nodes(), {});
+  for (int n = 0; n < g.n_nodes(); ++n) {
+    const int si = node_sig[n];
+    require(si >= 0 && si < (int)sigs.size(), "cost table: bad signature index");
+    const Sig& s = sigs[si];
+    const Node& nd = g.nodes[n];
+    const auto& slots = g.act_in[n];
+    require(s.op == nd.op, "cost table: node " + std::to_string(n) + " op mismatch");
+    if (!s.in_shapes.empty()) {
+      require(s.in_shapes.size() == slots.size(), "cost table: node " + std::to_string(n) + " slot count");
+      for (size_t i = 0; i < slots.size(); ++i)
+        require(s.in_shapes[i] == g.edge_shape(slots[i]), "cost table: node " + std::to_string(n) + " input shape");
+    }
+    if (!s.out_shape.empty()) require(s.out_shape == nd.out_shape, "cost table: node " + std::to_string(n) + " output shape");
+    nodes[n] = dense(slots, g.out_edge(n), s, "node " + std::to_string(n), &nd);
+  }
+  fused.clear();
+  for (const FusedRef& f : fused_refs) {
+    const std::string what = "chain (" + std::to_string(f.m) + ", " + std::to_string(f.t) + ")";
+    require(f.m >= 0 && f.m < g.n_nodes() && f.t >= 1 && f.t <= (int)chain_steps(g, f.m).size(),
+            "cost table: " + what + " is not a fusion chain of this graph");
+    require(f.sig >= 0 && f.sig < (int)fused_sigs.size(), "cost table: bad fused signature index");
+    require(!fused.count({f.m, f.t}), "cost table: " + what + " listed twice");
+    fused[{f.m, f.t}] = dense(chain_slots(g, f.m, f.t), g.out_edge(f.m + f.t), fused_sigs[f.sig], what, nullptr);
   }
   graph_serial = 0;
 }
@@ -162,34 +178,46 @@ std::string cost_table_to_json(const CostTable& t) {
     for (size_t i = 0; i < t.L[e].size(); ++i) { if (i) o << ','; perm(t.L[e][i]); }
     o << ']';
   }
+  auto write_sigs = [&](const std::vector<Sig>& sigs) {
+    for (size_t si = 0; si < sigs.size(); ++si) {
+      const Sig& s = sigs[si];
+      o << (si ? ",\n" : "") << "{\"op\": \"" << op_name(s.op) << "\", \"in_shapes\": [";
+      for (size_t i = 0; i < s.in_shapes.size(); ++i) {
+        if (i) o << ',';
+        o << '[';
+        for (size_t k = 0; k < s.in_shapes[i].size(); ++k) o << (k ? "," : "") << s.in_shapes[i][k];
+        o << ']';
+      }
+      o << "], \"out_shape\": [";
+      for (size_t k = 0; k < s.out_shape.size(); ++k) o << (k ? "," : "") << s.out_shape[k];
+      o << "], \"entries\": [";
+      for (size_t k = 0; k < s.entries.size(); ++k) {
+        const SigEntry& en = s.entries[k];
+        o << (k ? ",\n" : "") << "[[";
+        for (size_t i = 0; i < en.in.size(); ++i) { if (i) o << ','; perm(en.in[i]); }
+        o << "],";
+        perm(en.out);
+        o << ",[";
+        for (size_t i = 0; i < en.costs.size(); ++i) o << (i ? "," : "") << en.costs[i];
+        o << "]]";
+      }
+      o << "]}";
+    }
+  };
   o << "],\n\"sigs\": [";
-  for (size_t si = 0; si < t.sigs.size(); ++si) {
-    const Sig& s = t.sigs[si];
-    o << (si ? ",\n" : "") << "{\"op\": \"" << op_name(s.op) << "\", \"in_shapes\": [";
-    for (size_t i = 0; i < s.in_shapes.size(); ++i) {
-      if (i) o << ',';
-      o << '[';
-      for (size_t k = 0; k < s.in_shapes[i].size(); ++k) o << (k ? "," : "") << s.in_shapes[i][k];
-      o << ']';
-    }
-    o << "], \"out_shape\": [";
-    for (size_t k = 0; k < s.out_shape.size(); ++k) o << (k ? "," : "") << s.out_shape[k];
-    o << "], \"entries\": [";
-    for (size_t k = 0; k < s.entries.size(); ++k) {
-      const SigEntry& en = s.entries[k];
-      o << (k ? ",\n" : "") << "[[";
-      for (size_t i = 0; i < en.in.size(); ++i) { if (i) o << ','; perm(en.in[i]); }
-      o << "],";
-      perm(en.out);
-      o << ",[";
-      for (size_t i = 0; i < en.costs.size(); ++i) o << (i ? "," : "") << en.costs[i];
-      o << "]]";
-    }
-    o << "]}";
-  }
+  write_sigs(t.sigs);
   o << "],\n\"node_sig\": [";
   for (size_t n = 0; n < t.node_sig.size(); ++n) o << (n ? "," : "") << t.node_sig[n];
-  o << "]}\n";
+  o << "]";
+  if (!t.fused_refs.empty()) {
+    o << ",\n\"fused_sigs\": [";
+    write_sigs(t.fused_sigs);
+    o << "],\n\"fused\": [";
+    for (size_t i = 0; i < t.fused_refs.size(); ++i)
+      o << (i ? "," : "") << '[' << t.fused_refs[i].m << ',' << t.fused_refs[i].t << ',' << t.fused_refs[i].sig << ']';
+    o << "]";
+  }
+  o << "}\n";
   return o.str();
 }
 

@@ -2,7 +2,9 @@
 // output layouts (Alg. 3's eval), per kernel variant.
 #pragma once
 
+#include <map>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "graph.h"
@@ -32,11 +34,21 @@ struct NodeCost {
   std::vector<int64_t> v0;       // variant-0 cost, kInf if unavailable
 };
 
+// A fused entry: the chain of MatMul node m and length t (fusion.h) costs
+// fused_sigs[sig], whose entries list the chain's slot layouts and the
+// layout of node m+t's output.
+struct FusedRef {
+  int m = 0, t = 0, sig = 0;
+};
+
 struct CostTable {
   std::vector<std::vector<Perm>> L;  // candidate layouts per edge, identity first
   std::vector<Sig> sigs;
   std::vector<int> node_sig;
-  std::vector<NodeCost> nodes;       // filled by bind()
+  std::vector<Sig> fused_sigs;
+  std::vector<FusedRef> fused_refs;
+  std::vector<NodeCost> nodes;                    // filled by bind()
+  std::map<std::pair<int, int>, NodeCost> fused;  // (m, t) -> costs, filled by bind()
   uint64_t graph_serial = 0;
 
   // Validates against g and builds the dense per-node arrays.

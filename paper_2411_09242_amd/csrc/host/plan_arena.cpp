@@ -33,17 +33,32 @@ struct Buffers {
   std::vector<uint64_t> size;
 };
 
-Buffers collect(const Graph& g, const std::vector<Perm>& perm, uint64_t align, const std::vector<int>& until) {
+Buffers collect(const Graph& g, const std::vector<Perm>& perm, uint64_t align, const std::vector<int>& until_in,
+                const std::vector<int>& fuse) {
   Buffers B;
   const int E = g.n_edges();
   B.root.resize(E);
   for (int e = 0; e < E; ++e) B.root[e] = e;
+  // fused chains: results kept on chip, operands read until the chain's end
+  std::vector<char> on_chip(E, 0);
+  std::vector<int> until = until_in;
+  if (!fuse.empty()) {
+    if (until.empty()) {
+      until.resize(g.n_nodes());
+      for (int n = 0; n < g.n_nodes(); ++n) until[n] = n;
+    }
+    for (int m = 0; m < g.n_nodes(); ++m)
+      if (fuse[m]) {
+        for (int i = 0; i < fuse[m]; ++i) on_chip[g.out_edge(m + i)] = 1;
+        until[m] = std::max(until[m], m + fuse[m]);
+      }
+  }
   std::vector<char> is_buf(E, 0);
   for (int n = 0; n < g.n_nodes(); ++n) {
     const int eo = g.out_edge(n);
     if (node_is_view(g, n, perm)) {
       B.root[eo] = B.root[g.act_in[n][0]];
-    } else if (!g.is_output[eo]) {
+    } else if (!g.is_output[eo] && !on_chip[eo]) {
       is_buf[eo] = 1;
       B.list.push_back(eo);
     }
@@ -69,8 +84,8 @@ bool overlaps(const Buffers& B, int a, int b) { return B.def[a] <= B.last[b] && 
 }  // namespace
 
 ArenaPlan plan_arena(const Graph& g, const std::vector<Perm>& perm, uint64_t align, bool no_reuse,
-                     const std::vector<int>& reads_until) {
-  Buffers B = collect(g, perm, align, reads_until);
+                     const std::vector<int>& reads_until, const std::vector<int>& fuse) {
+  Buffers B = collect(g, perm, align, reads_until, fuse);
   ArenaPlan ap;
   const int E = g.n_edges();
   ap.root = B.root;
@@ -127,7 +142,7 @@ ArenaPlan plan_arena(const Graph& g, const std::vector<Perm>& perm, uint64_t ali
   {
     std::vector<Perm> ident;
     for (int e = 0; e < E; ++e) ident.push_back(identity_perm((int)g.edge_shape(e).size()));
-    Buffers N = collect(g, ident, align, {});
+    Buffers N = collect(g, ident, align, {}, {});
     uint64_t s = 0;
     for (int b : N.list) s += N.size[b];
     ap.naive = s;

@@ -23,6 +23,7 @@
 #include <map>
 #include <numeric>
 
+#include "fusion.h"
 #include "layouts.h"
 #include "planner.h"
 
@@ -148,16 +149,12 @@ struct Planner {
     std::vector<int> be;
   };
 
-  Gain node_gain(const PathInfo& info, size_t j, const Fix& F) const {
+  // G[a, b] = min over boundary layouts beta of C[slot layouts..., b] with
+  // the chain edge ce in layout a; argmin beta lexicographically smallest.
+  Gain gain(const std::vector<int>& slots, int ce, const std::vector<int>& be, int eo, const NodeCost& nc,
+            const std::vector<int64_t>& C, const Fix& F) const {
     Gain r;
-    const int n = info.path[j];
-    const auto& slots = g.act_in[n];
-    const NodeCost& nc = t.nodes[n];
-    const auto& C = costs(n);
-    const int cs = info.chain_slot[j];
-    const int ce = cs >= 0 ? slots[cs] : -1;
-    r.be = info.bnd[j];
-    const int eo = g.out_edge(n);
+    r.be = be;
     r.A = ce >= 0 ? (int)t.L[ce].size() : 1;
     r.Bn = (int)t.L[eo].size();
     r.G.assign((size_t)r.A * r.Bn, kInf);
@@ -204,96 +201,211 @@ struct Planner {
     return r;
   }
 
+  Gain node_gain(const PathInfo& info, size_t j, const Fix& F) const {
+    const int n = info.path[j];
+    const auto& slots = g.act_in[n];
+    const int cs = info.chain_slot[j];
+    return gain(slots, cs >= 0 ? slots[cs] : -1, info.bnd[j], g.out_edge(n), t.nodes[n], costs(n), F);
+  }
+
+  // chain lengths t with measured costs whose nodes m+1 .. m+t follow the
+  // MatMul at step j on this path
+  std::vector<int> fused_options(const PathInfo& info, size_t j) const {
+    std::vector<int> out;
+    const int m = info.path[j];
+    for (int tt = 1; tt <= 3; ++tt) {
+      if (!t.fused.count({m, tt}) || j + tt >= info.path.size()) continue;
+      bool ok = true;
+      for (int i = 1; i <= tt; ++i) ok = ok && info.path[j + i] == m + i;
+      if (ok) out.push_back(tt);
+    }
+    return out;
+  }
+
+  // the fused launch of steps j .. j+tt as one virtual node
+  Gain fused_gain(const PathInfo& info, size_t j, int tt, const Fix& F) const {
+    const int m = info.path[j];
+    const std::vector<int> slots = chain_slots(g, m, tt);
+    const int cs = info.chain_slot[j];
+    const int ce = cs >= 0 ? g.act_in[m][cs] : -1;
+    std::vector<int> be;
+    for (int e : slots)
+      if (e != ce && std::find(be.begin(), be.end(), e) == be.end()) be.push_back(e);
+    const NodeCost& nc = t.fused.at({m, tt});
+    return gain(slots, ce, be, g.out_edge(m + tt), nc, use_v0 ? nc.v0 : nc.best, F);
+  }
+
   struct DP {
     int64_t total = kInf;
     std::vector<int> states;
     std::vector<std::map<int, int>> betas;
+    std::vector<int> fused;  // per step: length of the fused chain starting there
   };
 
-  DP dp_path(const PathInfo& info, const Fix& F) const {
+  // Viterbi over one path; with fusion priced, a step's output layout is
+  // also reached by the fused launch of the chain ending there, from the
+  // layout of the step before the chain (ties: the node on its own, then
+  // the shorter chain, then the smaller predecessor layout).
+  DP dp_path(const PathInfo& info, const Fix& F, bool fuse) const {
     const size_t m = info.path.size();
-    std::vector<std::vector<int>> backs(m);
-    std::vector<Gain> gains(m);
-    std::vector<int64_t> V;
+    struct Cand {
+      int tt;
+      size_t s;
+      Gain gn;
+    };
+    std::vector<std::vector<int>> opts(m);
+    if (fuse)
+      for (size_t j = 0; j < m; ++j) opts[j] = fused_options(info, j);
+    std::vector<std::vector<std::pair<int, int>>> backs(m);  // (t, a)
+    std::vector<std::vector<Cand>> cands(m);
+    std::vector<std::vector<int64_t>> Vs(m);
     for (size_t j = 0; j < m; ++j) {
-      const int n = info.path[j];
-      const int eo = g.out_edge(n);
-      gains[j] = node_gain(info, j, F);
-      Gain& gn = gains[j];
-      std::vector<char> ok(gn.Bn, 0);
+      const int eo = g.out_edge(info.path[j]);
+      cands[j].push_back({0, j, node_gain(info, j, F)});
+      for (int s = (int)j - 1; s >= std::max(0, (int)j - 3); --s) {
+        const int tt = (int)j - s;
+        if (std::find(opts[s].begin(), opts[s].end(), tt) != opts[s].end())
+          cands[j].push_back({tt, (size_t)s, fused_gain(info, (size_t)s, tt, F)});
+      }
+      const int Bn = (int)t.L[eo].size();
+      std::vector<char> ok(Bn, 0);
       for (int b : allowed(F, eo)) ok[b] = 1;
-      std::vector<int64_t> Vn(gn.Bn, kInf);
-      std::vector<int> back(gn.Bn, -1);
-      for (int b = 0; b < gn.Bn; ++b) {
-        if (j == 0) {
-          Vn[b] = ok[b] ? gn.G[b] : kInf;
-          continue;
+      std::vector<int64_t> Vn(Bn, kInf);
+      std::vector<std::pair<int, int>> back(Bn, {0, 0});
+      for (const Cand& c : cands[j]) {
+        const Gain& gn = c.gn;
+        for (int b = 0; b < Bn; ++b) {
+          int64_t tot;
+          int ba = 0;
+          if (c.s == 0) {
+            tot = ok[b] ? gn.G[b] : kInf;
+          } else {
+            int64_t best = kInf + 1;  // so that an all-INF column keeps a = 0
+            const auto& V = Vs[c.s - 1];
+            for (int a = 0; a < gn.A; ++a) {
+              int64_t gab = ok[b] ? gn.G[(size_t)a * gn.Bn + b] : kInf;
+              int64_t v = sat_add(V[a], gab);
+              if (v < best) { best = v; ba = a; }
+            }
+            tot = best > kInf ? kInf : best;
+          }
+          // the node on its own always sets the state; a fused launch
+          // replaces it only when strictly cheaper
+          if (c.tt == 0 || tot < Vn[b]) { Vn[b] = tot; back[b] = {c.tt, ba}; }
         }
-        int64_t best = kInf + 1;  // so that an all-INF column keeps a = 0
-        int ba = 0;
-        for (int a = 0; a < gn.A; ++a) {
-          int64_t gab = ok[b] ? gn.G[(size_t)a * gn.Bn + b] : kInf;
-          int64_t v = sat_add(V[a], gab);
-          if (v < best) { best = v; ba = a; }
-        }
-        Vn[b] = best > kInf ? kInf : best;
-        back[b] = ba;
       }
       backs[j] = std::move(back);
-      V = std::move(Vn);
+      Vs[j] = std::move(Vn);
     }
     DP r;
+    const auto& V = Vs[m - 1];
     int b = 0;
     int64_t best = kInf + 1;
     for (int i = 0; i < (int)V.size(); ++i)
       if (V[i] < best) { best = V[i]; b = i; }
     r.total = best > kInf ? kInf : best;
     r.states.assign(m, 0);
-    std::vector<int> chosen_a(m, 0);
-    for (int j = (int)m - 1; j >= 0; --j) {
+    r.fused.assign(m, 0);
+    r.betas.assign(m, {});
+    for (int j = (int)m - 1; j >= 0;) {
+      const auto [tt, a] = backs[j][b];
+      const Cand* c = nullptr;
+      for (const Cand& x : cands[j])
+        if (x.tt == tt) c = &x;
+      const Gain& gn = c->gn;
+      const int s = (int)c->s;
       r.states[j] = b;
-      int a = j > 0 ? backs[j][b] : 0;
-      chosen_a[j] = a;
+      const int bi = gn.arg[(size_t)(s > 0 ? a : 0) * gn.Bn + b];
+      std::map<int, int> chosen;
+      for (size_t i = 0; i < gn.be.size(); ++i) chosen[gn.be[i]] = bi >= 0 ? gn.betas[bi][i] : 0;
+      if (s > 0) chosen.emplace(g.act_in[info.path[s]][info.chain_slot[s]], a);
+      // a boundary edge's layout is recorded at every step of the launch
+      // that reads it as a boundary edge
+      for (int k = s; k <= j; ++k)
+        for (int e : info.bnd[k]) {
+          auto it = chosen.find(e);
+          if (it != chosen.end()) r.betas[k][e] = it->second;
+        }
+      r.fused[s] = tt;
+      j = s - 1;
       b = a;
-    }
-    r.betas.resize(m);
-    for (size_t j = 0; j < m; ++j) {
-      const Gain& gn = gains[j];
-      int bi = gn.arg[(size_t)(j > 0 ? chosen_a[j] : 0) * gn.Bn + r.states[j]];
-      for (size_t i = 0; i < gn.be.size(); ++i) r.betas[j][gn.be[i]] = bi >= 0 ? gn.betas[bi][i] : 0;
     }
     return r;
   }
 
-  int64_t plan_cost(const std::vector<int>& lay) const {
+  // flat index of (slot layouts..., out layout) into a dense cost array
+  static size_t flat_of(const NodeCost& nc, const std::vector<int>& slots, int eo, const std::vector<int>& lay) {
+    size_t flat = 0;
+    for (size_t s = 0; s < slots.size(); ++s) flat = flat * nc.dims[s] + lay[slots[s]];
+    return flat * nc.dims[slots.size()] + lay[eo];
+  }
+
+  // summed table cost: every node on its own, except the fused chains
+  // (fuse[m] = t), which cost their fused entry
+  int64_t plan_cost(const std::vector<int>& lay, const std::vector<int>& fuse = {}) const {
     int64_t total = 0;
-    for (int n = 0; n < g.n_nodes(); ++n) {
-      const NodeCost& nc = t.nodes[n];
-      size_t flat = 0;
-      const auto& slots = g.act_in[n];
-      for (size_t s = 0; s < slots.size(); ++s) flat = flat * nc.dims[s] + lay[slots[s]];
-      flat = flat * nc.dims[slots.size()] + lay[g.out_edge(n)];
-      total = sat_add(total, costs(n)[flat]);
+    for (int n = 0; n < g.n_nodes();) {
+      const int tt = fuse.empty() ? 0 : fuse[n];
+      if (tt) {
+        const NodeCost& nc = t.fused.at({n, tt});
+        const auto& C = use_v0 ? nc.v0 : nc.best;
+        total = sat_add(total, C[flat_of(nc, chain_slots(g, n, tt), g.out_edge(n + tt), lay)]);
+        n += tt + 1;
+        continue;
+      }
+      total = sat_add(total, costs(n)[flat_of(t.nodes[n], g.act_in[n], g.out_edge(n), lay)]);
+      ++n;
     }
     return total;
   }
 
-  LayoutPlan finish(const std::vector<int>& lay, int64_t total, int guard, const std::vector<std::vector<int>>& paths) const {
+  // The cheapest set of disjoint fusion chains for fixed layouts (fuse[m] =
+  // t for a chain run as one launch): chains cover consecutive node ids, so
+  // an interval DP from the last node back -- f(n) = min(n on its own +
+  // f(n+1), min over chains (n, t) of their fused entry + f(n+t+1)); ties
+  // keep the node on its own, then the shorter chain.
+  std::vector<int> best_chains(const std::vector<int>& lay) const {
+    const int N = g.n_nodes();
+    std::vector<int64_t> f(N + 1, 0);
+    std::vector<int> pick(N, 0);
+    for (int n = N - 1; n >= 0; --n) {
+      f[n] = sat_add(costs(n)[flat_of(t.nodes[n], g.act_in[n], g.out_edge(n), lay)], f[n + 1]);
+      for (int tt = 1;; ++tt) {
+        auto it = t.fused.find({n, tt});
+        if (it == t.fused.end()) break;
+        const NodeCost& nc = it->second;
+        const auto& C = use_v0 ? nc.v0 : nc.best;
+        const int64_t c = sat_add(C[flat_of(nc, chain_slots(g, n, tt), g.out_edge(n + tt), lay)], f[n + tt + 1]);
+        if (c < f[n]) { f[n] = c; pick[n] = tt; }
+      }
+    }
+    std::vector<int> fuse(N, 0);
+    for (int n = 0; n < N; n += pick[n] + 1) fuse[n] = pick[n];
+    return fuse;
+  }
+
+  LayoutPlan finish(const std::vector<int>& lay, int64_t total, int guard, const std::vector<std::vector<int>>& paths,
+                    const std::vector<int>& fuse = {}) const {
     LayoutPlan p;
     p.layout_idx = lay;
     p.total = total;
     p.guard_used = guard;
     p.paths = paths;
+    p.fuse = fuse.empty() ? std::vector<int>(g.n_nodes(), 0) : fuse;
+    std::vector<char> absorbed(g.n_nodes(), 0);
+    for (int m = 0; m < g.n_nodes(); ++m)
+      for (int i = 1; i <= p.fuse[m]; ++i) absorbed[m + i] = 1;
     for (int e = 0; e < g.n_edges(); ++e) p.perm.push_back(t.L[e][lay[e]]);
     for (int n = 0; n < g.n_nodes(); ++n) {
+      if (absorbed[n]) { p.variant.push_back(-2); continue; }
       if (node_is_view(g, n, p.perm)) { p.variant.push_back(-1); continue; }
       if (use_v0) { p.variant.push_back(0); continue; }
-      const NodeCost& nc = t.nodes[n];
-      size_t flat = 0;
-      const auto& slots = g.act_in[n];
-      for (size_t s = 0; s < slots.size(); ++s) flat = flat * nc.dims[s] + lay[slots[s]];
-      flat = flat * nc.dims[slots.size()] + lay[g.out_edge(n)];
-      p.variant.push_back(nc.var[flat]);
+      if (p.fuse[n]) {
+        const NodeCost& nc = t.fused.at({n, p.fuse[n]});
+        p.variant.push_back(nc.var[flat_of(nc, chain_slots(g, n, p.fuse[n]), g.out_edge(n + p.fuse[n]), lay)]);
+        continue;
+      }
+      p.variant.push_back(t.nodes[n].var[flat_of(t.nodes[n], g.act_in[n], g.out_edge(n), lay)]);
     }
     return p;
   }
@@ -310,15 +422,18 @@ std::vector<std::vector<int>> split_paths(const Graph& g) {
 }
 
 LayoutPlan plan_layouts(const Graph& g, const CostTable& t, uint32_t flags) {
-  Planner P{g, t, (flags & FLUID_NO_VARIANTS) != 0};
-  auto paths = split_paths(g);
-  std::vector<int> ident(g.n_edges(), 0);
-  const int64_t ident_cost = P.plan_cost(ident);
-  if (ident_cost >= kInf) fail(FLUID_E_INFEASIBLE, "the all-row-major plan has no cost entry");
-  if (flags & FLUID_NO_DP) return P.finish(ident, ident_cost, 0, paths);
+  LayoutPlan p = plan_layouts_dp(g, t, flags);
+  p.fusion_priced = !(flags & FLUID_NO_FUSION) && !(flags & FLUID_NO_DP) && !t.fused.empty();
+  return p;
+}
 
-  std::vector<PathInfo> infos;
-  for (auto& p : paths) infos.push_back(make_info(g, p));
+namespace {
+
+// The first DP of every path, the vote on shared edges and the
+// re-optimisation with the voted layouts fixed: the layout index per edge;
+// false when a path has no feasible plan after the vote.
+bool voted_layouts(const Graph& g, const Planner& P, const std::vector<std::vector<int>>& paths,
+                   const std::vector<PathInfo>& infos, bool fz, std::vector<int>& lay) {
   std::vector<int> owner(g.n_edges(), -1), step_of(g.n_nodes(), -1);
   for (size_t pi = 0; pi < paths.size(); ++pi)
     for (size_t j = 0; j < paths[pi].size(); ++j) {
@@ -337,7 +452,7 @@ LayoutPlan plan_layouts(const Graph& g, const CostTable& t, uint32_t flags) {
   Fix F;
   std::vector<Planner::DP> first;
   for (size_t pi = 0; pi < infos.size(); ++pi) {
-    first.push_back(P.dp_path(infos[pi], F));
+    first.push_back(P.dp_path(infos[pi], F, fz));
     if (first.back().total >= kInf) fail(FLUID_E_INFEASIBLE, "path " + std::to_string(pi) + " has no feasible layout");
   }
   for (auto& kv : readers) {
@@ -368,24 +483,61 @@ LayoutPlan plan_layouts(const Graph& g, const CostTable& t, uint32_t flags) {
         Fix F2 = F;
         F2[e] = l;
         int64_t c = 0;
-        for (int pi : touch) c = sat_add(c, P.dp_path(infos[pi], F2).total);
+        for (int pi : touch) c = sat_add(c, P.dp_path(infos[pi], F2, fz).total);
         if (best < 0 || c < best) { best = c; win = l; }
       }
     }
     F[e] = win;
   }
-  std::vector<int> lay(ident);
+  lay.assign(g.n_edges(), 0);
   for (size_t pi = 0; pi < infos.size(); ++pi) {
-    Planner::DP d = P.dp_path(infos[pi], F);
-    if (d.total >= kInf) {
-      if (flags & FLUID_NO_GUARD) fail(FLUID_E_INFEASIBLE, "path " + std::to_string(pi) + " infeasible after the vote");
-      return P.finish(ident, ident_cost, 1, paths);
-    }
+    Planner::DP d = P.dp_path(infos[pi], F, fz);
+    if (d.total >= kInf) return false;
     for (size_t j = 0; j < infos[pi].path.size(); ++j) lay[g.out_edge(infos[pi].path[j])] = d.states[j];
   }
-  const int64_t total = P.plan_cost(lay);
-  if (!(flags & FLUID_NO_GUARD) && total > ident_cost) return P.finish(ident, ident_cost, 1, paths);
-  return P.finish(lay, total, 0, paths);
+  return true;
+}
+
+}  // namespace
+
+// Sections 3.1-3.3 (Alg. 1-3, Eq. 1, the vote), with the row-major guard;
+// when the table prices fusion chains, two voted layout assignments compete
+// (from the fusion-aware path DP and from the plain one), each with the
+// cheapest chains for its layouts (Planner::best_chains); the cheaper total
+// wins, the fusion-aware one on ties.
+LayoutPlan plan_layouts_dp(const Graph& g, const CostTable& t, uint32_t flags) {
+  Planner P{g, t, (flags & FLUID_NO_VARIANTS) != 0};
+  const bool priced = !(flags & FLUID_NO_FUSION) && !t.fused.empty();
+  auto paths = split_paths(g);
+  std::vector<int> ident(g.n_edges(), 0);
+  if (P.plan_cost(ident) >= kInf) fail(FLUID_E_INFEASIBLE, "the all-row-major plan has no cost entry");
+  if (flags & FLUID_NO_DP) return P.finish(ident, P.plan_cost(ident), 0, paths);
+  const std::vector<int> ident_fuse = priced ? P.best_chains(ident) : std::vector<int>{};
+  const int64_t ident_cost = P.plan_cost(ident, ident_fuse);
+
+  std::vector<PathInfo> infos;
+  for (auto& p : paths) infos.push_back(make_info(g, p));
+  bool have = false;
+  int64_t total = 0;
+  std::vector<int> lay, fuse;
+  for (bool fz : priced ? std::vector<bool>{true, false} : std::vector<bool>{false}) {
+    std::vector<int> l;
+    if (!voted_layouts(g, P, paths, infos, fz, l)) continue;
+    std::vector<int> f = priced ? P.best_chains(l) : std::vector<int>{};
+    const int64_t c = P.plan_cost(l, f);
+    if (!have || c < total) {
+      have = true;
+      total = c;
+      lay = std::move(l);
+      fuse = std::move(f);
+    }
+  }
+  if (!have) {
+    if (flags & FLUID_NO_GUARD) fail(FLUID_E_INFEASIBLE, "every path plan is infeasible after the vote");
+    return P.finish(ident, ident_cost, 1, paths, ident_fuse);
+  }
+  if (!(flags & FLUID_NO_GUARD) && total > ident_cost) return P.finish(ident, ident_cost, 1, paths, ident_fuse);
+  return P.finish(lay, total, 0, paths, fuse);
 }
 
 LayoutPlan identity_plan(const Graph& g) {
@@ -393,6 +545,7 @@ LayoutPlan identity_plan(const Graph& g) {
   p.layout_idx.assign(g.n_edges(), 0);
   for (int e = 0; e < g.n_edges(); ++e) p.perm.push_back(identity_perm((int)g.edge_shape(e).size()));
   for (int n = 0; n < g.n_nodes(); ++n) p.variant.push_back(node_is_view(g, n, p.perm) ? -1 : 0);
+  p.fuse.assign(g.n_nodes(), 0);
   return p;
 }
 

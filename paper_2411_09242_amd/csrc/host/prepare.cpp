@@ -13,7 +13,7 @@ namespace {
 // Bases are validated to be 256-byte (arena) or 16-byte (caller tensors)
 // aligned, so preparing with base address 0 keeps every alignment decision
 // valid for the real addresses.
-const void* fake_ptr(const Bind& b) { return (const void*)(uintptr_t)b.off; }
+const void* fake_ptr(const Bind& b) { return (const void*)(uintptr_t)(b.off < 0 ? 0 : b.off); }
 
 Bind bind_edge(const Graph& g, const ArenaPlan* ap, int e) {
   Bind b;
@@ -31,12 +31,49 @@ Bind bind_edge(const Graph& g, const ArenaPlan* ap, int e) {
   return b;
 }
 
-// Bytes [lo, hi) an arena-bound edge occupies (empty for caller tensors).
+// Bytes [lo, hi) an arena-bound edge occupies (empty for caller tensors and
+// for results a planned fused launch keeps on chip, offset -1).
 std::pair<int64_t, int64_t> arena_range(const Graph& g, const ArenaPlan* ap, int e, const Bind& b) {
-  if (!ap || b.kind != BK_ARENA) return {0, 0};
+  if (!ap || b.kind != BK_ARENA || b.off < 0) return {0, 0};
   const int64_t bytes = numel(g.edge_shape(e)) * (g.dtype == FLUID_BF16 ? 2 : 4);
   return {b.off, b.off + bytes};
 }
+
+}  // namespace
+
+NodeKernel fused_gemm_kernel(const Node& mn, int variant, int dtype, const std::vector<Operand>& mm_ops,
+                             const Operand& out, uint32_t act, uint32_t rop, const Operand* r) {
+  NodeKernel kf = prepare_node(mn, variant, dtype, mm_ops, out);
+  if (!kf.available) return kf;
+  const int caps = gemm_epilogue_caps(variant, dtype);
+  if ((act && !(caps & EPI_ACT)) || (rop && !(caps & EPI_ROP))) {
+    kf.available = false;
+    kf.why = "this tile does not perform that epilogue";
+    return kf;
+  }
+  if (rop) {
+    // R's strides in the output's batch / row decomposition: prepare the
+    // product as if it wrote R
+    const NodeKernel kr = prepare_node(mn, variant, dtype, mm_ops, *r);
+    if (!kr.available) {
+      kf.available = false;
+      kf.why = kr.why;
+      return kf;
+    }
+    kf.gemm.r_g1 = kr.gemm.c_g1;
+    kf.gemm.r_g2 = kr.gemm.c_g2;
+    kf.gemm.r_m1 = kr.gemm.c_m1;
+    kf.gemm.r_m2 = kr.gemm.c_m2;
+    kf.gemm.r_n = kr.gemm.c_n;
+    kf.gemm.r_m2div = kf.gemm.m2div;
+  }
+  kf.gemm.epi_bf16 = dtype == FLUID_BF16 ? 1u : 0u;
+  kf.gemm.act = act;
+  kf.gemm.rop = rop;
+  return kf;
+}
+
+namespace {
 
 // Epilogue fusion.  A MatMul absorbs the node `nx` launched right after the
 // chain it already performs when nx is the chain output's only reader (which
@@ -91,25 +128,16 @@ void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan* ap
     const auto ri = arena_range(g, ap, mn.ins[i], mm.in[i]);
     if (ro.first < ro.second && ri.first < ri.second && ro.first < ri.second && ri.first < ro.second) return;
   }
-  NodeKernel kf = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, nx_out);
+  NodeKernel kf = fused_gemm_kernel(mn, lp.variant[mm.node], g.dtype, mm.ops, nx_out, act, rop,
+                                    rop ? &nx.ops[rslot] : nullptr);
   if (!kf.available) return;
   if (rop) {
-    // R's strides in the output's batch / row decomposition: prepare the
-    // product as if it wrote R
-    const NodeKernel kr = prepare_node(mn, lp.variant[mm.node], g.dtype, mm.ops, nx.ops[rslot]);
-    if (!kr.available) return;
-    kf.gemm.r_g1 = kr.gemm.c_g1;
-    kf.gemm.r_g2 = kr.gemm.c_g2;
-    kf.gemm.r_m1 = kr.gemm.c_m1;
-    kf.gemm.r_m2 = kr.gemm.c_m2;
-    kf.gemm.r_n = kr.gemm.c_n;
-    kf.gemm.r_m2div = kf.gemm.m2div;
     mm.fr = nx.in[rslot];
     mm.fr_edge = xn.ins[rslot];
   }
-  kf.gemm.epi_bf16 = g.dtype == FLUID_BF16 ? 1u : 0u;
-  kf.gemm.act = act;
-  kf.gemm.rop = rop;
+  // a placeholder until each run binds the constant (fused_kernel): the
+  // launch's name shows the bias step
+  if (bias >= 0) kf.gemm.bias = (const void*)(uintptr_t)256;
   mm.fuse_n += 1;
   mm.kf = kf;
   mm.fout = nx.out;
@@ -197,30 +225,31 @@ void group_launches(const Graph& g, const ArenaPlan* ap, Prepared& P) {
 std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const ArenaPlan* ap) {
   auto P = std::make_shared<Prepared>();
   for (int n = 0; n < g.n_nodes(); ++n) {
-    if (lp.variant[n] < 0) continue;  // view: no kernel
+    const int v = lp.variant[n];
+    if (v == -1) continue;  // view: no kernel
     const Node& nd = g.nodes[n];
     PreparedNode pn;
     pn.node = n;
-    std::vector<Operand> ins;
-    if (packs_weight(nd.op, lp.variant[n]) && nd.ins.size() == 2 && nd.ins[1] < 0 &&
+    if (v >= 0 && packs_weight(nd.op, v) && nd.ins.size() == 2 && nd.ins[1] < 0 &&
         g.const_readers[~nd.ins[1]].size() != 1)
       fail(FLUID_E_INVALID, "node " + std::to_string(n) + ": a packed-weight variant needs a weight read by this "
                                                           "node only");
+    std::vector<Operand> ins;
     for (size_t slot = 0; slot < nd.ins.size(); ++slot) {
-      const int v = nd.ins[slot];
+      const int vin = nd.ins[slot];
       Operand o;
       Bind b;
-      if (v >= 0) {
-        b = bind_edge(g, ap, v);
-        o.shape = g.edge_shape(v);
-        o.stride = dense_strides(o.shape, lp.perm[v]);
+      if (vin >= 0) {
+        b = bind_edge(g, ap, vin);
+        o.shape = g.edge_shape(vin);
+        o.stride = dense_strides(o.shape, lp.perm[vin]);
         o.dtype = g.dtype;
       } else {
         b.kind = BK_CONST;
-        b.index = ~v;
-        o.shape = g.consts[~v].shape;
-        o.stride = const_strides(nd, (int)slot, lp.variant[n], o.shape);
-        o.dtype = g.consts[~v].dtype;
+        b.index = ~vin;
+        o.shape = g.consts[~vin].shape;
+        o.stride = const_strides(nd, (int)slot, v >= 0 ? v : 0, o.shape);
+        o.dtype = g.consts[~vin].dtype;
       }
       o.ptr = fake_ptr(b);
       ins.push_back(o);
@@ -233,12 +262,26 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
     out.stride = dense_strides(out.shape, lp.perm[eo]);
     out.dtype = g.dtype;
     out.ptr = fake_ptr(pn.out);
-    pn.k = prepare_node(nd, lp.variant[n], g.dtype, ins, out);
-    if (!pn.k.available)
-      fail(FLUID_E_INVALID, "node " + std::to_string(n) + ": variant " + std::to_string(lp.variant[n]) +
-                                " cannot run with these layouts (" + pn.k.why + ")");
     pn.ops = ins;
-    if (!P->nodes.empty()) {
+    if (v == -2) {
+      // performed by the fused MatMul before it (the plan priced that launch)
+      size_t j = P->nodes.empty() ? 0 : P->nodes.size() - 1;
+      while (j > 0 && P->nodes[j].fused_away) --j;
+      require(!P->nodes.empty() && j + P->nodes[j].fuse_n == P->nodes.size() - 1 &&
+                  lp.fuse[P->nodes[j].node] >= n - P->nodes[j].node,
+              "node " + std::to_string(n) + ": marked fused, but no fused MatMul launch precedes it");
+      try_fuse_epilogue(g, lp, ap, P->nodes[j], g.out_edge(P->nodes.back().node), pn, out);
+      require(pn.fused_away, "node " + std::to_string(n) + ": the plan fuses it into MatMul node " +
+                                 std::to_string(P->nodes[j].node) + ", which cannot perform it with variant " +
+                                 std::to_string(lp.variant[P->nodes[j].node]));
+      P->nodes.push_back(std::move(pn));
+      continue;
+    }
+    pn.k = prepare_node(nd, v, g.dtype, ins, out);
+    if (!pn.k.available)
+      fail(FLUID_E_INVALID, "node " + std::to_string(n) + ": variant " + std::to_string(v) +
+                                " cannot run with these layouts (" + pn.k.why + ")");
+    if (!lp.fusion_priced && !P->nodes.empty()) {
       // the MatMul whose fused chain ends at the previous launch, if any
       size_t j = P->nodes.size() - 1;
       while (j > 0 && P->nodes[j].fused_away) --j;

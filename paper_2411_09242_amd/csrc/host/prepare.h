@@ -64,6 +64,13 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
 // done with its operands once it has written that node's output.
 std::vector<int> epilogue_reads_until(const Graph& g, const LayoutPlan& lp);
 
+// The fused launch of MatMul mn (variant, operands as prepared) writing out
+// with the epilogue steps act (0 none, 1 GELU, 2 SiLU) and rop (0 none,
+// 1 Add, 2 Mul of R); unavailable when the tile lacks a step.  The bias and
+// R pointers are bound at launch.
+NodeKernel fused_gemm_kernel(const Node& mn, int variant, int dtype, const std::vector<Operand>& mm_ops,
+                             const Operand& out, uint32_t act, uint32_t rop, const Operand* r);
+
 // The layout constant c must be stored in for a run of this plan: the
 // identity (row-major as supplied), or (1, 0) -- K-contiguous -- for a
 // weight whose one reader runs a packed-weight MatMul variant.

@@ -31,7 +31,7 @@ OPS = {"matmul": 0, "add": 1, "mul": 2, "transpose": 3, "reshape": 4, "softmax":
 ROLES = {"other": 0, "weight": 1, "bias": 2, "gamma": 3, "beta": 4, "rope_cos": 5, "rope_sin": 6}
 ARCH = {"post_ln": 0, "pre_ln": 1, "llama": 2, "vgg": 3}
 MAX_STAGES = 8
-NO_DP, NO_VARIANTS, NO_GUARD = 1, 2, 4
+NO_DP, NO_VARIANTS, NO_GUARD, NO_FUSION = 1, 2, 4, 8
 ARENA_NO_REUSE, ARENA_EPILOGUE = 1, 2
 STATUS = {0: "OK", -1: "INVALID", -2: "UNSUPPORTED", -3: "INFEASIBLE", -4: "ARENA_TOO_SMALL",
           -5: "HIP", -6: "NOMEM"}
@@ -84,6 +84,7 @@ _PROTOS = {
     "fluid_layout_plan_get": (C.c_int, [_VP, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                                         C.POINTER(C.c_int64), C.POINTER(C.c_int32)]),
     "fluid_edge_layout": (C.c_int, [_VP, _VP, C.c_int32, C.POINTER(C.c_int32)]),
+    "fluid_layout_plan_fusion": (C.c_int, [_VP, C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
     "fluid_plan_arena": (C.c_int, [_VP, _VP, C.c_uint64, C.c_uint32, C.POINTER(_VP)]),
     "fluid_arena_plan_get": (C.c_int, [_VP, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                                        C.POINTER(C.c_uint64), C.POINTER(C.c_int64), C.POINTER(C.c_int32)]),
@@ -424,6 +425,11 @@ class LayoutPlan:
         self.h = fluid_plan_layouts(graph.h, table.h, flags)
         self.layout_idx, self.variant, self.total_ns, self.guard_used = fluid_layout_plan_get(
             self.h, graph.n_edges, graph.n_nodes)
+        fz = (C.c_int32 * max(graph.n_nodes, 1))()
+        priced = C.c_int32(0)
+        _check(_L().fluid_layout_plan_fusion(self.h, fz, C.byref(priced)))
+        self.fuse = list(fz)[:graph.n_nodes]
+        self.fusion_priced = bool(priced.value)
 
     def perm(self, e):
         return fluid_edge_layout(self.graph.h, self.h, e, len(self.graph.edge_shape(e)))

@@ -12,6 +12,10 @@ Checks, in order:
     paper's, and offsets and peak equal to the oracle's Greedy-by-Size run on
     exactly those lifetimes, with no two lifetime-overlapping buffers sharing
     a byte.
+When the table prices fusion chains, the layout plan's chosen chains
+(per MatMul) must match too, and both arena requests must equal the
+oracle's arena planned with exactly those chains (their intermediates get
+no buffer).
 """
 from __future__ import annotations
 
@@ -32,6 +36,21 @@ def assert_plans_match_oracle(og, g, table_obj, lp, flags=0):
     assert lp.total_ns == ref.total, (lp.total_ns, ref.total)
     assert lp.guard_used == ref.guard_used
     lay = {e: ct.L[e][ref.layout_idx[e]] for e in range(og.n_edges)}
+    assert lp.fusion_priced == (bool(ct.fused) and not flags & (PL.NO_FUSION | PL.NO_DP))
+    if lp.fusion_priced:
+        assert lp.fuse == ref.fuse, "fusion chain length per MatMul"
+        oap = PA.plan_arena(og, lay, fuse=ref.fuse)
+        for epi in (False, True):
+            ap = F.ArenaPlan(g, lp, epilogue=epi)
+            assert ap.peak == oap.peak
+            for e in range(og.n_edges):
+                assert ap.root[e] == oap.root[e], e
+                r = oap.root[e]
+                assert ap.offset[e] == (oap.offset[r] if r in oap.offset else -1), e
+            assert ap.lower_bound == PA.lower_bound(oap.buffers, oap.size, oap.defn, oap.last, len(og.nodes))
+        return {"total_ns": ref.total, "guard_used": ref.guard_used, "peak": oap.peak,
+                "peak_fusion_lifetimes": oap.peak, "extended_lifetimes": 0,
+                "fused_chains": sum(1 for t in ref.fuse if t)}
 
     # the paper's lifetimes
     oap = PA.plan_arena(og, lay)

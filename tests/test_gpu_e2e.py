@@ -116,7 +116,7 @@ def test_random_forced_layouts_on_one_layer(tmp_path):
 
 
 def test_run_nodes_replays_the_run_bit_for_bit():
-    """fluid_run_nodes over every launched node, in launch order, is the same
+    """fluid_run_nodes over every non-view node, in node order, is the same
     computation as fluid_run: the output matches bit for bit; a view node or
     an empty list is rejected before any launch."""
     import torch
@@ -130,13 +130,13 @@ def test_run_nodes_replays_the_run_bit_for_bit():
     ex = F.Executor(g, lp, ap, consts, [x])
     ref = ex.run()[0].clone()
     torch.cuda.synchronize()
-    launched = [n for n in range(g.n_nodes) if lp.variant[n] >= 0]
+    launched = [n for n in range(g.n_nodes) if lp.variant[n] != -1]
     ex.arena.fill_(0xFF)
     ex.outputs[0].fill_(float("nan"))
     ex.run_nodes(launched, repeat=2)
     torch.cuda.synchronize()
     assert torch.equal(ex.outputs[0], ref)
-    views = [n for n in range(g.n_nodes) if lp.variant[n] < 0]
+    views = [n for n in range(g.n_nodes) if lp.variant[n] == -1]
     if views:
         with pytest.raises(F.FluidError, match="view"):
             ex.run_nodes([views[0]])
@@ -193,3 +193,48 @@ def test_run_rejects_bad_arguments_before_any_launch():
     run()
     torch.cuda.synchronize()
     assert_close(ex.outputs[0].float().cpu().numpy(), ref, "f32", "after rejected calls")
+
+
+PRICED = [("post_ln", "f32"), ("pre_ln", "f32"), ("llama", "f32"), ("llama", "bf16")]
+
+
+@pytest.mark.parametrize("arch,dtype", PRICED)
+@pytest.mark.parametrize("seed", [0, 1])
+def test_priced_fusion_chains_run_to_parity(arch, dtype, seed, tmp_path):
+    """Plans whose layout DP chose fusion chains (random tables that price
+    every chain, for MatMul variant 1, whose tile performs every step): the
+    run -- each chosen chain one launch that stores only its last output --
+    matches the oracle.  fluid_run_nodes replays it bit for bit when the
+    list holds each chain whole, and refuses, before any launch, a list that
+    splits a chain (the chain's intermediate results have no buffer)."""
+    import torch
+    from paper_2411_09242_amd import fluid as F
+    from tables import add_fused, synthetic_table, write_table
+    cfg = synth_inputs.config(1, arch=arch, dtype=dtype, layers=2, batch=2, seq=37, hidden=72, heads=3, ffn=100)
+    og = OG.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), 11 + seed)
+    (ref,) = execute.run_canonical(og, [x], consts)
+    tab = synthetic_table(og, seed=seed, mode="random", lo=1, hi=1000, n_variants=1)
+    add_fused(tab, og, seed, n_variants=2, lo=1, hi=1500)
+    for fs in tab["fused_sigs"]:
+        for ent in fs["entries"]:
+            ent[2][0] = -1
+    path = write_table(tab, tmp_path / "t.json")
+    out, g, lp, ap, _ = _device_run(cfg, x, consts, table=lambda gg: F.CostTable.load(str(path), gg))
+    assert lp.fusion_priced and any(lp.fuse)
+    say(f"{arch} {dtype} seed {seed}: {sum(1 for t in lp.fuse if t)} priced chains")
+    assert_close(out, ref, dtype, f"{arch} {dtype} priced fusion")
+    ex = F.Executor(g, lp, ap, consts, [x])
+    want = ex.run()[0].clone()
+    torch.cuda.synchronize()
+    ex.outputs[0].fill_(float("nan"))
+    ex.run_nodes([n for n in range(g.n_nodes) if lp.variant[n] != -1])
+    torch.cuda.synchronize()
+    assert torch.equal(ex.outputs[0], want)
+    m = next(i for i, t in enumerate(lp.fuse) if t)
+    before = ex.outputs[0].clone()
+    for bad in ([m], [m + lp.fuse[m]], list(range(m, m + lp.fuse[m]))):
+        with pytest.raises(F.FluidError, match="fusion chain"):
+            ex.run_nodes(bad)
+    torch.cuda.synchronize()
+    assert torch.equal(ex.outputs[0], before)

@@ -136,3 +136,48 @@ def test_epilogue_arena_on_transformers(cfg, seed, tmp_path):
         if launch[n] >= 0 and not written[n]:
             readers = [m for m, md in enumerate(og.nodes) if e in md.ins]
             assert readers and all(launch[m] == launch[n] for m in readers), (n, readers)
+
+
+@pytest.mark.parametrize("cfg", CFGS, ids=lambda c: c["arch"])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_priced_fusions_are_the_launches(cfg, seed, tmp_path):
+    """A table that prices fusion chains: the run performs exactly the chains
+    the layout DP chose -- each in one launch that stores only the chain's
+    last output, the intermediates without an arena buffer -- and no other
+    fusion; without pricing (FLUID_NO_FUSION) the epilogue fusion by
+    adjacency is back."""
+    from tables import add_fused
+    og = OG.build_transformer(cfg)
+    tab = synthetic_table(og, seed=seed, mode="random", lo=1, hi=1000, n_variants=1)
+    # chains priced for variant 1 only (its tile performs every epilogue
+    # step; variant 0 has no R operand)
+    add_fused(tab, og, seed, n_variants=2, lo=1, hi=1500)
+    for fs in tab["fused_sigs"]:
+        for ent in fs["entries"]:
+            ent[2][0] = -1
+    g, lp = _plan(og, tab, tmp_path)
+    assert lp.fusion_priced and any(lp.fuse)
+    n, ap = _launches(g, lp, epilogue=True)
+    launch, written, names = F.fluid_run_schedule(g.h, lp.h, ap.h, g.n_nodes)
+    kernels = [lp.kernel(i) for i in range(g.n_nodes)]
+    assert n == len(names) == sum(1 for k in kernels if k not in ("view", "fused"))
+    covered = set()
+    for m, t in enumerate(lp.fuse):
+        if not t:
+            continue
+        assert og.nodes[m].op == "matmul" and lp.variant[m] == 1
+        chain = list(range(m, m + t + 1))
+        covered.update(chain)
+        assert all(lp.variant[k] == -2 and kernels[k] == "fused" for k in chain[1:])
+        assert {launch[k] for k in chain} == {launch[m]}
+        assert not any(written[k] for k in chain[:-1]) and written[chain[-1]]
+        assert all(ap.offset[og.out_edge(k)] == -1 for k in chain[:-1])
+        assert "_e" in names[launch[m]]
+    for k in range(g.n_nodes):
+        if k not in covered and kernels[k] != "view":
+            assert written[k] and list(launch).count(launch[k]) == 1, k
+    # without pricing: no -2, and adjacency fusion performs at least one chain
+    g2, lp2 = _plan(og, tab, tmp_path, F.NO_FUSION)
+    assert not lp2.fusion_priced and not any(lp2.fuse) and -2 not in lp2.variant
+    n2, _ = _launches(g2, lp2, epilogue=True)
+    assert n2 < sum(1 for i in range(g2.n_nodes) if lp2.kernel(i) != "view")

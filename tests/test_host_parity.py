@@ -12,7 +12,7 @@ import synth_inputs
 from oracle import costtable, graph as OG, layouts, plan_arena as PA, plan_layout as PL
 from paper_2411_09242_amd import fluid as F
 from plan_check import assert_plans_match_oracle
-from tables import fanout_costs, rank2_table, synthetic_table, write_table
+from tables import add_fused, fanout_costs, rank2_table, synthetic_table, write_table
 from tinygraphs import chain_graph, diamond_graph, fanout_graph, ffn_block, mlp_graph, t1_graph, t2_graph
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol(name):
     import ctypes
     lib = ctypes.CDLL(os.path.join(F.LIBDIR, name))
     syms = _header_symbols()
-    assert len(syms) == 29
+    assert len(syms) == 30
     for s in syms:
         assert hasattr(lib, s), s
     assert set(syms) == set(F.SYMBOLS)
@@ -93,11 +93,14 @@ def _compare_plans(og, obj, tmp_path, flags=0):
     assert lp.variant == ref.variant
     assert lp.total_ns == ref.total
     assert lp.guard_used == ref.guard_used
-    # arena on the chosen layouts
+    assert lp.fuse == ref.fuse
+    priced = bool(ct.fused) and not (flags & (PL.NO_FUSION | PL.NO_DP))
+    assert lp.fusion_priced == priced
+    # arena on the chosen layouts (and fusions)
     lay = {e: ct.L[e][ref.layout_idx[e]] for e in range(og.n_edges)}
     for e in range(og.n_edges):
         assert lp.perm(e) == lay[e]
-    oap = PA.plan_arena(og, lay)
+    oap = PA.plan_arena(og, lay, fuse=ref.fuse if priced else None)
     ap = F.ArenaPlan(g, lp)
     assert ap.peak == oap.peak
     for e in range(og.n_edges):
@@ -106,6 +109,8 @@ def _compare_plans(og, obj, tmp_path, flags=0):
         assert ap.offset[e] == (oap.offset[r] if r in oap.offset else -1)
     assert ap.lower_bound == PA.lower_bound(oap.buffers, oap.size, oap.defn, oap.last, len(og.nodes))
     assert ap.naive == PA.naive_plan(og).peak
+    if priced:
+        return lp
     nv = F.ArenaPlan(g, lp, no_reuse=True)
     off = 0
     for b in sorted(oap.buffers):
@@ -163,6 +168,28 @@ def test_planner_parity_guard_branches(infeasible, flags, tmp_path):
     else:
         assert (lp.guard_used, lp.total_ns) == (1, 70)
         assert lp.layout_idx == [0] * og.n_edges
+
+
+FUSE_GRAPHS = [lambda: mlp_graph(2), lambda: mlp_graph(3), ffn_block, t1_graph]
+
+
+@pytest.mark.parametrize("gi", range(len(FUSE_GRAPHS)))
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("flags", [0, PL.NO_GUARD, PL.NO_FUSION, PL.NO_VARIANTS])
+def test_planner_parity_fused_tiny(gi, seed, flags, tmp_path):
+    """Tables with priced fusion chains: both planners choose the same
+    fusions, layouts, variants (-2 on absorbed nodes) and arena."""
+    og = FUSE_GRAPHS[gi]()
+    obj = add_fused(synthetic_table(og, seed=seed, mode="random", lo=1, hi=40), og, seed, lo=1, hi=70)
+    _compare_plans(og, obj, tmp_path, flags)
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 5])
+def test_planner_parity_fused_config_graphs(idx, tmp_path):
+    og = OG.build_transformer(synth_inputs.config(idx))
+    obj = add_fused(synthetic_table(og, seed=idx, mode="random"), og, idx, lo=1, hi=1500)
+    lp = _compare_plans(og, obj, tmp_path)
+    assert any(lp.fuse)
 
 
 def test_ragged_config_parity(tmp_path):
