@@ -291,3 +291,45 @@ def test_fused_plan_arena_and_permuted_execution():
     ref = execute.run_canonical(g, [x], cs)
     out = execute.run_in_arena(g, lay, ap.root, ap.offset, ap.peak, [x], cs, fuse=plan.fuse)
     assert np.array_equal(out[0], ref[0])
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("builder", ["mlp2", "mlp3", "ffn_block"])
+def test_best_chains_is_the_cheapest_chain_set(seed, builder):
+    """For fixed layouts the chain choice is exact: best_chains' set costs
+    the minimum over every set of disjoint chains (enumerated), and no
+    plan the planner returns could lower its total by choosing its chains
+    differently."""
+    import tinygraphs
+    from oracle import fusion
+    from tables import add_fused
+    g = {"mlp2": lambda: tinygraphs.mlp_graph(2), "mlp3": lambda: tinygraphs.mlp_graph(3),
+         "ffn_block": tinygraphs.ffn_block}[builder]()
+    obj = add_fused(synthetic_table(g, seed=seed, mode="random", lo=1, hi=40), g, seed, lo=1, hi=70)
+    ct = costtable.load(obj, g)
+    chains = sorted(ct.fused)
+    assert chains
+    rng = np.random.default_rng(seed)
+
+    def brute_min(lay):
+        best = None
+        for k in range(len(chains) + 1):
+            for sel in itertools.combinations(chains, k):
+                spans = [set(range(m, m + t + 1)) for m, t in sel]
+                if any(a & b for i, a in enumerate(spans) for b in spans[i + 1:]):
+                    continue
+                fz = [0] * len(g.nodes)
+                for m, t in sel:
+                    fz[m] = t
+                c = PL.plan_cost(g, ct, False, lay, fz)
+                best = c if best is None else min(best, c)
+        return best
+
+    for _ in range(4):
+        lay = [int(rng.integers(0, len(ct.L[e]))) for e in range(g.n_edges)]
+        fz = PL.best_chains(g, ct, False, lay)
+        assert PL.plan_cost(g, ct, False, lay, fz) == brute_min(lay)
+        # every chosen chain is a chain of the graph, disjoint from the others
+        assert all((m, t) in fusion.all_chains(g) for m, t in enumerate(fz) if t)
+    plan = PL.plan_layouts(g, ct)
+    assert plan.total == brute_min(plan.layout_idx)
