@@ -143,7 +143,9 @@ def launch_units(g, ex):
     name (with the fused epilogue steps and the group size), the nodes it
     performs (node order) and its algorithmic work -- the flops of its
     products for a GEMM launch (grouped products summed; a fused bias or
-    activation adds no flops), else the bytes of its one node."""
+    activation adds no flops), else the bytes of its one node (for a
+    residual Add and its normalisation in one launch: the summands read
+    once, the normalised output written once; its class is the norm's)."""
     launch, _, names = ex.schedule()
     units = [{"name": nm, "nodes": []} for nm in names]
     for n, l in enumerate(launch):
@@ -154,6 +156,13 @@ def launch_units(g, ex):
         if mm:
             u["op"], u["kind"] = g.desc["nodes"][mm[0]]["op"], "flop"
             u["work"] = sum(node_work(g, n)[1] for n in mm)
+        elif len(u["nodes"]) == 2 and g.desc["nodes"][u["nodes"][0]]["op"] == "add":
+            h, n = u["nodes"]
+            u["op"] = g.desc["nodes"][n]["op"]
+            isz = 2 if g.dtype == "bf16" else 4
+            u["kind"] = "bytes"
+            u["work"] = float(sum(int(np.prod(g.edge_shape(v))) * isz for v in g.desc["nodes"][h]["ins"]) +
+                              int(np.prod(g.desc["nodes"][n]["out_shape"])) * isz)
         else:
             assert len(u["nodes"]) == 1, u
             n = u["nodes"][0]

@@ -399,8 +399,9 @@ fluid_status fluid_trace_collect(const fluid_graph* g, double* ms_per_node, int3
 
 /* Name of the kernel a node runs under a plan, e.g.
  * "gemm_f32_m128n128_ak_bn_cn": "view" for views, "fused" for a node the
- * plan performs inside the launch of the MatMul before it (variant -2);
- * the MatMul's own name is that of its unfused product. */
+ * plan performs inside the launch of the node before it (variant -2); a
+ * chain's MatMul names its unfused product, a residual Add heading a chain
+ * the summed normalisation kernel (e.g. "add_layernorm_row_f32_v4"). */
 fluid_status fluid_node_kernel(const fluid_graph* g, const fluid_layout_plan* lp, int32_t node,
                                char* buf, uint64_t cap);
 

@@ -153,9 +153,11 @@ def _const_values(g, consts):
     return out
 
 
-def run_canonical(g, inputs, consts, keep=False, arith=np.float64):
+def run_canonical(g, inputs, consts, keep=False, arith=np.float64, on_chip=()):
     """Row-major reference execution.  Returns the graph outputs (float64
     arrays of dtype-representable values); with ``keep`` also every edge.
+    Edges in ``on_chip`` keep their unrounded values (results that a fused
+    launch never stores).
 
     ``arith`` is the type every operator computes in before its result is
     rounded to the edge dtype: float64 is the definition; float32 gives a
@@ -172,7 +174,8 @@ def run_canonical(g, inputs, consts, keep=False, arith=np.float64):
             args = [a.astype(arith) for a in args]
         y = eval_node(nd, args, arith)
         assert tuple(y.shape) == tuple(nd.out_shape), (n, nd.op, y.shape, nd.out_shape)
-        vals[g.out_edge(n)] = numerics.round_to(y, g.dtype)
+        e = g.out_edge(n)
+        vals[e] = y if e in on_chip else numerics.round_to(y, g.dtype)
     outs = [vals[e] for e in g.outputs]
     return (outs, vals) if keep else outs
 

@@ -11,8 +11,13 @@ chain when, step by step,
     [N] (N the product's last dim; first step only), one GELU or SiLU, and
     an Add or Mul of the chain value with another activation R of the
     product's shape, produced before m (last step).
-The launch then writes only the last node's output: the intermediate
-results never reach memory.  t is 1..3; every prefix of a chain is a chain.
+A second kind of chain starts at an Add of two activations of its own
+output's shape (a residual sum) whose result has exactly one reader, the
+next node, a LayerNorm or RMSNorm over it (with constant scale and shift),
+and is not a graph output: the normalisation launch then also forms the sum
+(t = 1).
+The launch writes only the last node's output: the intermediate results
+never reach memory.  t is 1..3; every prefix of a chain is a chain.
 """
 from __future__ import annotations
 
@@ -23,10 +28,12 @@ def _readers(g, e):
 
 def chain_steps(g, m):
     """The longest fusion chain starting at node m, as a list of
-    (node, kind, R) with kind in {"bias", "act", "add_r", "mul_r"} and R the
-    other activation of an Add / Mul step (None otherwise).  Empty when m is
-    not a MatMul or nothing can follow it."""
+    (node, kind, R) with kind in {"bias", "act", "add_r", "mul_r", "norm"}
+    and R the other activation of an Add / Mul step (None otherwise).  Empty
+    when m heads no chain."""
     nd = g.nodes[m]
+    if nd.op == "add":
+        return _norm_chain(g, m)
     if nd.op != "matmul" or len(nd.ins) != 2:
         return []
     out_shape = tuple(nd.out_shape)
@@ -63,6 +70,22 @@ def chain_steps(g, m):
     return steps
 
 
+def _norm_chain(g, m):
+    """Add m of two activations followed by the normalisation of its sum."""
+    nd = g.nodes[m]
+    out_shape = tuple(nd.out_shape)
+    if len(nd.ins) != 2 or min(nd.ins) < 0 or nd.ins[0] == nd.ins[1] or \
+            any(tuple(g.edge_shape(e)) != out_shape for e in nd.ins):
+        return []
+    cur, n = g.out_edge(m), m + 1
+    if n >= len(g.nodes) or cur in g.outputs or _readers(g, cur) != [n]:
+        return []
+    x = g.nodes[n]
+    if x.op not in ("layernorm", "rmsnorm") or x.ins[0] != cur or min(x.ins[1:]) >= 0:
+        return []
+    return [(n, "norm", None)]
+
+
 def chain_slots(g, m, t):
     """Activation edges a fused launch of the chain (m, t) reads, in slot
     order: the MatMul's activation inputs, then R of an Add / Mul step."""
@@ -74,7 +97,7 @@ def chain_slots(g, m, t):
 
 
 def all_chains(g):
-    """{(m, t): [node ids m .. m+t]} for every MatMul m and chain length t."""
+    """{(m, t): [node ids m .. m+t]} for every chain head m and length t."""
     out = {}
     for m in range(len(g.nodes)):
         steps = chain_steps(g, m)

@@ -12,7 +12,10 @@
 //    writes coalesced; the row is streamed twice (three times for
 //    LayerNorm's exact two-pass variance).
 // Causal softmax: keys k > q (q = index along the second-to-last logical
-// dim) get probability exactly 0.  All arithmetic is fp32.
+// dim) get probability exactly 0.  The RED_SUM_* norms read a second
+// tensor x1 (own layout) and normalise x + x1, the sum formed on load (a
+// residual Add performed in the normalisation's launch).  All arithmetic is
+// fp32.
 #include <math.h>
 
 #include "dev.h"
@@ -20,8 +23,9 @@
 
 namespace fluid {
 
-__device__ __forceinline__ void row_offsets(const RedParams& p, uint32_t row, int32_t& io, int32_t& oo, uint32_t& qi) {
-  io = 0; oo = 0; qi = 0;
+__device__ __forceinline__ void row_offsets(const RedParams& p, uint32_t row, int32_t& io, int32_t& oo, int32_t& io1,
+                                            uint32_t& qi) {
+  io = 0; oo = 0; io1 = 0; qi = 0;
   uint32_t rest = row;
 #pragma unroll
   for (int d = kMaxDims - 1; d >= 0; --d) {
@@ -31,6 +35,7 @@ __device__ __forceinline__ void row_offsets(const RedParams& p, uint32_t row, in
       rest = q;
       io += (int32_t)i * p.ris[d];
       oo += (int32_t)i * p.ros[d];
+      io1 += (int32_t)i * p.ris1[d];
       if (d == p.qdim) qi = i;
     }
   }
@@ -38,12 +43,14 @@ __device__ __forceinline__ void row_offsets(const RedParams& p, uint32_t row, in
 
 template <typename T, int NPL, int OP>
 __global__ __launch_bounds__(256) void red_row_kernel(RedParams p) {
+  constexpr int BOP = red_base_op(OP);
+  constexpr bool SUM = red_has_sum(OP);
   const uint32_t row = blockIdx.x * 4u + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= p.nrows) return;  // uniform per wavefront
-  int32_t io, oo;
+  int32_t io, oo, io1;
   uint32_t qi;
-  row_offsets(p, row, io, oo, qi);
+  row_offsets(p, row, io, oo, io1, qi);
   const uint32_t R = p.R;
   const uint32_t valid = (OP == RED_SOFTMAX && p.causal) ? min(R, qi + 1u) : R;
   float v[NPL];
@@ -51,6 +58,7 @@ __global__ __launch_bounds__(256) void red_row_kernel(RedParams p) {
   for (int j = 0; j < NPL; ++j) {
     const uint32_t k = (uint32_t)lane + 64u * j;
     v[j] = k < valid ? Elem<T>::load(p.x, io + (int32_t)k * p.irs) : 0.f;
+    if constexpr (SUM) v[j] += k < valid ? Elem<T>::load(p.x1, io1 + (int32_t)k * p.irs1) : 0.f;
   }
   if constexpr (OP == RED_SOFTMAX) {
     float m = -INFINITY;
@@ -78,11 +86,11 @@ __global__ __launch_bounds__(256) void red_row_kernel(RedParams p) {
   } else {
     float s = 0.f;
 #pragma unroll
-    for (int j = 0; j < NPL; ++j) s += (OP == RED_LAYERNORM) ? v[j] : v[j] * v[j];
+    for (int j = 0; j < NPL; ++j) s += (BOP == RED_LAYERNORM) ? v[j] : v[j] * v[j];
     s = wave_sum(s);
     const float invR = 1.0f / (float)R;
     float mean = 0.f, rstd;
-    if constexpr (OP == RED_LAYERNORM) {
+    if constexpr (BOP == RED_LAYERNORM) {
       mean = s * invR;
       float q = 0.f;
 #pragma unroll
@@ -101,7 +109,7 @@ __global__ __launch_bounds__(256) void red_row_kernel(RedParams p) {
       const uint32_t k = (uint32_t)lane + 64u * j;
       if (k < R) {
         float y = (v[j] - mean) * rstd * Elem<T>::load(p.gamma, k);
-        if constexpr (OP == RED_LAYERNORM) y += Elem<T>::load(p.beta, k);
+        if constexpr (BOP == RED_LAYERNORM) y += Elem<T>::load(p.beta, k);
         Elem<T>::store(p.y, oo + (int32_t)k * p.ors, y);
       }
     }
@@ -144,16 +152,19 @@ struct Piece<uint16_t> {
 // pieces per lane, piece c of lane l at l + 64 c.
 template <typename T, int NC, int OP>
 __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
+  constexpr int BOP = red_base_op(OP);
+  constexpr bool SUM = red_has_sum(OP);
   constexpr int VEC = Piece<T>::VEC;
   const uint32_t row = blockIdx.x * 4u + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= p.nrows) return;  // uniform per wavefront
-  int32_t io, oo;
+  int32_t io, oo, io1;
   uint32_t qi;
-  row_offsets(p, row, io, oo, qi);
+  row_offsets(p, row, io, oo, io1, qi);
   const uint32_t R = p.R;
   const uint32_t valid = (OP == RED_SOFTMAX && p.causal) ? min(R, qi + 1u) : R;
   const T* x = (const T*)p.x + io;
+  const T* x1 = (const T*)p.x1 + io1;
   T* y = (T*)p.y + oo;
   float v[NC][VEC];
 #pragma unroll
@@ -162,16 +173,24 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
     uint4 u = make_uint4(0, 0, 0, 0);
     if (e0 < valid) u = *(const uint4*)(x + e0);
     Piece<T>::unpack(u, v[c]);
+    if constexpr (SUM) {
+      uint4 u1 = make_uint4(0, 0, 0, 0);
+      if (e0 < valid) u1 = *(const uint4*)(x1 + e0);
+      float w[VEC];
+      Piece<T>::unpack(u1, w);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) v[c][i] += w[i];
+    }
   }
   // gamma / beta pieces are fetched with the row, not after the reduction,
   // so the row costs one memory round trip
-  uint4 gq[OP == RED_SOFTMAX ? 1 : NC], bq[OP == RED_LAYERNORM ? NC : 1];
+  uint4 gq[OP == RED_SOFTMAX ? 1 : NC], bq[BOP == RED_LAYERNORM ? NC : 1];
   if constexpr (OP != RED_SOFTMAX) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const uint32_t e0 = (uint32_t)(lane + 64 * c) * VEC;
       gq[c] = e0 < R ? *(const uint4*)((const T*)p.gamma + e0) : make_uint4(0, 0, 0, 0);
-      if constexpr (OP == RED_LAYERNORM) bq[c] = e0 < R ? *(const uint4*)((const T*)p.beta + e0) : make_uint4(0, 0, 0, 0);
+      if constexpr (BOP == RED_LAYERNORM) bq[c] = e0 < R ? *(const uint4*)((const T*)p.beta + e0) : make_uint4(0, 0, 0, 0);
     }
   }
   if constexpr (OP == RED_SOFTMAX) {
@@ -210,11 +229,11 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) s += (OP == RED_LAYERNORM) ? v[c][i] : v[c][i] * v[c][i];
+      for (int i = 0; i < VEC; ++i) s += (BOP == RED_LAYERNORM) ? v[c][i] : v[c][i] * v[c][i];
     s = wave_sum(s);
     const float invR = 1.0f / (float)R;
     float mean = 0.f, rstd;
-    if constexpr (OP == RED_LAYERNORM) {
+    if constexpr (BOP == RED_LAYERNORM) {
       mean = s * invR;
       float q = 0.f;
 #pragma unroll
@@ -237,11 +256,11 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
       if (e0 < R) {
         float g[VEC], b[VEC];
         Piece<T>::unpack(gq[c], g);
-        if constexpr (OP == RED_LAYERNORM) Piece<T>::unpack(bq[c], b);
+        if constexpr (BOP == RED_LAYERNORM) Piece<T>::unpack(bq[c], b);
 #pragma unroll
         for (int i = 0; i < VEC; ++i) {
           v[c][i] = (v[c][i] - mean) * rstd * g[i];
-          if constexpr (OP == RED_LAYERNORM) v[c][i] += b[i];
+          if constexpr (BOP == RED_LAYERNORM) v[c][i] += b[i];
         }
         *(uint4*)(y + e0) = Piece<T>::pack(v[c]);
       }
@@ -255,28 +274,39 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
 // thread, piece c of thread t at t + 256 c; reductions through LDS.
 template <typename T, int NC, int OP>
 __global__ __launch_bounds__(256) void red_rowb_kernel(RedParams p) {
+  constexpr int BOP = red_base_op(OP);
+  constexpr bool SUM = red_has_sum(OP);
   constexpr int VEC = Piece<T>::VEC;
   __shared__ float part[4];
   const uint32_t row = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int32_t io, oo;
+  int32_t io, oo, io1;
   uint32_t qi;
-  row_offsets(p, row, io, oo, qi);
+  row_offsets(p, row, io, oo, io1, qi);
   const uint32_t R = p.R;
   const uint32_t valid = (OP == RED_SOFTMAX && p.causal) ? min(R, qi + 1u) : R;
   const T* x = (const T*)p.x + io;
+  const T* x1 = (const T*)p.x1 + io1;
   T* y = (T*)p.y + oo;
   float v[NC][VEC];
-  uint4 gq[OP == RED_SOFTMAX ? 1 : NC], bq[OP == RED_LAYERNORM ? NC : 1];
+  uint4 gq[OP == RED_SOFTMAX ? 1 : NC], bq[BOP == RED_LAYERNORM ? NC : 1];
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const uint32_t e0 = (uint32_t)(tid + 256 * c) * VEC;
     uint4 u = make_uint4(0, 0, 0, 0);
     if (e0 < valid) u = *(const uint4*)(x + e0);
     Piece<T>::unpack(u, v[c]);
+    if constexpr (SUM) {
+      uint4 u1 = make_uint4(0, 0, 0, 0);
+      if (e0 < valid) u1 = *(const uint4*)(x1 + e0);
+      float w[VEC];
+      Piece<T>::unpack(u1, w);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) v[c][i] += w[i];
+    }
     if constexpr (OP != RED_SOFTMAX) {
       gq[c] = e0 < R ? *(const uint4*)((const T*)p.gamma + e0) : make_uint4(0, 0, 0, 0);
-      if constexpr (OP == RED_LAYERNORM) bq[c] = e0 < R ? *(const uint4*)((const T*)p.beta + e0) : make_uint4(0, 0, 0, 0);
+      if constexpr (BOP == RED_LAYERNORM) bq[c] = e0 < R ? *(const uint4*)((const T*)p.beta + e0) : make_uint4(0, 0, 0, 0);
     }
   }
   // block-wide sum / max: wavefront butterflies, then the four partials
@@ -332,11 +362,11 @@ __global__ __launch_bounds__(256) void red_rowb_kernel(RedParams p) {
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) s += (OP == RED_LAYERNORM) ? v[c][i] : v[c][i] * v[c][i];
+      for (int i = 0; i < VEC; ++i) s += (BOP == RED_LAYERNORM) ? v[c][i] : v[c][i] * v[c][i];
     s = block_sum(s);
     const float invR = 1.0f / (float)R;
     float mean = 0.f, rstd;
-    if constexpr (OP == RED_LAYERNORM) {
+    if constexpr (BOP == RED_LAYERNORM) {
       mean = s * invR;
       float q = 0.f;
 #pragma unroll
@@ -359,11 +389,11 @@ __global__ __launch_bounds__(256) void red_rowb_kernel(RedParams p) {
       if (e0 < R) {
         float g[VEC], b[VEC];
         Piece<T>::unpack(gq[c], g);
-        if constexpr (OP == RED_LAYERNORM) Piece<T>::unpack(bq[c], b);
+        if constexpr (BOP == RED_LAYERNORM) Piece<T>::unpack(bq[c], b);
 #pragma unroll
         for (int i = 0; i < VEC; ++i) {
           v[c][i] = (v[c][i] - mean) * rstd * g[i];
-          if constexpr (OP == RED_LAYERNORM) v[c][i] += b[i];
+          if constexpr (BOP == RED_LAYERNORM) v[c][i] += b[i];
         }
         *(uint4*)(y + e0) = Piece<T>::pack(v[c]);
       }
@@ -373,17 +403,25 @@ __global__ __launch_bounds__(256) void red_rowb_kernel(RedParams p) {
 
 template <typename T, int OP>
 __global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
+  constexpr int BOP = red_base_op(OP);
+  constexpr bool SUM = red_has_sum(OP);
   const uint32_t row = blockIdx.x * 256u + threadIdx.x;
   if (row >= p.nrows) return;
-  int32_t io, oo;
+  int32_t io, oo, io1;
   uint32_t qi;
-  row_offsets(p, row, io, oo, qi);
+  row_offsets(p, row, io, oo, io1, qi);
   const uint32_t R = p.R;
+  // element k of the row (of the sum for RED_SUM_*)
+  auto ldx = [&](uint32_t k) {
+    float a = Elem<T>::load(p.x, io + (int32_t)k * p.irs);
+    if constexpr (SUM) a += Elem<T>::load(p.x1, io1 + (int32_t)k * p.irs1);
+    return a;
+  };
   if constexpr (OP == RED_SOFTMAX) {
     const uint32_t valid = p.causal ? min(R, qi + 1u) : R;
     float m = -INFINITY, s = 0.f;
     for (uint32_t k = 0; k < valid; ++k) {
-      const float z = p.attr * Elem<T>::load(p.x, io + (int32_t)k * p.irs);
+      const float z = p.attr * ldx(k);
       if (z > m) {
         s = s * expf(m - z) + 1.f;
         m = z;
@@ -394,33 +432,33 @@ __global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
     const float inv = 1.0f / s;
     for (uint32_t k = 0; k < R; ++k) {
       float y = 0.f;
-      if (k < valid) y = expf(p.attr * Elem<T>::load(p.x, io + (int32_t)k * p.irs) - m) * inv;
+      if (k < valid) y = expf(p.attr * ldx(k) - m) * inv;
       Elem<T>::store(p.y, oo + (int32_t)k * p.ors, y);
     }
   } else {
     const float invR = 1.0f / (float)R;
     float mean = 0.f, rstd;
-    if constexpr (OP == RED_LAYERNORM) {
+    if constexpr (BOP == RED_LAYERNORM) {
       float s = 0.f;
-      for (uint32_t k = 0; k < R; ++k) s += Elem<T>::load(p.x, io + (int32_t)k * p.irs);
+      for (uint32_t k = 0; k < R; ++k) s += ldx(k);
       mean = s * invR;
       float q = 0.f;
       for (uint32_t k = 0; k < R; ++k) {
-        const float d = Elem<T>::load(p.x, io + (int32_t)k * p.irs) - mean;
+        const float d = ldx(k) - mean;
         q += d * d;
       }
       rstd = 1.0f / sqrtf(q * invR + p.attr);
     } else {
       float q = 0.f;
       for (uint32_t k = 0; k < R; ++k) {
-        const float x = Elem<T>::load(p.x, io + (int32_t)k * p.irs);
+        const float x = ldx(k);
         q += x * x;
       }
       rstd = 1.0f / sqrtf(q * invR + p.attr);
     }
     for (uint32_t k = 0; k < R; ++k) {
-      float y = (Elem<T>::load(p.x, io + (int32_t)k * p.irs) - mean) * rstd * Elem<T>::load(p.gamma, k);
-      if constexpr (OP == RED_LAYERNORM) y += Elem<T>::load(p.beta, k);
+      float y = (ldx(k) - mean) * rstd * Elem<T>::load(p.gamma, k);
+      if constexpr (BOP == RED_LAYERNORM) y += Elem<T>::load(p.beta, k);
       Elem<T>::store(p.y, oo + (int32_t)k * p.ors, y);
     }
   }
@@ -435,6 +473,8 @@ __global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
 // lane shuffles and over the 16 wavefronts through LDS, in a fixed order.
 template <typename T, int RT, int KPL, int OP>
 __global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
+  constexpr int BOP = red_base_op(OP);
+  constexpr bool SUM = red_has_sum(OP);
   constexpr int KQ = 64 / RT;
   __shared__ float part[16][RT];
   // the wavefront index is uniform: keep it in a scalar register
@@ -454,9 +494,9 @@ __global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
   const uint32_t row = tile * (uint32_t)RT + (uint32_t)r;
   // rows past the end compute on the last row and store nothing
   const bool live = row < p.nrows;
-  int32_t io, oo;
+  int32_t io, oo, io1;
   uint32_t qi;
-  row_offsets(p, live ? row : p.nrows - 1u, io, oo, qi);
+  row_offsets(p, live ? row : p.nrows - 1u, io, oo, io1, qi);
   const uint32_t R = p.R;
   const uint32_t valid = (OP == RED_SOFTMAX && p.causal) ? min(R, qi + 1u) : R;
   const uint32_t kb = (uint32_t)wave * (KQ * KPL);  // uniform
@@ -475,11 +515,22 @@ __global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
   const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(p.y, 0, 0x7fffffff, 0x00020000);
   const uint32_t xstep = (uint32_t)p.irs * ES, ystep = (uint32_t)p.ors * ES;
   const uint32_t xo = (uint32_t)io * ES + (uint32_t)q * xstep;
+  // the second summand (RED_SUM_*): its own resource, lane offset and step
+  const __amdgpu_buffer_rsrc_t rx1 =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(SUM ? p.x1 : p.x), 0, 0x7fffffff, 0x00020000);
+  const uint32_t xstep1 = (uint32_t)p.irs1 * ES;
+  const uint32_t xo1 = (uint32_t)io1 * ES + (uint32_t)q * xstep1;
   const uint32_t yo = live ? (uint32_t)oo * ES + (uint32_t)q * ystep : OOB;
-  auto ld = [&](int j, uint32_t vo) {
-    const uint32_t so = (kb + (uint32_t)(KQ * j)) * xstep;
-    if constexpr (ES == 4) return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rx, vo, so, 0));
-    else return bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rx, vo, so, 0));
+  auto ld1 = [&](const __amdgpu_buffer_rsrc_t& rs, uint32_t vo, uint32_t so) {
+    if constexpr (ES == 4) return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, vo, so, 0));
+    else return bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rs, vo, so, 0));
+  };
+  // element j of the lane (of the sum for RED_SUM_*); vo / vo1 the lane's
+  // offsets, or OOB for a masked load
+  auto ld = [&](int j, uint32_t vo, uint32_t vo1) {
+    float a = ld1(rx, vo, (kb + (uint32_t)(KQ * j)) * xstep);
+    if constexpr (SUM) a += ld1(rx1, vo1, (kb + (uint32_t)(KQ * j)) * xstep1);
+    return a;
   };
   auto st1 = [&](int j, uint32_t vo, float y) {
     const uint32_t so = (kb + (uint32_t)(KQ * j)) * ystep;
@@ -489,10 +540,13 @@ __global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
   float v[KPL];
   if (masked) {
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) v[j] = ld(j, kl + KQ * j < valid ? xo : OOB);
+    for (int j = 0; j < KPL; ++j) {
+      const bool in = kl + KQ * j < valid;
+      v[j] = ld(j, in ? xo : OOB, in ? xo1 : OOB);
+    }
   } else {
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) v[j] = ld(j, xo);
+    for (int j = 0; j < KPL; ++j) v[j] = ld(j, xo, xo1);
   }
   // y[j] for every j, stored where k < R
   auto store_all = [&](auto&& yfun) {
@@ -538,11 +592,11 @@ __global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
   } else {
     float sum = 0.f;
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) sum += (OP == RED_LAYERNORM) ? v[j] : v[j] * v[j];
+    for (int j = 0; j < KPL; ++j) sum += (BOP == RED_LAYERNORM) ? v[j] : v[j] * v[j];
     sum = combine(sum, false);
     const float invR = 1.0f / (float)R;
     float mean = 0.f, rstd;
-    if constexpr (OP == RED_LAYERNORM) {
+    if constexpr (BOP == RED_LAYERNORM) {
       mean = sum * invR;
       float qs = 0.f;
 #pragma unroll
@@ -559,7 +613,7 @@ __global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
     store_all([&](int j) {
       const uint32_t kc = min(kl + KQ * j, R - 1u);
       float y = (v[j] - mean) * rstd * Elem<T>::load(p.gamma, kc);
-      if constexpr (OP == RED_LAYERNORM) y += Elem<T>::load(p.beta, kc);
+      if constexpr (BOP == RED_LAYERNORM) y += Elem<T>::load(p.beta, kc);
       return y;
     });
   }
@@ -638,7 +692,10 @@ hipError_t red_dispatch(const NodeKernel& k, hipStream_t s) {
   switch (k.red.op) {
     case RED_SOFTMAX: return red_dispatch_op<T, RED_SOFTMAX>(k, s);
     case RED_LAYERNORM: return red_dispatch_op<T, RED_LAYERNORM>(k, s);
-    default: return red_dispatch_op<T, RED_RMSNORM>(k, s);
+    case RED_RMSNORM: return red_dispatch_op<T, RED_RMSNORM>(k, s);
+    case RED_SUM_LAYERNORM: return red_dispatch_op<T, RED_SUM_LAYERNORM>(k, s);
+    case RED_SUM_RMSNORM: return red_dispatch_op<T, RED_SUM_RMSNORM>(k, s);
+    default: return hipErrorInvalidValue;
   }
 }
 

@@ -77,9 +77,18 @@ void patch(NodeKernel& k, const PreparedNode& pn, const Bases& B) {
   }
 }
 
-// The fused launch of pn (fuse_n > 0): the MatMul and its epilogue.
+// The fused launch of pn (fuse_n > 0): the MatMul and its epilogue, or the
+// normalisation of the sum a residual Add forms.
 NodeKernel fused_kernel(const PreparedNode& pn, const Bases& B) {
   NodeKernel k = pn.kf;
+  if (k.family == KF_RED_ROW || k.family == KF_RED_COL) {
+    k.red.x = resolve(pn.in[0], B);
+    k.red.x1 = resolve(pn.in[1], B);
+    k.red.gamma = pn.fgamma >= 0 ? B.consts[pn.fgamma] : nullptr;
+    k.red.beta = pn.fbeta >= 0 ? B.consts[pn.fbeta] : nullptr;
+    k.red.y = resolve(pn.fout, B);
+    return k;
+  }
   k.gemm.A = resolve(pn.in[0], B);
   k.gemm.B = resolve(pn.in[1], B);
   k.gemm.C = resolve(pn.fout, B);
@@ -609,17 +618,15 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
       }
       t.sigs.push_back(std::move(sig));
     }
-    // fusion chains (fusion.h): one fused signature per (MatMul signature,
-    // epilogue steps); the MatMul's slots and R laid out as for the node,
-    // R in the output's layout only (a fused launch reading R in another
+    // fusion chains (fusion.h): one fused signature per (head signature,
+    // step signatures); the head's slots and R laid out as for the node, R
+    // in the output's layout only (a fused launch reading R in another
     // layout than it writes is never the cheap way to run the chain)
     {
       struct FusedKey {
         SigKey k;
-        uint32_t act, rop, bias;
-        bool operator<(const FusedKey& o) const {
-          return std::tie(k, act, rop, bias) < std::tie(o.k, o.act, o.rop, o.bias);
-        }
+        std::vector<SigKey> steps;
+        bool operator<(const FusedKey& o) const { return std::tie(k, steps) < std::tie(o.k, o.steps); }
       };
       std::map<FusedKey, int> fsig_of;
       std::vector<std::pair<int, int>> rep_chain;  // (m, t) per fused signature
@@ -627,12 +634,9 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
       std::vector<std::vector<Perm>> fout_lists;
       for (int m = 0; m < g.n_nodes(); ++m) {
         const std::vector<ChainStep> steps = chain_steps(g, m);
-        FusedKey fk{sig_key(g, m), 0u, 0u, 0u};
+        FusedKey fk{sig_key(g, m), {}};
         for (int tl = 1; tl <= (int)steps.size(); ++tl) {
-          const ChainStep& st = steps[tl - 1];
-          if (st.kind == CH_BIAS) fk.bias = 1u;
-          else if (st.kind == CH_ACT) fk.act = g.nodes[st.node].op == FLUID_OP_GELU ? 1u : 2u;
-          else fk.rop = st.kind == CH_ADD_R ? 1u : 2u;
+          fk.steps.push_back(sig_key(g, steps[tl - 1].node));
           auto it = fsig_of.find(fk);
           if (it == fsig_of.end()) {
             it = fsig_of.emplace(fk, (int)rep_chain.size()).first;
@@ -660,7 +664,8 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
         for (int i = 0; i < tl; ++i) {
           if (steps[i].kind == CH_BIAS) bias = steps[i].bias;
           else if (steps[i].kind == CH_ACT) act = g.nodes[steps[i].node].op == FLUID_OP_GELU ? 1u : 2u;
-          else rop = steps[i].kind == CH_ADD_R ? 1u : 2u;
+          else if (steps[i].kind == CH_ADD_R) rop = 1u;
+          else if (steps[i].kind == CH_MUL_R) rop = 2u;
         }
         Sig sig;
         sig.op = mn.op;
@@ -676,7 +681,36 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
           SigEntry en;
           for (int i = 0; i < ns; ++i) en.in.push_back(lists[i][idx[i]]);
           en.out = olist[idx[ns]];
-          if (!rop || en.in[nmm] == en.out) {
+          if (mn.op == FLUID_OP_ADD) {
+            // the residual sum and its normalisation: both summands, the
+            // norm's constants, the output
+            const Node& xn = g.nodes[m + 1];
+            uint64_t off = 0;
+            auto place = [&](const Shape& sh, std::vector<int64_t> st, int dt) {
+              Operand o;
+              o.shape = sh;
+              o.stride = std::move(st);
+              o.dtype = dt;
+              o.ptr = base + off;
+              off = align256(off + (uint64_t)numel(sh) * dtype_bytes(dt));
+              return o;
+            };
+            const Shape& xs = sig.out_shape;
+            const Operand x0 = place(xs, dense_strides(xs, en.in[0]), g.dtype);
+            const Operand x1 = place(xs, dense_strides(xs, en.in[1]), g.dtype);
+            std::vector<Operand> ins = {x0};
+            for (size_t s2 = 1; s2 < xn.ins.size(); ++s2) {
+              const Const& c = g.consts[~xn.ins[s2]];
+              ins.push_back(place(c.shape, row_major_strides(c.shape), c.dtype));
+            }
+            const Operand ou = place(xs, dense_strides(xs, en.out), g.dtype);
+            for (int v = 0; v < num_variants(xn.op); ++v) {
+              NodeKernel k = prepare_sum_norm(xn, v, g.dtype, ins, x1, ou);
+              if (!k.available) { en.costs.push_back(-1); continue; }
+              en.costs.push_back(time_kernel(k, best_so_far));
+            }
+            sig.entries.push_back(std::move(en));
+          } else if (!rop || en.in[nmm] == en.out) {
             std::vector<Operand> ins;
             uint64_t off = 0;
             int slot = 0;

@@ -33,9 +33,13 @@ uint64_t measure_scratch_bytes(const Graph& g) {
       s += (uint64_t)numel(sh) * b + 256;
     }
     s += (uint64_t)numel(g.nodes[n].out_shape) * isz + 256;
-    // a fused launch also reads R (the output's shape) and a bias [N]
+    // a fused launch also reads R (the output's shape) and a bias [N], or
+    // (a residual Add and its normalisation) the norm's constants
     if (g.nodes[n].op == FLUID_OP_MATMUL)
       s += (uint64_t)numel(g.nodes[n].out_shape) * isz + 256 + (uint64_t)g.nodes[n].out_shape.back() * isz + 256;
+    if (g.nodes[n].op == FLUID_OP_ADD && n + 1 < g.n_nodes())
+      for (int v : g.nodes[n + 1].ins)
+        if (v < 0) s += (uint64_t)numel(g.consts[~v].shape) * dtype_bytes(g.consts[~v].dtype) + 256;
     best = std::max(best, s);
   }
   return best;
@@ -324,21 +328,30 @@ fluid_status fluid_node_kernel(const fluid_graph* gh, const fluid_layout_plan* l
     require(node >= 0 && node < g.n_nodes(), "node out of range");
     std::string name = lh->p.variant[node] == -2 ? "fused" : "view";
     if (lh->p.variant[node] >= 0) {
-      const Node& nd = g.nodes[node];
-      std::vector<Operand> ins;
-      for (size_t slot = 0; slot < nd.ins.size(); ++slot) {
-        const int v = nd.ins[slot];
+      // a residual Add heading a planned chain names the normalisation's
+      // summed kernel (its variant is that kernel's)
+      const bool sum_head = lh->p.fusion_priced && lh->p.fuse[node] > 0 && g.nodes[node].op == FLUID_OP_ADD;
+      const Node& nd = g.nodes[sum_head ? node + 1 : node];
+      auto operand = [&](int v, int slot) {
         Operand o;
         o.shape = v >= 0 ? g.edge_shape(v) : g.consts[~v].shape;
         o.stride = v >= 0 ? dense_strides(o.shape, lh->p.perm[v])
-                          : const_strides(nd, (int)slot, lh->p.variant[node], o.shape);
+                          : const_strides(nd, slot, lh->p.variant[node], o.shape);
         o.dtype = v >= 0 ? g.dtype : g.consts[~v].dtype;
-        ins.push_back(o);
-      }
+        return o;
+      };
+      std::vector<Operand> ins;
+      for (size_t slot = 0; slot < nd.ins.size(); ++slot) ins.push_back(operand(nd.ins[slot], (int)slot));
       Operand ou;
       ou.shape = nd.out_shape;
-      ou.stride = dense_strides(ou.shape, lh->p.perm[g.out_edge(node)]);
-      NodeKernel k = prepare_node(nd, lh->p.variant[node], g.dtype, ins, ou);
+      ou.stride = dense_strides(ou.shape, lh->p.perm[g.out_edge(sum_head ? node + 1 : node)]);
+      NodeKernel k;
+      if (sum_head) {
+        ins[0] = operand(g.nodes[node].ins[0], 0);
+        k = prepare_sum_norm(nd, lh->p.variant[node], g.dtype, ins, operand(g.nodes[node].ins[1], 1), ou);
+      } else {
+        k = prepare_node(nd, lh->p.variant[node], g.dtype, ins, ou);
+      }
       name = k.name();
     }
     size_t n = std::min<size_t>(cap - 1, name.size());

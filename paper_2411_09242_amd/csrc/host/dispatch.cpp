@@ -240,7 +240,8 @@ NodeKernel prepare_rope(const Node&, int dtype, const std::vector<Operand>& ins,
   return k;
 }
 
-NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
+NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out,
+                       const Operand* x1 = nullptr) {
   NodeKernel k;
   k.family = variant == 0 ? KF_RED_ROW : KF_RED_COL;
   k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
@@ -249,16 +250,22 @@ NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector
   const int r = (int)x.shape.size();
   RedParams& p = k.red;
   p.op = nd.op == FLUID_OP_SOFTMAX ? RED_SOFTMAX : nd.op == FLUID_OP_LAYERNORM ? RED_LAYERNORM : RED_RMSNORM;
+  if (x1) {
+    if (p.op == RED_SOFTMAX || x1->shape != x.shape) fail(FLUID_E_INVALID, "summed reduction: bad second summand");
+    p.op += 2;
+  }
   p.causal = nd.op == FLUID_OP_SOFTMAX ? nd.iattr : 0;
   p.attr = nd.fattr;
   p.R = (uint32_t)x.shape[r - 1];
   p.irs = (int32_t)x.stride[r - 1];
   p.ors = (int32_t)out.stride[r - 1];
-  struct D { int64_t ext, is, os; bool q; };
+  p.irs1 = x1 ? (int32_t)x1->stride[r - 1] : 0;
+  p.x1 = x1 ? x1->ptr : nullptr;
+  struct D { int64_t ext, is, os, is1; bool q; };
   std::vector<D> rows;
   for (int i = 0; i < r - 1; ++i) {
     bool q = p.causal && i == r - 2;
-    if (x.shape[i] != 1 || q) rows.push_back({x.shape[i], x.stride[i], out.stride[i], q});
+    if (x.shape[i] != 1 || q) rows.push_back({x.shape[i], x.stride[i], out.stride[i], x1 ? x1->stride[i] : 0, q});
   }
   std::stable_sort(rows.begin(), rows.end(), [](const D& a, const D& b) { return a.is > b.is; });
   if (rows.size() > (size_t)kMaxDims) fail(FLUID_E_UNSUPPORTED, "reduction rank");
@@ -270,6 +277,7 @@ NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector
     p.rdiv[i] = make_fastdiv(p.rext[i]);
     p.ris[i] = (int32_t)rows[i].is;
     p.ros[i] = (int32_t)rows[i].os;
+    p.ris1[i] = (int32_t)rows[i].is1;
     if (rows[i].q) p.qdim = i;
     nrows *= p.rext[i];
   }
@@ -284,7 +292,12 @@ NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector
     const int VEC = k.dtype == DT_BF16 ? 8 : 4;
     bool ok = p.irs == 1 && p.ors == 1 && p.R % VEC == 0 && aligned16(p.x) && aligned16(p.y);
     for (int i = 0; i < p.nrd; ++i) ok = ok && p.ris[i] % VEC == 0 && p.ros[i] % VEC == 0;
-    if (p.op != RED_SOFTMAX) ok = ok && aligned16(p.gamma) && (p.op != RED_LAYERNORM || aligned16(p.beta));
+    if (x1) {
+      ok = ok && p.irs1 == 1 && aligned16(p.x1);
+      for (int i = 0; i < p.nrd; ++i) ok = ok && p.ris1[i] % VEC == 0;
+    }
+    if (p.op != RED_SOFTMAX)
+      ok = ok && aligned16(p.gamma) && (red_base_op(p.op) != RED_LAYERNORM || aligned16(p.beta));
     if (ok) k.vec = VEC;
   }
   k.available = true;
@@ -537,6 +550,17 @@ int gemm_epilogue_caps(int variant, int dtype) {
   return EPI_BIAS | EPI_ACT | (rop ? EPI_ROP : 0);
 }
 
+NodeKernel prepare_sum_norm(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& x1,
+                            const Operand& out) {
+  if (nd.op != FLUID_OP_LAYERNORM && nd.op != FLUID_OP_RMSNORM) fail(FLUID_E_INVALID, "summed reduction: not a norm");
+  if (variant < 0 || variant >= num_variants(nd.op)) {
+    NodeKernel k;
+    k.why = "no such variant";
+    return k;
+  }
+  return prepare_red(nd, variant, dtype, ins, out, &x1);
+}
+
 NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
   if (variant < 0 || variant >= num_variants(nd.op)) {
     NodeKernel k;
@@ -558,7 +582,7 @@ NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vecto
 
 std::string NodeKernel::name() const {
   static const char* ew_names[] = {"copy", "add", "mul", "gelu", "silu", "relu"};
-  static const char* red_names[] = {"softmax", "layernorm", "rmsnorm"};
+  static const char* red_names[] = {"softmax", "layernorm", "rmsnorm", "add_layernorm", "add_rmsnorm"};
   static const char* gm[] = {"g", "k", "mn"};
   const std::string dt = dtype == DT_BF16 ? "bf16" : "f32";
   switch (family) {

@@ -75,6 +75,11 @@ enum : int { EPI_BIAS = 1, EPI_ACT = 2, EPI_ROP = 4 };
 int gemm_epilogue_caps(int variant, int dtype);
 NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins,
                         const Operand& out);
+// The LayerNorm / RMSNorm node nd (variant, operands as for prepare_node)
+// applied to ins[0] + x1, the sum formed on load in fp32 (x1 of ins[0]'s
+// shape, any layout): the kernel of a residual Add and its normalisation.
+NodeKernel prepare_sum_norm(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& x1,
+                            const Operand& out);
 
 // Row-major strides of a shape.
 std::vector<int64_t> row_major_strides(const Shape& s);

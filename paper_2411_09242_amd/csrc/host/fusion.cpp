@@ -4,9 +4,29 @@
 
 namespace fluid {
 
+namespace {
+
+// Add m of two activations followed by the normalisation of its sum.
+std::vector<ChainStep> norm_chain(const Graph& g, int m) {
+  const Node& nd = g.nodes[m];
+  if (nd.ins.size() != 2 || nd.ins[0] < 0 || nd.ins[1] < 0 || nd.ins[0] == nd.ins[1]) return {};
+  for (int e : nd.ins)
+    if (g.edge_shape(e) != nd.out_shape) return {};
+  const int cur = g.out_edge(m), n = m + 1;
+  if (n >= g.n_nodes() || g.is_output[cur] || g.readers[cur].size() != 1 || g.readers[cur][0] != n) return {};
+  const Node& x = g.nodes[n];
+  if ((x.op != FLUID_OP_LAYERNORM && x.op != FLUID_OP_RMSNORM) || x.ins[0] != cur) return {};
+  for (size_t i = 1; i < x.ins.size(); ++i)
+    if (x.ins[i] >= 0) return {};
+  return {{n, CH_NORM, -1, -1}};
+}
+
+}  // namespace
+
 std::vector<ChainStep> chain_steps(const Graph& g, int m) {
   std::vector<ChainStep> steps;
   const Node& nd = g.nodes[m];
+  if (nd.op == FLUID_OP_ADD) return norm_chain(g, m);
   if (nd.op != FLUID_OP_MATMUL || nd.ins.size() != 2) return steps;
   const Shape& out_shape = nd.out_shape;
   int cur = g.out_edge(m);

@@ -5,8 +5,12 @@
 // reader (the next node) and is no graph output, and the steps are, in this
 // order and each optional: an Add of a bias constant [N] (first step only),
 // one GELU or SiLU, and an Add or Mul with another activation R of the
-// product's shape produced before m (last step).  t = 1..3; every prefix of
-// a chain is a chain.
+// product's shape produced before m (last step).  A second kind starts at
+// an Add of two activations of its output's shape (a residual sum) whose
+// result has one reader, the next node, a LayerNorm / RMSNorm over it (with
+// constant scale and shift), and is no graph output: the normalisation
+// launch also forms the sum (t = 1).
+// t = 1..3; every prefix of a chain is a chain.
 #pragma once
 
 #include <vector>
@@ -15,7 +19,7 @@
 
 namespace fluid {
 
-enum ChainKind : int { CH_BIAS = 0, CH_ACT = 1, CH_ADD_R = 2, CH_MUL_R = 3 };
+enum ChainKind : int { CH_BIAS = 0, CH_ACT = 1, CH_ADD_R = 2, CH_MUL_R = 3, CH_NORM = 4 };
 
 struct ChainStep {
   int node;

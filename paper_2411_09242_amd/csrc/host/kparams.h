@@ -58,7 +58,11 @@ struct RopeParams {
   const float* sin_t;
 };
 
-enum RedOp : int { RED_SOFTMAX = 0, RED_LAYERNORM = 1, RED_RMSNORM = 2 };
+// RED_SUM_*: the normalisation of x + x1 (a residual sum formed on load,
+// in fp32, never rounded or stored).
+enum RedOp : int { RED_SOFTMAX = 0, RED_LAYERNORM = 1, RED_RMSNORM = 2, RED_SUM_LAYERNORM = 3, RED_SUM_RMSNORM = 4 };
+constexpr int red_base_op(int op) { return op >= RED_SUM_LAYERNORM ? op - 2 : op; }
+constexpr bool red_has_sum(int op) { return op >= RED_SUM_LAYERNORM; }
 
 // Row reductions over the last logical dim (length R).  Row dims are
 // ordered by input stride, outer -> inner.
@@ -71,6 +75,9 @@ struct RedParams {
   uint32_t nrows;
   uint32_t R;
   int32_t irs, ors;           // input / output stride of the reduced dim
+  int32_t ris1[kMaxDims];     // the second summand's strides (RED_SUM_*)
+  int32_t irs1;
+  const void* x1;
   const void* x;
   void* y;
   const void* gamma;

@@ -145,6 +145,24 @@ void try_fuse_epilogue(const Graph& g, const LayoutPlan& lp, const ArenaPlan* ap
   nx.fused_away = true;
 }
 
+// A planned residual-norm chain: the normalisation nx of the sum that the
+// Add h forms, run as one reduction over h's two operands (the sum never
+// stored; nx's output lies apart from both operands in the arena, the
+// chain's lifetimes keeping them live until nx).
+void fuse_norm(const Graph& g, const LayoutPlan& lp, PreparedNode& h, PreparedNode& nx, const Operand& nx_out) {
+  const Node& xn = g.nodes[nx.node];
+  std::vector<Operand> ops = nx.ops;
+  ops[0] = h.ops[0];
+  NodeKernel kf = prepare_sum_norm(xn, lp.variant[h.node], g.dtype, ops, h.ops[1], nx_out);
+  if (!kf.available) return;
+  h.kf = kf;
+  h.fuse_n = 1;
+  h.fout = nx.out;
+  h.fgamma = xn.ins.size() > 1 ? ~xn.ins[1] : -1;
+  h.fbeta = xn.ins.size() > 2 ? ~xn.ins[2] : -1;
+  nx.fused_away = true;
+}
+
 // The output edge and binding a prepared launch writes.
 int written_edge(const Graph& g, const Prepared& P, size_t i) {
   return g.out_edge(P.nodes[i + P.nodes[i].fuse_n].node);
@@ -263,6 +281,13 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
     out.dtype = g.dtype;
     out.ptr = fake_ptr(pn.out);
     pn.ops = ins;
+    if (lp.fusion_priced && lp.fuse[n] > 0 && nd.op == FLUID_OP_ADD) {
+      // heads a residual-norm chain: variant v is the normalisation's, and
+      // the sum is formed in its launch (fuse_norm)
+      pn.k.why = "performed in the launch of the normalisation after it";
+      P->nodes.push_back(std::move(pn));
+      continue;
+    }
     if (v == -2) {
       // performed by the fused MatMul before it (the plan priced that launch)
       size_t j = P->nodes.empty() ? 0 : P->nodes.size() - 1;
@@ -270,8 +295,11 @@ std::shared_ptr<Prepared> prepare(const Graph& g, const LayoutPlan& lp, const Ar
       require(!P->nodes.empty() && j + P->nodes[j].fuse_n == P->nodes.size() - 1 &&
                   lp.fuse[P->nodes[j].node] >= n - P->nodes[j].node,
               "node " + std::to_string(n) + ": marked fused, but no fused MatMul launch precedes it");
-      try_fuse_epilogue(g, lp, ap, P->nodes[j], g.out_edge(P->nodes.back().node), pn, out);
-      require(pn.fused_away, "node " + std::to_string(n) + ": the plan fuses it into MatMul node " +
+      if (g.nodes[P->nodes[j].node].op == FLUID_OP_ADD)
+        fuse_norm(g, lp, P->nodes[j], pn, out);
+      else
+        try_fuse_epilogue(g, lp, ap, P->nodes[j], g.out_edge(P->nodes.back().node), pn, out);
+      require(pn.fused_away, "node " + std::to_string(n) + ": the plan fuses it into node " +
                                  std::to_string(P->nodes[j].node) + ", which cannot perform it with variant " +
                                  std::to_string(lp.variant[P->nodes[j].node]));
       P->nodes.push_back(std::move(pn));

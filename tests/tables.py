@@ -137,6 +137,6 @@ def add_fused(obj, g, seed, n_variants=3, lo=1, hi=1000, scale=1.0):
             costs = [int(scale * rng.integers(lo, hi + 1)) for _ in range(n_variants)]
             entries.append([[list(p) for p in combo[:-1]], list(combo[-1]), costs])
         obj["fused"].append([m, t, len(obj["fused_sigs"])])
-        obj["fused_sigs"].append({"op": "matmul", "steps": t, "in_shapes": [list(g.edge_shape(e)) for e in slots],
+        obj["fused_sigs"].append({"op": g.nodes[m].op, "steps": t, "in_shapes": [list(g.edge_shape(e)) for e in slots],
                                   "out_shape": list(g.edge_shape(eo)), "entries": entries})
     return obj

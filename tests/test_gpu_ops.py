@@ -482,6 +482,53 @@ def test_norm_layouts_and_variants(dtype, op, shape, tmp_path):
             _check(og, {a: L[ia], n: L[ib]}, {1: v}, tmp_path, seed=ia + 3 * ib, scale=2.0)
 
 
+def sum_norm_graph(B, S, H, dtype, op):
+    """x -> a = GELU(x), b = SiLU(x); s = a + b; n = norm(s); y = GELU(n):
+    the residual Add (node 2) and its normalisation (node 3) form a chain."""
+    g = Graph(dtype=dtype)
+    x = g.add_input((B, S, H))
+    a = g.add_node("gelu", [x], (B, S, H))
+    b = g.add_node("silu", [x], (B, S, H))
+    sm = g.add_node("add", [a, b], (B, S, H))
+    gm = g.add_const("gamma", (H,))
+    if op == "layernorm":
+        bt = g.add_const("beta", (H,))
+        n = g.add_node("layernorm", [sm, gm, bt], (B, S, H), fattr=1e-5)
+    else:
+        n = g.add_node("rmsnorm", [sm, gm], (B, S, H), fattr=1e-5)
+    y = g.add_node("gelu", [n], (B, S, H))
+    g.outputs = [y]
+    return g, a, b, sm, n
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("op", ["layernorm", "rmsnorm"])
+@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (1, 8, 768), (2, 5, 1024), (1, 3, 4096)], ids=str)
+def test_residual_norm_one_launch(dtype, op, shape, tmp_path):
+    """A residual Add and the LayerNorm / RMSNorm of its sum as one planned
+    launch (a table that prices the chain below the two nodes): both
+    summands and the output in many layouts, both reduction variants; the
+    sum is never stored, so the oracle keeps it unrounded too."""
+    og, a, b, sm, n = sum_norm_graph(*shape, dtype, op)
+    L = layouts.layout_list(shape)
+    combos = [(0, 0, 0)] + [(i, (5 * i + 1) % len(L), (2 * i + 3) % len(L)) for i in range(len(L))]
+    for ia, ib, io in combos:
+        for v in (0, 1):
+            say(f"sum-{op} {dtype} {shape} v{v} {L[ia]} {L[ib]} -> {L[io]}")
+            xs, cs = random_inputs(og, ia + 7 * ib + io, 2.0)
+            (ref,) = execute.run_canonical(og, xs, cs, on_chip={sm})
+            obj = forced_table(og, {a: L[ia], b: L[ib], n: L[io]}, {3: v})
+            obj["fused_sigs"] = [{"op": "add", "in_shapes": [list(shape)] * 2, "out_shape": list(shape),
+                                  "entries": [[[list(L[ia]), list(L[ib])], list(L[io]),
+                                               [1 if w == v else -1 for w in range(2)]]]}]
+            obj["fused"] = [[2, 1, 0]]
+            (out,), lp, ap = run_device(og, obj, xs, cs, tmp_path)
+            assert lp.fusion_priced and lp.fuse[2] == 1 and lp.variant[2] == v and lp.variant[3] == -2
+            assert ap.offset[sm] == -1
+            assert lp.kernel(2).startswith("add_" + op)
+            assert_close(out, ref, dtype, f"sum-{op} v{v} {L[ia]} {L[ib]} {L[io]}")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("op", ["layernorm", "rmsnorm", "softmax"])
 def test_column_reduction_many_rows(dtype, op, tmp_path):

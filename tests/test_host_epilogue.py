@@ -149,8 +149,9 @@ def test_priced_fusions_are_the_launches(cfg, seed, tmp_path):
     from tables import add_fused
     og = OG.build_transformer(cfg)
     tab = synthetic_table(og, seed=seed, mode="random", lo=1, hi=1000, n_variants=1)
-    # chains priced for variant 1 only (its tile performs every epilogue
-    # step; variant 0 has no R operand)
+    # chains priced for variant 1 only (a MatMul's: its tile performs every
+    # epilogue step, variant 0 has no R operand; a residual norm's: the
+    # column reduction, which runs on any layouts)
     add_fused(tab, og, seed, n_variants=2, lo=1, hi=1500)
     for fs in tab["fused_sigs"]:
         for ent in fs["entries"]:
@@ -165,14 +166,17 @@ def test_priced_fusions_are_the_launches(cfg, seed, tmp_path):
     for m, t in enumerate(lp.fuse):
         if not t:
             continue
-        assert og.nodes[m].op == "matmul" and lp.variant[m] == 1
+        assert og.nodes[m].op in ("matmul", "add") and lp.variant[m] == 1
         chain = list(range(m, m + t + 1))
         covered.update(chain)
         assert all(lp.variant[k] == -2 and kernels[k] == "fused" for k in chain[1:])
         assert {launch[k] for k in chain} == {launch[m]}
         assert not any(written[k] for k in chain[:-1]) and written[chain[-1]]
         assert all(ap.offset[og.out_edge(k)] == -1 for k in chain[:-1])
-        assert "_e" in names[launch[m]]
+        if og.nodes[m].op == "matmul":
+            assert "_e" in names[launch[m]]
+        else:
+            assert names[launch[m]] == kernels[m] and names[launch[m]].startswith("add_" + og.nodes[m + 1].op)
     for k in range(g.n_nodes):
         if k not in covered and kernels[k] != "view":
             assert written[k] and list(launch).count(launch[k]) == 1, k

@@ -333,3 +333,39 @@ def test_best_chains_is_the_cheapest_chain_set(seed, builder):
         assert all((m, t) in fusion.all_chains(g) for m, t in enumerate(fz) if t)
     plan = PL.plan_layouts(g, ct)
     assert plan.total == brute_min(plan.layout_idx)
+
+
+@pytest.mark.parametrize("arch", ["post_ln", "pre_ln", "llama"])
+def test_fusion_chains_of_transformer_layers(arch):
+    """The chain rules on one layer of each block kind, enumerated by hand
+    from the builder's node order: a MatMul with its bias, activation and
+    residual steps, and -- where the residual sum has the normalisation as
+    its only reader (post-LN; the last block of pre-LN / Llama, before the
+    final norm) -- the residual Add with that normalisation."""
+    from oracle import fusion
+    cfg = synth_inputs.config(1, arch=arch, layers=1, seq=8, hidden=32, heads=2, ffn=48)
+    g = graph.build_transformer(cfg)
+    ops = [nd.op for nd in g.nodes]
+    got = {k: [ops[n] for n in v] for k, v in fusion.all_chains(g).items()}
+    norm_heads = sorted(m for (m, t), v in got.items() if v[0] == "add" and t == 1)
+    for m in norm_heads:
+        assert got[(m, 1)][1] in ("layernorm", "rmsnorm")
+        assert fusion.chain_steps(g, m) == [(m + 1, "norm", None)]
+        assert fusion.chain_slots(g, m, 1) == list(g.nodes[m].ins)
+    # residual sums read only by the norm after them
+    expect = [m for m, nd in enumerate(g.nodes) if nd.op == "add" and min(nd.ins) >= 0 and m + 1 < len(ops)
+              and ops[m + 1] in ("layernorm", "rmsnorm")
+              and [n for n, x in enumerate(g.nodes) if g.out_edge(m) in x.ins] == [m + 1]]
+    assert norm_heads == expect
+    assert len(norm_heads) == {"post_ln": 2, "pre_ln": 1, "llama": 1}[arch]
+    # MatMul chains: the FFN up-projection with bias and GELU (post/pre-LN),
+    # the down-projection with bias and the residual (post/pre-LN) or with
+    # the residual alone (Llama)
+    mm = {m: v for (m, t), v in got.items() if v[0] == "matmul"}
+    if arch in ("post_ln", "pre_ln"):
+        assert ["matmul", "add", "gelu"] in mm.values()
+        assert ["matmul", "add", "add"] in mm.values()
+    else:
+        assert ["matmul", "silu"] in mm.values() and ["matmul", "add"] in mm.values()
+        # SiLU's product meets the up-projection only after another MatMul
+        assert ["matmul", "silu", "mul"] not in mm.values()
