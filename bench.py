@@ -61,6 +61,41 @@ FAMILY_SOURCES = {"gemm": ["k_gemm*.hip", "gemm_common.h", "dev.h"], "conv": ["k
                   "": ["k_elementwise.hip", "k_reduce.hip", "dev.h"]}
 
 
+# Cost tables measured on an MI355X for the benchmark workloads (Alg. 3's
+# eval is a compile-time step: measured once per graph, kernel build and GPU
+# model, then reused).  index.json records, per workload, the hash of the
+# library sources the numbers depend on; a table whose sources changed is
+# measured afresh instead.
+STORED_TABLES = os.path.join(ROOT, "paper_2411_09242_amd", "tables")
+
+
+def library_source_hash():
+    """Hash of the library sources a cost table's numbers depend on: the
+    device code (kernels and the measurement protocol), how a variant
+    becomes launch parameters, the candidate layouts, the fusion rules, the
+    graph builders and the table format."""
+    import glob
+    import hashlib
+    d = os.path.join(ROOT, "paper_2411_09242_amd", "csrc")
+    files = glob.glob(os.path.join(d, "gpu", "*"))
+    for stem in ("dispatch", "kparams", "layouts", "fusion", "graph", "costtable", "prepare"):
+        files += glob.glob(os.path.join(d, "host", stem + ".*"))
+    h = hashlib.sha256()
+    for f in sorted(files):
+        h.update(os.path.relpath(f, d).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_table_meta(wl):
+    p = os.path.join(STORED_TABLES, "index.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        return json.load(f).get(wl)
+
+
 def kernel_source_hash(launch_name):
     import glob
     import hashlib
@@ -360,24 +395,44 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
     """Cost table (untimed), plans, then the timed regions; returns a dict.
     tables: (directory, "save" | "load") -- keep each workload's measured
     table, or plan from a kept one instead of measuring (same plan, e.g. for
-    counter runs).  kernel_only: after planning, launch only the dominant
-    kernel's nodes K times (eagerly) and return which kernel that was."""
+    counter runs); (STORED_TABLES, "stored") -- plan from the stored table
+    while the library sources are those it was measured with, else measure;
+    (STORED_TABLES, "store") -- measure and store it.  kernel_only: after
+    planning, launch only the dominant kernel's nodes K times (eagerly) and
+    return which kernel that was."""
     g = F.Graph.transformer(cfg)
     wl = cfg["name"]
     stream = torch.cuda.current_stream().cuda_stream
     t = time.time()
     tpath = os.path.join(tables[0], wl + ".json") if tables else None
-    if tables and tables[1] == "load":
+    mode = tables[1] if tables else None
+    meta = stored_table_meta(wl) if mode == "stored" else None
+    src = library_source_hash()
+    if mode == "stored" and not (meta and meta.get("sources") == src and os.path.exists(tpath)):
+        log(f"{wl}: no stored cost table for these library sources; measuring")
+        mode = None
+    if mode in ("load", "stored"):
         table = F.CostTable.load(tpath, g)
+        table_info = {"source": "stored" if mode == "stored" else "loaded", "file": os.path.relpath(tpath, ROOT)}
+        if meta:
+            table_info.update({k: meta[k] for k in ("measure_s", "reps", "gpu", "sources") if k in meta})
     else:
         MARK.push(f"{wl}/cost_table")
         table = F.CostTable.measure(g, reps=reps)
         MARK.pop()
-        if tables:
+        table_info = {"source": "measured", "measure_s": round(time.time() - t, 1), "reps": reps, "sources": src}
+        if mode in ("save", "store"):
             os.makedirs(tables[0], exist_ok=True)
             table.save(tpath)
+        if mode == "store":
+            ip = os.path.join(tables[0], "index.json")
+            index = json.load(open(ip)) if os.path.exists(ip) else {}
+            index[wl] = {k: v for k, v in table_info.items() if k != "source"}
+            index[wl]["gpu"] = torch.cuda.get_device_name(0)
+            with open(ip, "w") as f:
+                json.dump(index, f, indent=1, sort_keys=True)
     t_measure = time.time() - t
-    log(f"{cfg['name']}: cost table ready in {t_measure:.1f} s")
+    log(f"{cfg['name']}: cost table ready in {t_measure:.1f} s ({table_info['source']})")
     if save_table:
         table.save(save_table)
     lp = F.LayoutPlan(g, table)
@@ -496,7 +551,7 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         "launches_per_step": n_launch, "naive_launches_per_step": n_launch_naive,
         "plan_table_ns": lp.total_ns, "naive_table_ns": lp_naive.total_ns, "guard_used": lp.guard_used,
         "fusion_priced": lp.fusion_priced, "priced_chains": sum(1 for t in lp.fuse if t),
-        "planned_vs_naive_max_abs_diff": agree, "cost_table_s": round(t_measure, 1),
+        "planned_vs_naive_max_abs_diff": agree, "cost_table": table_info,
         "roofline": roof,
         "op_classes": op_classes,
         "ablation": abl,
@@ -551,6 +606,10 @@ def main():
     ap.add_argument("--save-table", default=None)
     ap.add_argument("--tables-dir", default=None, help="directory for every workload's cost table")
     ap.add_argument("--tables-mode", choices=("save", "load"), default="save")
+    ap.add_argument("--measure", action="store_true",
+                    help="measure every cost table (default: the stored tables while the sources match)")
+    ap.add_argument("--store-tables", nargs="?", const=STORED_TABLES, default=None, metavar="DIR",
+                    help="measure every cost table and store it (default: with the library)")
     ap.add_argument("--kernel-only", action="store_true",
                     help="launch only each workload's dominant kernel (for counter runs); prints what ran")
     a = ap.parse_args()
@@ -572,7 +631,12 @@ def main():
         x, consts = device_inputs(torch, F, cfg, a.config)
     else:
         x, consts = synth_inputs.make_inputs(cfg, F.Graph.transformer(cfg).const_specs(), a.config)
-    tables = (a.tables_dir, a.tables_mode) if a.tables_dir else None
+    if a.tables_dir:
+        tables = (a.tables_dir, a.tables_mode)
+    elif a.store_tables:
+        tables = (a.store_tables, "store")
+    else:
+        tables = None if a.measure else (STORED_TABLES, "stored")
     r = measure_workload(F, torch, cfg, x, consts, a.steps, a.warmup, a.reps, a.save_table, tables, a.kernel_only)
     if a.kernel_only:
         print(json.dumps({"kernel_only": True, "workload": cfg["name"], **r}), flush=True)

@@ -274,3 +274,30 @@ def test_host_library_gpu_entry_points_are_unsupported():
     assert st == -2
     st = lib.fluid_measure_costs(None, 1, None, 0, None, None)
     assert st == -2
+
+
+STORED = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2411_09242_amd", "tables")
+
+
+def _stored_tables():
+    names = {synth_inputs.config(i)["name"]: i for i in range(1, 7)}
+    out = []
+    if os.path.isdir(STORED):
+        for f in sorted(os.listdir(STORED)):
+            if f.endswith(".json") and f[:-5] in names:
+                out.append((names[f[:-5]], os.path.join(STORED, f)))
+    return out
+
+
+@pytest.mark.parametrize("idx,path", _stored_tables(), ids=lambda v: str(v) if isinstance(v, int) else "")
+def test_planner_parity_on_stored_measured_tables(idx, path, tmp_path):
+    """The cost tables measured on an MI355X that the benchmark plans from
+    (full-size workloads, fused entries, workload 4's trimmed candidate
+    lists): layouts, variants, chains, totals, guard and every arena request
+    equal the oracle planners' on the same file."""
+    og = OG.build_transformer(synth_inputs.config(idx))
+    with open(path) as f:
+        obj = json.load(f)
+    lp = _compare_plans(og, obj, tmp_path)
+    summary = assert_plans_match_oracle(og, lp.graph, obj, lp)
+    assert lp.fusion_priced == bool(obj.get("fused")), summary
