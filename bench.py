@@ -43,17 +43,19 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 # its kernel family's device sources when it was taken and is reported as
 # `traffic` only while they are unchanged (else null).
 TRAFFIC = {
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm_eg',
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_t128_amn_bmn_cm_ebg',
      "[['matmul', '(8, 512, 4096)', \"((8, 512, 1024), ('c', 1024, 4096))\"], ['add', '(8, 512, 4096)', "
-     "\"((8, 512, 4096), ('c', 4096))\"], ['gelu', '(8, 512, 4096)', '((8, 512, 4096),)']]"): (235893161, "5d68c6d18b39ba47"),
+     "\"((8, 512, 4096), ('c', 4096))\"], ['gelu', '(8, 512, 4096)', '((8, 512, 4096),)']]"): (235615167, "5d68c6d18b39ba47"),
     ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn',
-     "[['matmul', '(1, 2048, 11008)', \"((1, 2048, 4096), ('c', 4096, 11008))\"]]"): (894260458, "5d68c6d18b39ba47"),
-    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm_eg',
+     "[['matmul', '(1, 2048, 11008)', \"((1, 2048, 4096), ('c', 4096, 11008))\"]]"): (894358952, "5d68c6d18b39ba47"),
+    ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm_ebg',
      "[['matmul', '(1, 512, 3072)', \"((1, 512, 768), ('c', 768, 3072))\"], ['add', '(1, 512, 3072)', "
-     "\"((1, 512, 3072), ('c', 3072))\"], ['gelu', '(1, 512, 3072)', '((1, 512, 3072),)']]"): (28487123, "5d68c6d18b39ba47"),
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm_eg',
+     "\"((1, 512, 3072), ('c', 3072))\"], ['gelu', '(1, 512, 3072)', '((1, 512, 3072),)']]"): (28487081, "5d68c6d18b39ba47"),
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn_ebg',
      "[['matmul', '(1, 128, 3072)', \"((1, 128, 768), ('c', 768, 3072))\"], ['add', '(1, 128, 3072)', "
-     "\"((1, 128, 3072), ('c', 3072))\"], ['gelu', '(1, 128, 3072)', '((1, 128, 3072),)']]"): (14374435, "5d68c6d18b39ba47"),
+     "\"((1, 128, 3072), ('c', 3072))\"], ['gelu', '(1, 128, 3072)', '((1, 128, 3072),)']]"): (14367268, "5d68c6d18b39ba47"),
+    ('vgg16-b1-224', 'conv_f32_t64_kuvc',
+     "[['conv', '(1, 256, 56, 56)', \"((1, 256, 58, 58), ('c', 256, 256, 3, 3), ('c', 256))\"]]"): (35126066, "a9c5d2d4cd2fcc40"),
 }
 
 # the device sources of each kernel family (by launch-name prefix)
@@ -428,7 +430,8 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
             ip = os.path.join(tables[0], "index.json")
             index = json.load(open(ip)) if os.path.exists(ip) else {}
             index[wl] = {k: v for k, v in table_info.items() if k != "source"}
-            index[wl]["gpu"] = torch.cuda.get_device_name(0)
+            props = torch.cuda.get_device_properties(0)
+            index[wl]["gpu"] = f"{props.name} ({props.gcnArchName.split(':')[0]})"
             with open(ip, "w") as f:
                 json.dump(index, f, indent=1, sort_keys=True)
     t_measure = time.time() - t
