@@ -14,12 +14,15 @@
 //           input's unit-stride dim (NCHW-like layouts);
 //   KORD 1: k = (u, v, c); a wavefront loads 16 consecutive k of 4 pixels --
 //           coalesced when C is unit-stride (NHWC-like layouts).
-// A 64 x 64 output tile per 256-thread workgroup (4 wavefronts, 2 x 2, each
+// A 64 x 64 output tile per group of 256 threads (4 wavefronts, 2 x 2, each
 // 32 x 32 with v_mfma_f32_32x32x2_f32: lane l reads A[l%32][l/32] and
 // B[l/32][l%32]; accumulator v of lane l holds C[8(v/4) + 4(l/32) + v%4][l%32]),
 // operands staged in LDS K-major, the next K-tile loaded into registers
-// while the current one is multiplied.  The bias is added in fp32 before the
-// store.
+// while the current one is multiplied.  KS groups share a workgroup and a
+// tile, group g taking K-tiles g, g + KS, ...: KS times the wavefronts and
+// K-tiles in flight per tile, for layers with fewer tiles than compute
+// units; the groups' partial sums are added through LDS in group order
+// (deterministic).  The bias is added in fp32 before the store.
 #include "dev.h"
 #include "launch.h"
 
@@ -47,15 +50,21 @@ __device__ __forceinline__ int32_t conv_col_off(const ConvParams& p, uint32_t k,
   return (int32_t)c * p.x_c + (int32_t)u * p.x_h + (int32_t)v * p.x_w;
 }
 
-template <int KORD>
-__global__ __launch_bounds__(256) void conv_f32_kernel(ConvParams p) {
+template <int KORD, int KS>
+__global__ __launch_bounds__(256 * KS) void conv_f32_kernel(ConvParams p) {
   constexpr int BM = 64, BN = 64, BK = 16;
   constexpr int AP = BM + 4, BP = BN + 4;
-  __shared__ float As[BK * AP];
-  __shared__ float Bs[BK * BP];
+  constexpr int STAGE = BK * AP + BK * BP;            // one group's A and B tiles
+  constexpr int RED = (KS - 1) * 16 * 256;            // partial sums of groups 1 .. KS-1
+  constexpr int SMEM = KS * STAGE > RED ? KS * STAGE : RED;
+  __shared__ float smem[SMEM];
+  // the group index is uniform per wavefront: keep it in a scalar register
+  const int grp = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 8));
+  float* As = smem + grp * STAGE;
+  float* Bs = As + BK * AP;
   const uint32_t tm = blockIdx.x / p.tiles_n, tn = blockIdx.x - tm * p.tiles_n;
   const uint32_t m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 
   auto row_off = [&](uint32_t m, int32_t sn, int32_t sh, int32_t sw) {
@@ -131,18 +140,35 @@ __global__ __launch_bounds__(256) void conv_f32_kernel(ConvParams p) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[v] = 0.f;
   const int lr = lane & 31, lk = lane >> 5;
-  gload(0);
-  for (uint32_t k0 = 0; k0 < p.K; k0 += BK) {
+  // every group runs the same number of rounds (the barriers are
+  // workgroup-wide); a group's K-tile past the end loads zeros
+  const uint32_t rounds = (p.K + KS * BK - 1) / (KS * BK);
+  gload((uint32_t)grp * BK);
+  for (uint32_t r = 0; r < rounds; ++r) {
     __syncthreads();
     lstore();
     __syncthreads();
-    if (k0 + BK < p.K) gload(k0 + BK);
+    if (r + 1 < rounds) gload(((r + 1) * KS + (uint32_t)grp) * BK);
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 2) {
       const float a = As[(kk + lk) * AP + wm * 32 + lr];
       const float b = Bs[(kk + lk) * BP + wn * 32 + lr];
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
     }
+  }
+  if constexpr (KS > 1) {
+    // groups 1 .. KS-1 park their sums; group 0 adds them in group order
+    __syncthreads();
+    if (grp > 0) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) smem[((grp - 1) * 16 + v) * 256 + tid] = acc[v];
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int g = 0; g < KS - 1; ++g)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[v] += smem[(g * 16 + v) * 256 + tid];
   }
 
   const uint32_t o = n0 + wn * 32 + lr;
@@ -162,8 +188,15 @@ __global__ __launch_bounds__(256) void conv_f32_kernel(ConvParams p) {
 hipError_t launch_conv(const NodeKernel& k, hipStream_t s) {
   const ConvParams& p = k.conv;
   const uint32_t grid = ((p.M + 63) / 64) * p.tiles_n;
-  if (k.conv_kord == 0) hipLaunchKernelGGL(conv_f32_kernel<0>, dim3(grid), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL(conv_f32_kernel<1>, dim3(grid), dim3(256), 0, s, p);
+  if (k.conv_ks == 1) {
+    if (k.conv_kord == 0) hipLaunchKernelGGL((conv_f32_kernel<0, 1>), dim3(grid), dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((conv_f32_kernel<1, 1>), dim3(grid), dim3(256), 0, s, p);
+  } else if (k.conv_ks == 4) {
+    if (k.conv_kord == 0) hipLaunchKernelGGL((conv_f32_kernel<0, 4>), dim3(grid), dim3(1024), 0, s, p);
+    else hipLaunchKernelGGL((conv_f32_kernel<1, 4>), dim3(grid), dim3(1024), 0, s, p);
+  } else {
+    return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -1,5 +1,5 @@
 // Row reductions over the last logical dim: Softmax (with fused scale and
-// causal mask), LayerNorm and RMSNorm, in two families.
+// causal mask), LayerNorm and RMSNorm, in three variants.
 //  * row (variant 0): one 64-lane wavefront per row; the row is held in
 //    registers (up to 4096 values), reduced with cross-lane butterflies, and
 //    written once -- one HBM read and one write per element.  Coalesced when
@@ -7,6 +7,9 @@
 //    boundaries, each lane moves 16-byte pieces (lane l takes pieces
 //    l, l + 64, ...), so a wavefront load covers 1 KiB of contiguous row,
 //    and a causal softmax skips the pieces that lie wholly past the mask.
+//  * row, a workgroup per row (variant 2; 16-byte pieces only): four times
+//    the wavefronts per row, a quarter of the pieces each, sums through LDS
+//    -- for long rows and few of them; the cost table decides per shape.
 //  * column (variant 1): one lane per row, consecutive lanes on consecutive
 //    rows, so a layout whose unit-stride dim is a row dim still reads and
 //    writes coalesced; the row is streamed twice (three times for
@@ -268,10 +271,10 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
   }
 }
 
-// Row family with 16-byte pieces, one 256-thread workgroup per row (for
-// long rows when there are too few rows to keep one wavefront per row busy:
-// four times the wavefronts, a quarter of the pieces each).  NC pieces per
-// thread, piece c of thread t at t + 256 c; reductions through LDS.
+// Row family with 16-byte pieces, one 256-thread workgroup per row
+// (variant 2: four times the wavefronts of variant 0 per row, a quarter of
+// the pieces each).  NC pieces per thread, piece c of thread t at t + 256 c;
+// reductions through LDS.
 template <typename T, int NC, int OP>
 __global__ __launch_bounds__(256) void red_rowb_kernel(RedParams p) {
   constexpr int BOP = red_base_op(OP);
@@ -656,8 +659,9 @@ hipError_t red_dispatch_op(const NodeKernel& k, hipStream_t s) {
   const dim3 grid((p.nrows + 3u) / 4u);
   if (k.vec > 1) {
     const uint32_t pieces = p.R / Piece<T>::VEC;
-    // long rows and few of them: a workgroup per row
-    if (pieces >= 256 && p.nrows < 16384) {
+    // variant 2: a workgroup per row (rows of at most 4096 values: at most
+    // 4 pieces per thread)
+    if (k.red_block) {
       const uint32_t ncb = (pieces + 255u) / 256u;
       const dim3 gb(p.nrows);
       if (ncb <= 1) hipLaunchKernelGGL((red_rowb_kernel<T, 1, OP>), gb, dim3(256), 0, s, p);

@@ -28,10 +28,10 @@ int num_variants(int op) {
     case FLUID_OP_RELU:
     case FLUID_OP_TRANSPOSE:
     case FLUID_OP_RESHAPE: return 2;
-    case FLUID_OP_CONV: return 2;
+    case FLUID_OP_CONV: return 4;
     case FLUID_OP_SOFTMAX:
     case FLUID_OP_LAYERNORM:
-    case FLUID_OP_RMSNORM: return 2;
+    case FLUID_OP_RMSNORM: return 3;
     default: return 1;
   }
 }
@@ -243,7 +243,7 @@ NodeKernel prepare_rope(const Node&, int dtype, const std::vector<Operand>& ins,
 NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out,
                        const Operand* x1 = nullptr) {
   NodeKernel k;
-  k.family = variant == 0 ? KF_RED_ROW : KF_RED_COL;
+  k.family = variant == 1 ? KF_RED_COL : KF_RED_ROW;
   k.dtype = dtype == FLUID_BF16 ? DT_BF16 : DT_F32;
   const Operand& x = ins[0];
   check_small(out, "reduction");
@@ -286,8 +286,8 @@ NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector
   p.y = const_cast<void*>(out.ptr);
   p.gamma = ins.size() > 1 ? ins[1].ptr : nullptr;
   p.beta = ins.size() > 2 ? ins[2].ptr : nullptr;
-  if (variant == 0 && p.R > 4096) { k.why = "row variant holds at most 4096 values per row"; return k; }
-  if (variant == 0) {
+  if (variant != 1 && p.R > 4096) { k.why = "row variants hold at most 4096 values per row"; return k; }
+  if (variant != 1) {
     // 16-byte pieces: unit-stride rows starting on 16-byte boundaries
     const int VEC = k.dtype == DT_BF16 ? 8 : 4;
     bool ok = p.irs == 1 && p.ors == 1 && p.R % VEC == 0 && aligned16(p.x) && aligned16(p.y);
@@ -299,6 +299,11 @@ NodeKernel prepare_red(const Node& nd, int variant, int dtype, const std::vector
     if (p.op != RED_SOFTMAX)
       ok = ok && aligned16(p.gamma) && (red_base_op(p.op) != RED_LAYERNORM || aligned16(p.beta));
     if (ok) k.vec = VEC;
+    if (variant == 2) {
+      // a workgroup per row: 16-byte pieces only, at most 4 per thread
+      if (!ok) { k.why = "the workgroup-per-row variant needs unit-stride, 16-byte aligned rows"; return k; }
+      k.red_block = true;
+    }
   }
   k.available = true;
   return k;
@@ -486,7 +491,9 @@ NodeKernel prepare_window(const Node& nd, int dtype, const std::vector<Operand>&
 }
 
 // Conv: variant 0 reduces over (c, u, v) with wavefronts along pixels, 1
-// over (u, v, c) with wavefronts along channels (k_conv.hip).
+// over (u, v, c) with wavefronts along channels; variants 2 and 3 are 0 and
+// 1 with the K-tiles of a tile split over 4 groups of wavefronts in one
+// workgroup (k_conv.hip).
 NodeKernel prepare_conv(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
   NodeKernel k;
   k.family = KF_CONV;
@@ -525,7 +532,8 @@ NodeKernel prepare_conv(const Node& nd, int variant, int dtype, const std::vecto
   p.y_n = (int32_t)out.stride[0]; p.y_c = (int32_t)out.stride[1]; p.y_h = (int32_t)out.stride[2];
   p.y_w = (int32_t)out.stride[3];
   p.tiles_n = (p.Co + 63) / 64;
-  k.conv_kord = variant;
+  k.conv_kord = variant & 1;
+  k.conv_ks = variant >= 2 ? 4 : 1;
   k.available = true;
   return k;
 }
@@ -590,10 +598,13 @@ std::string NodeKernel::name() const {
     case KF_EW: return "ew_" + std::string(ew_names[ew.op]) + "_" + dt + "_v" + std::to_string(vec);
     case KF_EW_TILED: return "ew_tiled_" + std::string(ew_names[ew.op]) + "_" + dt;
     case KF_ROPE: return "rope_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
-    case KF_RED_ROW: return std::string(red_names[red.op]) + "_row_" + dt + (vec > 1 ? "_v" + std::to_string(vec) : "");
+    case KF_RED_ROW:
+      return std::string(red_names[red.op]) + (red_block ? "_rowblock_" : "_row_") + dt +
+             (vec > 1 ? "_v" + std::to_string(vec) : "");
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
     case KF_WIN: return std::string(win.op == 0 ? "pad_" : "maxpool_") + dt;
-    case KF_CONV: return "conv_" + dt + (conv_kord == 0 ? "_t64_kcuv" : "_t64_kuvc");
+    case KF_CONV:
+      return "conv_" + dt + (conv_kord == 0 ? "_t64_kcuv" : "_t64_kuvc") + (conv_ks > 1 ? "_ks" + std::to_string(conv_ks) : "");
     case KF_GEMM: {
       // fused epilogue steps: b bias, g GELU, s SiLU, a / m Add / Mul of R
       auto epi_suffix = [&]() {

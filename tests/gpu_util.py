@@ -51,8 +51,8 @@ def forced_table(og, want, variants=None):
         else:
             assert p in L[e], (e, p, "not a candidate (use the first of equivalent layouts)")
     sigs, node_sig = [], []
-    nvar = {"matmul": 20, "gelu": 2, "silu": 2, "relu": 2, "conv": 2, "transpose": 2, "reshape": 2,
-            "softmax": 2, "layernorm": 2, "rmsnorm": 2}
+    nvar = {"matmul": 20, "gelu": 2, "silu": 2, "relu": 2, "conv": 4, "transpose": 2, "reshape": 2,
+            "softmax": 3, "layernorm": 3, "rmsnorm": 3}
     for n, nd in enumerate(og.nodes):
         slots = og.act_inputs(n)
         eo = og.out_edge(n)

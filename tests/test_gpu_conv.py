@@ -51,10 +51,12 @@ CONV_CASES = [((1, 3, 9, 7), (5, 3, 3, 3), True), ((2, 8, 10, 12), (16, 8, 3, 3)
 
 
 @pytest.mark.parametrize("case", CONV_CASES, ids=str)
-@pytest.mark.parametrize("variant", [0, 1])
+@pytest.mark.parametrize("variant", [0, 1, 2, 3])
 def test_conv_layouts(case, variant, tmp_path):
     """Input and output of the convolution in (a sample of) every layout
-    pair; both reduction orders; ragged pixel and channel tiles."""
+    pair; both reduction orders, with and without the K split over wave
+    groups (K-tiles past the end in the last round); ragged pixel and
+    channel tiles."""
     xs_, ws_, bias = case
     og, a, c = conv_graph(xs_, ws_, bias)
     for pa, pc in _pairs(layouts.layout_list(og.edge_shape(a)), layouts.layout_list(og.edge_shape(c)), 24,

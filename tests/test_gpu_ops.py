@@ -33,6 +33,14 @@ def _check_gemm(og, want, variants, tmp_path, seed, dtype):
         raise
 
 
+def row_block_ok(shape, dtype, *perms):
+    """Whether reduction variant 2 (a workgroup per row, 16-byte pieces)
+    runs: the reduced (last) dim innermost in every layout, rows a multiple
+    of 16 bytes and at most 4096 values."""
+    R, vec = shape[-1], (8 if dtype == "bf16" else 4)
+    return R % vec == 0 and R <= 4096 and all(p[-1] == len(shape) - 1 for p in perms)
+
+
 def _check(og, want, variants, tmp_path, seed=0, scale=1.0):
     xs, cs = random_inputs(og, seed, scale)
     ref = execute.run_canonical(og, xs, cs)
@@ -450,7 +458,9 @@ def test_softmax_layouts_and_variants(dtype, shape, causal, tmp_path):
     rng = np.random.default_rng(shape[2] + causal)
     combos = [(0, 0)] + [tuple(int(v) for v in rng.integers(0, len(L), 2)) for _ in range(8)]
     for ia, ip in combos:
-        for v in (0, 1):
+        for v in (0, 1, 2):
+            if v == 2 and not row_block_ok(shape, dtype, L[ia], L[ip]):
+                continue
             say(f"softmax {dtype} {shape} causal={causal} v{v} {L[ia]} {L[ip]}")
             _check(og, {a: L[ia], p: L[ip]}, {1: v}, tmp_path, seed=ia * 7 + ip, scale=3.0)
 
@@ -477,7 +487,9 @@ def test_norm_layouts_and_variants(dtype, op, shape, tmp_path):
     og, a, n = norm_graph(*shape, dtype, op)
     L = layouts.layout_list(shape)
     for ia, ib in itertools.product(range(len(L)), range(len(L))):
-        for v in (0, 1):
+        for v in (0, 1, 2):
+            if v == 2 and not row_block_ok(shape, dtype, L[ia], L[ib]):
+                continue
             say(f"{op} {dtype} {shape} v{v} {L[ia]} {L[ib]}")
             _check(og, {a: L[ia], n: L[ib]}, {1: v}, tmp_path, seed=ia + 3 * ib, scale=2.0)
 
@@ -507,20 +519,22 @@ def sum_norm_graph(B, S, H, dtype, op):
 def test_residual_norm_one_launch(dtype, op, shape, tmp_path):
     """A residual Add and the LayerNorm / RMSNorm of its sum as one planned
     launch (a table that prices the chain below the two nodes): both
-    summands and the output in many layouts, both reduction variants; the
+    summands and the output in many layouts, every reduction variant; the
     sum is never stored, so the oracle keeps it unrounded too."""
     og, a, b, sm, n = sum_norm_graph(*shape, dtype, op)
     L = layouts.layout_list(shape)
     combos = [(0, 0, 0)] + [(i, (5 * i + 1) % len(L), (2 * i + 3) % len(L)) for i in range(len(L))]
     for ia, ib, io in combos:
-        for v in (0, 1):
+        for v in (0, 1, 2):
+            if v == 2 and not row_block_ok(shape, dtype, L[ia], L[ib], L[io]):
+                continue
             say(f"sum-{op} {dtype} {shape} v{v} {L[ia]} {L[ib]} -> {L[io]}")
             xs, cs = random_inputs(og, ia + 7 * ib + io, 2.0)
             (ref,) = execute.run_canonical(og, xs, cs, on_chip={sm})
             obj = forced_table(og, {a: L[ia], b: L[ib], n: L[io]}, {3: v})
             obj["fused_sigs"] = [{"op": "add", "in_shapes": [list(shape)] * 2, "out_shape": list(shape),
                                   "entries": [[[list(L[ia]), list(L[ib])], list(L[io]),
-                                               [1 if w == v else -1 for w in range(2)]]]}]
+                                               [1 if w == v else -1 for w in range(3)]]]}]
             obj["fused"] = [[2, 1, 0]]
             (out,), lp, ap = run_device(og, obj, xs, cs, tmp_path)
             assert lp.fusion_priced and lp.fuse[2] == 1 and lp.variant[2] == v and lp.variant[3] == -2
