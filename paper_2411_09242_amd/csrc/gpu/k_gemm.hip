@@ -21,8 +21,12 @@
 namespace fluid {
 
 // ============================================================== fp32
+// The register budget of four wavefronts per SIMD: four 128 x 128
+// workgroups share a compute unit (without it the compiler's 139 registers
+// left room for three, and a 1024-tile launch ran a second, quarter-full
+// round).
 template <int BM, int BN, int AM, int BMD, bool RES>
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void gemm_f32_kernel(GemmParams p) {
   constexpr int BK = 16;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int FM = WM / 32, FN = WN / 32;
@@ -684,6 +688,7 @@ hipError_t gemm_sk_dispatch(const NodeKernel& k, hipStream_t s) {
     default: return gemm_sk_go<T, 1, 1, 16, 2>(k, s);
   }
 }
+
 
 template <int T, int AM, int BMD>
 hipError_t gemm_go(const NodeKernel& k, hipStream_t s) {
