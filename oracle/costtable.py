@@ -96,6 +96,10 @@ def load(path_or_obj, g):
     for m, t, si in obj.get("fused", []):
         if (m, t) not in chains:
             raise ValueError(f"fused entry ({m}, {t}) is not a fusion chain of this graph")
+        if (m, t) in fused:
+            raise ValueError(f"fused entry ({m}, {t}) listed twice")
+        if not 0 <= si < len(obj.get("fused_sigs", [])):
+            raise ValueError(f"fused entry ({m}, {t}): no signature {si}")
         fused[(m, t)] = dense(fusion.chain_slots(g, m, t), g.out_edge(m + t), obj["fused_sigs"][si]["entries"],
                               f"chain ({m}, {t})")
     return CostTable(L, nodes, fused)

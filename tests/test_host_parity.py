@@ -301,3 +301,33 @@ def test_planner_parity_on_stored_measured_tables(idx, path, tmp_path):
     lp = _compare_plans(og, obj, tmp_path)
     summary = assert_plans_match_oracle(og, lp.graph, obj, lp)
     assert lp.fusion_priced == bool(obj.get("fused")), summary
+
+
+def test_loader_rejects_bad_fused_entries(tmp_path):
+    """Fused entries are validated against the graph's chains: a reference
+    to a (m, t) that is no fusion chain, one listed twice, a signature index
+    out of range, or entries whose arity does not match the chain's slots
+    are refused; a valid table round-trips through save with its fused
+    entries intact."""
+    og = mlp_graph(2)
+    g = _cpp_graph_from_oracle(og)
+    obj = add_fused(synthetic_table(og, seed=3), og, 3)
+    assert obj["fused"]
+    t = F.CostTable.load(write_table(obj, tmp_path / "ok.json"), g)
+    t.save(str(tmp_path / "again.json"))
+    again = json.load(open(tmp_path / "again.json"))
+    assert again["fused"] == obj["fused"]
+    assert [s["entries"] for s in again["fused_sigs"]] == [s["entries"] for s in obj["fused_sigs"]]
+    m, tl, si = obj["fused"][0]
+    not_head = next(n for n, nd in enumerate(og.nodes) if nd.op not in ("matmul", "add"))
+    for mut in (lambda o: o["fused"].append([not_head, 1, si]),            # no chain there
+                lambda o: o["fused"].append([m, 9, si]),                   # longer than the chain
+                lambda o: o["fused"].append(list(o["fused"][0])),          # listed twice
+                lambda o: o["fused"].__setitem__(0, [m, tl, 99]),          # no such signature
+                lambda o: o["fused_sigs"][si]["entries"][0][0].append([0, 1, 2])):  # arity
+        bad = json.loads(json.dumps(obj))
+        mut(bad)
+        with pytest.raises(F.FluidError):
+            F.CostTable.load(write_table(bad, tmp_path / "bad.json"), g)
+        with pytest.raises((ValueError, IndexError, KeyError)):   # the oracle's loader refuses it too
+            costtable.load(bad, og)
