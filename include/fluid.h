@@ -199,7 +199,11 @@ fluid_status fluid_measure_scratch_bytes(const fluid_graph* g, uint64_t* bytes);
  * more than 8x slower than the best so far of its signature keeps that
  * time), then three batches of `reps` back-to-back launches, each batch
  * between two HIP events; the cost is the median per-launch time of the
- * batches, rounded to integer nanoseconds.  View
+ * batches, rounded to integer nanoseconds.  Successive launches of a
+ * MatMul or Conv with a constant weight read it from rotating copies that
+ * total at least 512 MiB (at most 64 copies), so that each launch fetches
+ * its weight from HBM, as in a run.  Fusion chains get entries measured
+ * the same way as one launch (the R operand in the output's layout).  View
  * combinations of Transpose/Reshape cost 0.  Candidate lists: all
  * dimension permutations (deduplicated), trimmed for tensors with more than
  * six candidates to those whose innermost dim is one of the last two

@@ -521,11 +521,14 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
     // signature's best so far) get no more launches -- then three batches
     // of R back-to-back launches between two events (the per-launch time
     // includes the kernel's start-up and the gap to the next launch, as in
-    // a run); the median, in integer ns
-    auto time_kernel = [&](const NodeKernel& k, int64_t& best_so_far) -> int64_t {
-      hip_check(launch_node_kernel(k, s), "warm-up launch");
+    // a run); the median, in integer ns.  Successive launches take the
+    // kernels of ks in turn (copies of a constant weight, cold_weight_copies).
+    auto time_kernel = [&](const std::vector<NodeKernel>& ks, int64_t& best_so_far) -> int64_t {
+      size_t li = 0;
+      auto next = [&]() -> const NodeKernel& { return ks[li++ % ks.size()]; };
+      hip_check(launch_node_kernel(next(), s), "warm-up launch");
       hip_check(hipEventRecord(ev[0], s), "hipEventRecord");
-      hip_check(launch_node_kernel(k, s), "first timed launch");
+      hip_check(launch_node_kernel(next(), s), "first timed launch");
       hip_check(hipEventRecord(ev[1], s), "hipEventRecord");
       hip_check(hipEventSynchronize(ev[1]), "hipEventSynchronize");
       float first = 0.f;
@@ -536,7 +539,7 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
         times.clear();
         for (int b = 0; b < 3; ++b) {
           hip_check(hipEventRecord(ev[2 + 2 * b], s), "hipEventRecord");
-          for (uint32_t r = 0; r < R; ++r) hip_check(launch_node_kernel(k, s), "timed launch");
+          for (uint32_t r = 0; r < R; ++r) hip_check(launch_node_kernel(next(), s), "timed launch");
           hip_check(hipEventRecord(ev[3 + 2 * b], s), "hipEventRecord");
         }
         hip_check(hipEventSynchronize(ev[7]), "hipEventSynchronize");
@@ -550,6 +553,23 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
       const int64_t ns_ = std::max<int64_t>(1, (int64_t)std::llround((double)times[times.size() / 2] * 1e6));
       if (best_so_far < 0 || ns_ < best_so_far) best_so_far = ns_;
       return ns_;
+    };
+    // k and its copies reading the constant weight (MatMul / Conv operand 1,
+    // wbytes) from the copies placed at `copies` onwards
+    auto with_weight_copies = [&](const NodeKernel& k, const Node& nd, char* copies) {
+      std::vector<NodeKernel> ks = {k};
+      if (!(nd.op == FLUID_OP_MATMUL || nd.op == FLUID_OP_CONV) || nd.ins.size() < 2 || nd.ins[1] >= 0) return ks;
+      const Const& w = g.consts[~nd.ins[1]];
+      const uint64_t wb = (uint64_t)numel(w.shape) * dtype_bytes(w.dtype);
+      const int W = cold_weight_copies(wb);
+      for (int i = 1; i < W; ++i) {
+        NodeKernel c = k;
+        char* p = copies + (uint64_t)(i - 1) * align256(wb);
+        if (c.family == KF_GEMM) c.gemm.B = p;
+        else if (c.family == KF_CONV) c.conv.w = (const float*)p;
+        ks.push_back(c);
+      }
+      return ks;
     };
     char* base = (char*)scratch;
     for (size_t si = 0; si < rep_node.size(); ++si) {
@@ -604,7 +624,8 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
               if (nd.ins[s2] < 0) vins[s2].stride = const_strides(nd, (int)s2, v, vins[s2].shape);
             NodeKernel k = prepare_node(nd, v, g.dtype, vins, ou);
             if (!k.available) { en.costs.push_back(-1); continue; }
-            en.costs.push_back(time_kernel(k, best_so_far));
+            char* copies = base + align256(off + (uint64_t)numel(ou.shape) * dtype_bytes(g.dtype));
+            en.costs.push_back(time_kernel(with_weight_copies(k, nd, copies), best_so_far));
           }
         }
         sig.entries.push_back(std::move(en));
@@ -707,7 +728,7 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
             for (int v = 0; v < num_variants(xn.op); ++v) {
               NodeKernel k = prepare_sum_norm(xn, v, g.dtype, ins, x1, ou);
               if (!k.available) { en.costs.push_back(-1); continue; }
-              en.costs.push_back(time_kernel(k, best_so_far));
+              en.costs.push_back(time_kernel({k}, best_so_far));
             }
             sig.entries.push_back(std::move(en));
           } else if (!rop || en.in[nmm] == en.out) {
@@ -756,7 +777,8 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
               if (!k.available) { en.costs.push_back(-1); continue; }
               k.gemm.bias = bias_ptr;
               k.gemm.R = rop ? r.ptr : nullptr;
-              en.costs.push_back(time_kernel(k, best_so_far));
+              char* copies = (char*)ou.ptr + align256((uint64_t)numel(ou.shape) * dtype_bytes(g.dtype));
+              en.costs.push_back(time_kernel(with_weight_copies(k, mn, copies), best_so_far));
             }
             sig.entries.push_back(std::move(en));
           }

@@ -40,6 +40,13 @@ uint64_t measure_scratch_bytes(const Graph& g) {
     if (g.nodes[n].op == FLUID_OP_ADD && n + 1 < g.n_nodes())
       for (int v : g.nodes[n + 1].ins)
         if (v < 0) s += (uint64_t)numel(g.consts[~v].shape) * dtype_bytes(g.consts[~v].dtype) + 256;
+    // the copies of a constant weight the timed launches rotate over
+    const Node& nd = g.nodes[n];
+    if ((nd.op == FLUID_OP_MATMUL || nd.op == FLUID_OP_CONV) && nd.ins.size() > 1 && nd.ins[1] < 0) {
+      const Const& w = g.consts[~nd.ins[1]];
+      const uint64_t wb = (uint64_t)numel(w.shape) * dtype_bytes(w.dtype);
+      s += (uint64_t)(cold_weight_copies(wb) - 1) * ((wb + 255) & ~uint64_t(255)) + 256;
+    }
     best = std::max(best, s);
   }
   return best;

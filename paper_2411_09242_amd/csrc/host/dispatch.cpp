@@ -36,6 +36,12 @@ int num_variants(int op) {
   }
 }
 
+int cold_weight_copies(uint64_t bytes) {
+  const uint64_t target = 512ull << 20;
+  if (bytes == 0) return 1;
+  return (int)std::min<uint64_t>(64, std::max<uint64_t>(1, (target + bytes - 1) / bytes));
+}
+
 std::vector<int64_t> const_strides(const Node& nd, int slot, int variant, const Shape& shape) {
   if (packs_weight(nd.op, variant) && slot == 1 && shape.size() == 2) return {1, shape[0]};
   return row_major_strides(shape);

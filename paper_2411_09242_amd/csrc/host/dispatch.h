@@ -82,6 +82,13 @@ NodeKernel prepare_node(const Node& nd, int variant, int dtype, const std::vecto
 NodeKernel prepare_sum_norm(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& x1,
                             const Operand& out);
 
+// Cost measurement: the copies of a MatMul's or Conv's constant weight
+// (bytes each) that the timed launches rotate over, so that each launch
+// reads its weight from HBM, as in a run, where the layers in between have
+// evicted it: copies totalling at least twice the 256 MiB last-level cache,
+// at most 64.
+int cold_weight_copies(uint64_t bytes);
+
 // Row-major strides of a shape.
 std::vector<int64_t> row_major_strides(const Shape& s);
 
