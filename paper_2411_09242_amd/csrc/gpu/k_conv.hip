@@ -15,7 +15,8 @@
 //   KORD 1: k = (u, v, c); a wavefront loads 16 consecutive k of 4 pixels --
 //           coalesced when C is unit-stride (NHWC-like layouts).
 // A 64 x 64 output tile per group of 256 threads (4 wavefronts, 2 x 2, each
-// 32 x 32 with v_mfma_f32_32x32x2_f32: lane l reads A[l%32][l/32] and
+// 32 x 32 -- or a 32 x 32 tile per single-wavefront group -- with
+// v_mfma_f32_32x32x2_f32: lane l reads A[l%32][l/32] and
 // B[l/32][l%32]; accumulator v of lane l holds C[8(v/4) + 4(l/32) + v%4][l%32]),
 // operands staged in LDS K-major, the next K-tile loaded into registers
 // while the current one is multiplied.  KS groups share a workgroup and a
@@ -50,22 +51,26 @@ __device__ __forceinline__ int32_t conv_col_off(const ConvParams& p, uint32_t k,
   return (int32_t)c * p.x_c + (int32_t)u * p.x_h + (int32_t)v * p.x_w;
 }
 
-template <int KORD, int KS>
-__global__ __launch_bounds__(256 * KS) void conv_f32_kernel(ConvParams p) {
-  constexpr int BM = 64, BN = 64, BK = 16;
+template <int KORD, int KS, int TW>
+__global__ __launch_bounds__(64 * (TW / 32) * (TW / 32) * KS) void conv_f32_kernel(ConvParams p) {
+  // TW x TW output tile per group of WPG wavefronts ((TW/32)^2, each a
+  // 32 x 32 block); NT threads per group
+  constexpr int WPG = (TW / 32) * (TW / 32), NT = 64 * WPG;
+  constexpr int BM = TW, BN = TW, BK = 16;
   constexpr int AP = BM + 4, BP = BN + 4;
+  constexpr int AE = BM * BK / NT, BE = BN * BK / NT;  // elements per thread per K-tile
   constexpr int STAGE = BK * AP + BK * BP;            // one group's A and B tiles
-  constexpr int RED = (KS - 1) * 16 * 256;            // partial sums of groups 1 .. KS-1
+  constexpr int RED = (KS - 1) * 16 * NT;             // partial sums of groups 1 .. KS-1
   constexpr int SMEM = KS * STAGE > RED ? KS * STAGE : RED;
   __shared__ float smem[SMEM];
   // the group index is uniform per wavefront: keep it in a scalar register
-  const int grp = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 8));
+  const int grp = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / NT));
   float* As = smem + grp * STAGE;
   float* Bs = As + BK * AP;
   const uint32_t tm = blockIdx.x / p.tiles_n, tn = blockIdx.x - tm * p.tiles_n;
   const uint32_t m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int tid = threadIdx.x % NT, lane = tid & 63, wave = tid >> 6;
+  const int wm = WPG > 1 ? wave >> 1 : 0, wn = WPG > 1 ? wave & 1 : 0;
 
   auto row_off = [&](uint32_t m, int32_t sn, int32_t sh, int32_t sw) {
     const uint32_t n = fdiv(m, p.ohw_div);
@@ -75,65 +80,69 @@ __global__ __launch_bounds__(256 * KS) void conv_f32_kernel(ConvParams p) {
     return (int32_t)n * sn + (int32_t)i * sh + (int32_t)j * sw;
   };
 
-  // A: 4 elements per thread per K-tile
-  int a_m[4], a_k[4];
-  int32_t a_off[4];
-  bool a_ok[4];
+  // A: AE elements per thread per K-tile; element r of thread t is index
+  // t + NT r of the tile, pixel-fastest (KORD 0) or k-fastest (KORD 1)
+  int a_m[AE], a_k[AE];
+  int32_t a_off[AE];
+  bool a_ok[AE];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
+  for (int r = 0; r < AE; ++r) {
+    const int idx = tid + NT * r;
     if constexpr (KORD == 0) {
-      a_m[r] = tid & 63;
-      a_k[r] = (tid >> 6) + 4 * r;
+      a_m[r] = idx % BM;
+      a_k[r] = idx / BM;
     } else {
-      a_k[r] = tid & 15;
-      a_m[r] = (tid >> 4) + 16 * r;
+      a_k[r] = idx % BK;
+      a_m[r] = idx / BK;
     }
     const uint32_t m = m0 + a_m[r];
     a_ok[r] = m < p.M;
     a_off[r] = a_ok[r] ? row_off(m, p.x_n, p.x_h, p.x_w) : 0;
   }
   // B (weights): 16 consecutive k of one channel per 16 lanes
-  int b_k[4], b_n[4];
-  bool b_ok[4];
+  int b_k[BE], b_n[BE];
+  bool b_ok[BE];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    b_k[r] = tid & 15;
-    b_n[r] = (tid >> 4) + 16 * r;
+  for (int r = 0; r < BE; ++r) {
+    const int idx = tid + NT * r;
+    b_k[r] = idx % BK;
+    b_n[r] = idx / BK;
     b_ok[r] = n0 + b_n[r] < p.Co;
   }
 
-  float ra[4], rb[4];
+  float ra[AE], rb[BE];
   auto gload = [&](uint32_t k0) {
     if constexpr (KORD == 0) {
-      // one k per thread, four pixels
+      // per element its own k
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
+      for (int r = 0; r < AE; ++r) {
         const uint32_t k = k0 + a_k[r];
         int32_t wa;
         const int32_t co = k < p.K ? conv_col_off<0>(p, k, &wa) : 0;
         ra[r] = (a_ok[r] && k < p.K) ? p.x[a_off[r] + co] : 0.f;
       }
     } else {
+      // one k per thread (NT is a multiple of BK), several pixels
       const uint32_t k = k0 + a_k[0];
       int32_t wa;
       const int32_t co = k < p.K ? conv_col_off<1>(p, k, &wa) : 0;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) ra[r] = (a_ok[r] && k < p.K) ? p.x[a_off[r] + co] : 0.f;
+      for (int r = 0; r < AE; ++r) ra[r] = (a_ok[r] && k < p.K) ? p.x[a_off[r] + co] : 0.f;
     }
     {
       const uint32_t k = k0 + b_k[0];
       int32_t wa = 0;
       if (k < p.K) (void)conv_col_off<KORD>(p, k, &wa);
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+      for (int r = 0; r < BE; ++r)
         rb[r] = (b_ok[r] && k < p.K) ? p.w[(int32_t)(n0 + b_n[r]) * (int32_t)p.K + wa] : 0.f;
     }
   };
   auto lstore = [&]() {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) As[a_k[r] * AP + a_m[r]] = ra[r];
+    for (int r = 0; r < AE; ++r) As[a_k[r] * AP + a_m[r]] = ra[r];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) Bs[b_k[r] * BP + b_n[r]] = rb[r];
+    for (int r = 0; r < BE; ++r) Bs[b_k[r] * BP + b_n[r]] = rb[r];
   };
 
   f32x16 acc;
@@ -161,14 +170,14 @@ __global__ __launch_bounds__(256 * KS) void conv_f32_kernel(ConvParams p) {
     __syncthreads();
     if (grp > 0) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) smem[((grp - 1) * 16 + v) * 256 + tid] = acc[v];
+      for (int v = 0; v < 16; ++v) smem[((grp - 1) * 16 + v) * NT + tid] = acc[v];
     }
     __syncthreads();
     if (grp > 0) return;
 #pragma unroll
     for (int g = 0; g < KS - 1; ++g)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[v] += smem[(g * 16 + v) * 256 + tid];
+      for (int v = 0; v < 16; ++v) acc[v] += smem[(g * 16 + v) * NT + tid];
   }
 
   const uint32_t o = n0 + wn * 32 + lr;
@@ -187,16 +196,23 @@ __global__ __launch_bounds__(256 * KS) void conv_f32_kernel(ConvParams p) {
 
 hipError_t launch_conv(const NodeKernel& k, hipStream_t s) {
   const ConvParams& p = k.conv;
-  const uint32_t grid = ((p.M + 63) / 64) * p.tiles_n;
-  if (k.conv_ks == 1) {
-    if (k.conv_kord == 0) hipLaunchKernelGGL((conv_f32_kernel<0, 1>), dim3(grid), dim3(256), 0, s, p);
-    else hipLaunchKernelGGL((conv_f32_kernel<1, 1>), dim3(grid), dim3(256), 0, s, p);
-  } else if (k.conv_ks == 4) {
-    if (k.conv_kord == 0) hipLaunchKernelGGL((conv_f32_kernel<0, 4>), dim3(grid), dim3(1024), 0, s, p);
-    else hipLaunchKernelGGL((conv_f32_kernel<1, 4>), dim3(grid), dim3(1024), 0, s, p);
+  const uint32_t tw = k.conv_tile;
+  const uint32_t grid = ((p.M + tw - 1) / tw) * p.tiles_n;
+#define FLUID_CONV(KO, KSv, TWv) \
+  hipLaunchKernelGGL((conv_f32_kernel<KO, KSv, TWv>), dim3(grid), dim3(64 * (TWv / 32) * (TWv / 32) * KSv), 0, s, p)
+  if (tw == 64 && k.conv_ks == 1) {
+    if (k.conv_kord == 0) FLUID_CONV(0, 1, 64);
+    else FLUID_CONV(1, 1, 64);
+  } else if (tw == 64 && k.conv_ks == 4) {
+    if (k.conv_kord == 0) FLUID_CONV(0, 4, 64);
+    else FLUID_CONV(1, 4, 64);
+  } else if (tw == 32 && k.conv_ks == 8) {
+    if (k.conv_kord == 0) FLUID_CONV(0, 8, 32);
+    else FLUID_CONV(1, 8, 32);
   } else {
     return hipErrorInvalidValue;
   }
+#undef FLUID_CONV
   return hipGetLastError();
 }
 

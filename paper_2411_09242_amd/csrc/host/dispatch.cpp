@@ -28,7 +28,7 @@ int num_variants(int op) {
     case FLUID_OP_RELU:
     case FLUID_OP_TRANSPOSE:
     case FLUID_OP_RESHAPE: return 2;
-    case FLUID_OP_CONV: return 4;
+    case FLUID_OP_CONV: return 6;
     case FLUID_OP_SOFTMAX:
     case FLUID_OP_LAYERNORM:
     case FLUID_OP_RMSNORM: return 3;
@@ -499,7 +499,8 @@ NodeKernel prepare_window(const Node& nd, int dtype, const std::vector<Operand>&
 // Conv: variant 0 reduces over (c, u, v) with wavefronts along pixels, 1
 // over (u, v, c) with wavefronts along channels; variants 2 and 3 are 0 and
 // 1 with the K-tiles of a tile split over 4 groups of wavefronts in one
-// workgroup (k_conv.hip).
+// workgroup; variants 4 and 5 take 32 x 32 tiles with the K-tiles split
+// over 8 single-wavefront groups (k_conv.hip).
 NodeKernel prepare_conv(const Node& nd, int variant, int dtype, const std::vector<Operand>& ins, const Operand& out) {
   NodeKernel k;
   k.family = KF_CONV;
@@ -537,9 +538,10 @@ NodeKernel prepare_conv(const Node& nd, int variant, int dtype, const std::vecto
   p.x_n = (int32_t)x.stride[0]; p.x_c = (int32_t)x.stride[1]; p.x_h = (int32_t)x.stride[2]; p.x_w = (int32_t)x.stride[3];
   p.y_n = (int32_t)out.stride[0]; p.y_c = (int32_t)out.stride[1]; p.y_h = (int32_t)out.stride[2];
   p.y_w = (int32_t)out.stride[3];
-  p.tiles_n = (p.Co + 63) / 64;
   k.conv_kord = variant & 1;
-  k.conv_ks = variant >= 2 ? 4 : 1;
+  k.conv_ks = variant >= 4 ? 8 : variant >= 2 ? 4 : 1;
+  k.conv_tile = variant >= 4 ? 32 : 64;
+  p.tiles_n = (p.Co + k.conv_tile - 1) / k.conv_tile;
   k.available = true;
   return k;
 }
@@ -610,7 +612,8 @@ std::string NodeKernel::name() const {
     case KF_RED_COL: return std::string(red_names[red.op]) + "_col_" + dt;
     case KF_WIN: return std::string(win.op == 0 ? "pad_" : "maxpool_") + dt;
     case KF_CONV:
-      return "conv_" + dt + (conv_kord == 0 ? "_t64_kcuv" : "_t64_kuvc") + (conv_ks > 1 ? "_ks" + std::to_string(conv_ks) : "");
+      return "conv_" + dt + "_t" + std::to_string(conv_tile) + (conv_kord == 0 ? "_kcuv" : "_kuvc") +
+             (conv_ks > 1 ? "_ks" + std::to_string(conv_ks) : "");
     case KF_GEMM: {
       // fused epilogue steps: b bias, g GELU, s SiLU, a / m Add / Mul of R
       auto epi_suffix = [&]() {

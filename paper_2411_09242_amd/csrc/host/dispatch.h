@@ -50,7 +50,7 @@ struct NodeKernel {
   GemmParams gemm{};
   WinParams win{};
   ConvParams conv{};
-  int conv_kord = 0, conv_ks = 1;  // conv: reduction order; K groups per workgroup
+  int conv_kord = 0, conv_ks = 1, conv_tile = 64;  // conv: reduction order; K groups per workgroup; tile width
   bool red_block = false;       // row reduction: one 256-thread workgroup per row (variant 2)
   int gemm_tile = 0, amode = 0, bmode = 0, cmode = 0;  // cmode 0 generic, 1 N-contig, 2 M-contig
   std::string name() const;

@@ -51,7 +51,7 @@ def forced_table(og, want, variants=None):
         else:
             assert p in L[e], (e, p, "not a candidate (use the first of equivalent layouts)")
     sigs, node_sig = [], []
-    nvar = {"matmul": 20, "gelu": 2, "silu": 2, "relu": 2, "conv": 4, "transpose": 2, "reshape": 2,
+    nvar = {"matmul": 20, "gelu": 2, "silu": 2, "relu": 2, "conv": 6, "transpose": 2, "reshape": 2,
             "softmax": 3, "layernorm": 3, "rmsnorm": 3}
     for n, nd in enumerate(og.nodes):
         slots = og.act_inputs(n)

@@ -51,12 +51,12 @@ CONV_CASES = [((1, 3, 9, 7), (5, 3, 3, 3), True), ((2, 8, 10, 12), (16, 8, 3, 3)
 
 
 @pytest.mark.parametrize("case", CONV_CASES, ids=str)
-@pytest.mark.parametrize("variant", [0, 1, 2, 3])
+@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5])
 def test_conv_layouts(case, variant, tmp_path):
     """Input and output of the convolution in (a sample of) every layout
     pair; both reduction orders, with and without the K split over wave
-    groups (K-tiles past the end in the last round); ragged pixel and
-    channel tiles."""
+    groups (64 x 64 tiles over 4 groups, 32 x 32 tiles over 8; K-tiles past
+    the end in the last round); ragged pixel and channel tiles."""
     xs_, ws_, bias = case
     og, a, c = conv_graph(xs_, ws_, bias)
     for pa, pc in _pairs(layouts.layout_list(og.edge_shape(a)), layouts.layout_list(og.edge_shape(c)), 24,
