@@ -225,11 +225,15 @@ fluid_status fluid_measure_costs(const fluid_graph* g, uint32_t reps, void* scra
  * fixed; then, unless FLUID_NO_GUARD, the all-row-major plan if it is
  * cheaper.  Fusion (Section 4: the compiler fuses operators before it plans
  * layouts): when the table carries fused entries, a MatMul and the bias
- * Add / GELU or SiLU / Add or Mul with an earlier tensor right after it on
- * its path (consecutive node ids, single readers) may run as one launch;
- * the path DP weighs that launch's measured cost against the nodes' own
- * (ties go to the nodes on their own), and runs then perform exactly the
- * plan's fusions (fluid_layout_plan_fusion).  Errors: FLUID_E_INFEASIBLE
+ * Add / GELU or SiLU / Add or Mul with an earlier tensor right after it, or
+ * a residual Add and the LayerNorm / RMSNorm of its sum (consecutive node
+ * ids, single readers), may run as one launch; the path DP weighs that
+ * launch's measured cost against the nodes' own (ties go to the nodes on
+ * their own); after the vote the cheapest disjoint chains are chosen
+ * exactly for the final layouts, the voted layouts of the fusion-aware and
+ * of the plain DP compete (the cheaper total wins), and the guard compares
+ * with the row-major plan with its best chains.  Runs then perform exactly
+ * the plan's fusions (fluid_layout_plan_fusion).  Errors: FLUID_E_INFEASIBLE
  * (no identity entry, or no finite plan), FLUID_E_INVALID. */
 fluid_status fluid_plan_layouts(const fluid_graph* g, const fluid_cost_table* t, uint32_t flags,
                                 fluid_layout_plan** out);
@@ -259,8 +263,9 @@ fluid_status fluid_pack_constant(const fluid_graph* g, const fluid_layout_plan* 
 fluid_status fluid_layout_plan_get(const fluid_layout_plan* lp, int32_t* layout_idx_per_edge,
                                    int32_t* variant_per_node, int64_t* total_ns, int32_t* guard_used);
 /* The plan's fusions: fuse_per_node[n] (n_nodes entries) is the number t
- * of nodes after MatMul n that its launch performs (nodes n+1 .. n+t have
- * variant -2 and results n .. n+t-1 never reach memory), 0 otherwise;
+ * of nodes after node n (a MatMul, or a residual Add whose normalisation
+ * follows) that its launch performs (nodes n+1 .. n+t have variant -2 and
+ * results n .. n+t-1 never reach memory), 0 otherwise;
  * *priced is 1 when the plan priced fusion chains (fluid_run then performs
  * exactly these fusions), 0 when it did not (FLUID_NO_FUSION, FLUID_NO_DP, or
  * a table without fused entries: fluid_run fuses by its own rule, see
@@ -357,11 +362,14 @@ fluid_status fluid_run_static(const fluid_graph* g, const fluid_layout_plan* lp,
  * fluid_run; nodes: n_nodes node ids, each a non-view node under the plan
  * (else FLUID_E_INVALID); repeat >= 1.  A MatMul that fluid_run fuses with
  * the nodes after it does so here too when all those nodes follow it in the
- * list; otherwise each listed node runs its own kernel.  Products that
- * fluid_run groups into one launch run as that launch when the list holds
- * all its nodes (the products and the nodes they absorb) consecutively in
- * node order, else one launch each (the same tile code, so the same
- * results).  Reads and writes the arena like a run would, so it leaves the
+ * list; otherwise each listed node runs its own kernel -- except where the
+ * plan priced the chain (fluid_layout_plan_fusion): its intermediate
+ * results have no buffer, so a list that splits such a chain (its head
+ * without every node it absorbs, or an absorbed node alone) is refused
+ * with FLUID_E_INVALID before any launch.  Products that fluid_run groups
+ * into one launch run as that launch when the list holds all its nodes
+ * (the products and the nodes they absorb) consecutively in node order,
+ * else one launch each (the same tile code, so the same results).  Reads and writes the arena like a run would, so it leaves the
  * arena contents of a partial run.  GPU build only. */
 fluid_status fluid_run_nodes(const fluid_graph* g, const fluid_layout_plan* lp, const fluid_arena_plan* ap,
                              void* arena, uint64_t arena_bytes, const void* const* consts,
