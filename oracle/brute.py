@@ -110,7 +110,14 @@ def best_layouts_fused(g, ct, use_v0=False):
                     other = [v for v in last.ins if v >= 0 and v != g.out_edge(m + t - 1)]
                     slots += other[:1]
                 key = tuple(lay[e] for e in slots) + (lay[g.out_edge(m + t)],)
-                tot = min(tot + int(C[key]), INF)
+                c = int(C[key])
+                # a residual sum read also after its norm is stored by the
+                # launch, in the norm output's layout
+                e0, eo = g.out_edge(m), g.out_edge(m + t)
+                if g.nodes[m].op == "add" and sum(1 for x in g.nodes if e0 in x.ins) > 1 and \
+                        ct.L[e0][lay[e0]] != ct.L[eo][lay[eo]]:
+                    c = INF
+                tot = min(tot + c, INF)
             for n in range(len(g.nodes)):
                 if n in covered:
                     continue

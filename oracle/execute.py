@@ -35,6 +35,7 @@ from __future__ import annotations
 import numpy as np
 from scipy.special import erf
 
+from . import fusion
 from . import numerics
 from .layouts import node_is_view
 
@@ -202,8 +203,8 @@ def run_in_arena(g, layout_of_edge, root_of_edge, offset_of_root, peak,
 
     on_chip = {}
     for m, t in enumerate(fuse or []):
-        for i in range(t):
-            on_chip[g.out_edge(m + i)] = None
+        for e in fusion.on_chip_edges(g, m, t):
+            on_chip[e] = None
 
     def buf(e):
         r = root_of_edge[e]

@@ -12,12 +12,14 @@ chain when, step by step,
     an Add or Mul of the chain value with another activation R of the
     product's shape, produced before m (last step).
 A second kind of chain starts at an Add of two activations of its own
-output's shape (a residual sum) whose result has exactly one reader, the
-next node, a LayerNorm or RMSNorm over it (with constant scale and shift),
-and is not a graph output: the normalisation launch then also forms the sum
-(t = 1).
-The launch writes only the last node's output: the intermediate results
-never reach memory.  t is 1..3; every prefix of a chain is a chain.
+output's shape (a residual sum) read by the next node, a LayerNorm or
+RMSNorm over it (with constant scale and shift), and is not a graph output:
+the normalisation launch then also forms the sum (t = 1).
+A MatMul chain's launch writes only the last node's output: the
+intermediate results never reach memory.  A residual sum that has further
+readers (a pre-norm block's next residual) is stored by the launch as well,
+in the layout of the normalisation's output ("norm_store"); otherwise it
+stays on chip ("norm").  t is 1..3; every prefix of a chain is a chain.
 """
 from __future__ import annotations
 
@@ -78,12 +80,26 @@ def _norm_chain(g, m):
             any(tuple(g.edge_shape(e)) != out_shape for e in nd.ins):
         return []
     cur, n = g.out_edge(m), m + 1
-    if n >= len(g.nodes) or cur in g.outputs or _readers(g, cur) != [n]:
+    if n >= len(g.nodes) or cur in g.outputs or n not in _readers(g, cur):
         return []
     x = g.nodes[n]
-    if x.op not in ("layernorm", "rmsnorm") or x.ins[0] != cur or min(x.ins[1:]) >= 0:
+    if x.op not in ("layernorm", "rmsnorm") or x.ins[0] != cur or cur in x.ins[1:] or min(x.ins[1:]) >= 0:
         return []
-    return [(n, "norm", None)]
+    return [(n, "norm" if _readers(g, cur) == [n] else "norm_store", None)]
+
+
+def stored_edges(g, m, t):
+    """Intermediate results of the chain (m, t) that its launch stores (in
+    the layout of the last node's output): a residual sum with further
+    readers."""
+    steps = chain_steps(g, m)[:t]
+    return [g.out_edge(m)] if steps and steps[0][1] == "norm_store" else []
+
+
+def on_chip_edges(g, m, t):
+    """Intermediate results of the chain (m, t) that never reach memory."""
+    st = stored_edges(g, m, t)
+    return [g.out_edge(m + i) for i in range(t) if g.out_edge(m + i) not in st]
 
 
 def chain_slots(g, m, t):

@@ -31,7 +31,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import numerics
+from . import fusion, numerics
 from .layouts import node_is_view
 
 
@@ -64,7 +64,7 @@ def buffers_and_lifetimes(g, layout_of_edge, align=256, fuse=None):
     on_chip, until = set(), {}
     for m, t in enumerate(fuse or []):
         if t:
-            on_chip.update(g.out_edge(m + i) for i in range(t))
+            on_chip.update(fusion.on_chip_edges(g, m, t))
             until[m] = m + t
     buffers = [g.out_edge(n) for n in range(len(g.nodes))
                if not view[n] and g.out_edge(n) not in outs and g.out_edge(n) not in on_chip]

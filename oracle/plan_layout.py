@@ -218,10 +218,27 @@ def fused_options(g, ct, info, j):
     return out
 
 
+def store_index(L, e_store, e_out, b):
+    """The index in L(e_store) of the permutation L(e_out)[b] -- the layout
+    a chain's stored intermediate takes when the chain's output takes b --
+    or None when e_store has no such candidate."""
+    p = L[e_out][b]
+    return L[e_store].index(p) if p in L[e_store] else None
+
+
+def chain_layouts_ok(g, L, m, t, lay):
+    """Whether every intermediate the chain (m, t) stores has the layout of
+    the chain's output under the assignment lay."""
+    eo = g.out_edge(m + t)
+    return all(lay[e] == store_index(L, e, eo, lay[eo]) for e in fusion.stored_edges(g, m, t))
+
+
 def _fused_gain(g, ct, use_v0, info, j, t, FIX):
     """The gain of steps j .. j+t run as one fused launch: a virtual node
     whose slots are the chain's (the MatMul's activation inputs, then R) and
-    whose output is the last node's."""
+    whose output is the last node's.  An output layout b that a stored
+    intermediate cannot take (no such candidate, or fixed otherwise) is
+    infeasible."""
     m = info.path[j]
     slots = fusion.chain_slots(g, m, t)
     cs = info.chain_slot[j]
@@ -231,7 +248,15 @@ def _fused_gain(g, ct, use_v0, info, j, t, FIX):
         if e != chain_edge and e not in be:
             be.append(e)
     NC = ct.fused[(m, t)]
-    return _gain(ct.L, NC.v0 if use_v0 else NC.best, slots, chain_edge, be, g.out_edge(m + t), FIX)
+    eo = g.out_edge(m + t)
+    G, arg, betas, be = _gain(ct.L, NC.v0 if use_v0 else NC.best, slots, chain_edge, be, eo, FIX)
+    for e in fusion.stored_edges(g, m, t):
+        for b in range(len(ct.L[eo])):
+            k = store_index(ct.L, e, eo, b)
+            if k is None or (e in FIX and FIX[e] != k):
+                G[:, b] = INF
+                arg[:, b] = -1
+    return G, arg, betas, be
 
 
 def dp_path(g, ct, use_v0, info, FIX, fuse=True):
@@ -303,6 +328,11 @@ def dp_path(g, ct, use_v0, info, FIX, fuse=True):
         # that reads it as a boundary edge
         for k in range(s, j + 1):
             bsel[k] = {e: chosen[e] for e in info.bnd_edges[k] if e in chosen}
+        if t:
+            # an intermediate the launch stores takes the output's layout
+            m0 = info.path[s]
+            for e in fusion.stored_edges(g, m0, t):
+                states[s + (g.producer(e) - m0)] = store_index(ct.L, e, g.out_edge(m0 + t), b)
         fused[s] = t
         j = s - 1
         b = a
@@ -338,7 +368,8 @@ def plan_cost(g, ct, use_v0, lay, fuse=None):
         if fuse[n]:
             NC = ct.fused[(n, fuse[n])]
             C = NC.v0 if use_v0 else NC.best
-            total = int(sat_add(total, C[_chain_key(g, n, fuse[n], lay)]))
+            c = int(C[_chain_key(g, n, fuse[n], lay)]) if chain_layouts_ok(g, ct.L, n, fuse[n], lay) else INF
+            total = int(sat_add(total, c))
             n += fuse[n] + 1
             continue
         C = ct.nodes[n].v0 if use_v0 else ct.nodes[n].best
@@ -418,10 +449,11 @@ def best_chains(g, ct, use_v0, lay):
         f[n] = int(sat_add(C[_node_key(g, n, lay)], f[n + 1]))
         t = 1
         while (n, t) in ct.fused:
-            NC = ct.fused[(n, t)]
-            c = int(sat_add((NC.v0 if use_v0 else NC.best)[_chain_key(g, n, t, lay)], f[n + t + 1]))
-            if c < f[n]:
-                f[n], pick[n] = c, t
+            if chain_layouts_ok(g, ct.L, n, t, lay):
+                NC = ct.fused[(n, t)]
+                c = int(sat_add((NC.v0 if use_v0 else NC.best)[_chain_key(g, n, t, lay)], f[n + t + 1]))
+                if c < f[n]:
+                    f[n], pick[n] = c, t
             t += 1
     fuse = [0] * N
     n = 0

@@ -339,25 +339,32 @@ def test_best_chains_is_the_cheapest_chain_set(seed, builder):
 def test_fusion_chains_of_transformer_layers(arch):
     """The chain rules on one layer of each block kind, enumerated by hand
     from the builder's node order: a MatMul with its bias, activation and
-    residual steps, and -- where the residual sum has the normalisation as
-    its only reader (post-LN; the last block of pre-LN / Llama, before the
-    final norm) -- the residual Add with that normalisation."""
+    residual steps, and the residual Add with the normalisation right after
+    it -- on chip where the sum has that norm as its only reader (post-LN;
+    the last sum of pre-LN / Llama, before the final norm), stored by the
+    launch where the next residual reads it too (pre-LN, Llama)."""
     from oracle import fusion
     cfg = synth_inputs.config(1, arch=arch, layers=1, seq=8, hidden=32, heads=2, ffn=48)
     g = graph.build_transformer(cfg)
     ops = [nd.op for nd in g.nodes]
     got = {k: [ops[n] for n in v] for k, v in fusion.all_chains(g).items()}
     norm_heads = sorted(m for (m, t), v in got.items() if v[0] == "add" and t == 1)
+    kinds = []
     for m in norm_heads:
         assert got[(m, 1)][1] in ("layernorm", "rmsnorm")
-        assert fusion.chain_steps(g, m) == [(m + 1, "norm", None)]
+        (step,) = fusion.chain_steps(g, m)
+        readers = [n for n, x in enumerate(g.nodes) if g.out_edge(m) in x.ins]
+        assert step == (m + 1, "norm" if readers == [m + 1] else "norm_store", None)
         assert fusion.chain_slots(g, m, 1) == list(g.nodes[m].ins)
-    # residual sums read only by the norm after them
+        assert fusion.stored_edges(g, m, 1) == ([] if step[1] == "norm" else [g.out_edge(m)])
+        assert fusion.on_chip_edges(g, m, 1) == ([g.out_edge(m)] if step[1] == "norm" else [])
+        kinds.append(step[1])
+    # residual sums (two activations) with a norm right after them
     expect = [m for m, nd in enumerate(g.nodes) if nd.op == "add" and min(nd.ins) >= 0 and m + 1 < len(ops)
-              and ops[m + 1] in ("layernorm", "rmsnorm")
-              and [n for n, x in enumerate(g.nodes) if g.out_edge(m) in x.ins] == [m + 1]]
+              and ops[m + 1] in ("layernorm", "rmsnorm") and g.nodes[m + 1].ins[0] == g.out_edge(m)]
     assert norm_heads == expect
-    assert len(norm_heads) == {"post_ln": 2, "pre_ln": 1, "llama": 1}[arch]
+    assert kinds == {"post_ln": ["norm", "norm"], "pre_ln": ["norm_store", "norm"],
+                     "llama": ["norm_store", "norm"]}[arch]
     # MatMul chains: the FFN up-projection with bias and GELU (post/pre-LN),
     # the down-projection with bias and the residual (post/pre-LN) or with
     # the residual alone (Llama)
@@ -369,3 +376,81 @@ def test_fusion_chains_of_transformer_layers(arch):
         assert ["matmul", "silu"] in mm.values() and ["matmul", "add"] in mm.values()
         # SiLU's product meets the up-projection only after another MatMul
         assert ["matmul", "silu", "mul"] not in mm.values()
+
+
+@pytest.mark.parametrize("arch", ["pre_ln", "llama"])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_stored_residual_sums(arch, seed):
+    """Pre-norm stacks: a residual sum read by its norm and by the next
+    residual.  When the plan fuses such a sum with its norm, the launch
+    stores the sum too, in the norm output's layout: the sum keeps its
+    arena buffer (live to its last reader), its layout equals the norm's,
+    the plan's total is its recomputed cost, and the permuted execution in
+    the poisoned arena equals the row-major result."""
+    from oracle import execute, fusion, plan_arena
+    from tables import add_fused
+    cfg = synth_inputs.config(1, arch=arch, layers=1, batch=2, seq=5, hidden=8, heads=2, ffn=8)
+    g = graph.build_transformer(cfg)
+    # residual-norm entries well below the separate nodes, MatMul chains
+    # (which would take the same Add) well above, so that sums are fused
+    obj = add_fused(synthetic_table(g, seed=seed, mode="random", lo=50, hi=100), g, seed, lo=1, hi=20)
+    for fs in obj["fused_sigs"]:
+        if fs["op"] == "matmul":
+            for ent in fs["entries"]:
+                ent[2] = [c * 50 for c in ent[2]]
+    ct = costtable.load(obj, g)
+    plan = PL.plan_layouts(g, ct)
+    stored = [(m, t) for m, t in enumerate(plan.fuse) if t and fusion.stored_edges(g, m, t)]
+    assert stored
+    assert plan.total == PL.plan_cost(g, ct, False, plan.layout_idx, plan.fuse)
+    lay = {e: ct.L[e][plan.layout_idx[e]] for e in range(g.n_edges)}
+    ap = plan_arena.plan_arena(g, lay, fuse=plan.fuse)
+    assert plan_arena.check_disjoint(ap)
+    for m, t in stored:
+        (e,) = fusion.stored_edges(g, m, t)
+        assert e in ap.buffers and lay[e] == lay[g.out_edge(m + t)]
+        # live to its last reader (to that reader's chain end if it heads one)
+        last = max(n + plan.fuse[n] for n, x in enumerate(g.nodes) if e in x.ins)
+        assert ap.last[e] == last > m + t
+    for m, t in enumerate(plan.fuse):
+        for e in fusion.on_chip_edges(g, m, t) if t else []:
+            assert e not in ap.buffers
+    x, cs = synth_inputs.make_inputs(cfg, g.const_specs(), 9)
+    ref = execute.run_canonical(g, [x], cs)
+    out = execute.run_in_arena(g, lay, ap.root, ap.offset, ap.peak, [x], cs, fuse=plan.fuse)
+    assert np.array_equal(out[0], ref[0])
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_stored_sum_chain_choice_and_optimum(seed):
+    """A residual sum with a second reader (tiny pre-norm graph): its chain
+    with the LayerNorm is the stored kind; for random layout assignments the
+    chosen chain set costs what the definition gives -- the separate nodes,
+    or, when the sum's layout equals the norm output's, the cheaper of that
+    and the fused entry -- and the plan costs no less than the exhaustive
+    optimum over every layout assignment and chain set."""
+    from oracle import fusion
+    from tables import add_fused
+    from tinygraphs import prenorm_graph
+    g = prenorm_graph()
+    sm = next(m for m, nd in enumerate(g.nodes) if nd.op == "add" and g.nodes[m + 1].op == "layernorm")
+    assert fusion.chain_steps(g, sm) == [(sm + 1, "norm_store", None)]
+    obj = add_fused(synthetic_table(g, seed=seed, mode="random", lo=10, hi=60), g, seed, lo=1, hi=70)
+    ct = costtable.load(obj, g)
+    rng = np.random.default_rng(seed)
+    es, eo = g.out_edge(sm), g.out_edge(sm + 1)
+    for _ in range(60):
+        lay = [int(rng.integers(0, len(ct.L[e]))) for e in range(g.n_edges)]
+        if rng.random() < 0.5:    # often put the sum in the norm output's layout
+            lay[es] = ct.L[es].index(ct.L[eo][lay[eo]])
+        own = [int(ct.nodes[n].best[tuple(lay[e] for e in g.act_inputs(n)) + (lay[g.out_edge(n)],)])
+               for n in range(len(g.nodes))]
+        want = sum(own)
+        if ct.L[es][lay[es]] == ct.L[eo][lay[eo]]:
+            fz = int(ct.fused[(sm, 1)].best[tuple(lay[e] for e in g.nodes[sm].ins) + (lay[eo],)])
+            want = min(want, want - own[sm] - own[sm + 1] + fz)
+        assert PL.plan_cost(g, ct, False, lay, PL.best_chains(g, ct, False, lay)) == want
+    plan = PL.plan_layouts(g, ct, PL.NO_GUARD)
+    assert plan.total >= brute.best_layouts_fused(g, ct)
+    if plan.fuse[sm]:
+        assert ct.L[es][plan.layout_idx[es]] == ct.L[eo][plan.layout_idx[eo]]

@@ -113,3 +113,20 @@ def fanout_graph():
     y = g.add_node("add", [s, d], (2, 3))
     g.outputs = [y]
     return g
+
+
+def prenorm_graph(B=2, S=3, H=4):
+    """A residual sum read by its LayerNorm and again by a later Add (the
+    pre-norm pattern): x -> a = GELU(x), b = SiLU(x); s = a + b;
+    n = LN(s); y = GELU(n) + s."""
+    g = Graph(dtype="f32")
+    x = g.add_input((B, S, H))
+    a = g.add_node("gelu", [x], (B, S, H))
+    b = g.add_node("silu", [x], (B, S, H))
+    s = g.add_node("add", [a, b], (B, S, H))
+    gm = g.add_const("gamma", (H,)); bt = g.add_const("beta", (H,))
+    n = g.add_node("layernorm", [s, gm, bt], (B, S, H), fattr=1e-5)
+    y1 = g.add_node("gelu", [n], (B, S, H))
+    y = g.add_node("add", [y1, s], (B, S, H))
+    g.outputs = [y]
+    return g
