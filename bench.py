@@ -179,8 +179,9 @@ def launch_units(g, ex):
     products for a GEMM launch (grouped products summed; a fused bias or
     activation adds no flops), else the bytes of its one node (for a
     residual Add and its normalisation in one launch: the summands read
-    once, the normalised output written once; its class is the norm's)."""
-    launch, _, names = ex.schedule()
+    once, the normalised output written once, and the sum written once when
+    the launch stores it; its class is the norm's)."""
+    launch, written, names = ex.schedule()
     units = [{"name": nm, "nodes": []} for nm in names]
     for n, l in enumerate(launch):
         if l >= 0:
@@ -195,8 +196,9 @@ def launch_units(g, ex):
             u["op"] = g.desc["nodes"][n]["op"]
             isz = 2 if g.dtype == "bf16" else 4
             u["kind"] = "bytes"
+            out_b = int(np.prod(g.desc["nodes"][n]["out_shape"])) * isz
             u["work"] = float(sum(int(np.prod(g.edge_shape(v))) * isz for v in g.desc["nodes"][h]["ins"]) +
-                              int(np.prod(g.desc["nodes"][n]["out_shape"])) * isz)
+                              out_b * (2 if written[h] else 1))
         else:
             assert len(u["nodes"]) == 1, u
             n = u["nodes"][0]

@@ -227,9 +227,11 @@ fluid_status fluid_measure_costs(const fluid_graph* g, uint32_t reps, void* scra
  * layouts): when the table carries fused entries, a MatMul and the bias
  * Add / GELU or SiLU / Add or Mul with an earlier tensor right after it, or
  * a residual Add and the LayerNorm / RMSNorm of its sum (consecutive node
- * ids, single readers), may run as one launch; the path DP weighs that
- * launch's measured cost against the nodes' own (ties go to the nodes on
- * their own); after the vote the cheapest disjoint chains are chosen
+ * ids; the MatMul chain's results single-reader; a sum with further
+ * readers, as in a pre-norm block, is stored by that launch in the layout
+ * of the norm's output, which the plan then gives the sum), may run as one
+ * launch; the path DP weighs that launch's measured cost against the nodes'
+ * own (ties go to the nodes on their own); after the vote the cheapest disjoint chains are chosen
  * exactly for the final layouts, the voted layouts of the fusion-aware and
  * of the plain DP compete (the cheaper total wins), and the guard compares
  * with the row-major plan with its best chains.  Runs then perform exactly
@@ -265,7 +267,8 @@ fluid_status fluid_layout_plan_get(const fluid_layout_plan* lp, int32_t* layout_
 /* The plan's fusions: fuse_per_node[n] (n_nodes entries) is the number t
  * of nodes after node n (a MatMul, or a residual Add whose normalisation
  * follows) that its launch performs (nodes n+1 .. n+t have variant -2 and
- * results n .. n+t-1 never reach memory), 0 otherwise;
+ * results n .. n+t-1 never reach memory, except a residual sum with further
+ * readers, which the launch stores), 0 otherwise;
  * *priced is 1 when the plan priced fusion chains (fluid_run then performs
  * exactly these fusions), 0 when it did not (FLUID_NO_FUSION, FLUID_NO_DP, or
  * a table without fused entries: fluid_run fuses by its own rule, see
@@ -388,7 +391,8 @@ fluid_status fluid_run_launches(const fluid_graph* g, const fluid_layout_plan* l
  * epilogue fusion and grouped launches described at fluid_run).  Per node:
  * launch_of_node the index of the launch that performs it (-1 for a view),
  * output_written 1 if that launch stores the node's output (0 for a view
- * and for a node whose output a fused launch keeps on chip).  names: the
+ * and for a node whose output a fused launch keeps on chip; 1 for a
+ * residual sum the normalisation's launch stores).  names: the
  * kernel name of every launch, '\n'-separated, NUL-terminated (a grouped
  * launch of k products ends in "_x<k>"); names_len receives the bytes
  * needed including the NUL.  n_launches receives the launch count.  Any

@@ -17,8 +17,9 @@
 // Causal softmax: keys k > q (q = index along the second-to-last logical
 // dim) get probability exactly 0.  The RED_SUM_* norms read a second
 // tensor x1 (own layout) and normalise x + x1, the sum formed on load (a
-// residual Add performed in the normalisation's launch).  All arithmetic is
-// fp32.
+// residual Add performed in the normalisation's launch); given h, they also
+// store the sum there, in y's layout, and normalise the stored (rounded)
+// values.  All arithmetic is fp32.
 #include <math.h>
 
 #include "dev.h"
@@ -62,6 +63,16 @@ __global__ __launch_bounds__(256) void red_row_kernel(RedParams p) {
     const uint32_t k = (uint32_t)lane + 64u * j;
     v[j] = k < valid ? Elem<T>::load(p.x, io + (int32_t)k * p.irs) : 0.f;
     if constexpr (SUM) v[j] += k < valid ? Elem<T>::load(p.x1, io1 + (int32_t)k * p.irs1) : 0.f;
+  }
+  if constexpr (SUM) {
+    if (p.h) {
+#pragma unroll
+      for (int j = 0; j < NPL; ++j) {
+        const uint32_t k = (uint32_t)lane + 64u * j;
+        v[j] = Elem<T>::round(v[j]);
+        if (k < R) Elem<T>::store(p.h, oo + (int32_t)k * p.ors, v[j]);
+      }
+    }
   }
   if constexpr (OP == RED_SOFTMAX) {
     float m = -INFINITY;
@@ -183,6 +194,13 @@ __global__ __launch_bounds__(256) void red_rowv_kernel(RedParams p) {
       Piece<T>::unpack(u1, w);
 #pragma unroll
       for (int i = 0; i < VEC; ++i) v[c][i] += w[i];
+    }
+    if constexpr (SUM) {
+      if (p.h && e0 < R) {
+        const uint4 hs = Piece<T>::pack(v[c]);
+        *(uint4*)((T*)p.h + oo + e0) = hs;
+        Piece<T>::unpack(hs, v[c]);
+      }
     }
   }
   // gamma / beta pieces are fetched with the row, not after the reduction,
@@ -307,6 +325,13 @@ __global__ __launch_bounds__(256) void red_rowb_kernel(RedParams p) {
 #pragma unroll
       for (int i = 0; i < VEC; ++i) v[c][i] += w[i];
     }
+    if constexpr (SUM) {
+      if (p.h && e0 < R) {
+        const uint4 hs = Piece<T>::pack(v[c]);
+        *(uint4*)((T*)p.h + oo + e0) = hs;
+        Piece<T>::unpack(hs, v[c]);
+      }
+    }
     if constexpr (OP != RED_SOFTMAX) {
       gq[c] = e0 < R ? *(const uint4*)((const T*)p.gamma + e0) : make_uint4(0, 0, 0, 0);
       if constexpr (BOP == RED_LAYERNORM) bq[c] = e0 < R ? *(const uint4*)((const T*)p.beta + e0) : make_uint4(0, 0, 0, 0);
@@ -417,9 +442,16 @@ __global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
   // element k of the row (of the sum for RED_SUM_*)
   auto ldx = [&](uint32_t k) {
     float a = Elem<T>::load(p.x, io + (int32_t)k * p.irs);
-    if constexpr (SUM) a += Elem<T>::load(p.x1, io1 + (int32_t)k * p.irs1);
+    if constexpr (SUM) {
+      a += Elem<T>::load(p.x1, io1 + (int32_t)k * p.irs1);
+      if (p.h) a = Elem<T>::round(a);
+    }
     return a;
   };
+  if constexpr (SUM) {
+    if (p.h)
+      for (uint32_t k = 0; k < R; ++k) Elem<T>::store(p.h, oo + (int32_t)k * p.ors, ldx(k));
+  }
   if constexpr (OP == RED_SOFTMAX) {
     const uint32_t valid = p.causal ? min(R, qi + 1u) : R;
     float m = -INFINITY, s = 0.f;
@@ -550,6 +582,20 @@ __global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
   } else {
 #pragma unroll
     for (int j = 0; j < KPL; ++j) v[j] = ld(j, xo, xo1);
+  }
+  if constexpr (SUM) {
+    if (p.h) {
+      // the sum's own output: y's offsets, through its own resource
+      const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(p.h, 0, 0x7fffffff, 0x00020000);
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) {
+        v[j] = Elem<T>::round(v[j]);
+        const uint32_t vo = !masked || kl + KQ * j < R ? yo : OOB;
+        const uint32_t so = (kb + (uint32_t)(KQ * j)) * ystep;
+        if constexpr (ES == 4) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v[j]), rh, vo, so, 0);
+        else __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(v[j]), rh, vo, so, 0);
+      }
+    }
   }
   // y[j] for every j, stored where k < R
   auto store_all = [&](auto&& yfun) {

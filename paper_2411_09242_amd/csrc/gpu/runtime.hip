@@ -87,6 +87,7 @@ NodeKernel fused_kernel(const PreparedNode& pn, const Bases& B) {
     k.red.gamma = pn.fgamma >= 0 ? B.consts[pn.fgamma] : nullptr;
     k.red.beta = pn.fbeta >= 0 ? B.consts[pn.fbeta] : nullptr;
     k.red.y = resolve(pn.fout, B);
+    k.red.h = pn.fstore ? resolve(pn.out, B) : nullptr;
     return k;
   }
   k.gemm.A = resolve(pn.in[0], B);
@@ -647,7 +648,8 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
       struct FusedKey {
         SigKey k;
         std::vector<SigKey> steps;
-        bool operator<(const FusedKey& o) const { return std::tie(k, steps) < std::tie(o.k, o.steps); }
+        std::vector<int> kinds;  // a stored residual sum costs its extra write
+        bool operator<(const FusedKey& o) const { return std::tie(k, steps, kinds) < std::tie(o.k, o.steps, o.kinds); }
       };
       std::map<FusedKey, int> fsig_of;
       std::vector<std::pair<int, int>> rep_chain;  // (m, t) per fused signature
@@ -658,6 +660,7 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
         FusedKey fk{sig_key(g, m), {}};
         for (int tl = 1; tl <= (int)steps.size(); ++tl) {
           fk.steps.push_back(sig_key(g, steps[tl - 1].node));
+          fk.kinds.push_back(steps[tl - 1].kind);
           auto it = fsig_of.find(fk);
           if (it == fsig_of.end()) {
             it = fsig_of.emplace(fk, (int)rep_chain.size()).first;
@@ -725,9 +728,12 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
               ins.push_back(place(c.shape, row_major_strides(c.shape), c.dtype));
             }
             const Operand ou = place(xs, dense_strides(xs, en.out), g.dtype);
+            // a sum with further readers is also stored, in the output's layout
+            void* hs = steps[0].kind == CH_NORM_STORE ? (void*)place(xs, dense_strides(xs, en.out), g.dtype).ptr : nullptr;
             for (int v = 0; v < num_variants(xn.op); ++v) {
               NodeKernel k = prepare_sum_norm(xn, v, g.dtype, ins, x1, ou);
               if (!k.available) { en.costs.push_back(-1); continue; }
+              k.red.h = hs;
               en.costs.push_back(time_kernel({k}, best_so_far));
             }
             sig.entries.push_back(std::move(en));

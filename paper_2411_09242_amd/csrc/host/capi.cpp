@@ -34,12 +34,15 @@ uint64_t measure_scratch_bytes(const Graph& g) {
     }
     s += (uint64_t)numel(g.nodes[n].out_shape) * isz + 256;
     // a fused launch also reads R (the output's shape) and a bias [N], or
-    // (a residual Add and its normalisation) the norm's constants
+    // (a residual Add and its normalisation) the norm's constants and
+    // writes a second output (a stored sum)
     if (g.nodes[n].op == FLUID_OP_MATMUL)
       s += (uint64_t)numel(g.nodes[n].out_shape) * isz + 256 + (uint64_t)g.nodes[n].out_shape.back() * isz + 256;
-    if (g.nodes[n].op == FLUID_OP_ADD && n + 1 < g.n_nodes())
+    if (g.nodes[n].op == FLUID_OP_ADD && n + 1 < g.n_nodes()) {
       for (int v : g.nodes[n + 1].ins)
         if (v < 0) s += (uint64_t)numel(g.consts[~v].shape) * dtype_bytes(g.consts[~v].dtype) + 256;
+      s += (uint64_t)numel(g.nodes[n].out_shape) * isz + 256;
+    }
     // the copies of a constant weight the timed launches rotate over
     const Node& nd = g.nodes[n];
     if ((nd.op == FLUID_OP_MATMUL || nd.op == FLUID_OP_CONV) && nd.ins.size() > 1 && nd.ins[1] < 0) {
@@ -270,12 +273,12 @@ fluid_status fluid_run_schedule(const fluid_graph* gh, const fluid_layout_plan* 
     std::string all;
     int32_t L = 0;
     // a prepared launch performs its node and the fuse_n nodes after it, and
-    // writes the output of the last of them
+    // writes the output of the last of them (and a residual sum it stores)
     auto claim = [&](size_t i, int32_t l) {
       const PreparedNode& pn = P->nodes[i];
       for (int f = 0; f <= pn.fuse_n; ++f) {
         launch[P->nodes[i + f].node] = l;
-        written[P->nodes[i + f].node] = f == pn.fuse_n ? 1 : 0;
+        written[P->nodes[i + f].node] = f == pn.fuse_n || (f == 0 && pn.fstore) ? 1 : 0;
       }
     };
     for (size_t i = 0; i < P->nodes.size(); ++i) {

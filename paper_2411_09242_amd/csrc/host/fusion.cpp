@@ -13,12 +13,14 @@ std::vector<ChainStep> norm_chain(const Graph& g, int m) {
   for (int e : nd.ins)
     if (g.edge_shape(e) != nd.out_shape) return {};
   const int cur = g.out_edge(m), n = m + 1;
-  if (n >= g.n_nodes() || g.is_output[cur] || g.readers[cur].size() != 1 || g.readers[cur][0] != n) return {};
+  const auto& rd = g.readers[cur];
+  if (n >= g.n_nodes() || g.is_output[cur] || std::find(rd.begin(), rd.end(), n) == rd.end()) return {};
   const Node& x = g.nodes[n];
   if ((x.op != FLUID_OP_LAYERNORM && x.op != FLUID_OP_RMSNORM) || x.ins[0] != cur) return {};
   for (size_t i = 1; i < x.ins.size(); ++i)
     if (x.ins[i] >= 0) return {};
-  return {{n, CH_NORM, -1, -1}};
+  const bool alone = std::all_of(rd.begin(), rd.end(), [&](int r) { return r == n; });
+  return {{n, alone ? CH_NORM : CH_NORM_STORE, -1, -1}};
 }
 
 }  // namespace
@@ -59,6 +61,22 @@ std::vector<ChainStep> chain_steps(const Graph& g, int m) {
     cur = g.out_edge(n);
   }
   return steps;
+}
+
+std::vector<int> stored_edges(const Graph& g, int m, int t) {
+  const auto steps = chain_steps(g, m);
+  if (t >= 1 && !steps.empty() && steps[0].kind == CH_NORM_STORE) return {g.out_edge(m)};
+  return {};
+}
+
+std::vector<int> on_chip_edges(const Graph& g, int m, int t) {
+  const std::vector<int> st = stored_edges(g, m, t);
+  std::vector<int> out;
+  for (int i = 0; i < t; ++i) {
+    const int e = g.out_edge(m + i);
+    if (std::find(st.begin(), st.end(), e) == st.end()) out.push_back(e);
+  }
+  return out;
 }
 
 std::vector<int> chain_slots(const Graph& g, int m, int t) {

@@ -78,6 +78,7 @@ struct RedParams {
   int32_t ris1[kMaxDims];     // the second summand's strides (RED_SUM_*)
   int32_t irs1;
   const void* x1;
+  void* h;                    // RED_SUM_*: the sum's own output (y's layout), or null
   const void* x;
   void* y;
   const void* gamma;

@@ -10,6 +10,7 @@
 // after those buffers ("increase and allocate the last free block").
 #include <algorithm>
 
+#include "fusion.h"
 #include "layouts.h"
 #include "planner.h"
 
@@ -39,7 +40,8 @@ Buffers collect(const Graph& g, const std::vector<Perm>& perm, uint64_t align, c
   const int E = g.n_edges();
   B.root.resize(E);
   for (int e = 0; e < E; ++e) B.root[e] = e;
-  // fused chains: results kept on chip, operands read until the chain's end
+  // fused chains: results kept on chip (a stored one is an ordinary buffer),
+  // operands read until the chain's end
   std::vector<char> on_chip(E, 0);
   std::vector<int> until = until_in;
   if (!fuse.empty()) {
@@ -49,7 +51,7 @@ Buffers collect(const Graph& g, const std::vector<Perm>& perm, uint64_t align, c
     }
     for (int m = 0; m < g.n_nodes(); ++m)
       if (fuse[m]) {
-        for (int i = 0; i < fuse[m]; ++i) on_chip[g.out_edge(m + i)] = 1;
+        for (int e : on_chip_edges(g, m, fuse[m])) on_chip[e] = 1;
         until[m] = std::max(until[m], m + fuse[m]);
       }
   }

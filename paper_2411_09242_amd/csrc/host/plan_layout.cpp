@@ -222,7 +222,27 @@ struct Planner {
     return out;
   }
 
-  // the fused launch of steps j .. j+tt as one virtual node
+  // The index in L(e_store) of the permutation L(e_out)[b] -- the layout a
+  // chain's stored intermediate takes when the chain's output takes b --
+  // or -1 when e_store has no such candidate.
+  int store_index(int e_store, int e_out, int b) const {
+    const auto& ls = t.L[e_store];
+    auto it = std::find(ls.begin(), ls.end(), t.L[e_out][b]);
+    return it == ls.end() ? -1 : (int)(it - ls.begin());
+  }
+
+  // whether every intermediate the chain (m, tt) stores has the layout of
+  // the chain's output under lay
+  bool chain_layouts_ok(int m, int tt, const std::vector<int>& lay) const {
+    const int eo = g.out_edge(m + tt);
+    for (int e : stored_edges(g, m, tt))
+      if (lay[e] != store_index(e, eo, lay[eo])) return false;
+    return true;
+  }
+
+  // the fused launch of steps j .. j+tt as one virtual node; an output
+  // layout b that a stored intermediate cannot take (no such candidate, or
+  // fixed otherwise) is infeasible
   Gain fused_gain(const PathInfo& info, size_t j, int tt, const Fix& F) const {
     const int m = info.path[j];
     const std::vector<int> slots = chain_slots(g, m, tt);
@@ -232,7 +252,19 @@ struct Planner {
     for (int e : slots)
       if (e != ce && std::find(be.begin(), be.end(), e) == be.end()) be.push_back(e);
     const NodeCost& nc = t.fused.at({m, tt});
-    return gain(slots, ce, be, g.out_edge(m + tt), nc, use_v0 ? nc.v0 : nc.best, F);
+    const int eo = g.out_edge(m + tt);
+    Gain r = gain(slots, ce, be, eo, nc, use_v0 ? nc.v0 : nc.best, F);
+    for (int e : stored_edges(g, m, tt))
+      for (int b = 0; b < r.Bn; ++b) {
+        const int k = store_index(e, eo, b);
+        auto it = F.find(e);
+        if (k >= 0 && (it == F.end() || it->second == k)) continue;
+        for (int a = 0; a < r.A; ++a) {
+          r.G[(size_t)a * r.Bn + b] = kInf;
+          r.arg[(size_t)a * r.Bn + b] = -1;
+        }
+      }
+    return r;
   }
 
   struct DP {
@@ -326,6 +358,11 @@ struct Planner {
           auto it = chosen.find(e);
           if (it != chosen.end()) r.betas[k][e] = it->second;
         }
+      if (tt) {  // an intermediate the launch stores takes the output's layout
+        const int m0 = info.path[s];
+        for (int e : stored_edges(g, m0, tt))
+          r.states[s + (g.producer(e) - m0)] = store_index(e, g.out_edge(m0 + tt), b);
+      }
       r.fused[s] = tt;
       j = s - 1;
       b = a;
@@ -349,7 +386,9 @@ struct Planner {
       if (tt) {
         const NodeCost& nc = t.fused.at({n, tt});
         const auto& C = use_v0 ? nc.v0 : nc.best;
-        total = sat_add(total, C[flat_of(nc, chain_slots(g, n, tt), g.out_edge(n + tt), lay)]);
+        total = sat_add(total, chain_layouts_ok(n, tt, lay)
+                                   ? C[flat_of(nc, chain_slots(g, n, tt), g.out_edge(n + tt), lay)]
+                                   : kInf);
         n += tt + 1;
         continue;
       }
@@ -373,6 +412,7 @@ struct Planner {
       for (int tt = 1;; ++tt) {
         auto it = t.fused.find({n, tt});
         if (it == t.fused.end()) break;
+        if (!chain_layouts_ok(n, tt, lay)) continue;
         const NodeCost& nc = it->second;
         const auto& C = use_v0 ? nc.v0 : nc.best;
         const int64_t c = sat_add(C[flat_of(nc, chain_slots(g, n, tt), g.out_edge(n + tt), lay)], f[n + tt + 1]);

@@ -3,6 +3,7 @@
 #include <algorithm>
 #include <string>
 
+#include "fusion.h"
 #include "handles.h"
 #include "layouts.h"
 
@@ -155,6 +156,11 @@ void fuse_norm(const Graph& g, const LayoutPlan& lp, PreparedNode& h, PreparedNo
   ops[0] = h.ops[0];
   NodeKernel kf = prepare_sum_norm(xn, lp.variant[h.node], g.dtype, ops, h.ops[1], nx_out);
   if (!kf.available) return;
+  // a sum with further readers is stored with the normalisation's offsets:
+  // the plan gives it the layout of the normalisation's output
+  const bool store = !stored_edges(g, h.node, 1).empty();
+  if (store && dense_strides(g.nodes[h.node].out_shape, lp.perm[g.out_edge(h.node)]) != nx_out.stride) return;
+  h.fstore = store;
   h.kf = kf;
   h.fuse_n = 1;
   h.fout = nx.out;

@@ -34,12 +34,14 @@ struct PreparedNode {
   // another tensor) and writes the last one's output (fout) directly; those
   // nodes are then not launched by fluid_run.  A residual Add that heads a
   // planned chain is instead performed by the LayerNorm / RMSNorm after it
-  // (kf a RED_SUM_* reduction, fuse_n 1).
+  // (kf a RED_SUM_* reduction, fuse_n 1); when the sum has further readers
+  // that launch also stores it at out (fstore), in the layout of fout.
   int fuse_n = 0;
   NodeKernel kf;
   Bind fout;
   int fbias = -1;           // constant id of the bias, -1 when none
   int fgamma = -1, fbeta = -1;  // a summed normalisation's scale / shift constants
+  bool fstore = false;          // the summed normalisation also stores the sum
   Bind fr;                  // the other tensor of the Add / Mul (kf.gemm.rop set)
   int fr_edge = -1;         // its edge
   // Grouped launch: this product also launches the products of these nodes

@@ -240,3 +240,44 @@ def test_priced_fusion_chains_run_to_parity(arch, dtype, seed, tmp_path):
             ex.run_nodes(bad)
     torch.cuda.synchronize()
     assert torch.equal(ex.outputs[0], before)
+
+
+@pytest.mark.parametrize("arch,dtype", [("pre_ln", "f32"), ("llama", "bf16")])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_stored_residual_sums_run_to_parity(arch, dtype, seed, tmp_path):
+    """Pre-norm stacks with residual-norm chains priced well below their
+    nodes (and MatMul chains, which compete for the same Adds, well above):
+    the plan fuses residual sums that the next residual reads too, each
+    launch storing the sum in the norm output's layout, and the run matches
+    the oracle; fluid_run_nodes replays it bit for bit."""
+    import torch
+    from oracle import fusion
+    from paper_2411_09242_amd import fluid as F
+    from tables import add_fused, synthetic_table, write_table
+    cfg = synth_inputs.config(1, arch=arch, dtype=dtype, layers=2, batch=2, seq=37, hidden=72, heads=3, ffn=100)
+    og = OG.build_transformer(cfg)
+    x, consts = synth_inputs.make_inputs(cfg, og.const_specs(), 21 + seed)
+    (ref,) = execute.run_canonical(og, [x], consts)
+    tab = synthetic_table(og, seed=seed, mode="random", lo=50, hi=100, n_variants=1)
+    add_fused(tab, og, seed, n_variants=2, lo=1, hi=20)
+    for fs in tab["fused_sigs"]:
+        for ent in fs["entries"]:
+            ent[2][0] = -1
+            if fs["op"] == "matmul":
+                ent[2] = [c * 50 if c > 0 else c for c in ent[2]]
+    path = write_table(tab, tmp_path / "t.json")
+    out, g, lp, ap, _ = _device_run(cfg, x, consts, table=lambda gg: F.CostTable.load(str(path), gg))
+    stored = [(m, t) for m, t in enumerate(lp.fuse) if t and fusion.stored_edges(og, m, t)]
+    assert stored
+    for m, t in stored:
+        (e,) = fusion.stored_edges(og, m, t)
+        assert ap.offset[e] >= 0 and lp.perm(e) == lp.perm(og.out_edge(m + t))
+    say(f"{arch} {dtype} seed {seed}: stored sums at {stored}")
+    assert_close(out, ref, dtype, f"{arch} {dtype} stored residual sums")
+    ex = F.Executor(g, lp, ap, consts, [x])
+    want = ex.run()[0].clone()
+    torch.cuda.synchronize()
+    ex.outputs[0].fill_(float("nan"))
+    ex.run_nodes([n for n in range(g.n_nodes) if lp.variant[n] != -1])
+    torch.cuda.synchronize()
+    assert torch.equal(ex.outputs[0], want)

@@ -494,9 +494,11 @@ def test_norm_layouts_and_variants(dtype, op, shape, tmp_path):
             _check(og, {a: L[ia], n: L[ib]}, {1: v}, tmp_path, seed=ia + 3 * ib, scale=2.0)
 
 
-def sum_norm_graph(B, S, H, dtype, op):
+def sum_norm_graph(B, S, H, dtype, op, store=False):
     """x -> a = GELU(x), b = SiLU(x); s = a + b; n = norm(s); y = GELU(n):
-    the residual Add (node 2) and its normalisation (node 3) form a chain."""
+    the residual Add (node 2) and its normalisation (node 3) form a chain.
+    With store, y = GELU(n) + s: the sum has a second reader (the pre-norm
+    residual), so the chain's launch stores it."""
     g = Graph(dtype=dtype)
     x = g.add_input((B, S, H))
     a = g.add_node("gelu", [x], (B, S, H))
@@ -509,6 +511,8 @@ def sum_norm_graph(B, S, H, dtype, op):
     else:
         n = g.add_node("rmsnorm", [sm, gm], (B, S, H), fattr=1e-5)
     y = g.add_node("gelu", [n], (B, S, H))
+    if store:
+        y = g.add_node("add", [y, sm], (B, S, H))
     g.outputs = [y]
     return g, a, b, sm, n
 
@@ -541,6 +545,36 @@ def test_residual_norm_one_launch(dtype, op, shape, tmp_path):
             assert ap.offset[sm] == -1
             assert lp.kernel(2).startswith("add_" + op)
             assert_close(out, ref, dtype, f"sum-{op} v{v} {L[ia]} {L[ib]} {L[io]}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("op", ["layernorm", "rmsnorm"])
+@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (2, 5, 1024), (1, 3, 4096)], ids=str)
+def test_stored_residual_norm_one_launch(dtype, op, shape, tmp_path):
+    """The sum of a residual-norm chain with a second reader (a pre-norm
+    block's next residual): the one launch also stores the sum, in the norm
+    output's layout, and normalises the stored (rounded) values -- the
+    oracle rounds the sum like any stored tensor."""
+    og, a, b, sm, n = sum_norm_graph(*shape, dtype, op, store=True)
+    L = layouts.layout_list(shape)
+    combos = [(0, 0, 0)] + [(i, (5 * i + 1) % len(L), (2 * i + 3) % len(L)) for i in range(1, min(len(L), 4))]
+    for ia, ib, io in combos:
+        for v in (0, 1, 2):
+            if v == 2 and not row_block_ok(shape, dtype, L[ia], L[ib], L[io]):
+                continue
+            say(f"stored sum-{op} {dtype} {shape} v{v} {L[ia]} {L[ib]} -> {L[io]}")
+            xs, cs = random_inputs(og, ia + 7 * ib + io, 2.0)
+            (ref,) = execute.run_canonical(og, xs, cs)
+            obj = forced_table(og, {a: L[ia], b: L[ib], sm: L[io], n: L[io]}, {3: v})
+            obj["fused_sigs"] = [{"op": "add", "in_shapes": [list(shape)] * 2, "out_shape": list(shape),
+                                  "entries": [[[list(L[ia]), list(L[ib])], list(L[io]),
+                                               [1 if w == v else -1 for w in range(3)]]]}]
+            obj["fused"] = [[2, 1, 0]]
+            (out,), lp, ap = run_device(og, obj, xs, cs, tmp_path)
+            assert lp.fusion_priced and lp.fuse[2] == 1 and lp.variant[2] == v and lp.variant[3] == -2
+            assert ap.offset[sm] >= 0 and lp.perm(sm) == lp.perm(n)
+            assert lp.kernel(2).startswith("add_" + op)
+            assert_close(out, ref, dtype, f"stored sum-{op} v{v} {L[ia]} {L[ib]} {L[io]}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

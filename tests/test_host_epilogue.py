@@ -7,7 +7,7 @@ import pytest
 
 import synth_inputs
 from gpu_util import forced_table
-from oracle import graph as OG, plan_arena as PA
+from oracle import fusion, graph as OG, plan_arena as PA
 from paper_2411_09242_amd import fluid as F
 from tables import synthetic_table, write_table
 from test_gpu_ops import EPILOGUES, epilogue_graph, fusable_steps
@@ -142,9 +142,10 @@ def test_epilogue_arena_on_transformers(cfg, seed, tmp_path):
 @pytest.mark.parametrize("seed", [0, 1])
 def test_priced_fusions_are_the_launches(cfg, seed, tmp_path):
     """A table that prices fusion chains: the run performs exactly the chains
-    the layout DP chose -- each in one launch that stores only the chain's
-    last output, the intermediates without an arena buffer -- and no other
-    fusion; without pricing (FLUID_NO_FUSION) the epilogue fusion by
+    the layout DP chose -- each in one launch that stores the chain's last
+    output and the intermediates with further readers (a pre-norm block's
+    residual sum, in the layout of the chain's output), the others without
+    an arena buffer -- and no other fusion; without pricing (FLUID_NO_FUSION) the epilogue fusion by
     adjacency is back."""
     from tables import add_fused
     og = OG.build_transformer(cfg)
@@ -171,8 +172,12 @@ def test_priced_fusions_are_the_launches(cfg, seed, tmp_path):
         covered.update(chain)
         assert all(lp.variant[k] == -2 and kernels[k] == "fused" for k in chain[1:])
         assert {launch[k] for k in chain} == {launch[m]}
-        assert not any(written[k] for k in chain[:-1]) and written[chain[-1]]
-        assert all(ap.offset[og.out_edge(k)] == -1 for k in chain[:-1])
+        stored = fusion.stored_edges(og, m, t)
+        assert written[chain[-1]]
+        assert all(bool(written[k]) == (og.out_edge(k) in stored) for k in chain[:-1])
+        assert all((ap.offset[og.out_edge(k)] >= 0) == (og.out_edge(k) in stored) for k in chain[:-1])
+        for e in stored:
+            assert lp.perm(e) == lp.perm(og.out_edge(m + t))
         if og.nodes[m].op == "matmul":
             assert "_e" in names[launch[m]]
         else:

@@ -13,7 +13,7 @@ from oracle import costtable, graph as OG, layouts, plan_arena as PA, plan_layou
 from paper_2411_09242_amd import fluid as F
 from plan_check import assert_plans_match_oracle
 from tables import add_fused, fanout_costs, rank2_table, synthetic_table, write_table
-from tinygraphs import chain_graph, diamond_graph, fanout_graph, ffn_block, mlp_graph, t1_graph, t2_graph
+from tinygraphs import chain_graph, diamond_graph, fanout_graph, ffn_block, mlp_graph, prenorm_graph, t1_graph, t2_graph
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -170,7 +170,7 @@ def test_planner_parity_guard_branches(infeasible, flags, tmp_path):
         assert lp.layout_idx == [0] * og.n_edges
 
 
-FUSE_GRAPHS = [lambda: mlp_graph(2), lambda: mlp_graph(3), ffn_block, t1_graph]
+FUSE_GRAPHS = [lambda: mlp_graph(2), lambda: mlp_graph(3), ffn_block, t1_graph, prenorm_graph]
 
 
 @pytest.mark.parametrize("gi", range(len(FUSE_GRAPHS)))
@@ -190,6 +190,26 @@ def test_planner_parity_fused_config_graphs(idx, tmp_path):
     obj = add_fused(synthetic_table(og, seed=idx, mode="random"), og, idx, lo=1, hi=1500)
     lp = _compare_plans(og, obj, tmp_path)
     assert any(lp.fuse)
+
+
+@pytest.mark.parametrize("arch", ["pre_ln", "llama"])
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("flags", [0, PL.NO_GUARD])
+def test_planner_parity_stored_sums(arch, seed, flags, tmp_path):
+    """Pre-norm stacks, whose residual sums have a second reader: with
+    residual-norm chains priced well below their nodes, both planners fuse
+    the same sums (stored by the norm's launch in the norm output's layout),
+    with the same layouts, variants and arena."""
+    from oracle import fusion
+    cfg = synth_inputs.config(1, arch=arch, layers=2, batch=2, seq=5, hidden=8, heads=2, ffn=8)
+    og = OG.build_transformer(cfg)
+    obj = add_fused(synthetic_table(og, seed=seed, mode="random", lo=50, hi=100), og, seed, lo=1, hi=20)
+    for fs in obj["fused_sigs"]:
+        if fs["op"] == "matmul":
+            for ent in fs["entries"]:
+                ent[2] = [c * 50 for c in ent[2]]
+    lp = _compare_plans(og, obj, tmp_path, flags)
+    assert any(t and fusion.stored_edges(og, m, t) for m, t in enumerate(lp.fuse))
 
 
 def test_ragged_config_parity(tmp_path):
