@@ -29,13 +29,11 @@ template <>
 struct Elem<float> {
   __device__ static __forceinline__ float load(const void* p, int64_t i) { return ((const float*)p)[i]; }
   __device__ static __forceinline__ void store(void* p, int64_t i, float v) { ((float*)p)[i] = v; }
-  __device__ static __forceinline__ float round(float v) { return v; }
 };
 template <>
 struct Elem<uint16_t> {
   __device__ static __forceinline__ float load(const void* p, int64_t i) { return bf16_to_f32(((const uint16_t*)p)[i]); }
   __device__ static __forceinline__ void store(void* p, int64_t i, float v) { ((uint16_t*)p)[i] = f32_to_bf16(v); }
-  __device__ static __forceinline__ float round(float v) { return bf16_to_f32(f32_to_bf16(v)); }
 };
 
 __device__ __forceinline__ float load_any(const void* p, int64_t i, int dt) {

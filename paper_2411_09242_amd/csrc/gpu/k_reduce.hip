@@ -27,6 +27,13 @@
 
 namespace fluid {
 
+// v rounded to the storage type T (a stored sum is normalised as stored)
+template <typename T>
+__device__ __forceinline__ float round_to(float v) {
+  if constexpr (sizeof(T) == 2) return bf16_to_f32(f32_to_bf16(v));
+  else return v;
+}
+
 __device__ __forceinline__ void row_offsets(const RedParams& p, uint32_t row, int32_t& io, int32_t& oo, int32_t& io1,
                                             uint32_t& qi) {
   io = 0; oo = 0; io1 = 0; qi = 0;
@@ -69,7 +76,7 @@ __global__ __launch_bounds__(256) void red_row_kernel(RedParams p) {
 #pragma unroll
       for (int j = 0; j < NPL; ++j) {
         const uint32_t k = (uint32_t)lane + 64u * j;
-        v[j] = Elem<T>::round(v[j]);
+        v[j] = round_to<T>(v[j]);
         if (k < R) Elem<T>::store(p.h, oo + (int32_t)k * p.ors, v[j]);
       }
     }
@@ -444,7 +451,7 @@ __global__ __launch_bounds__(256) void red_col_kernel(RedParams p) {
     float a = Elem<T>::load(p.x, io + (int32_t)k * p.irs);
     if constexpr (SUM) {
       a += Elem<T>::load(p.x1, io1 + (int32_t)k * p.irs1);
-      if (p.h) a = Elem<T>::round(a);
+      if (p.h) a = round_to<T>(a);
     }
     return a;
   };
@@ -589,7 +596,7 @@ __global__ __launch_bounds__(1024) void red_colb_kernel(RedParams p) {
       const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(p.h, 0, 0x7fffffff, 0x00020000);
 #pragma unroll
       for (int j = 0; j < KPL; ++j) {
-        v[j] = Elem<T>::round(v[j]);
+        v[j] = round_to<T>(v[j]);
         const uint32_t vo = !masked || kl + KQ * j < R ? yo : OOB;
         const uint32_t so = (kb + (uint32_t)(KQ * j)) * ystep;
         if constexpr (ES == 4) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v[j]), rh, vo, so, 0);
