@@ -482,8 +482,10 @@ def norm_graph(B, S, H, dtype, op):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("op", ["layernorm", "rmsnorm"])
-@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (1, 8, 768), (2, 5, 1024), (1, 5, 3000), (1, 3, 4096)], ids=str)
+@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (1, 8, 768), (2, 5, 1024), (1, 5, 3000), (1, 3, 4096),
+                                   (2, 32, 96), (1, 48, 1024), (2, 8, 2048)], ids=str)
 def test_norm_layouts_and_variants(dtype, op, shape, tmp_path):
+    """Every pair of input / output layouts and every variant."""
     og, a, n = norm_graph(*shape, dtype, op)
     L = layouts.layout_list(shape)
     for ia, ib in itertools.product(range(len(L)), range(len(L))):
@@ -519,7 +521,8 @@ def sum_norm_graph(B, S, H, dtype, op, store=False):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("op", ["layernorm", "rmsnorm"])
-@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (1, 8, 768), (2, 5, 1024), (1, 3, 4096)], ids=str)
+@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (1, 8, 768), (2, 5, 1024), (1, 3, 4096), (2, 32, 1024),
+                                   (1, 8, 4096)], ids=str)
 def test_residual_norm_one_launch(dtype, op, shape, tmp_path):
     """A residual Add and the LayerNorm / RMSNorm of its sum as one planned
     launch (a table that prices the chain below the two nodes): both
@@ -549,7 +552,7 @@ def test_residual_norm_one_launch(dtype, op, shape, tmp_path):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("op", ["layernorm", "rmsnorm"])
-@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (2, 5, 1024), (1, 3, 4096)], ids=str)
+@pytest.mark.parametrize("shape", [(1, 37, 64), (2, 19, 130), (2, 5, 1024), (1, 3, 4096), (2, 32, 1024)], ids=str)
 def test_stored_residual_norm_one_launch(dtype, op, shape, tmp_path):
     """The sum of a residual-norm chain with a second reader (a pre-norm
     block's next residual): the one launch also stores the sum, in the norm
