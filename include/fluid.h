@@ -195,11 +195,13 @@ fluid_status fluid_measure_scratch_bytes(const fluid_graph* g, uint64_t* bytes);
 
 /* Measures the cost table on the GPU (Alg. 3's eval: real kernel time).
  * For every operator signature, every candidate layout combination and
- * every kernel variant: one warm-up launch timed on its own (a combination
- * more than 8x slower than the best so far of its signature keeps that
- * time), then three batches of `reps` back-to-back launches, each batch
- * between two HIP events; the cost is the median per-launch time of the
- * batches, rounded to integer nanoseconds.  Successive launches of a
+ * every kernel variant: one untimed warm-up launch, one launch timed on its
+ * own (a combination more than 8x slower than the best so far of its
+ * signature keeps that time), then `reps` back-to-back launches captured
+ * once as a HIP graph and replayed three times, each replay between two
+ * HIP events, on a stream of the library's own (launches issued as a run's
+ * graph issues them, without the host's per-launch cost); the cost is the
+ * median per-launch time of the replays, rounded to integer nanoseconds.  Successive launches of a
  * MatMul or Conv with a constant weight read it from rotating copies that
  * total at least 512 MiB (at most 64 copies), so that each launch fetches
  * its weight from HBM, as in a run.  Fusion chains get entries measured
@@ -208,8 +210,8 @@ fluid_status fluid_measure_scratch_bytes(const fluid_graph* g, uint64_t* bytes);
  * dimension permutations (deduplicated), trimmed for tensors with more than
  * six candidates to those whose innermost dim is one of the last two
  * logical dims.  scratch: caller device memory of at least
- * fluid_measure_scratch_bytes, 256-B aligned; its contents are overwritten.
- * Synchronises hip_stream.  GPU build only. */
+ * fluid_measure_scratch_bytes, 256-B aligned; its contents are overwritten
+ * (filled on hip_stream, which is then synchronised).  GPU build only. */
 fluid_status fluid_measure_costs(const fluid_graph* g, uint32_t reps, void* scratch,
                                  uint64_t scratch_bytes, void* hip_stream, fluid_cost_table** out);
 

@@ -468,8 +468,16 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
     const uint64_t need = measure_scratch_bytes(g);
     require(scratch && aligned(scratch, 256), "fluid_measure_costs: scratch must be non-NULL and 256-byte aligned");
     require(scratch_bytes >= need, "fluid_measure_costs: scratch needs " + std::to_string(need) + " bytes");
-    hipStream_t s = (hipStream_t)hip_stream;
-    hip_check(launch_fill(scratch, scratch_bytes, 12345u, s), "fill");
+    hip_check(launch_fill(scratch, scratch_bytes, 12345u, (hipStream_t)hip_stream), "fill");
+    hip_check(hipStreamSynchronize((hipStream_t)hip_stream), "hipStreamSynchronize");
+    // a stream of its own (default priority), which the timed batches are
+    // captured from: the caller's may be the null stream
+    hipStream_t s = nullptr;
+    hip_check(hipStreamCreateWithFlags(&s, hipStreamNonBlocking), "hipStreamCreateWithFlags");
+    struct StreamGuard {
+      hipStream_t s;
+      ~StreamGuard() { (void)hipStreamSynchronize(s); (void)hipStreamDestroy(s); }
+    } sg{s};
 
     CostTable t;
     for (int e = 0; e < g.n_edges(); ++e)
@@ -519,11 +527,14 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
     // one candidate: an untimed warm-up launch (the first launch of a kernel
     // instance also loads its code, which can take milliseconds), then one
     // launch timed on its own -- clearly losing candidates (over 8x the
-    // signature's best so far) get no more launches -- then three batches
-    // of R back-to-back launches between two events (the per-launch time
-    // includes the kernel's start-up and the gap to the next launch, as in
-    // a run); the median, in integer ns.  Successive launches take the
-    // kernels of ks in turn (copies of a constant weight, cold_weight_copies).
+    // signature's best so far) get no more launches -- then R back-to-back
+    // launches captured once as a HIP graph and replayed three times, each
+    // replay between two events (the per-launch time includes the kernel's
+    // start-up and the gap to the next launch as a run's graph issues them,
+    // without the host's launch cost, which would pace kernels of a few
+    // microseconds); the median, in integer ns.  Successive launches take
+    // the kernels of ks in turn (copies of a constant weight,
+    // cold_weight_copies).
     auto time_kernel = [&](const std::vector<NodeKernel>& ks, int64_t& best_so_far) -> int64_t {
       size_t li = 0;
       auto next = [&]() -> const NodeKernel& { return ks[li++ % ks.size()]; };
@@ -538,9 +549,24 @@ fluid_status fluid_measure_costs(const fluid_graph* gh, uint32_t reps, void* scr
       const int64_t first_ns = (int64_t)std::llround((double)first * 1e6);
       if (!(best_so_far >= 0 && first_ns > 8 * best_so_far)) {
         times.clear();
+        struct GraphGuard {
+          hipGraph_t g = nullptr;
+          hipGraphExec_t x = nullptr;
+          ~GraphGuard() {
+            if (x) (void)hipGraphExecDestroy(x);
+            if (g) (void)hipGraphDestroy(g);
+          }
+        } gg;
+        hip_check(hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+        hipError_t le = hipSuccess;
+        for (uint32_t r = 0; r < R && le == hipSuccess; ++r) le = launch_node_kernel(next(), s);
+        const hipError_t ce = hipStreamEndCapture(s, &gg.g);
+        hip_check(le, "captured launch");
+        hip_check(ce, "hipStreamEndCapture");
+        hip_check(hipGraphInstantiate(&gg.x, gg.g, nullptr, nullptr, 0), "hipGraphInstantiate");
         for (int b = 0; b < 3; ++b) {
           hip_check(hipEventRecord(ev[2 + 2 * b], s), "hipEventRecord");
-          for (uint32_t r = 0; r < R; ++r) hip_check(launch_node_kernel(next(), s), "timed launch");
+          hip_check(hipGraphLaunch(gg.x, s), "hipGraphLaunch");
           hip_check(hipEventRecord(ev[3 + 2 * b], s), "hipEventRecord");
         }
         hip_check(hipEventSynchronize(ev[7]), "hipEventSynchronize");
