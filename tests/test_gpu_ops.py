@@ -21,10 +21,9 @@ pytestmark = pytest.mark.gpu
 def _check_gemm(og, want, variants, tmp_path, seed, dtype):
     """_check for a forced GEMM variant (tile = variant % 10; variants 10-19
     read the weight packed K-contiguous); the fp32 direct-load tiles (6, 7)
-    need unit-stride K or M/N operands, tile 8 (bf16 only) a K-contiguous A
-    and a K- or N-contiguous B, and tile 9 a K-contiguous A and B (bf16 also
-    an N-contiguous B) with K <= 128 (bf16) or 64 (fp32): they are skipped
-    where they cannot run."""
+    need unit-stride K or M/N operands, and tiles 8 and 9 (bf16 only) a
+    K-contiguous A and a K- or N-contiguous B (9 also K <= 128): they are
+    skipped where they cannot run."""
     try:
         return _check(og, want, variants, tmp_path, seed=seed)
     except Exception as ex:  # noqa: BLE001
