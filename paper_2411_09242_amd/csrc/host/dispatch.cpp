@@ -429,13 +429,15 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   // 256x128 with a three-stage ring, two workgroups per CU, 9: 128x128
   // persistent with the whole K (at most 128) in LDS;
   // fp32 6: 16x32 with K split over 8 wavefronts, 7: 32x32 over 4, operands
-  // loaded straight into MFMA registers
+  // loaded straight into MFMA registers, 8: 128x128 double-buffered in LDS
+  // with the next K-tile in flight in registers
   static const uint32_t TM[] = {128, 64, 32, 32, 64, 32, 256, 128, 256, 128};
   static const uint32_t TN[] = {128, 64, 32, 32, 32, 32, 128, 128, 128, 128};
   uint32_t tm = TM[tile], tn = TN[tile];
-  if (tile >= 8 && (k.dtype != DT_BF16 || k.amode != GM_K || (k.bmode != GM_K && k.bmode != GM_MN))) {
+  const bool f32 = k.dtype != DT_BF16;
+  if ((tile == 9 || (tile == 8 && !f32)) && (f32 || k.amode != GM_K || (k.bmode != GM_K && k.bmode != GM_MN))) {
     k.available = false;
-    k.why = "tiles 8 and 9 are bf16 with a K-contiguous A and a K- or N-contiguous B";
+    k.why = "bf16 tiles 8 and 9 need a K-contiguous A and a K- or N-contiguous B; tile 9 is bf16 only";
     return k;
   }
   if (tile == 9 && p.K > 128) {
@@ -443,9 +445,9 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
     k.why = "tile 9 holds the whole K (at most 128) in LDS";
     return k;
   }
-  if (tile >= 6 && k.dtype != DT_BF16) {
-    tm = tile == 6 ? 16 : 32;
-    tn = 32;
+  if (tile >= 6 && f32) {
+    tm = tile == 6 ? 16 : tile == 7 ? 32 : 128;
+    tn = tile == 8 ? 128 : 32;
     if ((k.amode != GM_K && k.amode != GM_MN) || (k.bmode != GM_K && k.bmode != GM_MN)) {
       k.available = false;
       k.why = "the direct-load tiles need unit-stride K or M/N operands";
@@ -622,7 +624,7 @@ std::string NodeKernel::name() const {
         return e.empty() ? e : "_e" + e;
       };
       static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "p256x128", "p128", "p256x128s3", "q128"};
-      static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4", "-", "-"};
+      static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4", "r128", "-"};
       return "gemm_" + dt + "_" + (dtype == DT_BF16 ? tiles : tiles_f32)[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
              (cmode == 1 ? "n" : cmode == 2 ? "m" : "g") + (gemm.causal ? "_causal" + std::to_string(gemm.causal) : "") +
              epi_suffix();

@@ -20,10 +20,10 @@ pytestmark = pytest.mark.gpu
 
 def _check_gemm(og, want, variants, tmp_path, seed, dtype):
     """_check for a forced GEMM variant (tile = variant % 10; variants 10-19
-    read the weight packed K-contiguous); the fp32 direct-load tiles (6, 7)
-    need unit-stride K or M/N operands, and tiles 8 and 9 (bf16 only) a
-    K-contiguous A and a K- or N-contiguous B (9 also K <= 128): they are
-    skipped where they cannot run."""
+    read the weight packed K-contiguous); the fp32 direct-load tiles (6, 7,
+    8) need unit-stride K or M/N operands, the bf16 tiles 8 and 9 (9 is bf16
+    only) a K-contiguous A and a K- or N-contiguous B (9 also K <= 128):
+    they are skipped where they cannot run."""
     try:
         return _check(og, want, variants, tmp_path, seed=seed)
     except Exception as ex:  # noqa: BLE001
@@ -149,9 +149,9 @@ def fusable_steps(chain, v, dtype):
     """How many of the chain's steps a MatMul of variant v absorbs when
     nothing else stops it: variant 9 (short-K attention products) and the
     bf16 variants 6 and 8 take a bias only; the Add / Mul with another tensor
-    is taken by variants 1-5, and by the fp32 variants 6-7."""
+    is taken by variants 1-5, and by the fp32 variants 6-8."""
     bias_only = v == 9 or (dtype == "bf16" and v in (6, 8))
-    rop = 1 <= v <= 5 or (dtype == "f32" and v in (6, 7))
+    rop = 1 <= v <= 5 or (dtype == "f32" and v in (6, 7, 8))
     n = 0
     for step in EPILOGUES[chain]:
         if step == "bias" or (step in ("gelu", "silu") and not bias_only) or (step.endswith("_r") and rop):
