@@ -731,7 +731,7 @@ hipError_t gemm_a(const NodeKernel& k, hipStream_t s) {
 hipError_t launch_gemm(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
   if ((uint64_t)p.tiles_m * p.tiles_n * p.G >= (1ull << 31)) return hipErrorInvalidValue;
-  if (k.gemm_tile == 8 && k.dtype == DT_F32) return launch_gemm_f32_ring(k, s);
+  if (k.gemm_tile >= 8 && k.dtype == DT_F32) return launch_gemm_f32_ring(k, s);
   if (k.gemm_tile >= 6) return k.dtype == DT_BF16 ? launch_gemm_bf16_pipe(k, s) : launch_gemm_f32_dl(k, s);
   if (k.gemm_tile >= 2) return k.dtype == DT_BF16 ? gemm_sk_dispatch<uint16_t>(k, s) : gemm_sk_dispatch<float>(k, s);
   return k.gemm_tile == 0 ? gemm_a<128>(k, s) : gemm_a<64>(k, s);

@@ -3,14 +3,16 @@
 // A[l%32][l/32], B[l/32][l%32]; accumulator v of lane l holds
 // C[8(v/4) + 4(l/32) + v%4][l%32]).
 //
-// Four wavefronts of 64 x 64 (2 x 2 blocks of 32 x 32): 64 MFMAs of 64
-// cycles per wavefront and K-tile, one barrier per K-tile.  Two LDS stages
+// W = 4 wavefronts of 64 x 64 (2 x 2 blocks of 32 x 32; 64 MFMAs of 64
+// cycles per wavefront and K-tile) or W = 8 of 64 x 32 (two wavefronts per
+// SIMD within one workgroup, for outputs with about one tile per CU); one
+// barrier per K-tile.  Two LDS stages
 // of 32 KiB; the operands of K-tile t+2 are loaded into registers (16 bytes
 // per load) while tile t is multiplied and are written to LDS once tile t+1
 // is in place, so a load has a whole K-tile of MFMAs to land.  Two
 // workgroups share a CU where the output has tiles for it; where it has
-// few (a 4096 x 1024 product has 256), one workgroup per CU still keeps
-// the matrix cores fed.
+// few (a 4096 x 1024 product has 256), the eight-wavefront form gives each
+// SIMD a second wavefront to issue from while one waits.
 //
 // Each operand is staged in its HBM orientation:
 //  * K-contiguous (A [m][k], B [n][k]): rows of 32 floats (8 chunks of 16
@@ -20,7 +22,7 @@
 //  * M- or N-contiguous (A [k][m], B [k][n]): rows of 128 floats per k;
 //    row k keeps chunk c at c ^ 8 (k % 2), so that the two k of one read
 //    fall on disjoint banks.
-// Load q (0..3) of wavefront w carries the 1 KiB block 4 q + w of a stage,
+// Load q (0 .. 16/W - 1) of wavefront w carries the 1 KiB block W q + w of a stage,
 // lane l its 16 bytes at l * 16, so the LDS writes are contiguous and the
 // swizzle is applied by choosing which chunk each lane fetches.
 #include "gemm_common.h"
@@ -39,8 +41,11 @@ __device__ __forceinline__ int mnrow_swz(int k) { return (k & 1) << 3; }
 
 }  // namespace
 
-template <bool AK, bool BK, bool RES>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_f32_ring_kernel(GemmParams p) {
+template <int W, bool AK, bool BK, bool RES>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W / 2))) void gemm_f32_ring_kernel(GemmParams p) {
+  constexpr int NQ = 16 / W;          // 1 KiB blocks per operand, stage and wavefront
+  constexpr int WN = W / 2;           // wavefronts along N
+  constexpr int JN = 128 / WN / 32;   // 32-wide MFMA blocks per wavefront along N
   __shared__ __attribute__((aligned(1024))) uint8_t As[2][FR_STAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t Bs[2][FR_STAGE];
   const TileCoord tc = tile_coord(p, FR_T, FR_T);
@@ -50,7 +55,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   const uint32_t kend = (p.causal & 2u) ? min(p.K, tc.m0 + FR_T) : p.K;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int lr = lane & 31, lh = lane >> 5;
   const Rsrc ra = make_rsrc(p.A, p.a_bytes);
   const Rsrc rb = make_rsrc(p.B, p.b_bytes);
@@ -58,11 +63,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   // Load sources: rows of A past M and of B past N are clamped onto row /
   // column 0 (they only feed outputs that are never stored); only k past K
   // has to read as zero.
-  int32_t a_off[4], b_off[4];  // element offset without the K-tile's k0
-  int a_k[4], b_k[4];          // the k (within the K-tile) the lane's piece starts at
+  int32_t a_off[NQ], b_off[NQ];  // element offset without the K-tile's k0
+  int a_k[NQ], b_k[NQ];          // the k (within the K-tile) the lane's piece starts at
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int blk = 4 * q + wave;
+  for (int q = 0; q < NQ; ++q) {
+    const int blk = W * q + wave;
     if constexpr (AK) {
       const int row = 8 * blk + (lane >> 3);
       const int c = (lane & 7) ^ krow_swz(row);
@@ -94,11 +99,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   const int32_t a_ks = AK ? 1 : p.a_k, b_ks = BK ? 1 : p.b_k;
 
   struct Regs {
-    uint4 a[4], b[4];
+    uint4 a[NQ], b[NQ];
   };
   auto gload = [&](Regs& R, uint32_t k0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < NQ; ++q) {
       const uint32_t ka = k0 + (uint32_t)a_k[q], kb = k0 + (uint32_t)b_k[q];
       R.a[q] = bload16(ra, ka < kend ? 4u * (uint32_t)(a_off[q] + (int32_t)k0 * a_ks) : kOOB);
       R.b[q] = bload16(rb, kb < kend ? 4u * (uint32_t)(b_off[q] + (int32_t)k0 * b_ks) : kOOB);
@@ -106,8 +111,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   };
   auto lstore = [&](const Regs& R, int st) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int blk = 4 * q + wave;
+    for (int q = 0; q < NQ; ++q) {
+      const int blk = W * q + wave;
       *(uint4*)(As[st] + blk * 1024 + lane * 16) = R.a[q];
       *(uint4*)(Bs[st] + blk * 1024 + lane * 16) = R.b[q];
     }
@@ -125,11 +130,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
     else return *(const float*)(s + k * 512 + (((n >> 2) ^ mnrow_swz(k)) << 4) + (n & 3) * 4);
   };
 
-  f32x16 acc[2][2];
+  f32x16 acc[2][JN];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < JN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
@@ -137,15 +142,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
 #pragma unroll
     for (int s = 0; s < FR_BK / 2; ++s) {
       const int k = 2 * s + lh;
-      float a[2], b[2];
+      float a[2], b[JN];
 #pragma unroll
       for (int i = 0; i < 2; ++i) a[i] = a_at(st, wm * 64 + 32 * i + lr, k);
 #pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = b_at(st, wn * 64 + 32 * j + lr, k);
+      for (int j = 0; j < JN; ++j) b[j] = b_at(st, wn * 32 * JN + 32 * j + lr, k);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < JN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
     }
   };
 
@@ -180,13 +185,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      epi16<RES>(p, tc.r_base, tc.m0 + wm * 64 + 32 * i + 4 * lh, tc.n0 + wn * 64 + 32 * j + lr, acc[i][j]);
+    for (int j = 0; j < JN; ++j)
+      epi16<RES>(p, tc.r_base, tc.m0 + wm * 64 + 32 * i + 4 * lh, tc.n0 + wn * 32 * JN + 32 * j + lr, acc[i][j]);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint32_t n = tc.n0 + wn * 64 + 32 * j + lr;
+    for (int j = 0; j < JN; ++j) {
+      const uint32_t n = tc.n0 + wn * 32 * JN + 32 * j + lr;
 #pragma unroll
       for (int vg = 0; vg < 4; ++vg) {
         const uint32_t mb = tc.m0 + wm * 64 + 32 * i + 8 * vg + 4 * lh;
@@ -205,15 +210,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
     }
 }
 
-hipError_t launch_gemm_f32_ring(const NodeKernel& k, hipStream_t s) {
+template <int W>
+hipError_t ring_go(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
-  if (k.dtype != DT_F32 || (k.amode != GM_K && k.amode != GM_MN) || (k.bmode != GM_K && k.bmode != GM_MN))
-    return hipErrorInvalidValue;
   const dim3 grid(p.tiles_m * p.tiles_n * p.G);
-#define FLUID_FR(AKv, BKv)                                                                          \
-  do {                                                                                              \
-    if (p.rop) hipLaunchKernelGGL((gemm_f32_ring_kernel<AKv, BKv, true>), grid, dim3(256), 0, s, p); \
-    else hipLaunchKernelGGL((gemm_f32_ring_kernel<AKv, BKv, false>), grid, dim3(256), 0, s, p);      \
+#define FLUID_FR(AKv, BKv)                                                                                  \
+  do {                                                                                                      \
+    if (p.rop) hipLaunchKernelGGL((gemm_f32_ring_kernel<W, AKv, BKv, true>), grid, dim3(64 * W), 0, s, p); \
+    else hipLaunchKernelGGL((gemm_f32_ring_kernel<W, AKv, BKv, false>), grid, dim3(64 * W), 0, s, p);      \
   } while (0)
   const bool ak = k.amode == GM_K, bk = k.bmode == GM_K;
   if (ak && bk) FLUID_FR(true, true);
@@ -222,6 +226,14 @@ hipError_t launch_gemm_f32_ring(const NodeKernel& k, hipStream_t s) {
   else FLUID_FR(false, false);
 #undef FLUID_FR
   return hipGetLastError();
+}
+
+// fp32 tile 8: four wavefronts; tile 9: eight
+hipError_t launch_gemm_f32_ring(const NodeKernel& k, hipStream_t s) {
+  if (k.dtype != DT_F32 || (k.amode != GM_K && k.amode != GM_MN) || (k.bmode != GM_K && k.bmode != GM_MN) ||
+      (k.gemm_tile != 8 && k.gemm_tile != 9))
+    return hipErrorInvalidValue;
+  return k.gemm_tile == 8 ? ring_go<4>(k, s) : ring_go<8>(k, s);
 }
 
 }  // namespace fluid

@@ -429,25 +429,26 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   // 256x128 with a three-stage ring, two workgroups per CU, 9: 128x128
   // persistent with the whole K (at most 128) in LDS;
   // fp32 6: 16x32 with K split over 8 wavefronts, 7: 32x32 over 4, operands
-  // loaded straight into MFMA registers, 8: 128x128 double-buffered in LDS
-  // with the next K-tile in flight in registers
+  // loaded straight into MFMA registers, 8 and 9: 128x128 double-buffered
+  // in LDS with the next K-tile in flight in registers, over four or eight
+  // wavefronts
   static const uint32_t TM[] = {128, 64, 32, 32, 64, 32, 256, 128, 256, 128};
   static const uint32_t TN[] = {128, 64, 32, 32, 32, 32, 128, 128, 128, 128};
   uint32_t tm = TM[tile], tn = TN[tile];
   const bool f32 = k.dtype != DT_BF16;
-  if ((tile == 9 || (tile == 8 && !f32)) && (f32 || k.amode != GM_K || (k.bmode != GM_K && k.bmode != GM_MN))) {
+  if (tile >= 8 && !f32 && (k.amode != GM_K || (k.bmode != GM_K && k.bmode != GM_MN))) {
     k.available = false;
-    k.why = "bf16 tiles 8 and 9 need a K-contiguous A and a K- or N-contiguous B; tile 9 is bf16 only";
+    k.why = "bf16 tiles 8 and 9 need a K-contiguous A and a K- or N-contiguous B";
     return k;
   }
-  if (tile == 9 && p.K > 128) {
+  if (tile == 9 && !f32 && p.K > 128) {
     k.available = false;
     k.why = "tile 9 holds the whole K (at most 128) in LDS";
     return k;
   }
   if (tile >= 6 && f32) {
     tm = tile == 6 ? 16 : tile == 7 ? 32 : 128;
-    tn = tile == 8 ? 128 : 32;
+    tn = tile >= 8 ? 128 : 32;
     if ((k.amode != GM_K && k.amode != GM_MN) || (k.bmode != GM_K && k.bmode != GM_MN)) {
       k.available = false;
       k.why = "the direct-load tiles need unit-stride K or M/N operands";
@@ -551,9 +552,9 @@ NodeKernel prepare_conv(const Node& nd, int variant, int dtype, const std::vecto
 }  // namespace
 
 // Which steps pay off inside the product's launch was measured per tile
-// against the product followed by separate elementwise kernels.  Tile 9 (the
-// whole-K-in-LDS kernel for short-K attention products) has no registers to
-// spare: bias only.  On the large bf16 tiles (6, 8) the epilogue runs after
+// against the product followed by separate elementwise kernels.  bf16 tile 9
+// (the whole-K-in-LDS kernel for short-K attention products) has no
+// registers to spare: bias only.  On the large bf16 tiles (6, 8) the epilogue runs after
 // the last MFMA with nothing left to overlap it: a GELU or SiLU there costs
 // 13-41 us on a 2048 x 11008 output, more than its own kernel (17-21 us),
 // and the per-element reads of an Add / Mul tensor 15-75 us: bias only.  The
@@ -563,7 +564,7 @@ NodeKernel prepare_conv(const Node& nd, int variant, int dtype, const std::vecto
 int gemm_epilogue_caps(int variant, int dtype) {
   variant = gemm_tile_of(variant);
   const bool bf16 = dtype == FLUID_BF16;
-  if (variant == 9 || (bf16 && (variant == 6 || variant == 8))) return EPI_BIAS;
+  if (bf16 && (variant == 6 || variant == 8 || variant == 9)) return EPI_BIAS;
   const bool rop = (variant >= 1 && variant <= 5) || (!bf16 && variant >= 6);
   return EPI_BIAS | EPI_ACT | (rop ? EPI_ROP : 0);
 }
@@ -624,7 +625,7 @@ std::string NodeKernel::name() const {
         return e.empty() ? e : "_e" + e;
       };
       static const char* tiles[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "p256x128", "p128", "p256x128s3", "q128"};
-      static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4", "r128", "-"};
+      static const char* tiles_f32[] = {"t128", "t64", "sk32w4", "sk32w8", "sk64x32w4", "sk32w16", "dl16x32w8", "dl32w4", "r128", "r128w8"};
       return "gemm_" + dt + "_" + (dtype == DT_BF16 ? tiles : tiles_f32)[gemm_tile] + "_a" + gm[amode] + "_b" + gm[bmode] + "_c" +
              (cmode == 1 ? "n" : cmode == 2 ? "m" : "g") + (gemm.causal ? "_causal" + std::to_string(gemm.causal) : "") +
              epi_suffix();

@@ -86,12 +86,13 @@ def test_projection_gemm_all_layouts(dtype, shape, variant, tmp_path):
 
 
 @pytest.mark.parametrize("shape", [(1, 37, 1000, 70), (2, 65, 3100, 40)], ids=str)
-@pytest.mark.parametrize("variant", [6, 7, 16, 17])
+@pytest.mark.parametrize("variant", [6, 7, 8, 9, 16, 17, 18, 19])
 def test_projection_gemm_long_k(shape, variant, tmp_path):
     """The fp32 direct-load tiles on K slices of more than six 16-k groups
     (the rotating K loop), group counts not divisible by 4 and K not
-    divisible by 16, with A in every layout and the weight row-major (6, 7)
-    or K-contiguous (16, 17)."""
+    divisible by 16, and the fp32 128 x 128 tiles on odd counts of 32-k
+    tiles with a partial last one, with A in every layout and the weight
+    row-major (6-9) or K-contiguous (16-19)."""
     B, S, K, N = shape
     og, a, c = proj_graph(B, S, K, N, "f32")
     for pa, pc in itertools.product(layouts.layout_list((B, S, K)), layouts.layout_list((B, S, N))[:2]):
@@ -147,11 +148,11 @@ def epilogue_graph(B, S, K, N, dtype, keep_a, chain="bias_gelu"):
 
 def fusable_steps(chain, v, dtype):
     """How many of the chain's steps a MatMul of variant v absorbs when
-    nothing else stops it: variant 9 (short-K attention products) and the
-    bf16 variants 6 and 8 take a bias only; the Add / Mul with another tensor
-    is taken by variants 1-5, and by the fp32 variants 6-8."""
-    bias_only = v == 9 or (dtype == "bf16" and v in (6, 8))
-    rop = 1 <= v <= 5 or (dtype == "f32" and v in (6, 7, 8))
+    nothing else stops it: the bf16 variants 6, 8 and 9 (short-K attention
+    products) take a bias only; the Add / Mul with another tensor is taken
+    by variants 1-5, and by the fp32 variants 6-9."""
+    bias_only = dtype == "bf16" and v in (6, 8, 9)
+    rop = 1 <= v <= 5 or (dtype == "f32" and v in (6, 7, 8, 9))
     n = 0
     for step in EPILOGUES[chain]:
         if step == "bias" or (step in ("gelu", "silu") and not bias_only) or (step.endswith("_r") and rop):
