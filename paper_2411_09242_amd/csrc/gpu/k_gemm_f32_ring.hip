@@ -41,15 +41,14 @@ __device__ __forceinline__ int mnrow_swz(int k) { return (k & 1) << 3; }
 
 }  // namespace
 
-// One 128 x 128 output tile (tile index bid of p's row-major order).
 template <int W, bool AK, bool BK, bool RES>
-__device__ __forceinline__ void ring_tile(const GemmParams& p, uint32_t bid) {
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W / 2))) void gemm_f32_ring_kernel(GemmParams p) {
   constexpr int NQ = 16 / W;          // 1 KiB blocks per operand, stage and wavefront
   constexpr int WN = W / 2;           // wavefronts along N
   constexpr int JN = 128 / WN / 32;   // 32-wide MFMA blocks per wavefront along N
   __shared__ __attribute__((aligned(1024))) uint8_t As[2][FR_STAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t Bs[2][FR_STAGE];
-  const TileCoord tc = tile_coord_at(p, bid, FR_T, FR_T);
+  const TileCoord tc = tile_coord(p, FR_T, FR_T);
   // causal attention: a tile entirely above the diagonal is never read; a
   // row block's A is zero past its last row, so K stops there
   if ((p.causal & 1u) && tc.n0 > tc.m0 + FR_T - 1) return;
@@ -211,20 +210,6 @@ __device__ __forceinline__ void ring_tile(const GemmParams& p, uint32_t bid) {
     }
 }
 
-template <int W, bool AK, bool BK, bool RES>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W / 2))) void gemm_f32_ring_kernel(GemmParams p) {
-  ring_tile<W, AK, BK, RES>(p, blockIdx.x);
-}
-
-// The members of a group share the tile, operand modes and epilogue
-// instance; each workgroup runs one tile of its member.
-template <int W, bool AK, bool BK, bool RES>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W / 2))) void gemm_f32_ring_group_kernel(GemmGroup G) {
-  uint32_t i = 0;
-  while (i + 1 < G.n && blockIdx.x >= G.tiles[i + 1]) ++i;
-  ring_tile<W, AK, BK, RES>(G.p[i], blockIdx.x - G.tiles[i]);
-}
-
 template <int W>
 hipError_t ring_go(const NodeKernel& k, hipStream_t s) {
   const GemmParams& p = k.gemm;
@@ -241,30 +226,6 @@ hipError_t ring_go(const NodeKernel& k, hipStream_t s) {
   else FLUID_FR(false, false);
 #undef FLUID_FR
   return hipGetLastError();
-}
-
-template <int W>
-hipError_t ring_group_go(const NodeKernel& k, const GemmGroup& G, hipStream_t s) {
-  const dim3 grid(G.tiles[G.n]);
-#define FLUID_FRG(AKv, BKv)                                                                                       \
-  do {                                                                                                            \
-    if (k.gemm.rop) hipLaunchKernelGGL((gemm_f32_ring_group_kernel<W, AKv, BKv, true>), grid, dim3(64 * W), 0, s, G); \
-    else hipLaunchKernelGGL((gemm_f32_ring_group_kernel<W, AKv, BKv, false>), grid, dim3(64 * W), 0, s, G);      \
-  } while (0)
-  const bool ak = k.amode == GM_K, bk = k.bmode == GM_K;
-  if (ak && bk) FLUID_FRG(true, true);
-  else if (ak) FLUID_FRG(true, false);
-  else if (bk) FLUID_FRG(false, true);
-  else FLUID_FRG(false, false);
-#undef FLUID_FRG
-  return hipGetLastError();
-}
-
-hipError_t launch_gemm_f32_ring_group(const NodeKernel& k, const GemmGroup& G, hipStream_t s) {
-  if (k.dtype != DT_F32 || (k.amode != GM_K && k.amode != GM_MN) || (k.bmode != GM_K && k.bmode != GM_MN) ||
-      (k.gemm_tile != 8 && k.gemm_tile != 9) || G.n < 1 || G.n > (uint32_t)kMaxGroup)
-    return hipErrorInvalidValue;
-  return k.gemm_tile == 8 ? ring_group_go<4>(k, G, s) : ring_group_go<8>(k, G, s);
 }
 
 // fp32 tile 8: four wavefronts; tile 9: eight

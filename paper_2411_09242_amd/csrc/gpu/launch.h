@@ -16,8 +16,6 @@ hipError_t launch_gemm_bf16_dl(const NodeKernel& k, hipStream_t s);
 hipError_t launch_gemm_bf16_qk(const NodeKernel& k, hipStream_t s);
 hipError_t launch_gemm_f32_dl(const NodeKernel& k, hipStream_t s);
 hipError_t launch_gemm_f32_ring(const NodeKernel& k, hipStream_t s);
-// The same for the fp32 128 x 128 tiles (8 and 9).
-hipError_t launch_gemm_f32_ring_group(const NodeKernel& k, const GemmGroup& G, hipStream_t s);
 // One launch for the G.n products of G, all of k's tile, operand modes and
 // epilogue instance (fp32 tiles 6 and 7).
 hipError_t launch_gemm_f32_dl_group(const NodeKernel& k, const GemmGroup& G, hipStream_t s);

@@ -120,7 +120,7 @@ hipError_t launch_group(const Prepared& P, const PreparedNode& pn, const NodeKer
     G.p[t + 1] = q;
     G.tiles[t + 2] = G.tiles[t + 1] + q.tiles_m * q.tiles_n * q.G;
   }
-  return k.gemm_tile >= 8 ? launch_gemm_f32_ring_group(k, G, s) : launch_gemm_f32_dl_group(k, G, s);
+  return launch_gemm_f32_dl_group(k, G, s);
 }
 
 // ------------------------------------------------------------ tracing

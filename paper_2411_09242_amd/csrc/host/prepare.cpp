@@ -199,17 +199,16 @@ std::vector<std::pair<int, Bind>> read_operands(const Graph& g, const Prepared& 
 }
 
 // Grouped launches.  Consecutive launches of fp32 products with the same
-// tile (the direct-load tiles 6 and 7 or the 128 x 128 tiles 8 and 9),
-// operand modes and epilogue instance -- the Q, K and V projections of a
-// layer once their bias Adds are fused and their head reshapes are views
-// -- go out as one launch when none reads or overwrites what another
-// writes (they run concurrently).
+// direct-load tile (6 or 7), operand modes and epilogue instance -- the Q,
+// K and V projections of a layer once their bias Adds are fused and their
+// head reshapes are views -- go out as one launch when none reads or
+// overwrites what another writes (they run concurrently).
 void group_launches(const Graph& g, const ArenaPlan* ap, Prepared& P) {
   auto kern = [&](size_t i) -> const NodeKernel& { return P.nodes[i].fuse_n ? P.nodes[i].kf : P.nodes[i].k; };
   auto eligible = [&](size_t i) {
     const NodeKernel& k = kern(i);
     return !P.nodes[i].fused_away && k.family == KF_GEMM && k.dtype == DT_F32 &&
-           k.gemm_tile >= 6 && k.gemm_tile <= 9;
+           (k.gemm_tile == 6 || k.gemm_tile == 7);
   };
   auto next_launch = [&](size_t i) {
     size_t j = i + 1;

@@ -245,7 +245,7 @@ def siblings_graph(B, S, K, N, dtype, chained=False):
 
 
 @pytest.mark.parametrize("shape", [(1, 37, 64, 64), (2, 130, 96, 96)], ids=str)
-@pytest.mark.parametrize("variant", [6, 7, 8, 9])
+@pytest.mark.parametrize("variant", [6, 7])
 @pytest.mark.parametrize("chained", [False, True])
 def test_grouped_products(shape, variant, chained, tmp_path):
     """Sibling fp32 products launched as one grouped launch (each with its
@@ -265,8 +265,7 @@ def test_grouped_products(shape, variant, chained, tmp_path):
                                      epilogue=True)
         except Exception as ex:  # noqa: BLE001
             # chained: the second product reads the first's output, which in
-            # an M-contiguous layout with M % 4 != 0 no direct-load or
-            # 128 x 128 fp32 tile takes
+            # an M-contiguous layout with M % 4 != 0 no direct-load tile takes
             if chained and "cannot run with these layouts" in str(ex):
                 continue
             raise

@@ -53,13 +53,11 @@ def test_epilogue_arena_lets_every_chain_fuse(chain, v, dtype, tmp_path):
 
 
 @pytest.mark.parametrize("chained", [False, True])
-@pytest.mark.parametrize("variant,dtype,grouped", [(6, "f32", True), (7, "f32", True), (8, "f32", True),
-                                                   (9, "f32", True), (2, "f32", False), (6, "bf16", False),
-                                                   (9, "bf16", False)])
+@pytest.mark.parametrize("variant,dtype,grouped", [(6, "f32", True), (7, "f32", True), (2, "f32", False),
+                                                   (6, "bf16", False)])
 def test_grouped_launch_count(chained, variant, dtype, grouped, tmp_path):
-    """Sibling products of the fp32 direct-load and 128 x 128 tiles share
-    one launch unless one reads another's output; other tiles launch one by
-    one."""
+    """Sibling products of the fp32 direct-load tiles share one launch
+    unless one reads another's output; other tiles launch one by one."""
     from test_gpu_ops import siblings_graph
     og, prods, outs = siblings_graph(1, 37, 64, 64, dtype, chained)
     mms = [i for i, nd in enumerate(og.nodes) if nd.op == "matmul"]
