@@ -21,17 +21,37 @@ pytestmark = pytest.mark.gpu
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
+def _stored_table(F, g, cfg):
+    """The cost table stored with the library for this workload (the one
+    the benchmark plans from), or None when the library sources have
+    changed since it was measured (the benchmark then measures afresh)."""
+    import bench
+    meta = bench.stored_table_meta(cfg["name"])
+    path = os.path.join(bench.STORED_TABLES, cfg["name"] + ".json")
+    if not meta or meta.get("sources") != bench.library_source_hash() or not os.path.exists(path):
+        return None
+    return F.CostTable.load(path, g)
+
+
+@pytest.mark.parametrize("table", ["measured", "stored"])
 @pytest.mark.parametrize("idx", [4, 5])
-def test_large_config_matches_oracle_samples(idx, tmp_path):
+def test_large_config_matches_oracle_samples(idx, table, tmp_path):
+    """table: a cost table measured here, or the stored one the benchmark
+    plans from (its plan is then exactly the benchmark's)."""
     import torch
     from paper_2411_09242_amd import fluid as F
     gold = np.load(os.path.join(HERE, "golden", f"oracle_rows_cfg{idx}.npz"), allow_pickle=False)
     cfg = synth_inputs.config(idx)
     say(f"cfg{idx}: inputs")
     g = F.Graph.transformer(cfg)
+    if table == "stored":
+        t = _stored_table(F, g, cfg)
+        if t is None:
+            pytest.skip("the stored cost table was measured with other library sources")
     x, consts = synth_inputs.make_inputs(cfg, g.const_specs(), idx)
-    say(f"cfg{idx}: measuring the cost table")
-    t = F.CostTable.measure(g, reps=2)
+    if table == "measured":
+        say(f"cfg{idx}: measuring the cost table")
+        t = F.CostTable.measure(g, reps=2)
     lp = F.LayoutPlan(g, t)
     ap = F.ArenaPlan(g, lp, epilogue=True)   # the benchmark's configuration
     say(f"cfg{idx}: plan {lp.total_ns} ns (guard {lp.guard_used}); arena {ap.peak / 2**20:.1f} MiB "
