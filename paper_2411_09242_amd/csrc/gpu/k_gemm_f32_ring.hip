@@ -3,16 +3,16 @@
 // A[l%32][l/32], B[l/32][l%32]; accumulator v of lane l holds
 // C[8(v/4) + 4(l/32) + v%4][l%32]).
 //
-// W = 4 wavefronts of 64 x 64 (2 x 2 blocks of 32 x 32; 64 MFMAs of 64
-// cycles per wavefront and K-tile) or W = 8 of 64 x 32 (two wavefronts per
-// SIMD within one workgroup, for outputs with about one tile per CU); one
-// barrier per K-tile.  Two LDS stages
+// W = 8 wavefronts of 64 x 32 (2 x 1 blocks of 32 x 32; 32 MFMAs of 64
+// cycles per wavefront and K-tile: two wavefronts per SIMD within one
+// workgroup) or W = 16 of 32 x 32 (four per SIMD, for outputs with about
+// one tile per CU); one barrier per K-tile.  Two LDS stages
 // of 32 KiB; the operands of K-tile t+2 are loaded into registers (16 bytes
 // per load) while tile t is multiplied and are written to LDS once tile t+1
 // is in place, so a load has a whole K-tile of MFMAs to land.  Two
 // workgroups share a CU where the output has tiles for it; where it has
-// few (a 4096 x 1024 product has 256), the eight-wavefront form gives each
-// SIMD a second wavefront to issue from while one waits.
+// few (a 4096 x 1024 product has 256), the sixteen-wavefront form gives
+// each SIMD four wavefronts to issue from while one waits.
 //
 // Each operand is staged in its HBM orientation:
 //  * K-contiguous (A [m][k], B [n][k]): rows of 32 floats (8 chunks of 16
@@ -42,10 +42,12 @@ __device__ __forceinline__ int mnrow_swz(int k) { return (k & 1) << 3; }
 }  // namespace
 
 template <int W, bool AK, bool BK, bool RES>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W / 2))) void gemm_f32_ring_kernel(GemmParams p) {
-  constexpr int NQ = 16 / W;          // 1 KiB blocks per operand, stage and wavefront
-  constexpr int WN = W / 2;           // wavefronts along N
-  constexpr int JN = 128 / WN / 32;   // 32-wide MFMA blocks per wavefront along N
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W == 16 ? 4 : W / 2))) void gemm_f32_ring_kernel(GemmParams p) {
+  constexpr int NQ = 16 / W;            // 1 KiB blocks per operand, stage and wavefront
+  constexpr int WM = W == 16 ? 4 : 2;   // wavefronts along M
+  constexpr int WN = W / WM;            // wavefronts along N
+  constexpr int IM = 128 / WM / 32;     // 32-row MFMA blocks per wavefront along M
+  constexpr int JN = 128 / WN / 32;     // 32-wide MFMA blocks per wavefront along N
   __shared__ __attribute__((aligned(1024))) uint8_t As[2][FR_STAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t Bs[2][FR_STAGE];
   const TileCoord tc = tile_coord(p, FR_T, FR_T);
@@ -130,9 +132,9 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W
     else return *(const float*)(s + k * 512 + (((n >> 2) ^ mnrow_swz(k)) << 4) + (n & 3) * 4);
   };
 
-  f32x16 acc[2][JN];
+  f32x16 acc[IM][JN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < IM; ++i)
 #pragma unroll
     for (int j = 0; j < JN; ++j)
 #pragma unroll
@@ -142,13 +144,13 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W
 #pragma unroll
     for (int s = 0; s < FR_BK / 2; ++s) {
       const int k = 2 * s + lh;
-      float a[2], b[JN];
+      float a[IM], b[JN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = a_at(st, wm * 64 + 32 * i + lr, k);
+      for (int i = 0; i < IM; ++i) a[i] = a_at(st, wm * 32 * IM + 32 * i + lr, k);
 #pragma unroll
       for (int j = 0; j < JN; ++j) b[j] = b_at(st, wn * 32 * JN + 32 * j + lr, k);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < IM; ++i)
 #pragma unroll
         for (int j = 0; j < JN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
     }
@@ -183,18 +185,18 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W / 4, W
 
   float* C = (float*)p.C;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < IM; ++i)
 #pragma unroll
     for (int j = 0; j < JN; ++j)
-      epi16<RES>(p, tc.r_base, tc.m0 + wm * 64 + 32 * i + 4 * lh, tc.n0 + wn * 32 * JN + 32 * j + lr, acc[i][j]);
+      epi16<RES>(p, tc.r_base, tc.m0 + wm * 32 * IM + 32 * i + 4 * lh, tc.n0 + wn * 32 * JN + 32 * j + lr, acc[i][j]);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < IM; ++i)
 #pragma unroll
     for (int j = 0; j < JN; ++j) {
       const uint32_t n = tc.n0 + wn * 32 * JN + 32 * j + lr;
 #pragma unroll
       for (int vg = 0; vg < 4; ++vg) {
-        const uint32_t mb = tc.m0 + wm * 64 + 32 * i + 8 * vg + 4 * lh;
+        const uint32_t mb = tc.m0 + wm * 32 * IM + 32 * i + 8 * vg + 4 * lh;
         if (n >= p.N || mb >= p.M) continue;
         if (p.cmode == 2) {
           const int32_t o = tc.c_base + row_off(p, mb, p.c_m1, p.c_m2) + (int32_t)n * p.c_n;
@@ -228,12 +230,12 @@ hipError_t ring_go(const NodeKernel& k, hipStream_t s) {
   return hipGetLastError();
 }
 
-// fp32 tile 8: four wavefronts; tile 9: eight
+// fp32 tile 8: sixteen wavefronts; tile 9: eight
 hipError_t launch_gemm_f32_ring(const NodeKernel& k, hipStream_t s) {
   if (k.dtype != DT_F32 || (k.amode != GM_K && k.amode != GM_MN) || (k.bmode != GM_K && k.bmode != GM_MN) ||
       (k.gemm_tile != 8 && k.gemm_tile != 9))
     return hipErrorInvalidValue;
-  return k.gemm_tile == 8 ? ring_go<4>(k, s) : ring_go<8>(k, s);
+  return k.gemm_tile == 8 ? ring_go<16>(k, s) : ring_go<8>(k, s);
 }
 
 }  // namespace fluid

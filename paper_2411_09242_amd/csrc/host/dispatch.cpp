@@ -430,8 +430,8 @@ NodeKernel prepare_gemm(const Node& nd, int variant, int dtype, const std::vecto
   // persistent with the whole K (at most 128) in LDS;
   // fp32 6: 16x32 with K split over 8 wavefronts, 7: 32x32 over 4, operands
   // loaded straight into MFMA registers, 8 and 9: 128x128 double-buffered
-  // in LDS with the next K-tile in flight in registers, over four or eight
-  // wavefronts
+  // in LDS with the next K-tile in flight in registers, over sixteen or
+  // eight wavefronts
   static const uint32_t TM[] = {128, 64, 32, 32, 64, 32, 256, 128, 256, 128};
   static const uint32_t TN[] = {128, 64, 32, 32, 32, 32, 128, 128, 128, 128};
   uint32_t tm = TM[tile], tn = TN[tile];
