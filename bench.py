@@ -43,16 +43,16 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 # its kernel family's device sources when it was taken and is reported as
 # `traffic` only while they are unchanged (else null).
 TRAFFIC = {
-    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_r128w8_amn_bmn_cm_eb',
-     '[[\'matmul\', \'(8, 512, 1024)\', "((8, 512, 4096), (\'c\', 4096, 1024))"], [\'add\', \'(8, 512, 1024)\', "((8, 512, 1024), (\'c\', 1024))"]]'): (570758369, '5a8c98a206cf829d'),
-    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128s3_ak_bmn_cn',
-     '[[\'matmul\', \'(1, 2048, 11008)\', "((1, 2048, 4096), (\'c\', 4096, 11008))"]]'): (894170822, '5a8c98a206cf829d'),
+    ('bert-large-24l-b8-s512-h1024', 'gemm_f32_r128w8_ak_bk_cm_ebg',
+     '[[\'matmul\', \'(8, 512, 4096)\', "((8, 512, 1024), (\'c\', 1024, 4096))"], [\'add\', \'(8, 512, 4096)\', "((8, 512, 4096), (\'c\', 4096))"], [\'gelu\', \'(8, 512, 4096)\', \'((8, 512, 4096),)\']]'): (262219469, '63679b87022e08f9'),
+    ('llama-8l-b1-s2048-h4096-prefill', 'gemm_bf16_p256x128_ak_bk_cn',
+     '[[\'matmul\', \'(1, 2048, 11008)\', "((1, 2048, 4096), (\'c\', 4096, 11008))"]]'): (980160204, '63679b87022e08f9'),
     ('gpt2-small-12l-b1-s512-h768-prefill', 'gemm_f32_dl32w4_ak_bmn_cm_ebg',
-     '[[\'matmul\', \'(1, 512, 3072)\', "((1, 512, 768), (\'c\', 768, 3072))"], [\'add\', \'(1, 512, 3072)\', "((1, 512, 3072), (\'c\', 3072))"], [\'gelu\', \'(1, 512, 3072)\', \'((1, 512, 3072),)\']]'): (28486998, '5a8c98a206cf829d'),
-    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cm_ebg',
-     '[[\'matmul\', \'(1, 128, 3072)\', "((1, 128, 768), (\'c\', 768, 3072))"], [\'add\', \'(1, 128, 3072)\', "((1, 128, 3072), (\'c\', 3072))"], [\'gelu\', \'(1, 128, 3072)\', \'((1, 128, 3072),)\']]'): (14374405, '5a8c98a206cf829d'),
+     '[[\'matmul\', \'(1, 512, 3072)\', "((1, 512, 768), (\'c\', 768, 3072))"], [\'add\', \'(1, 512, 3072)\', "((1, 512, 3072), (\'c\', 3072))"], [\'gelu\', \'(1, 512, 3072)\', \'((1, 512, 3072),)\']]'): (28487074, '63679b87022e08f9'),
+    ('bert-base-12l-b1-s128-h768', 'gemm_f32_dl16x32w8_ak_bmn_cn_ebg',
+     '[[\'matmul\', \'(1, 128, 3072)\', "((1, 128, 768), (\'c\', 768, 3072))"], [\'add\', \'(1, 128, 3072)\', "((1, 128, 3072), (\'c\', 3072))"], [\'gelu\', \'(1, 128, 3072)\', \'((1, 128, 3072),)\']]'): (14367226, '63679b87022e08f9'),
     ('vgg16-b1-224', 'conv_f32_t64_kuvc_ks4',
-     '[[\'conv\', \'(1, 256, 56, 56)\', "((1, 256, 58, 58), (\'c\', 256, 256, 3, 3), (\'c\', 256))"]]'): (35115541, 'f2917c1c434b9f34'),
+     '[[\'conv\', \'(1, 256, 56, 56)\', "((1, 256, 58, 58), (\'c\', 256, 256, 3, 3), (\'c\', 256))"]]'): (35116555, 'f2917c1c434b9f34'),
 }
 
 # the device sources of each kernel family (by launch-name prefix)
