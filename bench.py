@@ -392,7 +392,7 @@ def row_major_weights(F, g, table):
 
 
 def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=None, tables=None,
-                     kernel_only=False):
+                     kernel_only=False, plan_steps=False):
     """Cost table (untimed), plans, then the timed regions; returns a dict.
     tables: (directory, "save" | "load") -- keep each workload's measured
     table, or plan from a kept one instead of measuring (same plan, e.g. for
@@ -477,6 +477,9 @@ def measure_workload(F, torch, cfg, x, consts, steps, warmup, reps, save_table=N
         torch.cuda.synchronize()
         return {"kernel": dom[0]["name"], "node_sigs": [list(map(str, x)) for x in dom_key[1:]],
                 "launches": steps * len(dom)}
+    if plan_steps:   # only the plan's own steps, eagerly (for a kernel trace of the graph)
+        ms, _ = time_steps(ex, steps, stream, torch)
+        return {"steps": steps, "eager_ms_per_step": round(ms, 4), "launches_per_step": len(units)}
     op_classes = op_class_rates(g, units, ex, steps, torch)
 
     # timed region 1: K eager steps (whole graph, no per-launch events)
@@ -614,6 +617,8 @@ def main():
                     help="measure every cost table and store it (default: with the library)")
     ap.add_argument("--kernel-only", action="store_true",
                     help="launch only each workload's dominant kernel (for counter runs); prints what ran")
+    ap.add_argument("--plan-steps", action="store_true",
+                    help="run only the plan's steps, eagerly (for a kernel trace of the whole graph)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the executor has no multi-GPU path "
@@ -629,7 +634,7 @@ def main():
     calibration_copy(torch)
     cfg = synth_inputs.config(a.config)
     log(f"workload {cfg['name']}")
-    if a.kernel_only:   # values do not matter for which kernel runs or the bytes it moves
+    if a.kernel_only or a.plan_steps:   # values do not matter for which kernels run or the bytes they move
         x, consts = device_inputs(torch, F, cfg, a.config)
     else:
         x, consts = synth_inputs.make_inputs(cfg, F.Graph.transformer(cfg).const_specs(), a.config)
@@ -639,9 +644,11 @@ def main():
         tables = (a.store_tables, "store")
     else:
         tables = None if a.measure else (STORED_TABLES, "stored")
-    r = measure_workload(F, torch, cfg, x, consts, a.steps, a.warmup, a.reps, a.save_table, tables, a.kernel_only)
-    if a.kernel_only:
-        print(json.dumps({"kernel_only": True, "workload": cfg["name"], **r}), flush=True)
+    r = measure_workload(F, torch, cfg, x, consts, a.steps, a.warmup, a.reps, a.save_table, tables, a.kernel_only,
+                         a.plan_steps)
+    if a.kernel_only or a.plan_steps:
+        print(json.dumps({"kernel_only" if a.kernel_only else "plan_steps": True, "workload": cfg["name"], **r}),
+              flush=True)
         return
     res = {
         "metric": "graph latency (ms) + peak arena MB vs naive plan; kernel % of roofline",
